@@ -1,0 +1,155 @@
+/*
+ * masq.h -- C ABI of the MI355X (gfx950) modality-aware W8A8 + low-rank linear.
+ *
+ * The layer is the inference rule of MASQuant (Modality-Aware Smoothing
+ * Quantization), Sec. 4.3, final case equation.  For a token row x_t of
+ * modality m (0 = text, the base modality; 1.. = vision, audio, ...):
+ *
+ *     xs_t  = x_t * inv_smooth[m]                       (X_m S_m^-1, Sec. 3.1/4.3)
+ *     q_t   = Q(xs_t)  per-token symmetric int8         (eq. PTQ, z = 0, [-127,127])
+ *     y_t   = (float(q_t . Wq^T) * delta_t) * w_scale   (the shared Q(S_t W))
+ *     y_t  += (xs_t L1^m) L2^m          for m != text   (Cross-Modal Compensation,
+ *                                                        eq. l1l2)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every array argument is a DEVICE pointer owned by the caller; it must stay
+ *    valid until the work enqueued on `stream` has completed.  Inputs are never
+ *    modified.  The library never allocates, frees or synchronises; scratch
+ *    space comes from the caller's workspace.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    Every entry point only enqueues work; device faults surface at the
+ *    caller's next synchronisation.
+ *  - Layouts are row-major.  Weight-like operands are [out][in] (the
+ *    nn.Linear convention), so every contraction reads K-contiguous rows:
+ *        x          [T][c_in]            f32 or bf16 (masq_dtype)
+ *        modality   [T]                  int32, values in [0, n_mod)
+ *        inv_smooth [n_mod][c_in]        f32, fl(1 / s^m)         (Sec. 4.2)
+ *        wq         [c_out][c_in]        int8, Q(S_t W) transposed (Sec. 4.3)
+ *        w_scale    [c_out]              f32, per-output-channel step
+ *        l_down     [n_mod-1][rank][c_in]  (L1^m)^T, slot m-1 for modality m
+ *        r_up       [n_mod-1][c_out][rank] (L2^m)^T
+ *        y          [T][c_out]           f32 or bf16
+ *  - Preconditions, checked before anything is enqueued (on failure nothing is
+ *    enqueued and outputs are untouched): non-null pointers (except where
+ *    marked nullable), T >= 0, c_in > 0 and c_in % 16 == 0, c_out > 0 and
+ *    c_out % 16 == 0, rank == 0 or rank % 16 == 0 (rank <= 256),
+ *    1 <= n_mod <= 4, 16-byte aligned pointers, a large enough workspace.
+ *    T == 0 is a successful no-op.
+ *  - Modality ids outside [0, n_mod) are treated as text (memory-safe, but
+ *    not a supported input); non-finite inputs give unspecified results.
+ *  - Rounding contract (bit-exact parts): the smoothing is one fp32 multiply;
+ *    delta_t = fl(amax_t / 127) and the codes use a multiply by
+ *    fl(127 / amax_t), both correctly rounded divisions; codes round half to
+ *    even; an all-zero row gives delta = 0 and zero codes; int32 accumulation
+ *    is exact; dequantisation is fl(fl(float(acc) * delta_t) * w_scale[o]);
+ *    bf16 outputs are one round-to-nearest-even of the fp32 result.
+ *  - No C++ exception crosses this boundary.  The library holds no mutable
+ *    global state; concurrent calls are safe if their outputs and workspaces
+ *    do not overlap.
+ */
+#ifndef MASQ_H
+#define MASQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MASQ_OK = 0,
+    MASQ_ERR_NULL = 1,        /* a required pointer is NULL                      */
+    MASQ_ERR_SHAPE = 2,       /* a size violates the preconditions above         */
+    MASQ_ERR_DTYPE = 3,       /* unknown or unsupported dtype combination        */
+    MASQ_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned                */
+    MASQ_ERR_WORKSPACE = 5,   /* workspace smaller than the query says           */
+    MASQ_ERR_HIP = 6,         /* a kernel launch was rejected by the runtime     */
+    MASQ_ERR_UNSUPPORTED = 7  /* valid request this build does not implement     */
+} masq_status;
+
+typedef enum { MASQ_F32 = 0, MASQ_BF16 = 1 } masq_dtype;
+
+/* Version of this interface (bumped on any signature or semantics change). */
+int masq_abi_version(void);
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* masq_status_str(masq_status s);
+
+/*
+ * Smoothing and per-token quantisation (Sec. 4.3 X_m S_m^-1; eq. PTQ).
+ * Writes q [T][c_in] int8 and x_scale [T] f32 (delta_t).
+ * x_dt: MASQ_F32 or MASQ_BF16.
+ */
+masq_status masq_smooth_quant(const void* x, masq_dtype x_dt, const int32_t* modality,
+                              const float* inv_smooth, int64_t T, int64_t c_in,
+                              int32_t n_mod, int8_t* q, float* x_scale, void* stream);
+
+/*
+ * Product with the shared quantised weight, Q(X S^-1) . Q(S_t W) (Sec. 4.3).
+ * acc (nullable): int32 [T][c_out] exact accumulators.
+ * y   (nullable): the dequantised product in y_dt (no compensation).
+ * At least one of acc, y must be non-null.
+ */
+masq_status masq_w8a8_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
+                           const float* w_scale, int64_t T, int64_t c_in, int64_t c_out,
+                           int32_t* acc, void* y, masq_dtype y_dt, void* stream);
+
+/*
+ * Cross-Modal Compensation alone (Sec. 4.3, eq. l1l2): for every row with
+ * modality m != 0, y[t] += (x_t S_m^-1 L1^m) L2^m, accumulated in fp32 and
+ * rounded once into y's dtype.  Text rows of y are left untouched.
+ * y is read-modify-write.  lr_dt is the dtype of l_down and r_up.
+ */
+masq_status masq_lowrank_comp(const void* x, masq_dtype x_dt, const int32_t* modality,
+                              const float* inv_smooth, const void* l_down,
+                              const void* r_up, masq_dtype lr_dt, int64_t T,
+                              int64_t c_in, int64_t c_out, int32_t rank, int32_t n_mod,
+                              void* y, masq_dtype y_dt, void* stream);
+
+/*
+ * The whole layer (Sec. 4.3 final case equation): smoothing, per-token int8
+ * quantisation, the shared-weight int8 GEMM with int32 accumulation,
+ * dequantisation and, on non-text rows only, the rank-r compensation; y is
+ * fully overwritten.  workspace: device scratch of at least
+ * masq_linear_fused_workspace_bytes(...) bytes, 256-byte aligned, whose
+ * contents need not be initialised; it must not be shared by calls that may
+ * run concurrently.
+ */
+masq_status masq_linear_fused(const void* x, masq_dtype x_dt, const int32_t* modality,
+                              const float* inv_smooth, const int8_t* wq,
+                              const float* w_scale, const void* l_down, const void* r_up,
+                              masq_dtype lr_dt, int64_t T, int64_t c_in, int64_t c_out,
+                              int32_t rank, int32_t n_mod, void* y, masq_dtype y_dt,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+size_t masq_linear_fused_workspace_bytes(int64_t T, int64_t c_in, int64_t c_out,
+                                         int32_t rank, int32_t n_mod);
+
+/*
+ * The two launch stages masq_linear_fused is made of, with identical
+ * arguments, exposed so that a caller can place events or other stream work
+ * between them.  stage1: smoothing, quantisation and the rank-r
+ * down-projection into the workspace.  stage2: the int8 GEMM with the fused
+ * dequantisation and compensation epilogue, reading the workspace stage1
+ * wrote.  stage1 followed by stage2 on one stream equals masq_linear_fused.
+ */
+masq_status masq_linear_stage1(const void* x, masq_dtype x_dt, const int32_t* modality,
+                               const float* inv_smooth, const int8_t* wq,
+                               const float* w_scale, const void* l_down, const void* r_up,
+                               masq_dtype lr_dt, int64_t T, int64_t c_in, int64_t c_out,
+                               int32_t rank, int32_t n_mod, void* y, masq_dtype y_dt,
+                               void* workspace, size_t workspace_bytes, void* stream);
+masq_status masq_linear_stage2(const void* x, masq_dtype x_dt, const int32_t* modality,
+                               const float* inv_smooth, const int8_t* wq,
+                               const float* w_scale, const void* l_down, const void* r_up,
+                               masq_dtype lr_dt, int64_t T, int64_t c_in, int64_t c_out,
+                               int32_t rank, int32_t n_mod, void* y, masq_dtype y_dt,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MASQ_H */

@@ -1,0 +1,184 @@
+"""Offline calibration: the per-layer artifacts the GPU linear consumes.
+
+Host-side, fp64 NumPy, run once per layer before inference (the paper's
+calibration stage, Sec. 4.2-4.3).  Produces, in the C library's layouts:
+
+  inv_smooth [M][K] float32   fl(1 / s^m), s^m_i = sqrt(R^m_i / max_j |w_ji|)
+                              (MAS initial factors, Sec. 4.2; R^m from Sec. 4.1)
+  wq         [N][K] int8      Q(S_t W), symmetric per output channel (eq. PTQ)
+  w_scale    [N]    float32   its scales
+  l_down     [M-1][r][K]      (L1^m)^T, L1^m = T_m^-1 U_r        (eq. l1l2)
+  r_up       [M-1][N][r]      (L2^m)^T, L2^m = Sigma_r V_r^T
+                              from the truncated SVD of T_m dW_m, where
+                              dW_m = S_m W - Q(S_t W) and T_m whitens
+                              X_m S_m^-1 (Sec. 4.3)
+
+Built for large layers: the whitening is never formed as a K x K matrix when
+a modality has fewer calibration rows than channels (a thin SVD of the
+smoothed activations gives it in closed form), and the rank-r truncation uses a
+seeded randomized SVD (Halko, Martinsson and Tropp 2011, oversampling 10, two
+power iterations) when min(K, N) is large.  For small layers the truncation
+is an exact dense SVD.
+
+The covariance gets a ridge eps * tr(C) / K * I (eps = 1e-6) so that T_m is
+invertible when a modality has fewer rows than channels.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+QMAX = 127
+FLOOR = 1e-5
+EXACT_SVD_MAX = 1024
+
+
+def _to_bf16_values(a: np.ndarray) -> np.ndarray:
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return t.to(torch.bfloat16).to(torch.float32).numpy()
+
+
+def smoothing_factors(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: int):
+    """(s32 [M][K], inv_s32 [M][K]) from per-modality activation ranges."""
+    x = np.asarray(x, np.float32)
+    wmax = np.abs(np.asarray(w, np.float32)).max(axis=1).astype(np.float64)
+    s32 = np.empty((n_mod, x.shape[1]), np.float32)
+    for m in range(n_mod):
+        rows = x[modality == m]
+        rng = np.abs(rows).max(axis=0).astype(np.float64) if rows.shape[0] else np.zeros(x.shape[1])
+        s32[m] = np.sqrt(np.maximum(rng, FLOOR) / np.maximum(wmax, FLOOR)).astype(np.float32)
+    inv = (np.float32(1.0) / s32).astype(np.float32)
+    return s32, inv
+
+
+def quantize_shared_weight(w: np.ndarray, s32_text: np.ndarray):
+    """Q(diag(s_t) W) per output channel -> (wq [N][K] int8, w_scale [N] f32).
+
+    fp64 throughout: s32 * w is exact, the step is one correctly rounded
+    division, codes round half to even (torch.round)."""
+    import torch
+    ws = torch.from_numpy(np.ascontiguousarray(w, np.float32)).double()
+    ws.mul_(torch.from_numpy(np.asarray(s32_text, np.float32)).double()[:, None])
+    step = ws.abs().amax(dim=0) / QMAX
+    safe = torch.where(step > 0, step, torch.ones_like(step))
+    codes = torch.round(ws.div_(safe[None, :])).clamp_(-QMAX, QMAX)
+    codes[:, step == 0] = 0
+    return codes.t().contiguous().to(torch.int8).numpy(), step.float().numpy()
+
+
+def _weight_difference(w: np.ndarray, s32_m: np.ndarray, wq: np.ndarray, w_scale: np.ndarray):
+    """dW = S_m W - Q(S_t W) in fp64 [K][N] (Sec. 4.3)."""
+    import torch
+    dw = torch.from_numpy(np.ascontiguousarray(w, np.float32)).double()
+    dw.mul_(torch.from_numpy(np.asarray(s32_m, np.float32)).double()[:, None])
+    wdq = torch.from_numpy(wq).t().double()
+    wdq.mul_(torch.from_numpy(np.asarray(w_scale, np.float32)).double()[None, :])
+    dw.sub_(wdq)
+    return dw.numpy()
+
+
+class _Whitening:
+    """T = C^1/2 and T^-1 for C = Z^T Z + eps' I, applied without forming K x K
+    matrices when Z has fewer rows than columns."""
+
+    def __init__(self, z: np.ndarray, ridge: float):
+        k = z.shape[1]
+        if z.shape[0] >= k:
+            c = z.T @ z
+            eps = ridge * np.trace(c) / k
+            lam, p = np.linalg.eigh(c + eps * np.eye(k))
+            lam = np.maximum(lam, 0.0)
+            self.mode = "dense"
+            self.p = p
+            self.sq = np.sqrt(lam)
+            self.isq = np.where(lam > 0, 1.0 / np.sqrt(np.where(lam > 0, lam, 1.0)), 0.0)
+        else:
+            # thin SVD of Z from the eigen-decomposition of its n x n Gram matrix
+            mu, uz = np.linalg.eigh(z @ z.T)
+            keep = mu > mu.max() * 1e-13 if mu.size and mu.max() > 0 else np.zeros(mu.shape, bool)
+            mu, uz = mu[keep], uz[:, keep]
+            sig = np.sqrt(mu)
+            eps = ridge * np.sum(mu) / k
+            self.mode = "thin"
+            self.p = (z.T @ uz) / sig[None, :]               # [K][n] orthonormal columns
+            self.root_eps = np.sqrt(eps)
+            self.sq = np.sqrt(sig ** 2 + eps) - self.root_eps
+            with np.errstate(divide="ignore"):
+                base = 1.0 / self.root_eps if eps > 0 else 0.0
+                self.isq = np.where(sig ** 2 + eps > 0, 1.0 / np.sqrt(sig ** 2 + eps), 0.0) - base
+            self.inv_root_eps = base
+
+    def apply(self, a: np.ndarray) -> np.ndarray:          # T @ a
+        if self.mode == "dense":
+            return self.p @ (self.sq[:, None] * (self.p.T @ a))
+        return self.p @ (self.sq[:, None] * (self.p.T @ a)) + self.root_eps * a
+
+    def apply_inv(self, a: np.ndarray) -> np.ndarray:      # T^-1 @ a
+        if self.mode == "dense":
+            return self.p @ (self.isq[:, None] * (self.p.T @ a))
+        return self.p @ (self.isq[:, None] * (self.p.T @ a)) + self.inv_root_eps * a
+
+
+def _truncated_svd(wh: "_Whitening", dw: np.ndarray, r: int, seed: int):
+    """Top-r SVD of T dW.  Small problems: dense SVD of the explicit product.
+    Large ones: randomized range finder on T dW applied implicitly (T is
+    symmetric, so (T dW)^T q = dW^T (T q)); T dW is never formed."""
+    k, n = dw.shape
+    if min(k, n) <= EXACT_SVD_MAX or r >= min(k, n) // 2:
+        u, s, vt = np.linalg.svd(wh.apply(dw), full_matrices=False)
+        return u[:, :r], s[:r], vt[:r]
+    rng = np.random.default_rng(seed)
+    ell = min(r + 10, k, n)
+    q, _ = np.linalg.qr(wh.apply(dw @ rng.standard_normal((n, ell))))
+    for _ in range(2):
+        q, _ = np.linalg.qr(dw.T @ wh.apply(q))
+        q, _ = np.linalg.qr(wh.apply(dw @ q))
+    b = (dw.T @ wh.apply(q)).T                           # q^T T dW, ell x n
+    ub, s, vt = np.linalg.svd(b, full_matrices=False)
+    return (q @ ub)[:, :r], s[:r], vt[:r]
+
+
+def cmc_factors(z: np.ndarray, dw: np.ndarray, rank: int, ridge: float = 1e-6, seed: int = 0):
+    """L1 [K][r], L2 [r][N] with dW ~ L1 L2 minimising ||Z (dW - L1 L2)||_F."""
+    k, n = dw.shape
+    l1 = np.zeros((k, rank))
+    l2 = np.zeros((rank, n))
+    if rank == 0 or z.shape[0] == 0 or not np.any(z):
+        return l1, l2
+    wh = _Whitening(z, ridge)
+    u, s, vt = _truncated_svd(wh, dw, min(rank, k, n), seed)
+    rr = s.shape[0]
+    l1[:, :rr] = wh.apply_inv(u)
+    l2[:rr] = s[:, None] * vt
+    return l1, l2
+
+
+def calibrate_layer(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: int,
+                    rank: int, lr_dtype: str = "bf16", ridge: float = 1e-6,
+                    seed: int = 0) -> dict:
+    """All inference artifacts of one linear from calibration activations.
+
+    x: [T][K] float32 calibration rows, modality: [T] ids, w: [K][N] float
+    weight in the paper's layout.  Returns a dict of NumPy arrays."""
+    x = np.asarray(x, np.float32)
+    modality = np.asarray(modality, np.int32)
+    w = np.asarray(w, np.float32)
+    s32, inv = smoothing_factors(x, modality, w, n_mod)
+    wq, w_scale = quantize_shared_weight(w, s32[0])
+    k, n = w.shape
+    l_down = np.zeros((max(n_mod - 1, 0), rank, k), np.float32)
+    r_up = np.zeros((max(n_mod - 1, 0), n, rank), np.float32)
+    if rank > 0 and n_mod > 1:
+        for m in range(1, n_mod):
+            rows = x[modality == m].astype(np.float64)
+            z = rows / s32[m].astype(np.float64)[None, :]
+            dw = _weight_difference(w, s32[m], wq, w_scale)
+            l1, l2 = cmc_factors(z, dw, rank, ridge, seed + m)
+            l_down[m - 1] = l1.T
+            r_up[m - 1] = l2.T
+    if lr_dtype == "bf16":
+        l_down = _to_bf16_values(l_down)
+        r_up = _to_bf16_values(r_up)
+    return dict(inv_smooth=inv, s32=s32, wq=wq, w_scale=w_scale,
+                l_down=np.ascontiguousarray(l_down), r_up=np.ascontiguousarray(r_up),
+                rank=rank, n_mod=n_mod, lr_dtype=lr_dtype)

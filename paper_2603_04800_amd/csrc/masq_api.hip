@@ -1,0 +1,211 @@
+// C ABI of the modality-aware W8A8 + low-rank linear: argument validation,
+// workspace planning and stream-ordered kernel dispatch.  Every check runs
+// before any HIP call, so a rejected call enqueues nothing and touches no
+// output.  The semantics of each entry point are documented in masq.h.
+
+#include "masq.h"
+#include "masq_common.h"
+
+namespace masq {
+
+static size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+
+Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, int n_mod) {
+    (void)N;
+    Workspace w{};
+    w.kslice = static_cast<int>(K);
+    w.n_kslices = 1;
+    size_t off = 0;
+    uint8_t* b = static_cast<uint8_t*>(base);
+    w.q = reinterpret_cast<int8_t*>(b ? b + off : nullptr);
+    off += align256(static_cast<size_t>(T) * static_cast<size_t>(K));
+    w.x_scale = reinterpret_cast<float*>(b ? b + off : nullptr);
+    off += align256(static_cast<size_t>(T) * sizeof(float));
+    w.u = nullptr;
+    if (rank > 0 && n_mod > 1) {
+        w.u = reinterpret_cast<float*>(b ? b + off : nullptr);
+        off += align256(static_cast<size_t>(w.n_kslices) * static_cast<size_t>(T) *
+                        static_cast<size_t>(rank) * sizeof(float));
+    }
+    w.bytes = off;
+    return w;
+}
+
+}  // namespace masq
+
+using masq::DT;
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool valid_dt(masq_dtype d) { return d == MASQ_F32 || d == MASQ_BF16; }
+
+DT to_dt(masq_dtype d) { return d == MASQ_BF16 ? DT::BF16 : DT::F32; }
+
+masq_status check_dims(int64_t T, int64_t c_in, int64_t c_out, bool need_out) {
+    if (T < 0 || c_in <= 0 || (c_in % 16) != 0) return MASQ_ERR_SHAPE;
+    if (need_out && (c_out <= 0 || (c_out % 16) != 0)) return MASQ_ERR_SHAPE;
+    // 32-bit indexing inside a row and a 2^31 bound on the grid
+    if (c_in > (1LL << 30) || c_out > (1LL << 30) || T > (1LL << 31) - 1) return MASQ_ERR_SHAPE;
+    return MASQ_OK;
+}
+
+masq_status check_rank(int32_t rank, int32_t n_mod) {
+    if (n_mod < 1 || n_mod > 4) return MASQ_ERR_SHAPE;
+    if (rank < 0 || rank > masq::kMaxRank || (rank % 16) != 0) return MASQ_ERR_SHAPE;
+    return MASQ_OK;
+}
+
+masq_status from_hip(hipError_t e) { return e == hipSuccess ? MASQ_OK : MASQ_ERR_HIP; }
+
+struct Fused {
+    const void* x; masq_dtype x_dt; const int32_t* modality; const float* inv_smooth;
+    const int8_t* wq; const float* w_scale; const void* l_down; const void* r_up;
+    masq_dtype lr_dt; int64_t T, c_in, c_out; int32_t rank, n_mod; void* y; masq_dtype y_dt;
+    void* workspace; size_t workspace_bytes; void* stream;
+};
+
+masq_status validate_fused(const Fused& a) {
+    masq_status st = check_dims(a.T, a.c_in, a.c_out, true);
+    if (st != MASQ_OK) return st;
+    if ((st = check_rank(a.rank, a.n_mod)) != MASQ_OK) return st;
+    if (!valid_dt(a.x_dt) || !valid_dt(a.y_dt) || !valid_dt(a.lr_dt)) return MASQ_ERR_DTYPE;
+    const bool cmc = a.rank > 0 && a.n_mod > 1;
+    if (!a.x || !a.modality || !a.inv_smooth || !a.wq || !a.w_scale || !a.y) return MASQ_ERR_NULL;
+    if (cmc && (!a.l_down || !a.r_up)) return MASQ_ERR_NULL;
+    if (a.T > 0 && !a.workspace) return MASQ_ERR_NULL;
+    if (!aligned16(a.x) || !aligned16(a.modality) || !aligned16(a.inv_smooth) ||
+        !aligned16(a.wq) || !aligned16(a.w_scale) || !aligned16(a.y))
+        return MASQ_ERR_ALIGN;
+    if (cmc && (!aligned16(a.l_down) || !aligned16(a.r_up))) return MASQ_ERR_ALIGN;
+    if (a.workspace && (reinterpret_cast<uintptr_t>(a.workspace) & 255u) != 0) return MASQ_ERR_ALIGN;
+    const masq::Workspace w = masq::plan_workspace(nullptr, a.T, a.c_in, a.c_out, a.rank, a.n_mod);
+    if (a.T > 0 && a.workspace_bytes < w.bytes) return MASQ_ERR_WORKSPACE;
+    return MASQ_OK;
+}
+
+masq_status fused_stage(const Fused& a, int stage) {
+    masq_status st = validate_fused(a);
+    if (st != MASQ_OK || a.T == 0) return st;
+    const bool cmc = a.rank > 0 && a.n_mod > 1;
+    const masq::Workspace w =
+        masq::plan_workspace(a.workspace, a.T, a.c_in, a.c_out, a.rank, a.n_mod);
+    hipStream_t s = static_cast<hipStream_t>(a.stream);
+    (void)hipGetLastError();
+    if (stage & 1) {
+        st = from_hip(masq::launch_smooth_quant(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
+                                                a.T, a.c_in, a.n_mod, w.q, w.x_scale, s));
+        if (st != MASQ_OK) return st;
+        if (cmc) {
+            st = from_hip(masq::launch_lowrank_down(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
+                                                    a.l_down, to_dt(a.lr_dt), a.T, a.c_in,
+                                                    a.rank, a.n_mod, w.kslice, w.n_kslices, w.u, s));
+            if (st != MASQ_OK) return st;
+        }
+    }
+    if (stage & 2) {
+        st = from_hip(masq::launch_gemm(w.q, w.x_scale, a.wq, a.w_scale, a.T, a.c_in, a.c_out,
+                                        a.modality, w.u, a.rank, a.n_mod, a.r_up, to_dt(a.lr_dt),
+                                        cmc, nullptr, a.y, to_dt(a.y_dt), s));
+    }
+    return st;
+}
+
+}  // namespace
+
+extern "C" {
+
+int masq_abi_version(void) { return 1; }
+
+const char* masq_status_str(masq_status s) {
+    switch (s) {
+        case MASQ_OK: return "MASQ_OK";
+        case MASQ_ERR_NULL: return "MASQ_ERR_NULL: a required pointer is NULL";
+        case MASQ_ERR_SHAPE: return "MASQ_ERR_SHAPE: a size violates the preconditions";
+        case MASQ_ERR_DTYPE: return "MASQ_ERR_DTYPE: unsupported dtype";
+        case MASQ_ERR_ALIGN: return "MASQ_ERR_ALIGN: a pointer is not suitably aligned";
+        case MASQ_ERR_WORKSPACE: return "MASQ_ERR_WORKSPACE: workspace too small";
+        case MASQ_ERR_HIP: return "MASQ_ERR_HIP: kernel launch failed";
+        case MASQ_ERR_UNSUPPORTED: return "MASQ_ERR_UNSUPPORTED: not implemented by this build";
+    }
+    return "MASQ_ERR_UNKNOWN";
+}
+
+masq_status masq_smooth_quant(const void* x, masq_dtype x_dt, const int32_t* modality,
+                              const float* inv_smooth, int64_t T, int64_t c_in, int32_t n_mod,
+                              int8_t* q, float* x_scale, void* stream) {
+    masq_status st = check_dims(T, c_in, 16, false);
+    if (st != MASQ_OK) return st;
+    if (n_mod < 1 || n_mod > 4) return MASQ_ERR_SHAPE;
+    if (!valid_dt(x_dt)) return MASQ_ERR_DTYPE;
+    if (!x || !modality || !inv_smooth || !q || !x_scale) return MASQ_ERR_NULL;
+    if (!aligned16(x) || !aligned16(modality) || !aligned16(inv_smooth) || !aligned16(q) ||
+        !aligned16(x_scale))
+        return MASQ_ERR_ALIGN;
+    if (T == 0) return MASQ_OK;
+    (void)hipGetLastError();
+    return from_hip(masq::launch_smooth_quant(x, to_dt(x_dt), modality, inv_smooth, T, c_in,
+                                              n_mod, q, x_scale,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+masq_status masq_w8a8_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
+                           const float* w_scale, int64_t T, int64_t c_in, int64_t c_out,
+                           int32_t* acc, void* y, masq_dtype y_dt, void* stream) {
+    masq_status st = check_dims(T, c_in, c_out, true);
+    if (st != MASQ_OK) return st;
+    if (!valid_dt(y_dt)) return MASQ_ERR_DTYPE;
+    if (!q || !x_scale || !wq || !w_scale || (!acc && !y)) return MASQ_ERR_NULL;
+    if (!aligned16(q) || !aligned16(x_scale) || !aligned16(wq) || !aligned16(w_scale) ||
+        (acc && !aligned16(acc)) || (y && !aligned16(y)))
+        return MASQ_ERR_ALIGN;
+    if (T == 0) return MASQ_OK;
+    (void)hipGetLastError();
+    return from_hip(masq::launch_gemm(q, x_scale, wq, w_scale, T, c_in, c_out, nullptr, nullptr,
+                                      0, 1, nullptr, DT::BF16, false, acc, y, to_dt(y_dt),
+                                      static_cast<hipStream_t>(stream)));
+}
+
+masq_status masq_lowrank_comp(const void* x, masq_dtype x_dt, const int32_t* modality,
+                              const float* inv_smooth, const void* l_down, const void* r_up,
+                              masq_dtype lr_dt, int64_t T, int64_t c_in, int64_t c_out,
+                              int32_t rank, int32_t n_mod, void* y, masq_dtype y_dt,
+                              void* stream) {
+    masq_status st = check_dims(T, c_in, c_out, true);
+    if (st != MASQ_OK) return st;
+    if ((st = check_rank(rank, n_mod)) != MASQ_OK) return st;
+    if (!valid_dt(x_dt) || !valid_dt(lr_dt) || !valid_dt(y_dt)) return MASQ_ERR_DTYPE;
+    const bool cmc = rank > 0 && n_mod > 1;
+    if (!x || !modality || !inv_smooth || !y) return MASQ_ERR_NULL;
+    if (cmc && (!l_down || !r_up)) return MASQ_ERR_NULL;
+    if (!aligned16(x) || !aligned16(modality) || !aligned16(inv_smooth) || !aligned16(y))
+        return MASQ_ERR_ALIGN;
+    if (cmc && (!aligned16(l_down) || !aligned16(r_up))) return MASQ_ERR_ALIGN;
+    if (T == 0 || !cmc) return MASQ_OK;
+    (void)hipGetLastError();
+    return from_hip(masq::launch_lowrank_comp(x, to_dt(x_dt), modality, inv_smooth, l_down, r_up,
+                                              to_dt(lr_dt), T, c_in, c_out, rank, n_mod, y,
+                                              to_dt(y_dt), static_cast<hipStream_t>(stream)));
+}
+
+size_t masq_linear_fused_workspace_bytes(int64_t T, int64_t c_in, int64_t c_out, int32_t rank,
+                                         int32_t n_mod) {
+    if (T < 0 || c_in <= 0 || c_out <= 0 || rank < 0) return 0;
+    return masq::plan_workspace(nullptr, T, c_in, c_out, rank, n_mod).bytes;
+}
+
+#define MASQ_FUSED_ARGS                                                                      \
+    const void *x, masq_dtype x_dt, const int32_t *modality, const float *inv_smooth,        \
+        const int8_t *wq, const float *w_scale, const void *l_down, const void *r_up,        \
+        masq_dtype lr_dt, int64_t T, int64_t c_in, int64_t c_out, int32_t rank, int32_t n_mod, \
+        void *y, masq_dtype y_dt, void *workspace, size_t workspace_bytes, void *stream
+#define MASQ_FUSED_PACK                                                                      \
+    Fused { x, x_dt, modality, inv_smooth, wq, w_scale, l_down, r_up, lr_dt, T, c_in, c_out, \
+            rank, n_mod, y, y_dt, workspace, workspace_bytes, stream }
+
+masq_status masq_linear_fused(MASQ_FUSED_ARGS) { return fused_stage(MASQ_FUSED_PACK, 3); }
+masq_status masq_linear_stage1(MASQ_FUSED_ARGS) { return fused_stage(MASQ_FUSED_PACK, 1); }
+masq_status masq_linear_stage2(MASQ_FUSED_ARGS) { return fused_stage(MASQ_FUSED_PACK, 2); }
+
+}  // extern "C"

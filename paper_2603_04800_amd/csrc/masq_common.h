@@ -1,0 +1,67 @@
+// Internal declarations shared by the kernel and C-ABI translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace masq {
+
+// Tile shape of the int8 GEMM: 256 x 256 output tile per workgroup of four
+// wave64s (2 x 2, each wave 128 x 128), 128-byte K stages, double-buffered.
+constexpr int kTileM = 256;
+constexpr int kTileN = 256;
+constexpr int kTileK = 128;
+constexpr int kRowsDown = 16;     // rows per down-projection tile
+constexpr int kMaxRank = 256;
+
+enum class DT : int { F32 = 0, BF16 = 1 };
+
+struct LinearArgs {
+    const void* x;
+    DT x_dt;
+    const int32_t* modality;
+    const float* inv_smooth;
+    const int8_t* wq;
+    const float* w_scale;
+    const void* l_down;
+    const void* r_up;
+    DT lr_dt;
+    int64_t T, K, N;
+    int rank, n_mod;
+    void* y;
+    DT y_dt;
+};
+
+// Workspace carve-up of the fused layer.
+struct Workspace {
+    int8_t* q;
+    float* x_scale;
+    float* u;          // [n_kslices][T][rank] fp32 partial down-projections
+    int n_kslices;
+    int kslice;
+    size_t bytes;
+};
+
+Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, int n_mod);
+
+hipError_t launch_smooth_quant(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
+                               int64_t T, int64_t K, int n_mod, int8_t* q, float* x_scale,
+                               hipStream_t s);
+
+hipError_t launch_lowrank_down(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
+                               const void* l_down, DT lr_dt, int64_t T, int64_t K, int rank,
+                               int n_mod, int kslice, int n_kslices, float* u, hipStream_t s);
+
+hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
+                       const float* w_scale, int64_t T, int64_t K, int64_t N,
+                       const int32_t* mod, const float* u, int rank, int n_mod,
+                       const void* r_up, DT lr_dt, bool cmc, int32_t* acc, void* y, DT y_dt,
+                       hipStream_t s);
+
+hipError_t launch_lowrank_comp(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
+                               const void* l_down, const void* r_up, DT lr_dt, int64_t T,
+                               int64_t K, int64_t N, int rank, int n_mod, void* y, DT y_dt,
+                               hipStream_t s);
+
+}  // namespace masq

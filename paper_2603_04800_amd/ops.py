@@ -1,0 +1,206 @@
+"""ctypes binding of libmasq.so (the C ABI declared in include/masq.h).
+
+Argument marshalling only: every computation runs in the library's HIP
+kernels.  torch is used for device memory, pointers and the current stream.
+If the library has not been built this module raises ImportError at import
+time; there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+from . import _libpath
+
+_LIB_PATH = _libpath.LIB
+if not os.path.exists(_LIB_PATH):
+    raise ImportError(
+        f"{_LIB_PATH} is missing: build the HIP library first "
+        "(python -m paper_2603_04800_amd.build)")
+_lib = ctypes.CDLL(_LIB_PATH)
+
+F32, BF16 = 0, 1
+STATUS = {0: "MASQ_OK", 1: "MASQ_ERR_NULL", 2: "MASQ_ERR_SHAPE", 3: "MASQ_ERR_DTYPE",
+          4: "MASQ_ERR_ALIGN", 5: "MASQ_ERR_WORKSPACE", 6: "MASQ_ERR_HIP",
+          7: "MASQ_ERR_UNSUPPORTED"}
+
+_p, _i32, _i64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+
+_FUSED_ARGS = [_p, _i32, _p, _p, _p, _p, _p, _p, _i32, _i64, _i64, _i64, _i32, _i32, _p, _i32,
+               _p, _sz, _p]
+_SIGS = {
+    "masq_abi_version": ([], ctypes.c_int),
+    "masq_status_str": ([_i32], ctypes.c_char_p),
+    "masq_smooth_quant": ([_p, _i32, _p, _p, _i64, _i64, _i32, _p, _p, _p], ctypes.c_int),
+    "masq_w8a8_gemm": ([_p, _p, _p, _p, _i64, _i64, _i64, _p, _p, _i32, _p], ctypes.c_int),
+    "masq_lowrank_comp": ([_p, _i32, _p, _p, _p, _p, _i32, _i64, _i64, _i64, _i32, _i32, _p,
+                           _i32, _p], ctypes.c_int),
+    "masq_linear_fused": (_FUSED_ARGS, ctypes.c_int),
+    "masq_linear_stage1": (_FUSED_ARGS, ctypes.c_int),
+    "masq_linear_stage2": (_FUSED_ARGS, ctypes.c_int),
+    "masq_linear_fused_workspace_bytes": ([_i64, _i64, _i64, _i32, _i32], ctypes.c_size_t),
+}
+for _name, (_args, _res) in _SIGS.items():
+    _fn = getattr(_lib, _name)
+    _fn.argtypes = _args
+    _fn.restype = _res
+
+EXPORTED = tuple(_SIGS)
+
+
+class MasqError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        msg = _lib.masq_status_str(code).decode()
+        super().__init__(f"{fn}: {msg}")
+        self.code = code
+
+
+def _check(fn: str, code: int):
+    if code != 0:
+        raise MasqError(fn, code)
+
+
+def raw():
+    """The ctypes library handle (for tests of the C ABI itself)."""
+    return _lib
+
+
+def abi_version() -> int:
+    return _lib.masq_abi_version()
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensors must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _need(t: torch.Tensor, dtype, name):
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+def smooth_quant(x, modality, inv_smooth, q=None, x_scale=None, stream=None):
+    """Per-token smoothing + int8 quantisation -> (q int8 [T][K], x_scale f32 [T])."""
+    T, K = x.shape
+    _need(modality, torch.int32, "modality")
+    _need(inv_smooth, torch.float32, "inv_smooth")
+    if q is None:
+        q = torch.empty((T, K), dtype=torch.int8, device=x.device)
+    if x_scale is None:
+        x_scale = torch.empty((T,), dtype=torch.float32, device=x.device)
+    _check("masq_smooth_quant", _lib.masq_smooth_quant(
+        _ptr(x), _dt(x), _ptr(modality), _ptr(inv_smooth), T, K, inv_smooth.shape[0],
+        _ptr(q), _ptr(x_scale), _stream(stream)))
+    return q, x_scale
+
+
+def w8a8_gemm(q, x_scale, wq, w_scale, want_acc=True, out_dtype=torch.float32, stream=None):
+    """Shared-weight int8 product -> (acc int32 [T][N] or None, y [T][N] or None)."""
+    T, K = q.shape
+    N = wq.shape[0]
+    acc = torch.empty((T, N), dtype=torch.int32, device=q.device) if want_acc else None
+    y = torch.empty((T, N), dtype=out_dtype, device=q.device) if out_dtype is not None else None
+    _check("masq_w8a8_gemm", _lib.masq_w8a8_gemm(
+        _ptr(q), _ptr(x_scale), _ptr(wq), _ptr(w_scale), T, K, N, _ptr(acc), _ptr(y),
+        _dt(y) if y is not None else F32, _stream(stream)))
+    return acc, y
+
+
+def lowrank_comp(x, modality, inv_smooth, l_down, r_up, y, stream=None):
+    """In place: y[t] += (x_t S_m^-1 L1^m) L2^m on non-text rows; returns y."""
+    T, K = x.shape
+    N = y.shape[1]
+    n_mod = inv_smooth.shape[0]
+    rank = l_down.shape[1] if l_down is not None and l_down.dim() == 3 else 0
+    lr_dt = _dt(l_down) if l_down is not None else F32
+    _check("masq_lowrank_comp", _lib.masq_lowrank_comp(
+        _ptr(x), _dt(x), _ptr(modality), _ptr(inv_smooth), _ptr(l_down), _ptr(r_up), lr_dt,
+        T, K, N, rank, n_mod, _ptr(y), _dt(y), _stream(stream)))
+    return y
+
+
+def workspace_bytes(T, K, N, rank, n_mod) -> int:
+    return int(_lib.masq_linear_fused_workspace_bytes(T, K, N, rank, n_mod))
+
+
+class Linear:
+    """One modality-aware quantized linear with device-resident artifacts.
+
+    Holds inv_smooth [M][K] f32, wq [N][K] int8, w_scale [N] f32 and the
+    low-rank factors l_down [M-1][r][K], r_up [M-1][N][r] (f32 or bf16)."""
+
+    def __init__(self, inv_smooth, wq, w_scale, l_down=None, r_up=None):
+        self.inv_smooth, self.wq, self.w_scale = inv_smooth, wq, w_scale
+        self.l_down, self.r_up = l_down, r_up
+        self.n_mod = inv_smooth.shape[0]
+        self.c_out, self.c_in = wq.shape
+        self.rank = l_down.shape[1] if l_down is not None and l_down.dim() == 3 else 0
+        self._ws = None
+
+    @classmethod
+    def from_arrays(cls, art: dict, device="cuda"):
+        """Move calibration arrays (NumPy, C-ABI layouts) to the device."""
+        lr = torch.bfloat16 if art.get("lr_dtype", "bf16") == "bf16" else torch.float32
+
+        def dev(a, dtype):
+            return torch.as_tensor(a).to(device=device, dtype=dtype).contiguous()
+
+        return cls(dev(art["inv_smooth"], torch.float32), dev(art["wq"], torch.int8),
+                   dev(art["w_scale"], torch.float32), dev(art["l_down"], lr),
+                   dev(art["r_up"], lr))
+
+    def workspace(self, T, device):
+        need = workspace_bytes(T, self.c_in, self.c_out, self.rank, self.n_mod)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=device)
+        return self._ws
+
+    def _call(self, fn, x, modality, out, workspace, stream):
+        T = x.shape[0]
+        ws = workspace if workspace is not None else self.workspace(T, x.device)
+        lr_dt = _dt(self.l_down) if self.l_down is not None else F32
+        _check(fn, getattr(_lib, fn)(
+            _ptr(x), _dt(x), _ptr(modality), _ptr(self.inv_smooth), _ptr(self.wq),
+            _ptr(self.w_scale), _ptr(self.l_down), _ptr(self.r_up), lr_dt, T, self.c_in,
+            self.c_out, self.rank, self.n_mod, _ptr(out), _dt(out), _ptr(ws), ws.numel(),
+            _stream(stream)))
+        return out
+
+    def __call__(self, x, modality, out=None, out_dtype=None, workspace=None, stream=None):
+        if out is None:
+            out = torch.empty((x.shape[0], self.c_out), device=x.device,
+                              dtype=out_dtype or x.dtype)
+        return self._call("masq_linear_fused", x, modality, out, workspace, stream)
+
+    def stage1(self, x, modality, out, workspace=None, stream=None):
+        return self._call("masq_linear_stage1", x, modality, out, workspace, stream)
+
+    def stage2(self, x, modality, out, workspace=None, stream=None):
+        return self._call("masq_linear_stage2", x, modality, out, workspace, stream)
+
+
+def linear_fused(x, modality, inv_smooth, wq, w_scale, l_down=None, r_up=None,
+                 out_dtype=None, stream=None):
+    """Functional form of :class:`Linear` (allocates its workspace per call)."""
+    return Linear(inv_smooth, wq, w_scale, l_down, r_up)(x, modality, out_dtype=out_dtype,
+                                                         stream=stream)

@@ -1,0 +1,125 @@
+"""The C ABI loads, exports every declared symbol, and rejects bad arguments
+before touching the GPU (no device needed: validation precedes any HIP call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "masq.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(masq_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2603_04800_amd import ops
+    return ops.raw()
+
+
+def test_header_declares_the_four_layer_calls():
+    names = _declared_functions()
+    for required in ("masq_smooth_quant", "masq_w8a8_gemm", "masq_lowrank_comp",
+                     "masq_linear_fused", "masq_linear_fused_workspace_bytes",
+                     "masq_status_str"):
+        assert required in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+    from paper_2603_04800_amd import ops
+    assert set(_declared_functions()) == set(ops.EXPORTED)
+
+
+def test_header_is_plain_c():
+    import shutil
+    import subprocess
+    import tempfile
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not available")
+    with tempfile.TemporaryDirectory() as d:
+        src = os.path.join(d, "t.c")
+        with open(src, "w") as f:
+            f.write('#include "masq.h"\nint main(void){return masq_abi_version();}\n')
+        r = subprocess.run([gcc, "-std=c99", "-Wall", "-Werror", "-fsyntax-only", "-I",
+                            os.path.join(ROOT, "include"), src], capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
+
+
+def test_status_strings(lib):
+    for code in range(8):
+        assert lib.masq_status_str(code).startswith(b"MASQ_")
+    assert lib.masq_abi_version() == 1
+
+
+P = 1 << 20          # a fake, 256-byte aligned "device" address; never dereferenced
+
+
+def _fused(lib, **kw):
+    a = dict(x=P, x_dt=1, mod=P, inv=P, wq=P, ws=P, ld=P, ru=P, lr_dt=1, T=16, K=64, N=64,
+             rank=16, n_mod=2, y=P, y_dt=1, work=P, work_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return lib.masq_linear_fused(a["x"], a["x_dt"], a["mod"], a["inv"], a["wq"], a["ws"],
+                                 a["ld"], a["ru"], a["lr_dt"], a["T"], a["K"], a["N"],
+                                 a["rank"], a["n_mod"], a["y"], a["y_dt"], a["work"],
+                                 a["work_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(x=None), 1), (dict(wq=None), 1), (dict(y=None), 1), (dict(ld=None), 1),
+    (dict(work=None), 1),
+    (dict(K=40), 2), (dict(N=24), 2), (dict(K=0), 2), (dict(T=-1), 2), (dict(rank=8), 2),
+    (dict(rank=272), 2), (dict(n_mod=0), 2), (dict(n_mod=5), 2),
+    (dict(x_dt=7), 3), (dict(y_dt=2), 3), (dict(lr_dt=-1), 3),
+    (dict(x=P + 8), 4), (dict(ru=P + 4), 4), (dict(work=P + 16), 4),
+    (dict(work_bytes=100), 5),
+])
+def test_fused_rejects_bad_arguments(lib, kw, code):
+    assert _fused(lib, **kw) == code
+
+
+def test_fused_accepts_empty_batch_and_text_only_without_factors(lib):
+    assert _fused(lib, T=0, work=None, work_bytes=0) == 0
+    # rank 0 (or a single modality) needs no factor pointers; T = 0 is a no-op
+    assert _fused(lib, T=0, rank=0, ld=None, ru=None) == 0
+    assert _fused(lib, T=0, n_mod=1, ld=None, ru=None) == 0
+
+
+def test_workspace_query_monotone(lib):
+    f = lib.masq_linear_fused_workspace_bytes
+    base = f(256, 512, 512, 16, 2)
+    assert base >= 256 * 512 + 256 * 4
+    assert f(512, 512, 512, 16, 2) > base
+    assert f(256, 512, 512, 0, 2) < base
+    assert f(0, 512, 512, 16, 2) <= 256 * 2
+    assert f(-1, 512, 512, 16, 2) == 0
+
+
+def test_unfused_calls_validate(lib):
+    # smooth_quant: K not a multiple of 16, null output, misaligned input
+    assert lib.masq_smooth_quant(P, 1, P, P, 8, 40, 2, P, P, None) == 2
+    assert lib.masq_smooth_quant(P, 1, P, P, 8, 64, 2, None, P, None) == 1
+    assert lib.masq_smooth_quant(P + 2, 1, P, P, 8, 64, 2, P, P, None) == 4
+    assert lib.masq_smooth_quant(P, 1, P, P, 0, 64, 2, P, P, None) == 0
+    # w8a8_gemm: both outputs null, bad dtype, empty batch
+    assert lib.masq_w8a8_gemm(P, P, P, P, 8, 64, 64, None, None, 0, None) == 1
+    assert lib.masq_w8a8_gemm(P, P, P, P, 8, 64, 64, None, P, 9, None) == 3
+    assert lib.masq_w8a8_gemm(P, P, P, P, 0, 64, 64, P, None, 0, None) == 0
+    # lowrank_comp: rank not a multiple of 16; rank 0 is a no-op
+    assert lib.masq_lowrank_comp(P, 1, P, P, P, P, 1, 8, 64, 64, 24, 2, P, 1, None) == 2
+    assert lib.masq_lowrank_comp(P, 1, P, P, None, None, 1, 8, 64, 64, 0, 2, P, 1, None) == 0
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    from paper_2603_04800_amd import ops
+    x = torch.zeros(4, 64)
+    with pytest.raises(ValueError):
+        ops.smooth_quant(x, torch.zeros(4, dtype=torch.int32), torch.ones(1, 64))

@@ -1,0 +1,194 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle.
+
+Bar: int8 codes, per-token scales and int32 accumulators bit-exact; the
+dequantised shared-weight product bit-exact; the layer output within
+max relative error 1e-3 (fp32 workloads) or 1e-2 (bf16 workloads) under the
+row-rms-guarded metric ``oracle.inference.relerr``; text rows, which take no
+compensation, bit-exact.  Full-size workloads compare every code and scale and
+a sample of rows through the oracle's GEMM; the small cases compare all.
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import inference as oinf
+
+pytestmark = pytest.mark.gpu
+
+
+def _require_gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X visible to torch"
+
+
+@pytest.fixture(scope="module")
+def ops():
+    _require_gpu()
+    from paper_2603_04800_amd import ops as o
+    return o
+
+
+def _np(t):
+    return t.detach().float().cpu().numpy() if t.dtype == torch.bfloat16 else t.detach().cpu().numpy()
+
+
+def _tol(act_dtype, lr_dtype="f32"):
+    return 1e-3 if act_dtype == "f32" and lr_dtype == "f32" else 1e-2
+
+
+def _sample_rows(modality, n=48, seed=0):
+    T = modality.shape[0]
+    rng = np.random.default_rng(seed)
+    rows = set(rng.choice(T, size=min(n, T), replace=False).tolist())
+    rows |= {0, T - 1}
+    edges = np.flatnonzero(np.diff(modality)) + 1            # run boundaries
+    for e in edges[:16]:
+        rows |= {int(e) - 1, int(e)}
+    return np.array(sorted(rows))
+
+
+def _check_layer(ops, L, rows=None, name=""):
+    """Run every entry point on one layer and compare with the oracle."""
+    from paper_2603_04800_amd import workload
+    x, mod, lin = workload.to_device(L)
+    xs_np, mod_np = L["x"], L["modality"]
+    act = L["act_dtype"]
+    out_dtype = torch.bfloat16 if act == "bf16" else torch.float32
+    T = xs_np.shape[0]
+    rows = np.arange(T) if rows is None else rows
+    print(f"[parity] {name} T={T} K={xs_np.shape[1]} N={L['wq'].shape[0]} r={L['rank']} "
+          f"M={L['n_mod']} rows={len(rows)}", flush=True)
+
+    # smoothing + quantisation: every code and scale
+    q, dx = ops.smooth_quant(x, mod, lin.inv_smooth)
+    q_ref, dx_ref = oinf.smooth_quant(xs_np, mod_np, L["inv_smooth"])
+    torch.cuda.synchronize()
+    assert np.array_equal(q.cpu().numpy(), q_ref), "int8 codes differ"
+    assert np.array_equal(dx.cpu().numpy().view(np.uint32), dx_ref.view(np.uint32)), "scales differ"
+
+    # shared-weight GEMM: int32 accumulators and the dequantised product
+    acc, y0 = ops.w8a8_gemm(q, dx, lin.wq, lin.w_scale, want_acc=True, out_dtype=torch.float32)
+    acc_ref, y0_ref = oinf.w8a8_gemm(q_ref[rows], dx_ref[rows], L["wq"], L["w_scale"])
+    rows_t = torch.from_numpy(rows).to(acc.device)
+    acc_np = acc.index_select(0, rows_t).cpu().numpy()
+    assert np.array_equal(acc_np, acc_ref), f"int32 accumulators differ ({np.sum(acc_np != acc_ref)})"
+    y0_np = y0.index_select(0, rows_t).cpu().numpy()
+    assert np.array_equal(y0_np.view(np.uint32), y0_ref.view(np.uint32)), "dequantised product differs"
+
+    # the fused layer
+    y = lin(x, mod, out_dtype=out_dtype)
+    y_ref = oinf.to_output(oinf.linear(xs_np[rows], mod_np[rows], L["inv_smooth"], L["wq"],
+                                       L["w_scale"], L["l_down"], L["r_up"]), act)
+    y_np = _np(y.index_select(0, rows_t))
+    err = oinf.relerr(y_np, y_ref)
+    assert err <= _tol(act, L["lr_dtype"]), f"fused relerr {err}"
+    text = mod_np[rows] == 0
+    assert np.array_equal(y_np[text], oinf.to_output(y0_ref, act)[text]), "text rows not exact"
+
+    # stage1 + stage2 equals the fused call, and reruns are bitwise identical
+    y2 = torch.empty_like(y)
+    ws = lin.workspace(T, x.device)
+    lin.stage1(x, mod, y2, ws)
+    lin.stage2(x, mod, y2, ws)
+    y3 = lin(x, mod, out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    assert torch.equal(y2.view(torch.int16) if y2.dtype == torch.bfloat16 else y2.view(torch.int32),
+                       y.view(torch.int16) if y.dtype == torch.bfloat16 else y.view(torch.int32))
+    assert torch.equal(y3, y)
+
+    # standalone compensation on top of the fp32 dequantised product
+    if lin.rank > 0 and lin.n_mod > 1:
+        yl = ops.lowrank_comp(x, mod, lin.inv_smooth, lin.l_down, lin.r_up, y0.clone())
+        yl_ref = oinf.lowrank_comp(xs_np[rows], mod_np[rows], L["inv_smooth"], L["l_down"],
+                                   L["r_up"], y0_ref)
+        yl_np = yl.index_select(0, rows_t).cpu().numpy()
+        err = oinf.relerr(yl_np, yl_ref)
+        assert err <= _tol(act, L["lr_dtype"]), f"lowrank_comp relerr {err}"
+        assert np.array_equal(yl_np[text], y0_ref[text])
+    return err
+
+
+# ------------------------------------------------------------------ workloads
+_FULL = [(c.index, p.name) for c in synth.CONFIGS for p in c.projections]
+
+
+@pytest.mark.parametrize("cfg_index,proj", _FULL, ids=[f"cfg{c}-{p}" for c, p in _FULL])
+def test_workload_parity(ops, cfg_index, proj):
+    from paper_2603_04800_amd import workload
+    L = workload.layer(cfg_index, proj)
+    rows = None if L["x"].shape[0] * L["wq"].shape[0] <= 256 * 4096 else _sample_rows(L["modality"])
+    _check_layer(ops, L, rows, name=f"cfg{cfg_index}/{proj}")
+
+
+# ------------------------------------------------------------------ edge cases
+def _random_layer(T, K, N, r, M, act, lr, layout="alternating", zero_rows=(), seed=0,
+                  counts=None):
+    rng = np.random.default_rng(seed)
+    if counts is None:
+        counts = [T // M + (1 if m < T % M else 0) for m in range(M)]
+    mod = synth.make_modality_layout(counts, layout, 0, seed)
+    x = rng.standard_normal((T, K)).astype(np.float32)
+    for m, s in enumerate([1.0, 30.0, 2.0, 5.0][:M]):
+        x[mod == m] *= np.float32(s)
+    x[:, : max(1, K // 64)] *= 20
+    for t in zero_rows:
+        x[t] = 0
+    from oracle.bf16 import bf16_round
+    if act == "bf16":
+        x = bf16_round(x)
+    inv = rng.uniform(0.05, 3.0, (M, K)).astype(np.float32)
+    wq = rng.integers(-127, 128, (N, K)).astype(np.int8)
+    ws = rng.uniform(1e-4, 1e-2, N).astype(np.float32)
+    ld = (rng.standard_normal((max(M - 1, 0), r, K)) / np.sqrt(K)).astype(np.float32)
+    ru = (rng.standard_normal((max(M - 1, 0), N, r)) * 0.05).astype(np.float32)
+    if lr == "bf16":
+        ld, ru = bf16_round(ld), bf16_round(ru)
+    return dict(x=x, modality=mod, inv_smooth=inv, wq=wq, w_scale=ws, l_down=ld, r_up=ru,
+                n_mod=M, rank=r, act_dtype=act, lr_dtype=lr)
+
+
+_EDGE = {
+    "T1_single_token": dict(T=1, K=64, N=32, r=16, M=2, act="bf16", lr="bf16"),
+    "ragged_T_N_K48_fp32": dict(T=300, K=48, N=80, r=16, M=2, act="f32", lr="f32",
+                                layout="contiguous"),
+    "tri_modal_alternating": dict(T=257, K=128, N=272, r=32, M=3, act="bf16", lr="bf16"),
+    "runs_bf16_multi_tile": dict(T=700, K=1024, N=528, r=64, M=3, act="bf16", lr="bf16",
+                                 layout="runs"),
+    "rank128_two_slots_global_path": dict(T=96, K=256, N=256, r=128, M=3, act="bf16", lr="bf16"),
+    "fp32_rank64_two_slots_global_path": dict(T=96, K=256, N=256, r=64, M=3, act="f32", lr="f32"),
+    "bf16_act_fp32_factors": dict(T=130, K=192, N=64, r=16, M=2, act="bf16", lr="f32"),
+    "fp32_act_bf16_factors": dict(T=130, K=192, N=64, r=16, M=2, act="f32", lr="bf16"),
+    "zero_rows": dict(T=40, K=64, N=48, r=16, M=2, act="bf16", lr="bf16", zero_rows=(0, 7, 39)),
+    "all_text": dict(T=100, K=128, N=64, r=16, M=2, act="bf16", lr="bf16", counts=[100, 0]),
+    "all_vision": dict(T=100, K=128, N=64, r=16, M=2, act="bf16", lr="bf16", counts=[0, 100]),
+    "rank0": dict(T=70, K=64, N=64, r=0, M=2, act="f32", lr="f32"),
+    "single_modality": dict(T=70, K=64, N=64, r=16, M=1, act="bf16", lr="bf16"),
+    "four_modalities": dict(T=260, K=128, N=96, r=16, M=4, act="bf16", lr="bf16"),
+}
+
+
+@pytest.mark.parametrize("name", list(_EDGE))
+def test_edge_case_parity(ops, name):
+    kw = dict(_EDGE[name])
+    L = _random_layer(kw.pop("T"), kw.pop("K"), kw.pop("N"), kw.pop("r"), kw.pop("M"),
+                      kw.pop("act"), kw.pop("lr"), **kw)
+    if L["rank"] == 0:
+        L["l_down"] = L["l_down"][:, :0]
+        L["r_up"] = L["r_up"][:, :, :0]
+    _check_layer(ops, L, name=name)
+
+
+def test_zero_row_gives_zero_scale_and_codes(ops):
+    L = _random_layer(8, 64, 32, 16, 2, "f32", "f32", zero_rows=(3,))
+    from paper_2603_04800_amd import workload
+    x, mod, lin = workload.to_device(L)
+    q, dx = ops.smooth_quant(x, mod, lin.inv_smooth)
+    assert float(dx[3]) == 0.0 and int(q[3].abs().sum()) == 0
+
+
+def test_empty_batch_is_a_noop(ops):
+    L = _random_layer(4, 64, 32, 16, 2, "bf16", "bf16")
+    from paper_2603_04800_amd import workload
+    x, mod, lin = workload.to_device(L)
+    y = lin(x[:0], mod[:0])
+    assert y.shape == (0, 32)
