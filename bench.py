@@ -47,7 +47,24 @@ def parse():
     ap.add_argument("--copies", type=int, default=2,
                     help="rotating input/output sets so no step reuses the last one's cache")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (5 times): the "
+                         "reference for scaling HBM traffic counters")
     return ap.parse_args()
+
+
+def copy_probe(mib: int):
+    """A plain copy of known size, profiled with the same counters as the GEMM
+    so that FETCH_SIZE / WRITE_SIZE can be scaled to bytes."""
+    import torch
+    n = mib * (1 << 20)
+    src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "launches": 5}))
 
 
 def kernel_source_hash() -> str:
@@ -105,6 +122,9 @@ def cpu_baseline(L, rows_every=4):
 
 def main():
     args = parse()
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(run with --gpus 1)", file=sys.stderr)

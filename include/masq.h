@@ -35,7 +35,8 @@
  *    marked nullable), T >= 0, c_in > 0 and c_in % 16 == 0, c_out > 0 and
  *    c_out % 16 == 0, rank == 0 or rank % 16 == 0 (rank <= 256),
  *    1 <= n_mod <= 4, 16-byte aligned pointers, a large enough workspace.
- *    T == 0 is a successful no-op.
+ *    T == 0 is a successful no-op once sizes and dtypes are valid (pointers
+ *    may then be NULL: nothing is read or written).
  *  - Modality ids outside [0, n_mod) are treated as text (memory-safe, but
  *    not a supported input); non-finite inputs give unspecified results.
  *  - Rounding contract (bit-exact parts): the smoothing is one fp32 multiply;

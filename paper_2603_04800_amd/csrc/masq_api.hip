@@ -71,6 +71,7 @@ masq_status validate_fused(const Fused& a) {
     if (st != MASQ_OK) return st;
     if ((st = check_rank(a.rank, a.n_mod)) != MASQ_OK) return st;
     if (!valid_dt(a.x_dt) || !valid_dt(a.y_dt) || !valid_dt(a.lr_dt)) return MASQ_ERR_DTYPE;
+    if (a.T == 0) return MASQ_OK;      // empty batch: nothing is read or written
     const bool cmc = a.rank > 0 && a.n_mod > 1;
     if (!a.x || !a.modality || !a.inv_smooth || !a.wq || !a.w_scale || !a.y) return MASQ_ERR_NULL;
     if (cmc && (!a.l_down || !a.r_up)) return MASQ_ERR_NULL;
@@ -139,6 +140,7 @@ masq_status masq_smooth_quant(const void* x, masq_dtype x_dt, const int32_t* mod
     if (st != MASQ_OK) return st;
     if (n_mod < 1 || n_mod > 4) return MASQ_ERR_SHAPE;
     if (!valid_dt(x_dt)) return MASQ_ERR_DTYPE;
+    if (T == 0) return MASQ_OK;
     if (!x || !modality || !inv_smooth || !q || !x_scale) return MASQ_ERR_NULL;
     if (!aligned16(x) || !aligned16(modality) || !aligned16(inv_smooth) || !aligned16(q) ||
         !aligned16(x_scale))
@@ -156,6 +158,7 @@ masq_status masq_w8a8_gemm(const int8_t* q, const float* x_scale, const int8_t* 
     masq_status st = check_dims(T, c_in, c_out, true);
     if (st != MASQ_OK) return st;
     if (!valid_dt(y_dt)) return MASQ_ERR_DTYPE;
+    if (T == 0) return MASQ_OK;
     if (!q || !x_scale || !wq || !w_scale || (!acc && !y)) return MASQ_ERR_NULL;
     if (!aligned16(q) || !aligned16(x_scale) || !aligned16(wq) || !aligned16(w_scale) ||
         (acc && !aligned16(acc)) || (y && !aligned16(y)))
@@ -176,6 +179,7 @@ masq_status masq_lowrank_comp(const void* x, masq_dtype x_dt, const int32_t* mod
     if (st != MASQ_OK) return st;
     if ((st = check_rank(rank, n_mod)) != MASQ_OK) return st;
     if (!valid_dt(x_dt) || !valid_dt(lr_dt) || !valid_dt(y_dt)) return MASQ_ERR_DTYPE;
+    if (T == 0) return MASQ_OK;
     const bool cmc = rank > 0 && n_mod > 1;
     if (!x || !modality || !inv_smooth || !y) return MASQ_ERR_NULL;
     if (cmc && (!l_down || !r_up)) return MASQ_ERR_NULL;

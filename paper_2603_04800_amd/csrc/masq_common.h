@@ -14,6 +14,7 @@ constexpr int kTileN = 256;
 constexpr int kTileK = 128;
 constexpr int kRowsDown = 16;     // rows per down-projection tile
 constexpr int kMaxRank = 256;
+constexpr int64_t kRowsPerWaveMinT = 256;   // batches this large quantise one row per wave
 
 enum class DT : int { F32 = 0, BF16 = 1 };
 

@@ -143,85 +143,225 @@ __global__ __launch_bounds__(256) void k_smooth_quant(const XT* __restrict__ x,
     }
 }
 
-// ================================================================ down-projection
-// One 16 x 16 block of u = (x S_m^-1) L1^m over k in [kb, ke): 16 token rows
-// (row0..row0+15) times 16 rank columns (c0..c0+15).  Rows whose modality is
-// not m contribute zeros.  MFMA operand layout: lane l holds row/column
-// (l % 16) and the k group (l / 16); A and B use the same k assignment.
-template <typename XT, typename LT> struct Down;
+__device__ __forceinline__ void split_bf16x8(const float (&v)[8], v4i& hi, v4i& lo) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const uint32_t h0 = f32_to_bf16(v[2 * j]), h1 = f32_to_bf16(v[2 * j + 1]);
+        const uint32_t l0 = f32_to_bf16(v[2 * j] - bf16_to_f32(h0));
+        const uint32_t l1 = f32_to_bf16(v[2 * j + 1] - bf16_to_f32(h1));
+        hi[j] = static_cast<int32_t>(h0 | (h1 << 16));
+        lo[j] = static_cast<int32_t>(l0 | (l1 << 16));
+    }
+}
 
-template <typename XT> struct Down<XT, bf16_t> {   // bf16 factors: bf16 MFMA
-    static __device__ __forceinline__ v4f block(const XT* x, const float* inv_s_m,
-                                                const bf16_t* ld_m, int64_t row0, int64_t T,
-                                                int K, int kb, int ke, int c0, const int* smod,
-                                                int m, v4f acc, int lane) {
+// One wave per token row (four rows per workgroup), the row's smoothed values
+// kept in registers between the absmax and the quantisation pass for rows up
+// to 64 * 8 * NC elements; longer rows stream their remainder twice.  Used
+// for large batches; k_smooth_quant (a whole workgroup per row) serves small
+// ones, where a row's latency matters more than the number of rows in flight.
+template <typename XT, int NC>
+__global__ __launch_bounds__(256) void k_smooth_quant_rows(const XT* __restrict__ x,
+                                                           const int32_t* __restrict__ mod,
+                                                           const float* __restrict__ inv_s,
+                                                           int64_t T, int K, int n_mod,
+                                                           int8_t* __restrict__ q,
+                                                           float* __restrict__ x_scale) {
+    const int lane = threadIdx.x & 63;
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    if (t >= T) return;
+    const int m = sane_mod(mod[t], n_mod);
+    const XT* xr = x + t * static_cast<int64_t>(K);
+    const float* sr = inv_s + static_cast<int64_t>(m) * K;
+    int8_t* qr = q + t * static_cast<int64_t>(K);
+    const int nv = K >> 3;
+
+    float xs[NC][8];
+    float amax = 0.f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const int v = lane + 64 * c;
+        if (v < nv) {
+            float xv[8], sv[8];
+            Elem<XT>::load8(xr + 8 * v, xv);
+            load8_f32(sr + 8 * v, sv);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                xs[c][j] = xv[j] * sv[j];
+                amax = fmaxf(amax, fabsf(xs[c][j]));
+            }
+        }
+    }
+    for (int v = lane + 64 * NC; v < nv; v += 64) {
+        float xv[8], sv[8];
+        Elem<XT>::load8(xr + 8 * v, xv);
+        load8_f32(sr + 8 * v, sv);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(xv[j] * sv[j]));
+    }
+    amax = wave_max(amax);
+    const bool nz = amax > 0.f;
+    const float dx = nz ? amax / 127.0f : 0.f;     // correctly rounded
+    const float rq = nz ? 127.0f / amax : 0.f;
+    if (lane == 0) x_scale[t] = dx;
+
+    auto store8 = [&](int v, const float (&vals)[8]) {
+        uint32_t w[2] = {0u, 0u};
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            float c = rintf(vals[j] * rq);
+            c = fminf(fmaxf(c, -127.0f), 127.0f);
+            w[j >> 2] |= (static_cast<uint32_t>(static_cast<int32_t>(c)) & 0xFFu) << (8 * (j & 3));
+        }
+        v2i out;
+        out.x = static_cast<int32_t>(w[0]);
+        out.y = static_cast<int32_t>(w[1]);
+        *reinterpret_cast<v2i*>(qr + 8 * v) = out;
+    };
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const int v = lane + 64 * c;
+        if (v < nv) store8(v, xs[c]);
+    }
+    for (int v = lane + 64 * NC; v < nv; v += 64) {
+        float xv[8], sv[8], vals[8];
+        Elem<XT>::load8(xr + 8 * v, xv);
+        load8_f32(sr + 8 * v, sv);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) vals[j] = xv[j] * sv[j];
+        store8(v, vals);
+    }
+}
+
+// ================================================================ down-projection
+// u = (x S_m^-1) L1^m for a tile of 16 token rows and a group of up to 64 rank
+// columns.  Each of the four waves takes a quarter of the k range for all the
+// group's columns (4 MFMA column blocks share one A fragment); the partial
+// sums are added across waves in LDS in a fixed order.  Rows whose modality
+// is not m contribute zeros.  MFMA operand layout: lane l holds row/column
+// (l % 16) and the k group (l / 16); A and B use the same k assignment.
+template <typename XT, typename LT> struct DownK;
+
+// bf16 factors: the smoothed row enters as two bf16 terms, hi = bf16(xs) and
+// lo = bf16(xs - hi), both multiplied with the exactly-bf16 factor, so the
+// product keeps about 16 significant bits of the fp32 row.
+template <typename XT> struct DownK<XT, bf16_t> {
+    static constexpr int kStep = 32;
+    static constexpr int kUnroll = 4;
+    static __device__ __forceinline__ void run(const XT* x, const float* inv_s_m,
+                                               const bf16_t* ld_m, int64_t row0, int64_t T,
+                                               int K, int kb, int ke, int c0, int ncb,
+                                               const int* smod, int m, v4f (&acc)[4], int lane) {
         const int ar = lane & 15, kg = lane >> 4;
         const int64_t t = row0 + ar;
         const bool live = (t < T) && (smod[ar] == m);
         const XT* xrow = x + (live ? t : row0) * static_cast<int64_t>(K);
-        const bf16_t* lrow = ld_m + static_cast<int64_t>(c0 + ar) * K;
-        for (int k0 = kb; k0 < ke; k0 += 32) {
-            const int k = k0 + 8 * kg;
-            v4i av = {0, 0, 0, 0};
-            v4i bv = {0, 0, 0, 0};
-            if (k < ke) {
-                bv = *reinterpret_cast<const v4i*>(lrow + k);
-                if (live) {
-                    float xv[8], sv[8];
-                    Elem<XT>::load8(xrow + k, xv);
-                    load8_f32(inv_s_m + k, sv);
+        const bf16_t* lrow[4];
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const uint32_t lo = f32_to_bf16(xv[2 * j] * sv[2 * j]);
-                        const uint32_t hi = f32_to_bf16(xv[2 * j + 1] * sv[2 * j + 1]);
-                        av[j] = static_cast<int32_t>(lo | (hi << 16));
-                    }
+        for (int j = 0; j < 4; ++j)
+            lrow[j] = ld_m + static_cast<int64_t>(c0 + 16 * min(j, ncb - 1) + ar) * K;
+        const v4i zero = {0, 0, 0, 0};
+        for (int k0 = kb; k0 < ke; k0 += kStep * kUnroll) {
+            float xv[kUnroll][8], sv[kUnroll][8];
+            v4i bv[kUnroll][4];
+            bool ok[kUnroll];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {       // all loads of the unrolled steps first
+                const int k = k0 + kStep * u + 8 * kg;
+                ok[u] = k < ke;
+                const int kc = ok[u] ? k : ke - 8;
+                Elem<XT>::load8(xrow + kc, xv[u]);
+                load8_f32(inv_s_m + kc, sv[u]);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) bv[u][j] = *reinterpret_cast<const v4i*>(lrow[j] + kc);
+            }
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                if (k0 + kStep * u >= ke) break;
+                float xs[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) xs[e] = xv[u][e] * sv[u][e];
+                v4i hi, lo;
+                split_bf16x8(xs, hi, lo);
+                const bool use = live && ok[u];
+                hi = use ? hi : zero;
+                lo = use ? lo : zero;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (j >= ncb) break;
+                    const v4i b = ok[u] ? bv[u][j] : zero;
+                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(v8bf, hi), __builtin_bit_cast(v8bf, b), acc[j], 0, 0, 0);
+                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(v8bf, lo), __builtin_bit_cast(v8bf, b), acc[j], 0, 0, 0);
                 }
             }
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, av),
-                                                          __builtin_bit_cast(v8bf, bv), acc, 0, 0, 0);
         }
-        return acc;
     }
 };
 
-template <typename XT> struct Down<XT, float> {    // fp32 factors: fp32 MFMA
-    static __device__ __forceinline__ v4f block(const XT* x, const float* inv_s_m,
-                                                const float* ld_m, int64_t row0, int64_t T,
-                                                int K, int kb, int ke, int c0, const int* smod,
-                                                int m, v4f acc, int lane) {
+template <typename XT> struct DownK<XT, float> {   // fp32 factors: fp32 MFMA
+    static constexpr int kStep = 4;
+    static __device__ __forceinline__ void run(const XT* x, const float* inv_s_m,
+                                               const float* ld_m, int64_t row0, int64_t T, int K,
+                                               int kb, int ke, int c0, int ncb, const int* smod,
+                                               int m, v4f (&acc)[4], int lane) {
         const int ar = lane & 15, kg = lane >> 4;
         const int64_t t = row0 + ar;
         const bool live = (t < T) && (smod[ar] == m);
         const XT* xrow = x + (live ? t : row0) * static_cast<int64_t>(K);
-        const float* lrow = ld_m + static_cast<int64_t>(c0 + ar) * K;
-        for (int k0 = kb; k0 < ke; k0 += 4) {
+        for (int k0 = kb; k0 < ke; k0 += kStep) {
             const int k = k0 + kg;
-            float a = 0.f, b = 0.f;
-            if (k < ke) {
-                b = lrow[k];
-                if (live) a = Elem<XT>::load1(xrow + k) * inv_s_m[k];
+            const bool ok = k < ke;
+            const int kc = ok ? k : ke - 1;
+            const float xs = Elem<XT>::load1(xrow + kc) * inv_s_m[kc];
+            const float a = (live && ok) ? xs : 0.f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (j >= ncb) break;
+                const float b = ok ? ld_m[static_cast<int64_t>(c0 + 16 * j + ar) * K + kc] : 0.f;
+                acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[j], 0, 0, 0);
             }
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
         }
-        return acc;
     }
 };
 
-// Sum over the modalities present in the tile of one 16 x 16 block of u.
-template <typename XT, typename LT>
-__device__ __forceinline__ v4f down_tile(const XT* x, const float* inv_s, const LT* l_down,
-                                         int64_t row0, int64_t T, int K, int r, int n_mod,
-                                         int kb, int ke, int c0, const int* smod,
-                                         unsigned present, int lane) {
-    v4f acc = {0.f, 0.f, 0.f, 0.f};
+// The 16 x rc block of u (rank columns c0..c0+rc) over k in [kb, ke), summed
+// over the modalities present, written as red-reduced fp32 to out(row, col).
+template <typename XT, typename LT, typename Out>
+__device__ __forceinline__ void down_group(const XT* x, const float* inv_s, const LT* l_down,
+                                           int64_t row0, int64_t T, int K, int r, int n_mod,
+                                           int kb, int ke, int c0, const int* smod,
+                                           unsigned present, float (*red)[kRowsDown][64],
+                                           Out out) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int rc = min(64, r - c0);
+    const int ncb = rc >> 4;
+    constexpr int step = DownK<XT, LT>::kStep;
+    const int span = ke - kb;
+    const int q = ((span + 4 * step - 1) / (4 * step)) * step;   // k per wave, step-aligned
+    const int wkb = min(ke, kb + wave * q);
+    const int wke = min(ke, wkb + q);
+    v4f acc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = v4f{0.f, 0.f, 0.f, 0.f};
     for (int m = 1; m < n_mod; ++m) {
         if (!(present & (1u << m))) continue;
-        acc = Down<XT, LT>::block(x, inv_s + static_cast<int64_t>(m) * K,
-                                  l_down + static_cast<int64_t>(m - 1) * r * K, row0, T, K, kb,
-                                  ke, c0, smod, m, acc, lane);
+        DownK<XT, LT>::run(x, inv_s + static_cast<int64_t>(m) * K,
+                           l_down + static_cast<int64_t>(m - 1) * r * K, row0, T, K, wkb, wke,
+                           c0, ncb, smod, m, acc, lane);
     }
-    return acc;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if (j >= ncb) break;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) red[wave][4 * (lane >> 4) + i][16 * j + (lane & 15)] = acc[j][i];
+    }
+    __syncthreads();
+    for (int idx = tid; idx < kRowsDown * rc; idx += 256) {
+        const int row = idx / rc, col = idx - row * rc;
+        out(row, c0 + col, ((red[0][row][col] + red[1][row][col]) + red[2][row][col]) + red[3][row][col]);
+    }
+    __syncthreads();
 }
 
 __device__ __forceinline__ unsigned tile_presence(const int* smod) {
@@ -241,6 +381,7 @@ __global__ __launch_bounds__(256) void k_lowrank_down(const XT* __restrict__ x,
                                                       int K, int r, int n_mod, int kslice,
                                                       float* __restrict__ u) {
     __shared__ int smod[kRowsDown];
+    __shared__ float red[4][kRowsDown][64];
     const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kRowsDown;
     const int s = blockIdx.y;
     const int kb = s * kslice;
@@ -252,17 +393,13 @@ __global__ __launch_bounds__(256) void k_lowrank_down(const XT* __restrict__ x,
     __syncthreads();
     const unsigned present = tile_presence(smod);
     if (!present) return;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (int c0 = wave * 16; c0 < r; c0 += 64) {
-        const v4f acc = down_tile<XT, LT>(x, inv_s, l_down, row0, T, K, r, n_mod, kb, ke, c0,
-                                          smod, present, lane);
-        const int col = c0 + (lane & 15);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int64_t t = row0 + 4 * (lane >> 4) + i;
-            if (t < T) u[(static_cast<int64_t>(s) * T + t) * r + col] = acc[i];
-        }
-    }
+    float* us = u + static_cast<int64_t>(s) * T * r;
+    for (int c0 = 0; c0 < r; c0 += 64)
+        down_group<XT, LT>(x, inv_s, l_down, row0, T, K, r, n_mod, kb, ke, c0, smod, present, red,
+                           [&](int row, int col, float v) {
+                               const int64_t t = row0 + row;
+                               if (t < T) us[t * r + col] = v;
+                           });
 }
 
 // ================================================================ standalone CMC
@@ -275,6 +412,7 @@ __global__ __launch_bounds__(256) void k_lowrank_comp(const XT* __restrict__ x,
                                                       int K, int N, int r, int n_mod,
                                                       YT* __restrict__ y) {
     __shared__ int smod[kRowsDown];
+    __shared__ float red[4][kRowsDown][64];
     __shared__ float su[kRowsDown][kMaxRank];
     const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kRowsDown;
     if (threadIdx.x < kRowsDown) {
@@ -284,14 +422,9 @@ __global__ __launch_bounds__(256) void k_lowrank_comp(const XT* __restrict__ x,
     __syncthreads();
     const unsigned present = tile_presence(smod);
     if (!present) return;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (int c0 = wave * 16; c0 < r; c0 += 64) {
-        const v4f acc = down_tile<XT, LT>(x, inv_s, l_down, row0, T, K, r, n_mod, 0, K, c0,
-                                          smod, present, lane);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) su[4 * (lane >> 4) + i][c0 + (lane & 15)] = acc[i];
-    }
-    __syncthreads();
+    for (int c0 = 0; c0 < r; c0 += 64)
+        down_group<XT, LT>(x, inv_s, l_down, row0, T, K, r, n_mod, 0, K, c0, smod, present, red,
+                           [&](int row, int col, float v) { su[row][col] = v; });
     for (int o = threadIdx.x; o < N; o += 256) {
         for (int i = 0; i < kRowsDown; ++i) {
             const int m = smod[i];
@@ -312,155 +445,447 @@ __device__ __forceinline__ int acc_row(int e, int lane) {
     return 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
 }
 
-// Cross-Modal Compensation inside the GEMM epilogue.  For each modality m
-// present in the tile and each chunk of up to 64 rank columns ("piece"), the
-// u rows of that modality (others zero) and the matching rows of L2^T are
-// staged in LDS; each 32 x 32 output block then accumulates u L2 onto its
-// dequantised fp32 values with MFMA.  Pieces that do not fit in the 128 KB of
-// LDS are read straight from global memory instead.
+// Cross-Modal Compensation inside the GEMM epilogue.  Per chunk of up to 64
+// rank columns, the tile's u rows (each row's own modality; text rows zero)
+// and, for every modality m present, the matching rows of (L2^m)^T are staged
+// in LDS.  Each 32 x 32 output block then accumulates u L2^m onto its
+// dequantised fp32 values with MFMA, the A operand masked to the rows of
+// modality m.  With bf16 factors u enters as a hi + lo pair of bf16 terms
+// (about 16 significant bits).  Tiles whose pieces do not fit in the 128 KB of
+// LDS read u and L2^T straight from global memory instead.
 template <typename LT> struct Cmc;
 
 template <> struct Cmc<bf16_t> {          // bf16 operands, v_mfma_f32_32x32x16_bf16
-    static constexpr int kPieceBytes = 2 * kTileM * 128;    // u + L2^T, 128-byte rows
+    static constexpr int kUBytes = 2 * kTileM * 128;   // u hi + u lo, 128-byte rows
+    static constexpr int kRBytes = kTileM * 128;       // one modality's L2^T rows
 
-    static __device__ __forceinline__ void stage(uint8_t* piece, const int* s_mod, int m,
-                                                 const float* u, const bf16_t* rm, int64_t row0,
-                                                 int64_t T, int col0, int N, int r, int c0,
-                                                 int tid) {
-        uint8_t* su = piece;
-        uint8_t* sr = piece + kTileM * 128;
+    // All of a thread's global loads are issued before any is consumed (from
+    // clamped, always valid addresses; unused values are replaced by zeros),
+    // so the staging pays the memory latency once rather than per row.
+    static __device__ __forceinline__ void stage_u(uint8_t* su, const int* s_mod, const float* u,
+                                                   int64_t row0, int64_t T, int r, int c0,
+                                                   int tid) {
         const int nch = min(64, r - c0) >> 3;
-        for (int idx = tid; idx < kTileM * 8; idx += 256) {
-            const int row = idx >> 3, ch = idx & 7;
-            const int64_t t = row0 + row;
-            v4i pk = {0, 0, 0, 0}, pr = {0, 0, 0, 0};
-            if (ch < nch) {
-                if (t < T && s_mod[row] == m) {
-                    float uv[8];
-                    load8_f32(u + t * r + c0 + 8 * ch, uv);
+        const int ch = tid & 7;
+        const int chc = min(ch, nch - 1);
+        v4f va[8], vb[8];
 #pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        pk[j] = static_cast<int32_t>(f32_to_bf16(uv[2 * j]) |
-                                                     (f32_to_bf16(uv[2 * j + 1]) << 16));
-                }
-                const int col = min(col0 + row, N - 1);
-                pr = *reinterpret_cast<const v4i*>(rm + static_cast<int64_t>(col) * r + c0 + 8 * ch);
-            }
+        for (int it = 0; it < 8; ++it) {
+            const int row = (tid >> 3) + 32 * it;
+            const int64_t t = min(row0 + row, T - 1);
+            const float* src = u + t * r + c0 + 8 * chc;
+            va[it] = *reinterpret_cast<const v4f*>(src);
+            vb[it] = *reinterpret_cast<const v4f*>(src + 4);
+        }
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+            const int row = (tid >> 3) + 32 * it;
+            const bool live = ch < nch && (row0 + row) < T && s_mod[row] > 0;
+            const float uv[8] = {va[it].x, va[it].y, va[it].z, va[it].w,
+                                 vb[it].x, vb[it].y, vb[it].z, vb[it].w};
+            v4i hi, lo;
+            split_bf16x8(uv, hi, lo);
+            const v4i zero = {0, 0, 0, 0};
             const int off = row * 128 + ((ch ^ swz(row)) << 4);
-            *reinterpret_cast<v4i*>(su + off) = pk;
-            *reinterpret_cast<v4i*>(sr + off) = pr;
+            *reinterpret_cast<v4i*>(su + off) = live ? hi : zero;
+            *reinterpret_cast<v4i*>(su + kTileM * 128 + off) = live ? lo : zero;
         }
     }
 
-    // yb += u[rows of block i] . L2^T[cols of block j] over this piece's columns.
-    static __device__ __forceinline__ v16f from_lds(const uint8_t* piece, int rc, int arow,
-                                                    int brow, int lane, v16f yb) {
-        const uint8_t* su = piece;
-        const uint8_t* sr = piece + kTileM * 128;
+    static __device__ __forceinline__ void stage_r(uint8_t* sr, const bf16_t* rm, int col0, int N,
+                                                   int r, int c0, int tid) {
+        const int nch = min(64, r - c0) >> 3;
+        const int ch = tid & 7;
+        const int chc = min(ch, nch - 1);
+        v4i pr[8];
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+            const int col = min(col0 + (tid >> 3) + 32 * it, N - 1);
+            pr[it] = *reinterpret_cast<const v4i*>(rm + static_cast<int64_t>(col) * r + c0 + 8 * chc);
+        }
+        const v4i zero = {0, 0, 0, 0};
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+            const int row = (tid >> 3) + 32 * it;
+            *reinterpret_cast<v4i*>(sr + row * 128 + ((ch ^ swz(row)) << 4)) = ch < nch ? pr[it] : zero;
+        }
+    }
+
+    // yb += [rows of modality m] u . L2^T over this chunk's rc columns.
+    static __device__ __forceinline__ v16f from_lds(const uint8_t* su, const uint8_t* sr, int rc,
+                                                    int arow, int brow, bool live, int lane,
+                                                    v16f yb) {
+        const v4i zero = {0, 0, 0, 0};
         for (int ks = 0; ks < (rc >> 4); ++ks) {
             const int c = 2 * ks + (lane >> 5);
-            const v4i fa = *reinterpret_cast<const v4i*>(su + arow * 128 + ((c ^ swz(arow)) << 4));
-            const v4i fb = *reinterpret_cast<const v4i*>(sr + brow * 128 + ((c ^ swz(brow)) << 4));
-            yb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, fa),
-                                                         __builtin_bit_cast(v8bf, fb), yb, 0, 0, 0);
+            const int offa = arow * 128 + ((c ^ swz(arow)) << 4);
+            v4i hi = *reinterpret_cast<const v4i*>(su + offa);
+            v4i lo = *reinterpret_cast<const v4i*>(su + kTileM * 128 + offa);
+            hi = live ? hi : zero;
+            lo = live ? lo : zero;
+            const v8bf b = __builtin_bit_cast(
+                v8bf, *reinterpret_cast<const v4i*>(sr + brow * 128 + ((c ^ swz(brow)) << 4)));
+            yb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, __builtin_bit_cast(v8bf, hi), yb, 0, 0, 0);
+            yb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, __builtin_bit_cast(v8bf, lo), yb, 0, 0, 0);
         }
         return yb;
     }
 
-    static __device__ __forceinline__ v16f from_global(const float* u, const bf16_t* rm, int m,
-                                                       int smod_row, int64_t t, int64_t T,
-                                                       int col, int r, int c0, int lane, v16f yb) {
+    static __device__ __forceinline__ v16f from_global(const float* u, const bf16_t* rm, bool live,
+                                                       int64_t t, int col, int r, int c0,
+                                                       int lane, v16f yb) {
         const int rc = min(64, r - c0);
-        const bool live = t < T && smod_row == m;
         for (int ks = 0; ks < (rc >> 4); ++ks) {
             const int k = c0 + 16 * ks + 8 * (lane >> 5);
-            v4i fa = {0, 0, 0, 0};
+            v4i hi = {0, 0, 0, 0}, lo = {0, 0, 0, 0};
             if (live) {
                 float uv[8];
                 load8_f32(u + t * r + k, uv);
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    fa[j] = static_cast<int32_t>(f32_to_bf16(uv[2 * j]) | (f32_to_bf16(uv[2 * j + 1]) << 16));
+                split_bf16x8(uv, hi, lo);
             }
-            const v4i fb = *reinterpret_cast<const v4i*>(rm + static_cast<int64_t>(col) * r + k);
-            yb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, fa),
-                                                         __builtin_bit_cast(v8bf, fb), yb, 0, 0, 0);
+            const v8bf b = __builtin_bit_cast(
+                v8bf, *reinterpret_cast<const v4i*>(rm + static_cast<int64_t>(col) * r + k));
+            yb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, __builtin_bit_cast(v8bf, hi), yb, 0, 0, 0);
+            yb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, __builtin_bit_cast(v8bf, lo), yb, 0, 0, 0);
         }
         return yb;
     }
 };
 
 template <> struct Cmc<float> {           // fp32 operands, v_mfma_f32_32x32x2f32
-    static constexpr int kPieceBytes = 2 * kTileM * 256;    // u + L2^T, 64 floats per row
+    static constexpr int kUBytes = kTileM * 256;       // 64 floats per row
+    static constexpr int kRBytes = kTileN * 256;
 
-    static __device__ __forceinline__ void stage(uint8_t* piece, const int* s_mod, int m,
-                                                 const float* u, const float* rm, int64_t row0,
-                                                 int64_t T, int col0, int N, int r, int c0,
-                                                 int tid) {
-        float* su = reinterpret_cast<float*>(piece);
-        float* sr = reinterpret_cast<float*>(piece + kTileM * 256);
+    static __device__ __forceinline__ void stage_u(uint8_t* base, const int* s_mod, const float* u,
+                                                   int64_t row0, int64_t T, int r, int c0,
+                                                   int tid) {
+        float* su = reinterpret_cast<float*>(base);
         const int rc = min(64, r - c0);
         for (int idx = tid; idx < kTileM * rc; idx += 256) {
             const int row = idx / rc, k = idx - row * rc;
             const int64_t t = row0 + row;
-            su[row * 64 + k] = (t < T && s_mod[row] == m) ? u[t * r + c0 + k] : 0.f;
+            su[row * 64 + k] = (t < T && s_mod[row] > 0) ? u[t * r + c0 + k] : 0.f;
+        }
+    }
+
+    static __device__ __forceinline__ void stage_r(uint8_t* base, const float* rm, int col0, int N,
+                                                   int r, int c0, int tid) {
+        float* sr = reinterpret_cast<float*>(base);
+        const int rc = min(64, r - c0);
+        for (int idx = tid; idx < kTileN * rc; idx += 256) {
+            const int row = idx / rc, k = idx - row * rc;
             const int col = min(col0 + row, N - 1);
             sr[row * 64 + k] = rm[static_cast<int64_t>(col) * r + c0 + k];
         }
     }
 
-    static __device__ __forceinline__ v16f from_lds(const uint8_t* piece, int rc, int arow,
-                                                    int brow, int lane, v16f yb) {
-        const float* su = reinterpret_cast<const float*>(piece);
-        const float* sr = reinterpret_cast<const float*>(piece + kTileM * 256);
+    static __device__ __forceinline__ v16f from_lds(const uint8_t* su_, const uint8_t* sr_, int rc,
+                                                    int arow, int brow, bool live, int lane,
+                                                    v16f yb) {
+        const float* su = reinterpret_cast<const float*>(su_);
+        const float* sr = reinterpret_cast<const float*>(sr_);
         for (int ks = 0; ks < (rc >> 1); ++ks) {
             const int k = 2 * ks + (lane >> 5);
-            yb = __builtin_amdgcn_mfma_f32_32x32x2f32(su[arow * 64 + k], sr[brow * 64 + k], yb, 0, 0, 0);
+            const float a = live ? su[arow * 64 + k] : 0.f;
+            yb = __builtin_amdgcn_mfma_f32_32x32x2f32(sr[brow * 64 + k], a, yb, 0, 0, 0);
         }
         return yb;
     }
 
-    static __device__ __forceinline__ v16f from_global(const float* u, const float* rm, int m,
-                                                       int smod_row, int64_t t, int64_t T,
-                                                       int col, int r, int c0, int lane, v16f yb) {
+    static __device__ __forceinline__ v16f from_global(const float* u, const float* rm, bool live,
+                                                       int64_t t, int col, int r, int c0,
+                                                       int lane, v16f yb) {
         const int rc = min(64, r - c0);
-        const bool live = t < T && smod_row == m;
         for (int ks = 0; ks < (rc >> 1); ++ks) {
             const int k = c0 + 2 * ks + (lane >> 5);
             const float a = live ? u[t * r + k] : 0.f;
-            yb = __builtin_amdgcn_mfma_f32_32x32x2f32(a, rm[static_cast<int64_t>(col) * r + k], yb, 0, 0, 0);
+            yb = __builtin_amdgcn_mfma_f32_32x32x2f32(rm[static_cast<int64_t>(col) * r + k], a, yb, 0, 0, 0);
         }
         return yb;
     }
 };
 
-template <typename YT, typename LT, bool CMC>
-__global__ __launch_bounds__(256, 1) void k_gemm(
-    const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
-    const float* __restrict__ w_scale, int64_t T, int K, int N, int tiles_m, int tiles_n,
-    const int32_t* __restrict__ mod, const float* __restrict__ u, int r, int n_mod,
-    const LT* __restrict__ r_up, int32_t* __restrict__ acc_out, YT* __restrict__ y) {
-    __shared__ __attribute__((aligned(16))) uint8_t smem[2 * 65536];
-    __shared__ float s_dx[kTileM];
-    __shared__ float s_ws[kTileN];
-    __shared__ int s_mod[kTileM];
-    __shared__ unsigned s_present;
-
-    // Workgroups are dealt round-robin to the 8 XCDs; give each XCD a
-    // contiguous range of tiles, ordered in groups of 8 tile-rows, so that
-    // tiles running together on one XCD share A and B stages in its L2.
+// Workgroups are dealt round-robin to the 8 XCDs; give each XCD a contiguous
+// range of tiles, ordered in groups of 8 tile-rows, so that tiles running
+// together on one XCD share A and B stages in its L2.  Returns false for the
+// padding workgroups of the last XCD range.
+__device__ __forceinline__ bool tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
     const int nt = tiles_m * tiles_n;
     const int per_xcd = (nt + 7) >> 3;
     const int L = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-    if (L >= nt) return;
+    if (L >= nt) return false;
     constexpr int GM = 8;
     const int gsize = GM * tiles_n;
     const int g = L / gsize;
     const int first_m = g * GM;
     const int gm = min(GM, tiles_m - first_m);
     const int li = L - g * gsize;
-    const int tm = first_m + li % gm;
-    const int tn = li / gm;
+    tm = first_m + li % gm;
+    tn = li / gm;
+    return true;
+}
+
+// Shared LDS of both GEMM kernels: the K stages during the main loop, then
+// the compensation pieces in the epilogue.
+struct GemmSmem {
+    uint8_t buf[2 * 65536];
+    float dx[kTileM];
+    float ws[kTileN];
+    int mod[kTileM];
+    unsigned present;
+};
+
+// Epilogue of a 256 x 256 tile whose int32 accumulators are in acc (this
+// wave's 128 x 128 quarter as 4 x 4 blocks of 32 x 32): optional int32 store,
+// dequantisation, Cross-Modal Compensation on non-text rows, cast and store.
+// Per-thread epilogue operands (thread t: token row0 + t, channel col0 + t),
+// loaded at the start of the kernel so that their latency hides behind the
+// main loop.
+struct EpiPrefetch {
+    float dx, ws;
+    int mod;
+};
+
+__device__ __forceinline__ EpiPrefetch epi_prefetch(const float* __restrict__ x_scale,
+                                                    const float* __restrict__ w_scale,
+                                                    const int32_t* __restrict__ mod, bool cmc,
+                                                    int64_t T, int N, int64_t row0, int col0,
+                                                    int n_mod) {
+    const int tid = threadIdx.x;
+    const int64_t t = row0 + tid;
+    EpiPrefetch e;
+    e.dx = t < T ? x_scale[t] : 0.f;
+    e.ws = (col0 + tid) < N ? w_scale[col0 + tid] : 0.f;
+    e.mod = (cmc && t < T) ? sane_mod(mod[t], n_mod) : 0;
+    return e;
+}
+
+template <typename YT, typename LT, bool CMC, bool ACC>
+__device__ __forceinline__ void gemm_epilogue(
+    v16i (&acc)[4][4], GemmSmem& sm, const EpiPrefetch& pf, int64_t T, int N, int64_t row0,
+    int col0, const float* __restrict__ u, int r, int n_mod, const LT* __restrict__ r_up,
+    int32_t* __restrict__ acc_out, YT* __restrict__ y) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    __syncthreads();                         // every wave is done with the K stages
+    sm.dx[tid] = pf.dx;
+    sm.ws[tid] = pf.ws;
+    if (CMC) sm.mod[tid] = pf.mod;
+    if (tid == 0) sm.present = 0u;
+    __syncthreads();
+
+    // ---- compensation: modalities present in the tile, LDS plan per 64-column chunk
+    int n_present = 0;
+    bool staged = false;
+    unsigned present = 0;
+    const int n_chunks = (r + 63) >> 6;
+    constexpr int kChunkBase = CMC ? Cmc<LT>::kUBytes : 0;
+    if constexpr (CMC) {
+        if (sm.mod[tid] > 0) atomicOr(&sm.present, 1u << sm.mod[tid]);
+        __syncthreads();
+        present = sm.present;
+        n_present = __builtin_popcount(present);
+        const int chunk_bytes = Cmc<LT>::kUBytes + n_present * Cmc<LT>::kRBytes;
+        staged = n_chunks * chunk_bytes <= static_cast<int>(sizeof(sm.buf));
+        if (n_present > 0 && staged && y != nullptr) {
+            for (int c = 0; c < n_chunks; ++c) {
+                uint8_t* base = sm.buf + c * chunk_bytes;
+                Cmc<LT>::stage_u(base, sm.mod, u, row0, T, r, 64 * c, tid);
+                int p = 0;
+                for (int m = 1; m < n_mod; ++m) {
+                    if (!(present & (1u << m))) continue;
+                    Cmc<LT>::stage_r(base + kChunkBase + p * Cmc<LT>::kRBytes,
+                                     r_up + static_cast<int64_t>(m - 1) * N * r, col0, N, r,
+                                     64 * c, tid);
+                    ++p;
+                }
+            }
+            __syncthreads();
+        }
+    }
+
+    // ---- accumulator layout: register e of a lane in block (i, j) holds token
+    // wm*128 + 32 i + (lane % 32) and channel wn*128 + 32 j + 8 (e / 4) +
+    // 4 (lane / 32) + e % 4.  The three phases below (dequantise in place,
+    // compensate, store) are written as short unrolled nests so that the
+    // epilogue stays compact in the instruction cache.
+    const bool interior = (row0 + kTileM <= T) && (col0 + kTileN <= N);
+    auto tok_of = [&](int i) { return wm * 128 + i * 32 + (lane & 31); };
+    auto ch_of = [&](int j, int g) { return wn * 128 + j * 32 + 8 * g + 4 * (lane >> 5); };
+
+    if constexpr (ACC) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t tok = row0 + tok_of(i);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int ch = col0 + ch_of(j, g);
+                    if (interior || (tok < T && ch < N)) {
+                        const v4i w = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                                       acc[i][j][4 * g + 3]};
+                        *reinterpret_cast<v4i*>(acc_out + tok * N + ch) = w;
+                    }
+                }
+        }
+    }
+    if (y == nullptr) return;
+
+    // ---- per 32 x 32 block: dequantise, compensate, cast and store.
+    // Compensation fast path (bf16 factors, rank <= 64, at most two non-text
+    // modalities present, all staged): the present modalities are laid side by
+    // side along the rank dimension, K = 16 * nks <= 128, so one block takes
+    // <= 16 MFMAs; the (masked) u fragments are read once per token block and
+    // the L2^T fragments per block.
+    constexpr bool kBf16Cmc = CMC && sizeof(LT) == 2;
+    int mods[2] = {0, 0};
+    if constexpr (CMC) {
+        int p = 0;
+        for (int m = 1; m < n_mod && p < 2; ++m)
+            if (present & (1u << m)) mods[p++] = m;
+    }
+    const bool fast = kBf16Cmc && n_present > 0 && n_present <= 2 && staged && n_chunks == 1;
+    const int nks_slot = fast ? (r >> 4) : 0;               // k steps of 16 per modality
+    const v4i zero4 = {0, 0, 0, 0};
+    v4i uh[8], ul[8];                                       // [k step] of the current token block
+    auto load_u = [&](const int i) __attribute__((always_inline)) {
+        if constexpr (kBf16Cmc) {
+            if (fast) {
+                const int trow = tok_of(i);
+                const int tm_ = sm.mod[trow];
+#pragma unroll
+                for (int kk = 0; kk < 8; ++kk) {
+                    const int p = kk >> 2, ks = kk & 3;
+                    const int c = 2 * ks + (lane >> 5);
+                    const int off = trow * 128 + ((c ^ swz(trow)) << 4);
+                    const bool live = p < n_present && ks < nks_slot && tm_ == mods[p];
+                    const v4i h = *reinterpret_cast<const v4i*>(sm.buf + off);
+                    const v4i l = *reinterpret_cast<const v4i*>(sm.buf + kTileM * 128 + off);
+                    uh[kk] = live ? h : zero4;
+                    ul[kk] = live ? l : zero4;
+                }
+            }
+        }
+    };
+    // general compensation of one block: any rank, any number of modalities,
+    // staged pieces or global memory (kept out of the fast path's code)
+    auto cmc_block_general = [&](const int i, const int j, v16f yb) __attribute__((always_inline)) {
+        if constexpr (CMC) {
+            const int trow = tok_of(i);
+            const int crow = wn * 128 + j * 32 + (lane & 31);
+            const int tm_ = sm.mod[trow];
+            const int chunk_bytes = Cmc<LT>::kUBytes + n_present * Cmc<LT>::kRBytes;
+            for (int c = 0; c < n_chunks; ++c) {
+                int p = 0;
+                for (int m = 1; m < n_mod; ++m) {
+                    if (!(present & (1u << m))) continue;
+                    const bool live = tm_ == m;
+                    if (staged) {
+                        const uint8_t* base = sm.buf + c * chunk_bytes;
+                        yb = Cmc<LT>::from_lds(base, base + kChunkBase + p * Cmc<LT>::kRBytes,
+                                               min(64, r - 64 * c), trow, crow, live, lane, yb);
+                    } else {
+                        yb = Cmc<LT>::from_global(u, r_up + static_cast<int64_t>(m - 1) * N * r,
+                                                  live && (row0 + trow) < T, row0 + trow,
+                                                  min(col0 + crow, N - 1), r, 64 * c, lane, yb);
+                    }
+                    ++p;
+                }
+            }
+        }
+        return yb;
+    };
+    auto epilogue_block = [&](const int i, const int j, const v16i a) __attribute__((always_inline)) {
+        const int64_t tok = row0 + tok_of(i);
+        const float dx = sm.dx[tok_of(i)];
+        v16f yb;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const v4f ws = *reinterpret_cast<const v4f*>(&sm.ws[ch_of(j, g)]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                yb[4 * g + e] = (static_cast<float>(a[4 * g + e]) * dx) * ws[e];
+        }
+        if constexpr (CMC) {
+            if (fast) {
+                if constexpr (kBf16Cmc) {
+                    const int crow = wn * 128 + j * 32 + (lane & 31);
+#pragma unroll
+                    for (int kk = 0; kk < 8; ++kk) {
+                        const int pp = kk >> 2, ks = kk & 3;
+                        if (pp >= n_present || ks >= nks_slot) continue;
+                        const uint8_t* sr = sm.buf + kChunkBase + pp * Cmc<LT>::kRBytes;
+                        const int c = 2 * ks + (lane >> 5);
+                        const v8bf b = __builtin_bit_cast(
+                            v8bf, *reinterpret_cast<const v4i*>(sr + crow * 128 + ((c ^ swz(crow)) << 4)));
+                        yb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, __builtin_bit_cast(v8bf, uh[kk]), yb, 0, 0, 0);
+                        yb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, __builtin_bit_cast(v8bf, ul[kk]), yb, 0, 0, 0);
+                    }
+                }
+            } else if (n_present > 0) {
+                yb = cmc_block_general(i, j, yb);
+            }
+        }
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int ch = col0 + ch_of(j, g);
+            if (!(interior || (tok < T && ch < N))) continue;
+            if constexpr (sizeof(YT) == 2) {
+                v2i w;
+                w.x = static_cast<int32_t>(f32_to_bf16(yb[4 * g]) | (f32_to_bf16(yb[4 * g + 1]) << 16));
+                w.y = static_cast<int32_t>(f32_to_bf16(yb[4 * g + 2]) | (f32_to_bf16(yb[4 * g + 3]) << 16));
+                *reinterpret_cast<v2i*>(y + tok * N + ch) = w;
+            } else {
+                const v4f w = {yb[4 * g], yb[4 * g + 1], yb[4 * g + 2], yb[4 * g + 3]};
+                *reinterpret_cast<v4f*>(y + tok * N + ch) = w;
+            }
+        }
+    };
+#define MASQ_EPI_ROW(I) load_u(I); epilogue_block(I, 0, acc[I][0]); epilogue_block(I, 1, acc[I][1]); \
+                        epilogue_block(I, 2, acc[I][2]); epilogue_block(I, 3, acc[I][3]);
+    MASQ_EPI_ROW(0) MASQ_EPI_ROW(1) MASQ_EPI_ROW(2) MASQ_EPI_ROW(3)
+#undef MASQ_EPI_ROW
+}
+
+// 16 x 32 x 32 MFMA steps of one wave's 128 x 128 quarter: fragments of the
+// 4 token blocks (q rows) and 4 channel blocks (Wq rows) for k chunk c (lane
+// group l / 32 selects the chunk), read through the row swizzle `sw`.  The
+// product is formed transposed, channels x tokens, so that each lane ends up
+// holding one token and 4 consecutive output channels per register group.
+template <int kRowBytes, typename Swz>
+__device__ __forceinline__ void mfma_kstep(const uint8_t* sa, const uint8_t* sb, int c, int wm,
+                                           int wn, int lane, Swz sw, v16i (&acc)[4][4]) {
+    v4i fa[4], fb[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = wm * 128 + i * 32 + (lane & 31);
+        fa[i] = *reinterpret_cast<const v4i*>(sa + row * kRowBytes + ((c ^ sw(row)) << 4));
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int row = wn * 128 + j * 32 + (lane & 31);
+        fb[j] = *reinterpret_cast<const v4i*>(sb + row * kRowBytes + ((c ^ sw(row)) << 4));
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[j], fa[i], acc[i][j], 0, 0, 0);
+}
+
+// ---------------------------------------------------------------- GEMM, general K
+// K stages of 128 bytes go global -> registers -> LDS, double-buffered; any
+// c_in that is a multiple of 16 (chunks past K are zero-filled).
+template <typename YT, typename LT, bool CMC, bool ACC>
+__global__ __launch_bounds__(256, 1) void k_gemm(
+    const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
+    const float* __restrict__ w_scale, int64_t T, int K, int N, int tiles_m, int tiles_n,
+    const int32_t* __restrict__ mod, const float* __restrict__ u, int r, int n_mod,
+    const LT* __restrict__ r_up, int32_t* __restrict__ acc_out, YT* __restrict__ y) {
+    __shared__ __attribute__((aligned(16))) GemmSmem sm;
+    int tm, tn;
+    if (!tile_coords(tiles_m, tiles_n, tm, tn)) return;
     const int64_t row0 = static_cast<int64_t>(tm) * kTileM;
     const int col0 = tn * kTileN;
 
@@ -475,40 +900,41 @@ __global__ __launch_bounds__(256, 1) void k_gemm(
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = v16i{0};
 
+    const EpiPrefetch pf = epi_prefetch(x_scale, w_scale, mod, CMC, T, N, row0, col0, n_mod);
     v4i ra[8], rb[8];
     // Row indices are clamped into the matrix (rows past T or N are computed
     // and discarded); chunks past K are loaded from a clamped in-bounds
-    // address and replaced by zeros, so every load is unconditional.
+    // address and replaced by zeros at the LDS store.
     int64_t a_off[8], b_off[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         a_off[j] = min(row0 + lr + 32 * j, T - 1) * K;
         b_off[j] = static_cast<int64_t>(min(col0 + lr + 32 * j, N - 1)) * K;
     }
+    bool kin = true;          // this thread's chunk of the stage lies inside K
     auto gload = [&](int k0) {
         const int kraw = k0 + lc * 16;
-        const bool kin = kraw < K;
+        kin = kraw < K;
         const int kk = kin ? kraw : K - 16;
-        const v4i zero = {0, 0, 0, 0};
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const v4i va = *reinterpret_cast<const v4i*>(A + a_off[j] + kk);
-            const v4i vb = *reinterpret_cast<const v4i*>(B + b_off[j] + kk);
-            ra[j] = kin ? va : zero;
-            rb[j] = kin ? vb : zero;
+            ra[j] = *reinterpret_cast<const v4i*>(A + a_off[j] + kk);
+            rb[j] = *reinterpret_cast<const v4i*>(B + b_off[j] + kk);
         }
     };
     auto sstore = [&](int buf) {
-        uint8_t* sa = smem + buf * 65536;
+        uint8_t* sa = sm.buf + buf * 65536;
         uint8_t* sb = sa + 32768;
+        const v4i zero = {0, 0, 0, 0};
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int row = lr + 32 * j;
             const int off = row * 128 + ((lc ^ swz(row)) << 4);
-            *reinterpret_cast<v4i*>(sa + off) = ra[j];
-            *reinterpret_cast<v4i*>(sb + off) = rb[j];
+            *reinterpret_cast<v4i*>(sa + off) = kin ? ra[j] : zero;
+            *reinterpret_cast<v4i*>(sb + off) = kin ? rb[j] : zero;
         }
     };
+    auto sw8 = [](int row) { return swz(row); };
 
     const int nk = (K + kTileK - 1) / kTileK;
     gload(0);
@@ -517,115 +943,150 @@ __global__ __launch_bounds__(256, 1) void k_gemm(
     for (int kt = 0; kt < nk; ++kt) {
         const int cur = kt & 1;
         if (kt + 1 < nk) gload((kt + 1) * kTileK);
-        const uint8_t* sa = smem + cur * 65536;
+        const uint8_t* sa = sm.buf + cur * 65536;
         const uint8_t* sb = sa + 32768;
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            const int c = 2 * ks + (lane >> 5);
-            v4i fa[4], fb[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int row = wm * 128 + i * 32 + (lane & 31);
-                fa[i] = *reinterpret_cast<const v4i*>(sa + row * 128 + ((c ^ swz(row)) << 4));
-            }
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int row = wn * 128 + j * 32 + (lane & 31);
-                fb[j] = *reinterpret_cast<const v4i*>(sb + row * 128 + ((c ^ swz(row)) << 4));
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
-        }
+        for (int ks = 0; ks < 4; ++ks)
+            mfma_kstep<128>(sa, sb, 2 * ks + (lane >> 5), wm, wn, lane, sw8, acc);
         if (kt + 1 < nk) sstore(cur ^ 1);
         __syncthreads();
     }
+    gemm_epilogue<YT, LT, CMC, ACC>(acc, sm, pf, T, N, row0, col0, u, r, n_mod, r_up, acc_out, y);
+}
 
-    // ---- epilogue: scales and modalities of this tile
-    {
-        const int64_t t = row0 + tid;
-        s_dx[tid] = t < T ? x_scale[t] : 0.f;
-        s_ws[tid] = (col0 + tid) < N ? w_scale[col0 + tid] : 0.f;
-        if (CMC) s_mod[tid] = t < T ? sane_mod(mod[t], n_mod) : 0;
-        if (tid == 0) s_present = 0u;
+// ---------------------------------------------------------------- GEMM, K % 64 == 0
+// Direct-to-LDS pipeline: 64-byte K stages (A and B tiles 256 x 64 each) go
+// from global memory straight into one of 4 LDS buffers with
+// global_load_lds_dwordx4, three stages ahead of the MFMAs.  Each wave waits
+// for its own loads of a stage (s_waitcnt vmcnt) before the barrier that
+// publishes the stage to the other waves.
+constexpr int kDmaStageK = 64;
+constexpr int kDmaStages = 4;
+constexpr int kDmaStageBytes = 2 * kTileM * kDmaStageK;     // A + B
+
+// 4-chunk swizzle of a 64-byte row.  Measured on gfx950 with a ds_read_b128
+// microbenchmark (SQ_LDS_BANK_CONFLICT = 0): 32 lanes reading one logical
+// chunk of 32 consecutive rows hit distinct banks.  (The LDS behaves as 64
+// four-byte banks served 16 lanes at a time: rows r..r+15 occupy distinct
+// 16-byte slots (r % 4) * 4 + (chunk ^ (r / 4 % 4)).)
+__device__ __forceinline__ int swz4(int row) { return (row >> 2) & 3; }
+
+// One 16-byte lane of an LDS-DMA load: the wave writes 64 x 16 contiguous
+// bytes at LDS address m0 (wave-uniform), lane i at m0 + 16 i.
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+                 :: "v"(src), "s"(lds_addr) : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(n) lgkmcnt(0) (expcnt unconstrained).
+#define MASQ_WAIT_VMCNT_LGKM0(n) \
+    __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (0 << 8))
+
+template <typename YT, typename LT, bool CMC, bool ACC>
+__global__ __launch_bounds__(256, 1) void k_gemm_dma(
+    const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
+    const float* __restrict__ w_scale, int64_t T, int K, int N, int tiles_m, int tiles_n,
+    const int32_t* __restrict__ mod, const float* __restrict__ u, int r, int n_mod,
+    const LT* __restrict__ r_up, int32_t* __restrict__ acc_out, YT* __restrict__ y) {
+    __shared__ __attribute__((aligned(16))) GemmSmem sm;
+    static_assert(kDmaStages * kDmaStageBytes <= static_cast<int>(sizeof(GemmSmem::buf)), "LDS");
+    int tm, tn;
+    if (!tile_coords(tiles_m, tiles_n, tm, tn)) return;
+    const int64_t row0 = static_cast<int64_t>(tm) * kTileM;
+    const int col0 = tn * kTileN;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    v16i acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = v16i{0};
+
+    const EpiPrefetch pf = epi_prefetch(x_scale, w_scale, mod, CMC, T, N, row0, col0, n_mod);
+
+    // Wave w loads rows [64 w, 64 w + 64) of the A and of the B tile, 16 rows
+    // per instruction; lane i covers row 16 j + i / 4 at LDS chunk i % 4,
+    // which holds logical chunk (i % 4) ^ swz4(row).  Rows past T or N are
+    // clamped into the matrix; their results are discarded.
+    const int8_t* src[8];                 // [0..3]: A rows, [4..7]: B rows
+    uint32_t dst_off[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int row = wave * 64 + 16 * j + (lane >> 2);
+        const int chunk = (lane & 3) ^ swz4(row);
+        src[j] = A + min(row0 + row, T - 1) * K + 16 * chunk;
+        src[4 + j] = B + static_cast<int64_t>(min(col0 + row, N - 1)) * K + 16 * chunk;
+        dst_off[j] = (wave * 64 + 16 * j) * kDmaStageK;
+        dst_off[4 + j] = kTileM * kDmaStageK + dst_off[j];
     }
-    __syncthreads();
-
-    // ---- compensation pieces: (modality, 64-column chunk) pairs present here
-    int n_pieces = 0;
-    bool staged = false;
-    unsigned present = 0;
-    const int n_chunks = (r + 63) >> 6;
-    if constexpr (CMC) {
-        if (s_mod[tid] > 0) atomicOr(&s_present, 1u << s_mod[tid]);
-        __syncthreads();
-        present = s_present;
-        n_pieces = __builtin_popcount(present) * n_chunks;
-        staged = n_pieces * Cmc<LT>::kPieceBytes <= static_cast<int>(sizeof(smem));
-        if (n_pieces > 0 && staged && y != nullptr) {
-            int p = 0;
-            for (int m = 1; m < n_mod; ++m) {
-                if (!(present & (1u << m))) continue;
-                const LT* rm = r_up + static_cast<int64_t>(m - 1) * N * r;
-                for (int c = 0; c < n_chunks; ++c, ++p)
-                    Cmc<LT>::stage(smem + p * Cmc<LT>::kPieceBytes, s_mod, m, u, rm, row0, T,
-                                   col0, N, r, 64 * c, tid);
-            }
-            __syncthreads();
-        }
-    }
-
-    // ---- per 32 x 32 block: (int32 store), dequantise, compensate, cast, store.
-    // Invoked with constant block indices so the accumulators stay in registers.
-    const bool interior = (row0 + kTileM <= T) && (col0 + kTileN <= N);
-    auto epilogue_block = [&](const int i, const int j, const v16i a) __attribute__((always_inline)) {
-        const int arow = wm * 128 + i * 32 + (lane & 31);   // A-operand row of this lane
-        const int bcol = wn * 128 + j * 32 + (lane & 31);
-        const int col = col0 + bcol;
-        if (acc_out != nullptr) {
+    const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sm.buf));
+    auto issue_one = [&](int st, int q) __attribute__((always_inline)) {
+        const uint32_t sbase = lds0 + (st % kDmaStages) * kDmaStageBytes;
+        lds_dma16(src[q] + st * kDmaStageK, __builtin_amdgcn_readfirstlane(sbase + dst_off[q]));
+    };
+    auto issue = [&](int st) __attribute__((always_inline)) {
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int64_t row = row0 + wm * 128 + i * 32 + acc_row(e, lane);
-                if (interior || (row < T && col < N)) acc_out[row * N + col] = a[e];
-            }
-        }
-        if (y == nullptr) return;
-        const float ws = s_ws[bcol];
-        v16f yb;
+        for (int q = 0; q < 8; ++q) issue_one(st, q);
+    };
+    // fragments of one 32-byte k step: 4 token blocks (q rows), 4 channel blocks (Wq rows)
+    auto read_frags = [&](int st, int ks, v4i (&fa)[4], v4i (&fb)[4]) __attribute__((always_inline)) {
+        const uint8_t* sa = sm.buf + (st % kDmaStages) * kDmaStageBytes;
+        const uint8_t* sb = sa + kTileM * kDmaStageK;
+        const int c = 2 * ks + (lane >> 5);
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const float dx = s_dx[wm * 128 + i * 32 + acc_row(e, lane)];
-            yb[e] = (static_cast<float>(a[e]) * dx) * ws;
-        }
-        if constexpr (CMC) {
-            if (n_pieces > 0) {
-                int p = 0;
-                for (int m = 1; m < n_mod; ++m) {
-                    if (!(present & (1u << m))) continue;
-                    const LT* rm = r_up + static_cast<int64_t>(m - 1) * N * r;
-                    for (int c = 0; c < n_chunks; ++c, ++p) {
-                        if (staged)
-                            yb = Cmc<LT>::from_lds(smem + p * Cmc<LT>::kPieceBytes,
-                                                   min(64, r - 64 * c), arow, bcol, lane, yb);
-                        else
-                            yb = Cmc<LT>::from_global(u, rm, m, s_mod[arow], row0 + arow, T,
-                                                      min(col, N - 1), r, 64 * c, lane, yb);
-                    }
-                }
-            }
+        for (int i = 0; i < 4; ++i) {
+            const int row = wm * 128 + i * 32 + (lane & 31);
+            fa[i] = *reinterpret_cast<const v4i*>(sa + row * kDmaStageK + ((c ^ swz4(row)) << 4));
         }
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const int64_t row = row0 + wm * 128 + i * 32 + acc_row(e, lane);
-            if (interior || (row < T && col < N)) Elem<YT>::store1(y + row * N + col, yb[e]);
+        for (int j = 0; j < 4; ++j) {
+            const int row = wn * 128 + j * 32 + (lane & 31);
+            fb[j] = *reinterpret_cast<const v4i*>(sb + row * kDmaStageK + ((c ^ swz4(row)) << 4));
         }
     };
-#define MASQ_EPI_ROW(I) epilogue_block(I, 0, acc[I][0]); epilogue_block(I, 1, acc[I][1]); \
-                        epilogue_block(I, 2, acc[I][2]); epilogue_block(I, 3, acc[I][3]);
-    MASQ_EPI_ROW(0) MASQ_EPI_ROW(1) MASQ_EPI_ROW(2) MASQ_EPI_ROW(3)
-#undef MASQ_EPI_ROW
+    // 16 MFMAs of one k step; with dma_st >= 0, one of that stage's 8 DMA
+    // loads goes out after every second MFMA, so the vector-memory pipeline
+    // works while the matrix cores do
+    auto mfma16 = [&](const v4i (&fa)[4], const v4i (&fb)[4], int dma_st) __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            acc[q >> 2][q & 3] =
+                __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[q & 3], fa[q >> 2], acc[q >> 2][q & 3], 0, 0, 0);
+            if ((q & 1) && dma_st >= 0) issue_one(dma_st, q >> 1);
+        }
+    };
+    // publish stage st to all waves: this wave's loads of st are complete
+    // once at most those of the `younger` later stages are in flight, and its
+    // LDS reads of the buffer about to be refilled are complete
+    auto publish = [&](int younger) __attribute__((always_inline)) {
+        if (younger >= 2) MASQ_WAIT_VMCNT_LGKM0(16);
+        else if (younger == 1) MASQ_WAIT_VMCNT_LGKM0(8);
+        else MASQ_WAIT_VMCNT_LGKM0(0);
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+
+    // Pipeline: stage kt is consumed as two 32-byte k steps; the fragments of
+    // the next k step are read while the current one's MFMAs run, and the
+    // barrier that publishes stage kt + 1 sits between the two MFMA groups.
+    // The DMA of stage kt + 3 refills the buffer of stage kt - 1, which every
+    // wave finished reading before the previous barrier.
+    const int nk = K / kDmaStageK;
+    for (int st = 0; st < kDmaStages - 1 && st < nk; ++st) issue(st);
+    v4i fa0[4], fb0[4], fa1[4], fb1[4];
+    publish(min(nk - 1, 2));
+    read_frags(0, 0, fa0, fb0);
+    for (int kt = 0; kt < nk; ++kt) {
+        read_frags(kt, 1, fa1, fb1);
+        mfma16(fa0, fb0, kt + kDmaStages - 1 < nk ? kt + kDmaStages - 1 : -1);
+        if (kt + 1 < nk) {
+            publish(min(nk - 2 - kt, 2));
+            read_frags(kt + 1, 0, fa0, fb0);
+        }
+        mfma16(fa1, fb1, -1);
+    }
+    gemm_epilogue<YT, LT, CMC, ACC>(acc, sm, pf, T, N, row0, col0, u, r, n_mod, r_up, acc_out, y);
 }
 
 }  // namespace
@@ -634,6 +1095,18 @@ __global__ __launch_bounds__(256, 1) void k_gemm(
 hipError_t launch_smooth_quant(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                int64_t T, int64_t K, int n_mod, int8_t* q, float* x_scale,
                                hipStream_t s) {
+    if (T >= kRowsPerWaveMinT) {
+        const dim3 grid(static_cast<unsigned>((T + 3) / 4)), block(256);
+        if (x_dt == DT::BF16)
+            hipLaunchKernelGGL((k_smooth_quant_rows<bf16_t, 8>), grid, block, 0, s,
+                               static_cast<const bf16_t*>(x), mod, inv_s, T, static_cast<int>(K),
+                               n_mod, q, x_scale);
+        else
+            hipLaunchKernelGGL((k_smooth_quant_rows<float, 8>), grid, block, 0, s,
+                               static_cast<const float*>(x), mod, inv_s, T, static_cast<int>(K),
+                               n_mod, q, x_scale);
+        return hipGetLastError();
+    }
     const dim3 grid(static_cast<unsigned>(T)), block(256);
     if (x_dt == DT::BF16)
         hipLaunchKernelGGL(k_smooth_quant<bf16_t>, grid, block, 0, s,
@@ -669,7 +1142,7 @@ hipError_t launch_lowrank_down(const void* x, DT x_dt, const int32_t* mod, const
     return hipGetLastError();
 }
 
-template <typename YT, typename LT, bool CMC>
+template <typename YT, typename LT, bool CMC, bool ACC>
 static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* wq,
                           const float* w_scale, int64_t T, int64_t K, int64_t N,
                           const int32_t* mod, const float* u, int rank, int n_mod,
@@ -678,9 +1151,14 @@ static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* w
     const int tiles_n = static_cast<int>((N + kTileN - 1) / kTileN);
     const int nt = tiles_m * tiles_n;
     const dim3 grid(8 * ((nt + 7) / 8)), block(256);
-    hipLaunchKernelGGL((k_gemm<YT, LT, CMC>), grid, block, 0, s, q, wq, x_scale, w_scale, T,
-                       static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u, rank,
-                       n_mod, static_cast<const LT*>(r_up), acc, static_cast<YT*>(y));
+    if (K % kDmaStageK == 0)
+        hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC>), grid, block, 0, s, q, wq, x_scale, w_scale,
+                           T, static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
+                           rank, n_mod, static_cast<const LT*>(r_up), acc, static_cast<YT*>(y));
+    else
+        hipLaunchKernelGGL((k_gemm<YT, LT, CMC, ACC>), grid, block, 0, s, q, wq, x_scale, w_scale, T,
+                           static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
+                           rank, n_mod, static_cast<const LT*>(r_up), acc, static_cast<YT*>(y));
 }
 
 hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
@@ -688,16 +1166,24 @@ hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        const int32_t* mod, const float* u, int rank, int n_mod,
                        const void* r_up, DT lr_dt, bool cmc, int32_t* acc, void* y, DT y_dt,
                        hipStream_t s) {
-#define MASQ_GEMM(YT, LT, C) launch_gemm_t<YT, LT, C>(q, x_scale, wq, w_scale, T, K, N, mod, u, rank, n_mod, r_up, acc, y, s)
+#define MASQ_GEMM(YT, LT, C, A) launch_gemm_t<YT, LT, C, A>(q, x_scale, wq, w_scale, T, K, N, mod, u, rank, n_mod, r_up, acc, y, s)
+    // the int32 accumulator output exists only for the plain product (no
+    // compensation); it is a separate instantiation because storing the
+    // accumulators as well raises the epilogue's register pressure
     if (!cmc) {
-        if (y_dt == DT::BF16) MASQ_GEMM(bf16_t, bf16_t, false);
-        else MASQ_GEMM(float, bf16_t, false);
+        if (acc != nullptr) {
+            if (y_dt == DT::BF16) MASQ_GEMM(bf16_t, bf16_t, false, true);
+            else MASQ_GEMM(float, bf16_t, false, true);
+        } else {
+            if (y_dt == DT::BF16) MASQ_GEMM(bf16_t, bf16_t, false, false);
+            else MASQ_GEMM(float, bf16_t, false, false);
+        }
     } else if (y_dt == DT::BF16) {
-        if (lr_dt == DT::BF16) MASQ_GEMM(bf16_t, bf16_t, true);
-        else MASQ_GEMM(bf16_t, float, true);
+        if (lr_dt == DT::BF16) MASQ_GEMM(bf16_t, bf16_t, true, false);
+        else MASQ_GEMM(bf16_t, float, true, false);
     } else {
-        if (lr_dt == DT::BF16) MASQ_GEMM(float, bf16_t, true);
-        else MASQ_GEMM(float, float, true);
+        if (lr_dt == DT::BF16) MASQ_GEMM(float, bf16_t, true, false);
+        else MASQ_GEMM(float, float, true, false);
     }
 #undef MASQ_GEMM
     return hipGetLastError();

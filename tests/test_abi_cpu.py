@@ -108,6 +108,7 @@ def test_unfused_calls_validate(lib):
     assert lib.masq_smooth_quant(P, 1, P, P, 8, 64, 2, None, P, None) == 1
     assert lib.masq_smooth_quant(P + 2, 1, P, P, 8, 64, 2, P, P, None) == 4
     assert lib.masq_smooth_quant(P, 1, P, P, 0, 64, 2, P, P, None) == 0
+    assert lib.masq_smooth_quant(None, 1, None, None, 0, 64, 2, None, None, None) == 0
     # w8a8_gemm: both outputs null, bad dtype, empty batch
     assert lib.masq_w8a8_gemm(P, P, P, P, 8, 64, 64, None, None, 0, None) == 1
     assert lib.masq_w8a8_gemm(P, P, P, P, 8, 64, 64, None, P, 9, None) == 3
