@@ -24,6 +24,8 @@
 // dequantisation is two fp32 multiplies in a fixed order.  The library is
 // compiled without FP contraction.
 
+#include <type_traits>
+
 #include "masq_common.h"
 
 namespace masq {
@@ -1045,15 +1047,17 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dma(
             fb[j] = *reinterpret_cast<const v4i*>(sb + row * kDmaStageK + ((c ^ swz4(row)) << 4));
         }
     };
-    // 16 MFMAs of one k step; with dma_st >= 0, one of that stage's 8 DMA
-    // loads goes out after every second MFMA, so the vector-memory pipeline
-    // works while the matrix cores do
-    auto mfma16 = [&](const v4i (&fa)[4], const v4i (&fb)[4], int dma_st) __attribute__((always_inline)) {
+    // 16 MFMAs of one k step; with DMA, one of stage dma_st's 8 DMA loads
+    // goes out after every second MFMA, so the vector-memory pipeline works
+    // while the matrix cores do
+    auto mfma16 = [&](const v4i (&fa)[4], const v4i (&fb)[4], auto with_dma, int dma_st)
+                      __attribute__((always_inline)) {
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
             acc[q >> 2][q & 3] =
                 __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[q & 3], fa[q >> 2], acc[q >> 2][q & 3], 0, 0, 0);
-            if ((q & 1) && dma_st >= 0) issue_one(dma_st, q >> 1);
+            if constexpr (decltype(with_dma)::value)
+                if (q & 1) issue_one(dma_st, q >> 1);
         }
     };
     // publish stage st to all waves: this wave's loads of st are complete
@@ -1071,21 +1075,29 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dma(
     // the next k step are read while the current one's MFMAs run, and the
     // barrier that publishes stage kt + 1 sits between the two MFMA groups.
     // The DMA of stage kt + 3 refills the buffer of stage kt - 1, which every
-    // wave finished reading before the previous barrier.
+    // wave finished reading before the previous barrier.  The loop is split
+    // into three uniform phases (DMA still to issue / none / last stage) so
+    // that each body has a single shape.
+    using yes = std::true_type;
+    using no = std::false_type;
     const int nk = K / kDmaStageK;
     for (int st = 0; st < kDmaStages - 1 && st < nk; ++st) issue(st);
     v4i fa0[4], fb0[4], fa1[4], fb1[4];
-    publish(min(nk - 1, 2));
-    read_frags(0, 0, fa0, fb0);
-    for (int kt = 0; kt < nk; ++kt) {
+    auto body = [&](int kt, auto with_dma, auto with_next) __attribute__((always_inline)) {
         read_frags(kt, 1, fa1, fb1);
-        mfma16(fa0, fb0, kt + kDmaStages - 1 < nk ? kt + kDmaStages - 1 : -1);
-        if (kt + 1 < nk) {
+        mfma16(fa0, fb0, with_dma, kt + kDmaStages - 1);
+        if constexpr (decltype(with_next)::value) {
             publish(min(nk - 2 - kt, 2));
             read_frags(kt + 1, 0, fa0, fb0);
         }
-        mfma16(fa1, fb1, -1);
-    }
+        mfma16(fa1, fb1, no{}, 0);
+    };
+    publish(min(nk - 1, 2));
+    read_frags(0, 0, fa0, fb0);
+    int kt = 0;
+    for (; kt + kDmaStages - 1 < nk; ++kt) body(kt, yes{}, yes{});
+    for (; kt + 1 < nk; ++kt) body(kt, no{}, yes{});
+    body(kt, no{}, no{});
     gemm_epilogue<YT, LT, CMC, ACC>(acc, sm, pf, T, N, row0, col0, u, r, n_mod, r_up, acc_out, y);
 }
 
