@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--copies", type=int, default=2,
                     help="rotating input/output sets so no step reuses the last one's cache")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--summarize-profiles", metavar="DIR", default=None,
+                    help="write the profiles/ summaries of the rocprofv3 runs under DIR "
+                         "(trace/, fetch/, write/, copy_fetch/, copy_write/ and their .log)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (5 times): the "
                          "reference for scaling HBM traffic counters")
@@ -87,43 +90,168 @@ def algorithmic_bytes(L) -> int:
             + present * L["rank"] * (K + N) * lr + T * 4)
 
 
+GEMM_KERNEL = "k_gemm"          # name stem of the stage-2 GEMM kernels
+COPY_KERNEL = "copyBuffer"      # the runtime's device-to-device copy (the probe)
+
+# The rocprofv3 runs whose output --summarize-profiles reads; <repo> is the
+# repository root, <out> the directory given to --summarize-profiles.
+PROFILE_COMMANDS = {
+    "trace": "cd /tmp && TMPDIR=/tmp rocprofv3 --kernel-trace --stats --output-format csv "
+             "-d <out>/trace -o run -- python3 <repo>/bench.py --workload {w} --steps 30 "
+             "--warmup 5 --no-cpu",
+    "fetch": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc FETCH_SIZE --output-format csv "
+             "-d <out>/fetch -o run -- python3 <repo>/bench.py --workload {w} --steps 3 "
+             "--warmup 1 --no-cpu",
+    "write": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc WRITE_SIZE --output-format csv "
+             "-d <out>/write -o run -- python3 <repo>/bench.py --workload {w} --steps 3 "
+             "--warmup 1 --no-cpu",
+    "copy_fetch": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc FETCH_SIZE --output-format csv "
+                  "-d <out>/copy_fetch -o run -- python3 <repo>/bench.py --copy-probe 512",
+    "copy_write": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc WRITE_SIZE --output-format csv "
+                  "-d <out>/copy_write -o run -- python3 <repo>/bench.py --copy-probe 512",
+}
+
+
+def _profile_path(kind: str, workload_name: str) -> str:
+    return os.path.join(ROOT, "profiles", f"k_gemm_{kind}_{workload_name}.txt")
+
+
 def traffic_from_profiles(workload_name: str, src_hash: str):
     """HBM bytes per GEMM launch from the committed rocprofv3 counter summary,
     only if it was taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", f"gemm_traffic_{workload_name}.json")
+    path = _profile_path("traffic", workload_name)
     if not os.path.exists(path):
         return None
+    kv = {}
     with open(path) as f:
-        d = json.load(f)
-    if d.get("kernel_source_sha256_16") != src_hash:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256_16") != src_hash:
         return None
-    return d.get("bytes_per_launch")
+    return int(kv["bytes_per_launch"])
 
 
-def cpu_baseline(L, rows_every=4):
-    """The CPU oracle on every `rows_every`-th token of the same workload."""
+def _csv_rows(directory: str, suffix: str):
+    import csv
+    import glob
+    paths = sorted(glob.glob(os.path.join(directory, "**", f"*{suffix}"), recursive=True))
+    if not paths:
+        raise FileNotFoundError(f"no *{suffix} under {directory}")
+    with open(paths[0], newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def _per_dispatch(directory: str, counter: str, name_part: str):
+    """{dispatch id: summed counter value} of the dispatches whose kernel name
+    contains name_part, from a rocprofv3 --pmc csv run."""
+    vals = {}
+    for r in _csv_rows(directory, "counter_collection.csv"):
+        if r["Counter_Name"] != counter or name_part not in r["Kernel_Name"]:
+            continue
+        d = r["Dispatch_Id"]
+        vals[d] = vals.get(d, 0.0) + float(r["Counter_Value"])
+    if not vals:
+        raise ValueError(f"no {counter} for kernels matching {name_part!r} in {directory}")
+    return vals
+
+
+def _bench_hash_in_log(path: str):
+    with open(path) as f:
+        for line in f:
+            if line.startswith('{"metric"'):
+                return json.loads(line).get("kernel_source_sha256_16")
+    return None
+
+
+def summarize_profiles(out: str, workload: int):
+    """Write the committed text summaries of the rocprofv3 runs listed in
+    PROFILE_COMMANDS (run beforehand, output under `out`)."""
+    from synth.workloads import CONFIGS
+    cfg = CONFIGS[workload]
+    src_hash = kernel_source_hash()
+    for kind in ("trace", "fetch", "write"):
+        h = _bench_hash_in_log(os.path.join(out, f"{kind}.log"))
+        if h != src_hash:
+            raise SystemExit(f"{kind} run was taken on kernel source {h}, tree is {src_hash}")
+    cmds = {k: v.format(w=workload) for k, v in PROFILE_COMMANDS.items()}
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+
+    stats = _csv_rows(os.path.join(out, "trace"), "kernel_stats.csv")
+    with open(_profile_path("trace", cfg.name), "w") as f:
+        f.write(f"# rocprofv3 kernel trace statistics, workload {cfg.name}\n")
+        f.write(f"# command: {cmds['trace']}\n")
+        f.write(f"# kernel_source_sha256_16: {src_hash}\n")
+        f.write("# calls  avg_us  min_us  max_us  share%  kernel\n")
+        for r in stats:
+            name = r["Name"]
+            short = name.replace("(anonymous namespace)::", "").replace("void ", "")
+            short = short.split("(")[0][:110]
+            f.write(f"{int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:8.2f} "
+                    f"{float(r['MinNs']) / 1e3:8.2f} {float(r['MaxNs']) / 1e3:8.2f} "
+                    f"{float(r['Percentage']):6.2f}  {short}\n")
+
+    copy_bytes = 512 << 20
+    cf = max(_per_dispatch(os.path.join(out, "copy_fetch"), "FETCH_SIZE", COPY_KERNEL).values())
+    cw = max(_per_dispatch(os.path.join(out, "copy_write"), "WRITE_SIZE", COPY_KERNEL).values())
+    fetch_scale = copy_bytes / (cf * 1024.0)
+    write_scale = copy_bytes / (cw * 1024.0)
+    gf = _per_dispatch(os.path.join(out, "fetch"), "FETCH_SIZE", GEMM_KERNEL)
+    gw = _per_dispatch(os.path.join(out, "write"), "WRITE_SIZE", GEMM_KERNEL)
+    fkib = sum(gf.values()) / len(gf)
+    wkib = sum(gw.values()) / len(gw)
+    nbytes = int(round(fkib * 1024 * fetch_scale + wkib * 1024 * write_scale))
+    with open(_profile_path("traffic", cfg.name), "w") as f:
+        f.write(f"# HBM traffic of the stage-2 GEMM kernel (k_gemm*), workload {cfg.name}\n")
+        for k in ("fetch", "write", "copy_fetch", "copy_write"):
+            f.write(f"# command ({k}): {cmds[k]}\n")
+        f.write("# bytes = FETCH_SIZE KiB * 1024 * fetch_scale + WRITE_SIZE KiB * 1024 * "
+                "write_scale; the scales make a 512 MiB device copy read and write 512 MiB\n")
+        f.write(f"kernel_source_sha256_16: {src_hash}\n")
+        f.write(f"gemm_dispatches_fetch: {len(gf)}\n")
+        f.write(f"gemm_dispatches_write: {len(gw)}\n")
+        f.write(f"fetch_size_kib_per_launch: {fkib:.1f}\n")
+        f.write(f"write_size_kib_per_launch: {wkib:.1f}\n")
+        f.write(f"copy_probe_fetch_size_kib: {cf:.1f}\n")
+        f.write(f"copy_probe_write_size_kib: {cw:.1f}\n")
+        f.write(f"fetch_scale: {fetch_scale:.4f}\n")
+        f.write(f"write_scale: {write_scale:.4f}\n")
+        f.write(f"bytes_per_launch: {nbytes}\n")
+    print(open(_profile_path("trace", cfg.name)).read())
+    print(open(_profile_path("traffic", cfg.name)).read())
+
+
+def cpu_baseline(L, min_seconds=10.0, max_runs=64):
+    """The CPU oracle (oracle.inference.linear, fp64) on the whole batch of the
+    same workload, repeated until at least `min_seconds` of CPU work; the
+    value is the mean over the runs."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
     from oracle import inference as oinf
-    sel = np.arange(0, L["x"].shape[0], rows_every)
-    x, mod = L["x"][sel], L["modality"][sel]
-    t0 = time.perf_counter()
-    oinf.linear(x, mod, L["inv_smooth"], L["wq"], L["w_scale"], L["l_down"], L["r_up"])
-    dt = time.perf_counter() - t0
-    K, N = L["x"].shape[1], L["wq"].shape[0]
+    x, mod = L["x"], L["modality"]
+    runs, dt = 0, 0.0
+    while runs < max_runs and (runs == 0 or dt < min_seconds):
+        t0 = time.perf_counter()
+        oinf.linear(x, mod, L["inv_smooth"], L["wq"], L["w_scale"], L["l_down"], L["r_up"])
+        dt += time.perf_counter() - t0
+        runs += 1
+    T, K, N = x.shape[0], x.shape[1], L["wq"].shape[0]
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    return {"value": round(2.0 * len(sel) * K * N / dt / 1e12, 4), "unit": "TOPS",
+    return {"value": round(2.0 * T * K * N * runs / dt / 1e12, 4), "unit": "TOPS",
             "cores": int(threads), "kind": "oracle",
-            "sample": f"{len(sel)} of {L['x'].shape[0]} tokens (every {rows_every}th, "
-                      f"{int((mod == 0).sum())} text) through oracle.inference.linear, "
-                      f"{dt:.2f} s"}
+            "sample": f"the whole {T}-token batch ({int((np.asarray(mod) == 0).sum())} text) "
+                      f"through oracle.inference.linear (fp64), {runs} runs, {dt:.1f} s total"}
 
 
 def main():
     args = parse()
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.summarize_profiles:
+        summarize_profiles(args.summarize_profiles, args.workload)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "

@@ -29,7 +29,8 @@ Pins (checked by the CPU test suite, not by retyping formulas):
   * full-rank truncation reproduces diag(s_m) W exactly (eq. l1l2);
   * Theorem 2 (optimal low-rank compensation) against an independent SVD of
     X_m S_m^-1 dW (Eckart-Young), and no worse than other rank-r choices;
-  * Theorem 1's SQNR gap on constructed uniform tokens;
+  * Theorem 1 (Sec. 4.2), qualitatively: per-modality factors recover the
+    activation SQNR that a unified factor set by another modality loses;
   * bf16 helpers exhaustively against torch's CPU casts.
 Whole-layer output values beyond these properties are "parity unpinned": the
 paper prints no worked numerical example for the layer.

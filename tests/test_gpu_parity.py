@@ -81,6 +81,7 @@ def _check_layer(ops, L, rows=None, name=""):
                                        L["w_scale"], L["l_down"], L["r_up"]), act)
     y_np = _np(y.index_select(0, rows_t))
     err = oinf.relerr(y_np, y_ref)
+    print(f"[parity] {name} fused relerr {err:.3e} (bar {_tol(act, L['lr_dtype']):.0e})", flush=True)
     assert err <= _tol(act, L["lr_dtype"]), f"fused relerr {err}"
     text = mod_np[rows] == 0
     assert np.array_equal(y_np[text], oinf.to_output(y0_ref, act)[text]), "text rows not exact"
@@ -192,3 +193,21 @@ def test_empty_batch_is_a_noop(ops):
     x, mod, lin = workload.to_device(L)
     y = lin(x[:0], mod[:0])
     assert y.shape == (0, 32)
+
+
+def test_invalid_modality_ids_read_as_text(ops):
+    """Ids outside [0, n_mod) are documented to be read as text: the layer then
+    equals the oracle run with those ids replaced by 0 (text rows exact)."""
+    from paper_2603_04800_amd import workload
+    L = _random_layer(300, 128, 96, 16, 3, "bf16", "bf16")
+    bad = np.array([0, 5, 17, 100, 257, 299])
+    mod_gpu = L["modality"].copy()
+    mod_gpu[bad] = np.array([3, -1, 4, 1 << 20, -(1 << 30), 7], np.int32)
+    L["modality"][bad] = 0
+    x, _, lin = workload.to_device(L)
+    y = lin(x, torch.from_numpy(mod_gpu).to(x.device), out_dtype=torch.bfloat16)
+    y_ref = oinf.to_output(oinf.linear(L["x"], L["modality"], L["inv_smooth"], L["wq"],
+                                       L["w_scale"], L["l_down"], L["r_up"]), "bf16")
+    y_np = _np(y)
+    assert oinf.relerr(y_np, y_ref) <= 1e-2
+    assert np.array_equal(y_np[bad], y_ref[bad])
