@@ -42,11 +42,15 @@ typedef uint16_t bf16_t;   // bfloat16 stored as its bit pattern
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
 
-// Round-to-nearest-even narrowing of a finite fp32 value to bf16 bits.
-__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-    const uint32_t u = __float_as_uint(f);
-    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+typedef float v2f __attribute__((ext_vector_type(2)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+
+// Two fp32 values narrowed to bf16 bits (a in the low half), round to nearest
+// even: one v_cvt_pk_bf16_f32 on gfx950.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v2f{a, b}, v2bf));
 }
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) { return pack_bf16x2(f, 0.f) & 0xFFFFu; }
 
 // ---------------------------------------------------------------- element IO
 template <typename T> struct Elem;
@@ -148,11 +152,10 @@ __global__ __launch_bounds__(256) void k_smooth_quant(const XT* __restrict__ x,
 __device__ __forceinline__ void split_bf16x8(const float (&v)[8], v4i& hi, v4i& lo) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-        const uint32_t h0 = f32_to_bf16(v[2 * j]), h1 = f32_to_bf16(v[2 * j + 1]);
-        const uint32_t l0 = f32_to_bf16(v[2 * j] - bf16_to_f32(h0));
-        const uint32_t l1 = f32_to_bf16(v[2 * j + 1] - bf16_to_f32(h1));
-        hi[j] = static_cast<int32_t>(h0 | (h1 << 16));
-        lo[j] = static_cast<int32_t>(l0 | (l1 << 16));
+        const uint32_t h = pack_bf16x2(v[2 * j], v[2 * j + 1]);
+        const float h0 = __uint_as_float(h << 16), h1 = __uint_as_float(h & 0xFFFF0000u);
+        hi[j] = static_cast<int32_t>(h);
+        lo[j] = static_cast<int32_t>(pack_bf16x2(v[2 * j] - h0, v[2 * j + 1] - h1));
     }
 }
 
@@ -634,7 +637,7 @@ struct GemmSmem {
     float dx[kTileM];
     float ws[kTileN];
     int mod[kTileM];
-    unsigned present;
+    unsigned wpresent[4];     // per wave: bit m set if a row of modality m is in its 64 rows
 };
 
 // Epilogue of a 256 x 256 tile whose int32 accumulators are in acc (this
@@ -672,20 +675,25 @@ __device__ __forceinline__ void gemm_epilogue(
     __syncthreads();                         // every wave is done with the K stages
     sm.dx[tid] = pf.dx;
     sm.ws[tid] = pf.ws;
-    if (CMC) sm.mod[tid] = pf.mod;
-    if (tid == 0) sm.present = 0u;
+    if constexpr (CMC) {
+        sm.mod[tid] = pf.mod;
+        unsigned wp = 0;
+        for (int m = 1; m < n_mod; ++m)
+            if (__ballot(pf.mod == m) != 0ull) wp |= 1u << m;
+        if (lane == 0) sm.wpresent[wave] = wp;
+    }
     __syncthreads();
 
-    // ---- compensation: modalities present in the tile, LDS plan per 64-column chunk
+    // ---- compensation: modalities present in the tile, LDS plan per 64-column chunk.
+    // Every quantity that selects a code path is wave-uniform (scalar registers).
     int n_present = 0;
     bool staged = false;
     unsigned present = 0;
     const int n_chunks = (r + 63) >> 6;
     constexpr int kChunkBase = CMC ? Cmc<LT>::kUBytes : 0;
     if constexpr (CMC) {
-        if (sm.mod[tid] > 0) atomicOr(&sm.present, 1u << sm.mod[tid]);
-        __syncthreads();
-        present = sm.present;
+        present = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(
+            static_cast<int>(sm.wpresent[0] | sm.wpresent[1] | sm.wpresent[2] | sm.wpresent[3])));
         n_present = __builtin_popcount(present);
         const int chunk_bytes = Cmc<LT>::kUBytes + n_present * Cmc<LT>::kRBytes;
         staged = n_chunks * chunk_bytes <= static_cast<int>(sizeof(sm.buf));
@@ -708,9 +716,8 @@ __device__ __forceinline__ void gemm_epilogue(
 
     // ---- accumulator layout: register e of a lane in block (i, j) holds token
     // wm*128 + 32 i + (lane % 32) and channel wn*128 + 32 j + 8 (e / 4) +
-    // 4 (lane / 32) + e % 4.  The three phases below (dequantise in place,
-    // compensate, store) are written as short unrolled nests so that the
-    // epilogue stays compact in the instruction cache.
+    // 4 (lane / 32) + e % 4.  Loops over blocks are fully unrolled: the
+    // accumulators are registers and must be indexed by constants.
     const bool interior = (row0 + kTileM <= T) && (col0 + kTileN <= N);
     auto tok_of = [&](int i) { return wm * 128 + i * 32 + (lane & 31); };
     auto ch_of = [&](int j, int g) { return wn * 128 + j * 32 + 8 * g + 4 * (lane >> 5); };
@@ -734,73 +741,13 @@ __device__ __forceinline__ void gemm_epilogue(
     }
     if (y == nullptr) return;
 
-    // ---- per 32 x 32 block: dequantise, compensate, cast and store.
-    // Compensation fast path (bf16 factors, rank <= 64, at most two non-text
-    // modalities present, all staged): the present modalities are laid side by
-    // side along the rank dimension, K = 16 * nks <= 128, so one block takes
-    // <= 16 MFMAs; the (masked) u fragments are read once per token block and
-    // the L2^T fragments per block.
-    constexpr bool kBf16Cmc = CMC && sizeof(LT) == 2;
-    int mods[2] = {0, 0};
-    if constexpr (CMC) {
-        int p = 0;
-        for (int m = 1; m < n_mod && p < 2; ++m)
-            if (present & (1u << m)) mods[p++] = m;
-    }
-    const bool fast = kBf16Cmc && n_present > 0 && n_present <= 2 && staged && n_chunks == 1;
-    const int nks_slot = fast ? (r >> 4) : 0;               // k steps of 16 per modality
-    const v4i zero4 = {0, 0, 0, 0};
-    v4i uh[8], ul[8];                                       // [k step] of the current token block
-    auto load_u = [&](const int i) __attribute__((always_inline)) {
-        if constexpr (kBf16Cmc) {
-            if (fast) {
-                const int trow = tok_of(i);
-                const int tm_ = sm.mod[trow];
-#pragma unroll
-                for (int kk = 0; kk < 8; ++kk) {
-                    const int p = kk >> 2, ks = kk & 3;
-                    const int c = 2 * ks + (lane >> 5);
-                    const int off = trow * 128 + ((c ^ swz(trow)) << 4);
-                    const bool live = p < n_present && ks < nks_slot && tm_ == mods[p];
-                    const v4i h = *reinterpret_cast<const v4i*>(sm.buf + off);
-                    const v4i l = *reinterpret_cast<const v4i*>(sm.buf + kTileM * 128 + off);
-                    uh[kk] = live ? h : zero4;
-                    ul[kk] = live ? l : zero4;
-                }
-            }
-        }
-    };
-    // general compensation of one block: any rank, any number of modalities,
-    // staged pieces or global memory (kept out of the fast path's code)
-    auto cmc_block_general = [&](const int i, const int j, v16f yb) __attribute__((always_inline)) {
-        if constexpr (CMC) {
-            const int trow = tok_of(i);
-            const int crow = wn * 128 + j * 32 + (lane & 31);
-            const int tm_ = sm.mod[trow];
-            const int chunk_bytes = Cmc<LT>::kUBytes + n_present * Cmc<LT>::kRBytes;
-            for (int c = 0; c < n_chunks; ++c) {
-                int p = 0;
-                for (int m = 1; m < n_mod; ++m) {
-                    if (!(present & (1u << m))) continue;
-                    const bool live = tm_ == m;
-                    if (staged) {
-                        const uint8_t* base = sm.buf + c * chunk_bytes;
-                        yb = Cmc<LT>::from_lds(base, base + kChunkBase + p * Cmc<LT>::kRBytes,
-                                               min(64, r - 64 * c), trow, crow, live, lane, yb);
-                    } else {
-                        yb = Cmc<LT>::from_global(u, r_up + static_cast<int64_t>(m - 1) * N * r,
-                                                  live && (row0 + trow) < T, row0 + trow,
-                                                  min(col0 + crow, N - 1), r, 64 * c, lane, yb);
-                    }
-                    ++p;
-                }
-            }
-        }
-        return yb;
-    };
-    auto epilogue_block = [&](const int i, const int j, const v16i a) __attribute__((always_inline)) {
-        const int64_t tok = row0 + tok_of(i);
+    // ---- per 32 x 32 block: dequantise, compensate, cast and store.  The
+    // tile takes one of three wave-uniform paths: no compensation (text-only
+    // tiles), the fast compensation (bf16 factors, rank <= 64, at most two
+    // non-text modalities present, all staged), or the general one.
+    auto dequant = [&](const int i, const int j) __attribute__((always_inline)) {
         const float dx = sm.dx[tok_of(i)];
+        const v16i a = acc[i][j];
         v16f yb;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
@@ -809,45 +756,134 @@ __device__ __forceinline__ void gemm_epilogue(
             for (int e = 0; e < 4; ++e)
                 yb[4 * g + e] = (static_cast<float>(a[4 * g + e]) * dx) * ws[e];
         }
-        if constexpr (CMC) {
-            if (fast) {
-                if constexpr (kBf16Cmc) {
-                    const int crow = wn * 128 + j * 32 + (lane & 31);
-#pragma unroll
-                    for (int kk = 0; kk < 8; ++kk) {
-                        const int pp = kk >> 2, ks = kk & 3;
-                        if (pp >= n_present || ks >= nks_slot) continue;
-                        const uint8_t* sr = sm.buf + kChunkBase + pp * Cmc<LT>::kRBytes;
-                        const int c = 2 * ks + (lane >> 5);
-                        const v8bf b = __builtin_bit_cast(
-                            v8bf, *reinterpret_cast<const v4i*>(sr + crow * 128 + ((c ^ swz(crow)) << 4)));
-                        yb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, __builtin_bit_cast(v8bf, uh[kk]), yb, 0, 0, 0);
-                        yb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, __builtin_bit_cast(v8bf, ul[kk]), yb, 0, 0, 0);
-                    }
-                }
-            } else if (n_present > 0) {
-                yb = cmc_block_general(i, j, yb);
-            }
-        }
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const int ch = col0 + ch_of(j, g);
-            if (!(interior || (tok < T && ch < N))) continue;
-            if constexpr (sizeof(YT) == 2) {
-                v2i w;
-                w.x = static_cast<int32_t>(f32_to_bf16(yb[4 * g]) | (f32_to_bf16(yb[4 * g + 1]) << 16));
-                w.y = static_cast<int32_t>(f32_to_bf16(yb[4 * g + 2]) | (f32_to_bf16(yb[4 * g + 3]) << 16));
-                *reinterpret_cast<v2i*>(y + tok * N + ch) = w;
-            } else {
-                const v4f w = {yb[4 * g], yb[4 * g + 1], yb[4 * g + 2], yb[4 * g + 3]};
-                *reinterpret_cast<v4f*>(y + tok * N + ch) = w;
-            }
+        return yb;
+    };
+    auto store4 = [&](YT* dst, const v16f& yb, const int g) __attribute__((always_inline)) {
+        if constexpr (sizeof(YT) == 2) {
+            v2i w;
+            w.x = static_cast<int32_t>(pack_bf16x2(yb[4 * g], yb[4 * g + 1]));
+            w.y = static_cast<int32_t>(pack_bf16x2(yb[4 * g + 2], yb[4 * g + 3]));
+            *reinterpret_cast<v2i*>(dst) = w;
+        } else {
+            const v4f w = {yb[4 * g], yb[4 * g + 1], yb[4 * g + 2], yb[4 * g + 3]};
+            *reinterpret_cast<v4f*>(dst) = w;
         }
     };
-#define MASQ_EPI_ROW(I) load_u(I); epilogue_block(I, 0, acc[I][0]); epilogue_block(I, 1, acc[I][1]); \
-                        epilogue_block(I, 2, acc[I][2]); epilogue_block(I, 3, acc[I][3]);
-    MASQ_EPI_ROW(0) MASQ_EPI_ROW(1) MASQ_EPI_ROW(2) MASQ_EPI_ROW(3)
-#undef MASQ_EPI_ROW
+    auto store_block = [&](const int i, const int j, const v16f& yb) __attribute__((always_inline)) {
+        const int64_t tok = row0 + tok_of(i);
+        YT* yrow = y + tok * N + col0;
+        if (interior) {                      // uniform: no per-lane bounds in full tiles
+#pragma unroll
+            for (int g = 0; g < 4; ++g) store4(yrow + ch_of(j, g), yb, g);
+        } else {
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                if (tok < T && col0 + ch_of(j, g) < N) store4(yrow + ch_of(j, g), yb, g);
+        }
+    };
+
+    if (!CMC || n_present == 0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) store_block(i, j, dequant(i, j));
+        return;
+    }
+
+    if constexpr (CMC && sizeof(LT) == 2) {
+        if (n_present <= 2 && staged && n_chunks == 1) {
+            // Fast path: the present modalities lie side by side along the
+            // rank dimension (slot p holds modality mods[p], r / 16 k steps
+            // of 16 each).  Per token block, the compensation of its four
+            // channel blocks runs as four independent MFMA chains from zero
+            // and is added to the dequantised values.
+            int mods[2] = {0, 0};
+            {
+                int p = 0;
+                for (int m = 1; m < n_mod && p < 2; ++m)
+                    if (present & (1u << m)) mods[p++] = m;
+            }
+            const int nks = r >> 4;
+            const v4i zero4 = {0, 0, 0, 0};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int trow = tok_of(i);
+                const int tm_ = sm.mod[trow];
+                v16f c[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) c[j][e] = 0.f;
+#pragma unroll
+                for (int kk = 0; kk < 8; ++kk) {
+                    const int p = kk >> 2, ks = kk & 3;
+                    if (p >= n_present || ks >= nks) continue;
+                    const int cc = 2 * ks + (lane >> 5);
+                    const int off = trow * 128 + ((cc ^ swz(trow)) << 4);
+                    // text rows are zero in the staged u; a second modality
+                    // present needs each slot masked to its own rows
+                    v4i h = *reinterpret_cast<const v4i*>(sm.buf + off);
+                    v4i l = *reinterpret_cast<const v4i*>(sm.buf + kTileM * 128 + off);
+                    if (n_present > 1) {
+                        const bool live = tm_ == mods[p];
+                        h = live ? h : zero4;
+                        l = live ? l : zero4;
+                    }
+                    const uint8_t* sr = sm.buf + kChunkBase + p * Cmc<LT>::kRBytes;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int crow = wn * 128 + j * 32 + (lane & 31);
+                        const v8bf bj = __builtin_bit_cast(
+                            v8bf, *reinterpret_cast<const v4i*>(sr + crow * 128 + ((cc ^ swz(crow)) << 4)));
+                        c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bj, __builtin_bit_cast(v8bf, h), c[j], 0, 0, 0);
+                        c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bj, __builtin_bit_cast(v8bf, l), c[j], 0, 0, 0);
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    v16f yb = dequant(i, j);
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) yb[e] += c[j][e];
+                    store_block(i, j, yb);
+                }
+            }
+            return;
+        }
+    }
+
+    // General compensation of one block: any rank, any number of modalities,
+    // staged pieces or global memory.
+    if constexpr (CMC) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int trow = tok_of(i);
+            const int tm_ = sm.mod[trow];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                v16f yb = dequant(i, j);
+                const int crow = wn * 128 + j * 32 + (lane & 31);
+                const int chunk_bytes = Cmc<LT>::kUBytes + n_present * Cmc<LT>::kRBytes;
+                for (int c = 0; c < n_chunks; ++c) {
+                    int p = 0;
+                    for (int m = 1; m < n_mod; ++m) {
+                        if (!(present & (1u << m))) continue;
+                        const bool live = tm_ == m;
+                        if (staged) {
+                            const uint8_t* base = sm.buf + c * chunk_bytes;
+                            yb = Cmc<LT>::from_lds(base, base + kChunkBase + p * Cmc<LT>::kRBytes,
+                                                   min(64, r - 64 * c), trow, crow, live, lane, yb);
+                        } else {
+                            yb = Cmc<LT>::from_global(u, r_up + static_cast<int64_t>(m - 1) * N * r,
+                                                      live && (row0 + trow) < T, row0 + trow,
+                                                      min(col0 + crow, N - 1), r, 64 * c, lane, yb);
+                        }
+                        ++p;
+                    }
+                }
+                store_block(i, j, yb);
+            }
+        }
+    }
 }
 
 // 16 x 32 x 32 MFMA steps of one wave's 128 x 128 quarter: fragments of the
