@@ -1012,9 +1012,13 @@ __device__ __forceinline__ int swz4(int row) { return (row >> 2) & 3; }
 // One 16-byte lane of an LDS-DMA load: the wave writes 64 x 16 contiguous
 // bytes at LDS address m0 (wave-uniform), lane i at m0 + 16 i.
 __device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                  :: "v"(src), "s"(lds_addr) : "memory", "m0");
 }
+
+// Scheduling fence: the compiler may move no instruction across it, so the
+// software pipeline below keeps the order it is written in.
+#define MASQ_SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
 
 // s_waitcnt vmcnt(n) lgkmcnt(0) (expcnt unconstrained).
 #define MASQ_WAIT_VMCNT_LGKM0(n) \
@@ -1055,45 +1059,53 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dma(
         const int chunk = (lane & 3) ^ swz4(row);
         src[j] = A + min(row0 + row, T - 1) * K + 16 * chunk;
         src[4 + j] = B + static_cast<int64_t>(min(col0 + row, N - 1)) * K + 16 * chunk;
-        dst_off[j] = (wave * 64 + 16 * j) * kDmaStageK;
+        dst_off[j] = static_cast<uint32_t>(
+            __builtin_amdgcn_readfirstlane((wave * 64 + 16 * j) * kDmaStageK));
         dst_off[4 + j] = kTileM * kDmaStageK + dst_off[j];
     }
     const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sm.buf));
     auto issue_one = [&](int st, int q) __attribute__((always_inline)) {
         const uint32_t sbase = lds0 + (st % kDmaStages) * kDmaStageBytes;
-        lds_dma16(src[q] + st * kDmaStageK, __builtin_amdgcn_readfirstlane(sbase + dst_off[q]));
+        lds_dma16(src[q] + st * kDmaStageK, sbase + dst_off[q]);
     };
     auto issue = [&](int st) __attribute__((always_inline)) {
 #pragma unroll
         for (int q = 0; q < 8; ++q) issue_one(st, q);
     };
-    // fragments of one 32-byte k step: 4 token blocks (q rows), 4 channel blocks (Wq rows)
-    auto read_frags = [&](int st, int ks, v4i (&fa)[4], v4i (&fb)[4]) __attribute__((always_inline)) {
+    // fragment f of one 32-byte k step (f < 4: token block f of the q rows,
+    // f >= 4: channel block f - 4 of the Wq rows)
+    auto read_frag = [&](int st, int ks, int f, v4i (&fa)[4], v4i (&fb)[4]) __attribute__((always_inline)) {
         const uint8_t* sa = sm.buf + (st % kDmaStages) * kDmaStageBytes;
-        const uint8_t* sb = sa + kTileM * kDmaStageK;
         const int c = 2 * ks + (lane >> 5);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int row = wm * 128 + i * 32 + (lane & 31);
-            fa[i] = *reinterpret_cast<const v4i*>(sa + row * kDmaStageK + ((c ^ swz4(row)) << 4));
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int row = wn * 128 + j * 32 + (lane & 31);
-            fb[j] = *reinterpret_cast<const v4i*>(sb + row * kDmaStageK + ((c ^ swz4(row)) << 4));
+        if (f < 4) {
+            const int row = wm * 128 + f * 32 + (lane & 31);
+            fa[f] = *reinterpret_cast<const v4i*>(sa + row * kDmaStageK + ((c ^ swz4(row)) << 4));
+        } else {
+            const int row = wn * 128 + (f - 4) * 32 + (lane & 31);
+            fb[f - 4] = *reinterpret_cast<const v4i*>(sa + kTileM * kDmaStageK + row * kDmaStageK +
+                                                      ((c ^ swz4(row)) << 4));
         }
     };
-    // 16 MFMAs of one k step; with DMA, one of stage dma_st's 8 DMA loads
-    // goes out after every second MFMA, so the vector-memory pipeline works
-    // while the matrix cores do
-    auto mfma16 = [&](const v4i (&fa)[4], const v4i (&fb)[4], auto with_dma, int dma_st)
+    // 16 MFMAs of one k step.  Interleaved with them, in a fixed order (each
+    // step is fenced against compiler reordering): two fragment reads of the
+    // next k step (st_next, ks_next) after each of the first four MFMAs, and
+    // with DMA one of stage dma_st's 8 loads after every second MFMA, so the
+    // LDS and vector-memory pipelines work while the matrix cores do.
+    auto mfma16 = [&](const v4i (&fa)[4], const v4i (&fb)[4], auto with_reads, int st_next,
+                      int ks_next, v4i (&na)[4], v4i (&nb)[4], auto with_dma, int dma_st)
                       __attribute__((always_inline)) {
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
             acc[q >> 2][q & 3] =
                 __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[q & 3], fa[q >> 2], acc[q >> 2][q & 3], 0, 0, 0);
+            if constexpr (decltype(with_reads)::value)
+                if (q < 4) {
+                    read_frag(st_next, ks_next, 2 * q, na, nb);
+                    read_frag(st_next, ks_next, 2 * q + 1, na, nb);
+                }
             if constexpr (decltype(with_dma)::value)
                 if (q & 1) issue_one(dma_st, q >> 1);
+            MASQ_SCHED_FENCE();
         }
     };
     // publish stage st to all waves: this wave's loads of st are complete
@@ -1107,29 +1119,32 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dma(
         asm volatile("" ::: "memory");
     };
 
-    // Pipeline: stage kt is consumed as two 32-byte k steps; the fragments of
-    // the next k step are read while the current one's MFMAs run, and the
-    // barrier that publishes stage kt + 1 sits between the two MFMA groups.
-    // The DMA of stage kt + 3 refills the buffer of stage kt - 1, which every
-    // wave finished reading before the previous barrier.  The loop is split
-    // into three uniform phases (DMA still to issue / none / last stage) so
-    // that each body has a single shape.
+    // Pipeline: stage kt is consumed as two 32-byte k steps.  The fragments of
+    // each k step are read during the MFMAs of the previous one; the barrier
+    // that publishes stage kt + 1 sits between the two MFMA groups of stage
+    // kt.  The DMA of stage kt + 3 refills the buffer of stage kt - 1, which
+    // every wave finished reading before the previous barrier.  The loop is
+    // split into three uniform phases (DMA still to issue / none / last
+    // stage) so that each body has a single shape.
     using yes = std::true_type;
     using no = std::false_type;
     const int nk = K / kDmaStageK;
     for (int st = 0; st < kDmaStages - 1 && st < nk; ++st) issue(st);
     v4i fa0[4], fb0[4], fa1[4], fb1[4];
     auto body = [&](int kt, auto with_dma, auto with_next) __attribute__((always_inline)) {
-        read_frags(kt, 1, fa1, fb1);
-        mfma16(fa0, fb0, with_dma, kt + kDmaStages - 1);
+        MASQ_SCHED_FENCE();
+        mfma16(fa0, fb0, yes{}, kt, 1, fa1, fb1, with_dma, kt + kDmaStages - 1);
         if constexpr (decltype(with_next)::value) {
             publish(min(nk - 2 - kt, 2));
-            read_frags(kt + 1, 0, fa0, fb0);
+            MASQ_SCHED_FENCE();
+            mfma16(fa1, fb1, yes{}, kt + 1, 0, fa0, fb0, no{}, 0);
+        } else {
+            mfma16(fa1, fb1, no{}, 0, 0, fa0, fb0, no{}, 0);
         }
-        mfma16(fa1, fb1, no{}, 0);
     };
     publish(min(nk - 1, 2));
-    read_frags(0, 0, fa0, fb0);
+#pragma unroll
+    for (int f = 0; f < 8; ++f) read_frag(0, 0, f, fa0, fb0);
     int kt = 0;
     for (; kt + kDmaStages - 1 < nk; ++kt) body(kt, yes{}, yes{});
     for (; kt + 1 < nk; ++kt) body(kt, no{}, yes{});
