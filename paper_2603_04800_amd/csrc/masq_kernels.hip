@@ -632,12 +632,18 @@ __device__ __forceinline__ bool tile_coords(int tiles_m, int tiles_n, int& tm, i
 
 // Shared LDS of both GEMM kernels: the K stages during the main loop, then
 // the compensation pieces in the epilogue.
+// Row pitch of the per-wave output transpose buffer: 32 rows of 64 bf16
+// channels, padded by 16 bytes (rows stay 16-byte aligned for the 16-byte
+// reads; the column writes, one row per lane, then hit distinct banks).
+constexpr int kTrPitch = 144;
+
 struct GemmSmem {
     uint8_t buf[2 * 65536];
     float dx[kTileM];
     float ws[kTileN];
     int mod[kTileM];
     unsigned wpresent[4];     // per wave: bit m set if a row of modality m is in its 64 rows
+    uint8_t tr[4][32 * kTrPitch];
 };
 
 // Epilogue of a 256 x 256 tile whose int32 accumulators are in acc (this
@@ -672,7 +678,9 @@ __device__ __forceinline__ void gemm_epilogue(
     int32_t* __restrict__ acc_out, YT* __restrict__ y) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    __syncthreads();                         // every wave is done with the K stages
+    // dx, ws, mod and wpresent lie outside the K-stage buffers, so they can be
+    // written before the barrier; after it every wave is also done with the
+    // K stages
     sm.dx[tid] = pf.dx;
     sm.ws[tid] = pf.ws;
     if constexpr (CMC) {
@@ -745,48 +753,86 @@ __device__ __forceinline__ void gemm_epilogue(
     // tile takes one of three wave-uniform paths: no compensation (text-only
     // tiles), the fast compensation (bf16 factors, rank <= 64, at most two
     // non-text modalities present, all staged), or the general one.
-    auto dequant = [&](const int i, const int j) __attribute__((always_inline)) {
+    // dequantisation of block (i, j) with the channel scales ws[g] of its
+    // four 4-channel groups
+    auto dequant_with = [&](const int i, const int j, const v4f (&ws)[4]) __attribute__((always_inline)) {
         const float dx = sm.dx[tok_of(i)];
         const v16i a = acc[i][j];
         v16f yb;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const v4f ws = *reinterpret_cast<const v4f*>(&sm.ws[ch_of(j, g)]);
+        for (int g = 0; g < 4; ++g)
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                yb[4 * g + e] = (static_cast<float>(a[4 * g + e]) * dx) * ws[e];
-        }
+                yb[4 * g + e] = (static_cast<float>(a[4 * g + e]) * dx) * ws[g][e];
         return yb;
     };
-    auto store4 = [&](YT* dst, const v16f& yb, const int g) __attribute__((always_inline)) {
-        if constexpr (sizeof(YT) == 2) {
-            v2i w;
-            w.x = static_cast<int32_t>(pack_bf16x2(yb[4 * g], yb[4 * g + 1]));
-            w.y = static_cast<int32_t>(pack_bf16x2(yb[4 * g + 2], yb[4 * g + 3]));
-            *reinterpret_cast<v2i*>(dst) = w;
-        } else {
-            const v4f w = {yb[4 * g], yb[4 * g + 1], yb[4 * g + 2], yb[4 * g + 3]};
-            *reinterpret_cast<v4f*>(dst) = w;
-        }
+    auto load_ws = [&](const int j, v4f (&ws)[4]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) ws[g] = *reinterpret_cast<const v4f*>(&sm.ws[ch_of(j, g)]);
     };
-    auto store_block = [&](const int i, const int j, const v16f& yb) __attribute__((always_inline)) {
-        const int64_t tok = row0 + tok_of(i);
-        YT* yrow = y + tok * N + col0;
-        if (interior) {                      // uniform: no per-lane bounds in full tiles
+    auto dequant = [&](const int i, const int j) __attribute__((always_inline)) {
+        v4f ws[4];
+        load_ws(j, ws);
+        return dequant_with(i, j, ws);
+    };
+    // Stores of one token block (32 rows x 128 channels of this wave).  bf16
+    // output goes through a small per-wave LDS transpose so that every store
+    // instruction writes 8 whole 128-byte row pieces (the MFMA layout would
+    // give 32 rows x 16 bytes per instruction); LDS operations of one wave
+    // execute in order, so the buffer needs no further synchronisation.
+    auto store_rowblock = [&](const int i, const v16f (&ybs)[4]) __attribute__((always_inline)) {
+        const int64_t tok0 = row0 + wm * 128 + i * 32;
+        if constexpr (sizeof(YT) == 2) {
+            uint8_t* scr = sm.tr[wave];
+            const int rw = lane & 31, h = lane >> 5;
 #pragma unroll
-            for (int g = 0; g < 4; ++g) store4(yrow + ch_of(j, g), yb, g);
+            for (int jp = 0; jp < 2; ++jp) {
+#pragma unroll
+                for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const v16f& yb = ybs[2 * jp + jj];
+                        v2i w;
+                        w.x = static_cast<int32_t>(pack_bf16x2(yb[4 * g], yb[4 * g + 1]));
+                        w.y = static_cast<int32_t>(pack_bf16x2(yb[4 * g + 2], yb[4 * g + 3]));
+                        *reinterpret_cast<v2i*>(scr + rw * kTrPitch + (jj * 32 + 8 * g + 4 * h) * 2) = w;
+                    }
+                const int ch = col0 + wn * 128 + jp * 64 + (lane & 7) * 8;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int rr = k * 8 + (lane >> 3);
+                    const v4i d = *reinterpret_cast<const v4i*>(scr + rr * kTrPitch + (lane & 7) * 16);
+                    const int64_t tok = tok0 + rr;
+                    if (interior || (tok < T && ch < N))
+                        *reinterpret_cast<v4i*>(y + tok * N + ch) = d;
+                }
+            }
         } else {
+            const int64_t tok = tok0 + (lane & 31);
 #pragma unroll
-            for (int g = 0; g < 4; ++g)
-                if (tok < T && col0 + ch_of(j, g) < N) store4(yrow + ch_of(j, g), yb, g);
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int ch = col0 + ch_of(j, g);
+                    if (interior || (tok < T && ch < N)) {
+                        const v4f w = {ybs[j][4 * g], ybs[j][4 * g + 1], ybs[j][4 * g + 2], ybs[j][4 * g + 3]};
+                        *reinterpret_cast<v4f*>(y + tok * N + ch) = w;
+                    }
+                }
         }
     };
 
     if (!CMC || n_present == 0) {
+        v4f wsv[4][4];                       // the wave's 128 channel scales, read once
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) load_ws(j, wsv[j]);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) store_block(i, j, dequant(i, j));
+        for (int i = 0; i < 4; ++i) {
+            v16f ybs[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) ybs[j] = dequant_with(i, j, wsv[j]);
+            store_rowblock(i, ybs);
+        }
         return;
     }
 
@@ -839,13 +885,14 @@ __device__ __forceinline__ void gemm_epilogue(
                         c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bj, __builtin_bit_cast(v8bf, l), c[j], 0, 0, 0);
                     }
                 }
+                v16f ybs[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    v16f yb = dequant(i, j);
+                    ybs[j] = dequant(i, j);
 #pragma unroll
-                    for (int e = 0; e < 16; ++e) yb[e] += c[j][e];
-                    store_block(i, j, yb);
+                    for (int e = 0; e < 16; ++e) ybs[j][e] += c[j][e];
                 }
+                store_rowblock(i, ybs);
             }
             return;
         }
@@ -858,9 +905,11 @@ __device__ __forceinline__ void gemm_epilogue(
         for (int i = 0; i < 4; ++i) {
             const int trow = tok_of(i);
             const int tm_ = sm.mod[trow];
+            v16f ybs[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                v16f yb = dequant(i, j);
+                v16f& yb = ybs[j];
+                yb = dequant(i, j);
                 const int crow = wn * 128 + j * 32 + (lane & 31);
                 const int chunk_bytes = Cmc<LT>::kUBytes + n_present * Cmc<LT>::kRBytes;
                 for (int c = 0; c < n_chunks; ++c) {
@@ -880,8 +929,8 @@ __device__ __forceinline__ void gemm_epilogue(
                         ++p;
                     }
                 }
-                store_block(i, j, yb);
             }
+            store_rowblock(i, ybs);
         }
     }
 }
