@@ -10,6 +10,21 @@ namespace masq {
 
 static size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
+// Number of k slices of the down-projection.  Small batches (at most 16 row
+// tiles) are split along k so that enough workgroups run; slices are
+// multiples of kDownStep.  Larger batches keep one slice: the cross-XCD
+// visibility that combining slices needs (a device-scope fence per
+// workgroup) costs more there than the extra parallelism gains.
+static void plan_kslices(int64_t T, int64_t K, int& n_kslices, int& kslice) {
+    const int64_t tiles = T > 0 ? (T + kDownRows - 1) / kDownRows : 1;
+    const int64_t steps = (K + kDownStep - 1) / kDownStep;
+    int64_t want = tiles <= 16 ? (512 + tiles - 1) / tiles : 1;
+    want = want < 1 ? 1 : (want > steps ? steps : want);
+    const int64_t per = (steps + want - 1) / want;          // steps per slice
+    kslice = static_cast<int>(per * kDownStep);
+    n_kslices = static_cast<int>((K + kslice - 1) / kslice);
+}
+
 Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, int n_mod) {
     (void)N;
     Workspace w{};
@@ -17,15 +32,25 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
     w.n_kslices = 1;
     size_t off = 0;
     uint8_t* b = static_cast<uint8_t*>(base);
-    w.q = reinterpret_cast<int8_t*>(b ? b + off : nullptr);
-    off += align256(static_cast<size_t>(T) * static_cast<size_t>(K));
-    w.x_scale = reinterpret_cast<float*>(b ? b + off : nullptr);
-    off += align256(static_cast<size_t>(T) * sizeof(float));
+    auto carve = [&](size_t bytes) {
+        uint8_t* p = b ? b + off : nullptr;
+        off += align256(bytes);
+        return p;
+    };
+    w.q = reinterpret_cast<int8_t*>(carve(static_cast<size_t>(T) * static_cast<size_t>(K)));
+    w.x_scale = reinterpret_cast<float*>(carve(static_cast<size_t>(T) * sizeof(float)));
     w.u = nullptr;
+    w.u_part = nullptr;
+    w.tickets = nullptr;
     if (rank > 0 && n_mod > 1) {
-        w.u = reinterpret_cast<float*>(b ? b + off : nullptr);
-        off += align256(static_cast<size_t>(w.n_kslices) * static_cast<size_t>(T) *
-                        static_cast<size_t>(rank) * sizeof(float));
+        plan_kslices(T, K, w.n_kslices, w.kslice);
+        const size_t ur = static_cast<size_t>(T) * static_cast<size_t>(rank) * sizeof(float);
+        w.u = reinterpret_cast<float*>(carve(ur));
+        if (w.n_kslices > 1) {
+            w.u_part = reinterpret_cast<float*>(carve(ur * static_cast<size_t>(w.n_kslices)));
+            w.tickets = reinterpret_cast<int*>(
+                carve(static_cast<size_t>((T + kDownRows - 1) / kDownRows) * sizeof(int)));
+        }
     }
     w.bytes = off;
     return w;
@@ -95,13 +120,15 @@ masq_status fused_stage(const Fused& a, int stage) {
     hipStream_t s = static_cast<hipStream_t>(a.stream);
     (void)hipGetLastError();
     if (stage & 1) {
+        const int n_tickets = w.tickets ? static_cast<int>((a.T + masq::kDownRows - 1) / masq::kDownRows) : 0;
         st = from_hip(masq::launch_smooth_quant(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
-                                                a.T, a.c_in, a.n_mod, w.q, w.x_scale, s));
+                                                a.T, a.c_in, a.n_mod, w.q, w.x_scale,
+                                                w.tickets, n_tickets, s));
         if (st != MASQ_OK) return st;
         if (cmc) {
             st = from_hip(masq::launch_lowrank_down(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                     a.l_down, to_dt(a.lr_dt), a.T, a.c_in,
-                                                    a.rank, a.n_mod, w.kslice, w.n_kslices, w.u, s));
+                                                    a.rank, a.n_mod, w, s));
             if (st != MASQ_OK) return st;
         }
     }
@@ -148,7 +175,7 @@ masq_status masq_smooth_quant(const void* x, masq_dtype x_dt, const int32_t* mod
     if (T == 0) return MASQ_OK;
     (void)hipGetLastError();
     return from_hip(masq::launch_smooth_quant(x, to_dt(x_dt), modality, inv_smooth, T, c_in,
-                                              n_mod, q, x_scale,
+                                              n_mod, q, x_scale, nullptr, 0,
                                               static_cast<hipStream_t>(stream)));
 }
 

@@ -13,6 +13,8 @@ constexpr int kTileM = 256;
 constexpr int kTileN = 256;
 constexpr int kTileK = 128;
 constexpr int kRowsDown = 16;     // rows per down-projection tile
+constexpr int kDownRows = kRowsDown;
+constexpr int kDownStep = 512;    // k granularity of a down-projection slice (128 per wave)
 constexpr int kMaxRank = 256;
 constexpr int64_t kRowsPerWaveMinT = 256;   // batches this large quantise one row per wave
 
@@ -38,7 +40,9 @@ struct LinearArgs {
 struct Workspace {
     int8_t* q;
     float* x_scale;
-    float* u;          // [n_kslices][T][rank] fp32 partial down-projections
+    float* u;          // [T][rank] fp32 down-projection u = (x S^-1) L1
+    float* u_part;     // [n_kslices][T][rank] fp32 partial sums over k slices (n_kslices > 1)
+    int* tickets;      // [ceil(T / kDownRows)] arrival counters of the slice workgroups
     int n_kslices;
     int kslice;
     size_t bytes;
@@ -46,13 +50,15 @@ struct Workspace {
 
 Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, int n_mod);
 
+// zero_ints / n_zero: optional array the kernel clears on the way (the
+// down-projection's tickets, which must start at zero).
 hipError_t launch_smooth_quant(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                int64_t T, int64_t K, int n_mod, int8_t* q, float* x_scale,
-                               hipStream_t s);
+                               int* zero_ints, int n_zero, hipStream_t s);
 
 hipError_t launch_lowrank_down(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, DT lr_dt, int64_t T, int64_t K, int rank,
-                               int n_mod, int kslice, int n_kslices, float* u, hipStream_t s);
+                               int n_mod, const Workspace& w, hipStream_t s);
 
 hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        const float* w_scale, int64_t T, int64_t K, int64_t N,

@@ -98,21 +98,50 @@ __device__ __forceinline__ int sane_mod(int m, int n_mod) {
 __device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
 
 // ================================================================ smoothing + quant
+// One workgroup per token row (small batches, where a row's latency
+// matters): the first 256 x 8 x kSqChunks elements of the row are loaded
+// with all requests in flight at once and kept in registers between the
+// absmax and the quantisation; a longer row streams its remainder twice.
+constexpr int kSqChunks = 10;
+
 template <typename XT>
 __global__ __launch_bounds__(256) void k_smooth_quant(const XT* __restrict__ x,
                                                       const int32_t* __restrict__ mod,
                                                       const float* __restrict__ inv_s, int K,
                                                       int n_mod, int8_t* __restrict__ q,
-                                                      float* __restrict__ x_scale) {
+                                                      float* __restrict__ x_scale,
+                                                      int* __restrict__ zero_ints, int n_zero) {
     __shared__ float red[4];
     const int64_t t = blockIdx.x;
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < n_zero; i += 256) zero_ints[i] = 0;
     const int m = sane_mod(mod[t], n_mod);
     const XT* xr = x + t * static_cast<int64_t>(K);
     const float* sr = inv_s + static_cast<int64_t>(m) * K;
+    int8_t* qr = q + t * static_cast<int64_t>(K);
     const int nv = K >> 3;
 
+    float xs[kSqChunks][8];
     float amax = 0.f;
-    for (int v = threadIdx.x; v < nv; v += 256) {
+    {
+        float xv[kSqChunks][8], sv[kSqChunks][8];
+#pragma unroll
+        for (int c = 0; c < kSqChunks; ++c) {
+            const int v = min(static_cast<int>(threadIdx.x) + 256 * c, nv - 1);   // clamped
+            Elem<XT>::load8(xr + 8 * v, xv[c]);
+            load8_f32(sr + 8 * v, sv[c]);
+        }
+#pragma unroll
+        for (int c = 0; c < kSqChunks; ++c) {
+            const bool in = static_cast<int>(threadIdx.x) + 256 * c < nv;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                xs[c][j] = xv[c][j] * sv[c][j];
+                if (in) amax = fmaxf(amax, fabsf(xs[c][j]));
+            }
+        }
+    }
+    for (int v = threadIdx.x + 256 * kSqChunks; v < nv; v += 256) {
         float xv[8], sv[8];
         Elem<XT>::load8(xr + 8 * v, xv);
         load8_f32(sr + 8 * v, sv);
@@ -129,16 +158,11 @@ __global__ __launch_bounds__(256) void k_smooth_quant(const XT* __restrict__ x,
     const float rq = nz ? 127.0f / amax : 0.f;
     if (threadIdx.x == 0) x_scale[t] = dx;
 
-    int8_t* qr = q + t * static_cast<int64_t>(K);
-    for (int v = threadIdx.x; v < nv; v += 256) {
-        float xv[8], sv[8];
-        Elem<XT>::load8(xr + 8 * v, xv);
-        load8_f32(sr + 8 * v, sv);
+    auto put8 = [&](int v, const float (&val)[8]) {
         uint32_t w[2] = {0u, 0u};
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const float xs = xv[j] * sv[j];
-            float c = rintf(xs * rq);
+            float c = rintf(val[j] * rq);
             c = fminf(fmaxf(c, -127.0f), 127.0f);
             w[j >> 2] |= (static_cast<uint32_t>(static_cast<int32_t>(c)) & 0xFFu) << (8 * (j & 3));
         }
@@ -146,6 +170,19 @@ __global__ __launch_bounds__(256) void k_smooth_quant(const XT* __restrict__ x,
         out.x = static_cast<int32_t>(w[0]);
         out.y = static_cast<int32_t>(w[1]);
         *reinterpret_cast<v2i*>(qr + 8 * v) = out;
+    };
+#pragma unroll
+    for (int c = 0; c < kSqChunks; ++c) {
+        const int v = static_cast<int>(threadIdx.x) + 256 * c;
+        if (v < nv) put8(v, xs[c]);
+    }
+    for (int v = threadIdx.x + 256 * kSqChunks; v < nv; v += 256) {
+        float xv[8], sv[8], val[8];
+        Elem<XT>::load8(xr + 8 * v, xv);
+        load8_f32(sr + 8 * v, sv);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) val[j] = xv[j] * sv[j];
+        put8(v, val);
     }
 }
 
@@ -170,7 +207,11 @@ __global__ __launch_bounds__(256) void k_smooth_quant_rows(const XT* __restrict_
                                                            const float* __restrict__ inv_s,
                                                            int64_t T, int K, int n_mod,
                                                            int8_t* __restrict__ q,
-                                                           float* __restrict__ x_scale) {
+                                                           float* __restrict__ x_scale,
+                                                           int* __restrict__ zero_ints,
+                                                           int n_zero) {
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < n_zero; i += 256) zero_ints[i] = 0;
     const int lane = threadIdx.x & 63;
     const int64_t t = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
     if (t >= T) return;
@@ -377,34 +418,74 @@ __device__ __forceinline__ unsigned tile_presence(const int* smod) {
     return present;
 }
 
-// grid: (ceil(T / 16), n_kslices); u[s][t][c] partial over k-slice s.
+// Down-projection u = (x S_m^-1) L1^m of the non-text rows (Sec. 4.3,
+// eq. l1l2).  grid: (ceil(T / 16), n_kslices).  A workgroup takes 16 rows
+// over the k slice [s kslice, (s + 1) kslice), split among its four waves
+// and summed across them in LDS (down_group).  With one slice the result
+// goes straight to u; otherwise each slice writes its partial sums to
+// u_part[s], and the last slice workgroup of a row tile to arrive (counted
+// on tickets[tile], cleared beforehand by the quantisation kernel) adds the
+// partials in slice order, so the result does not depend on timing.  Tiles
+// without non-text rows are skipped (their u rows are never read).
 template <typename XT, typename LT>
 __global__ __launch_bounds__(256) void k_lowrank_down(const XT* __restrict__ x,
                                                       const int32_t* __restrict__ mod,
                                                       const float* __restrict__ inv_s,
                                                       const LT* __restrict__ l_down, int64_t T,
                                                       int K, int r, int n_mod, int kslice,
-                                                      float* __restrict__ u) {
+                                                      int n_kslices, float* __restrict__ u,
+                                                      float* __restrict__ u_part,
+                                                      int* __restrict__ tickets) {
     __shared__ int smod[kRowsDown];
     __shared__ float red[4][kRowsDown][64];
+    __shared__ int last;
+    const int tid = threadIdx.x;
     const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kRowsDown;
     const int s = blockIdx.y;
     const int kb = s * kslice;
     const int ke = min(K, kb + kslice);
-    if (threadIdx.x < kRowsDown) {
-        const int64_t t = row0 + threadIdx.x;
-        smod[threadIdx.x] = t < T ? sane_mod(mod[t], n_mod) : 0;
+    if (tid < kRowsDown) {
+        const int64_t t = row0 + tid;
+        smod[tid] = t < T ? sane_mod(mod[t], n_mod) : 0;
     }
     __syncthreads();
     const unsigned present = tile_presence(smod);
-    if (!present) return;
-    float* us = u + static_cast<int64_t>(s) * T * r;
+    if (!present) return;                                            // uniform per tile
+    float* out = n_kslices > 1 ? u_part + static_cast<int64_t>(s) * T * r : u;
     for (int c0 = 0; c0 < r; c0 += 64)
         down_group<XT, LT>(x, inv_s, l_down, row0, T, K, r, n_mod, kb, ke, c0, smod, present, red,
                            [&](int row, int col, float v) {
                                const int64_t t = row0 + row;
-                               if (t < T) us[t * r + col] = v;
+                               if (t < T) out[t * r + col] = v;
                            });
+    if (n_kslices == 1) return;
+
+    __threadfence();                 // this slice's partials are visible device-wide ...
+    __syncthreads();
+    if (tid == 0) last = atomicAdd(&tickets[blockIdx.x], 1) == n_kslices - 1;
+    __syncthreads();
+    if (!last) return;
+    __threadfence();                 // ... before the last arrival reads them all
+    // 4 consecutive values per thread (r % 16 == 0); the partials of 8 slices
+    // are loaded together and added in slice order
+    const int rows = static_cast<int>(min<int64_t>(kDownRows, T - row0));
+    const int64_t slice = T * r;
+    for (int idx = 4 * tid; idx < rows * r; idx += 4 * 256) {
+        const int64_t e = row0 * r + idx;
+        v4f v = *reinterpret_cast<const v4f*>(u_part + e);
+        for (int q0 = 1; q0 < n_kslices; q0 += 8) {
+            v4f part[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int q = min(q0 + k, n_kslices - 1);
+                part[k] = *reinterpret_cast<const v4f*>(u_part + q * slice + e);
+            }
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+                if (q0 + k < n_kslices) v += part[k];
+        }
+        *reinterpret_cast<v4f*>(u + e) = v;
+    }
 }
 
 // ================================================================ standalone CMC
@@ -1201,57 +1282,146 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dma(
     gemm_epilogue<YT, LT, CMC, ACC>(acc, sm, pf, T, N, row0, col0, u, r, n_mod, r_up, acc_out, y);
 }
 
+// ================================================================ small-batch GEMM
+// For batches of at most 16 tokens (decoding) the layer is bound by
+// streaming Wq from HBM.  A workgroup owns 16 output channels; its four
+// waves split K and keep kSmallDepth 64-byte k steps of Wq and q loads in
+// flight, feeding v_mfma_i32_16x16x64_i8 (tokens as the 16 rows).  The
+// per-wave int32 partials are added in a fixed order in LDS (exact), then
+// each thread finishes one (token, channel): dequantisation, the rank-r
+// compensation u L2^m in fp32 for non-text tokens, and the store.
+constexpr int kSmallMaxT = 16;
+constexpr int kSmallDepth = 16;
+
+template <typename YT, typename LT>
+__global__ __launch_bounds__(256) void k_gemm_small(
+    const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
+    const float* __restrict__ w_scale, int T, int K, int N, const int32_t* __restrict__ mod,
+    const float* __restrict__ u, int r, int n_mod, const LT* __restrict__ r_up,
+    int32_t* __restrict__ acc_out, YT* __restrict__ y) {
+    __shared__ int part[4][16][16];
+    const int tid = threadIdx.x, lane = tid & 63;
+    // wave-uniform k range (scalar registers), so the loop below branches on
+    // it: MFMA instructions ignore EXEC and must not sit under a lane mask
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int col0 = blockIdx.x * 16;
+    const int nsteps = K >> 6;
+    const int per = (nsteps + 3) >> 2;
+    const int sb = min(nsteps, wave * per);
+    const int se = min(nsteps, sb + per);
+    // lane: row (token / channel) lane % 16, 16-byte k group lane / 16
+    const int8_t* ap = A + static_cast<int64_t>(min(lane & 15, T - 1)) * K + 16 * (lane >> 4);
+    const int8_t* bp = B + static_cast<int64_t>(col0 + (lane & 15)) * K + 16 * (lane >> 4);
+    auto step_addr = [&](int st) { return static_cast<int64_t>(min(st, nsteps - 1)) * 64; };
+    v4i acc = {0, 0, 0, 0};
+    v4i fa[kSmallDepth], fb[kSmallDepth];
+#pragma unroll
+    for (int d = 0; d < kSmallDepth; ++d) {
+        fa[d] = *reinterpret_cast<const v4i*>(ap + step_addr(sb + d));
+        fb[d] = *reinterpret_cast<const v4i*>(bp + step_addr(sb + d));
+    }
+    const v4i zero = {0, 0, 0, 0};
+    for (int st0 = sb; st0 < se; st0 += kSmallDepth) {
+#pragma unroll
+        for (int d = 0; d < kSmallDepth; ++d) {
+            // steps past the wave's range (last round) contribute zeros
+            const bool in = st0 + d < se;
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(in ? fa[d] : zero, fb[d], acc, 0, 0, 0);
+            fa[d] = *reinterpret_cast<const v4i*>(ap + step_addr(st0 + d + kSmallDepth));
+            fb[d] = *reinterpret_cast<const v4i*>(bp + step_addr(st0 + d + kSmallDepth));
+        }
+    }
+    // acc[e]: token 4 (lane / 16) + e, channel col0 + lane % 16
+#pragma unroll
+    for (int e = 0; e < 4; ++e) part[wave][4 * (lane >> 4) + e][lane & 15] = acc[e];
+    __syncthreads();
+    const int t = tid >> 4, o = tid & 15;
+    if (t >= T) return;
+    const int a = ((part[0][t][o] + part[1][t][o]) + part[2][t][o]) + part[3][t][o];
+    const int ch = col0 + o;
+    if (acc_out != nullptr) acc_out[static_cast<int64_t>(t) * N + ch] = a;
+    if (y == nullptr) return;
+    float v = (static_cast<float>(a) * x_scale[t]) * w_scale[ch];
+    const int m = (u != nullptr) ? sane_mod(mod[t], n_mod) : 0;
+    if (m > 0) {
+        const float* ur = u + static_cast<int64_t>(t) * r;
+        const LT* rr = r_up + (static_cast<int64_t>(m - 1) * N + ch) * r;
+        float c = 0.f;
+        for (int k0 = 0; k0 < r; k0 += 8) {
+            float uv[8], rv[8];
+            load8_f32(ur + k0, uv);
+            Elem<LT>::load8(rr + k0, rv);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) c = fmaf(uv[k], rv[k], c);
+        }
+        v += c;
+    }
+    Elem<YT>::store1(y + static_cast<int64_t>(t) * N + ch, v);
+}
+
 }  // namespace
 
 // ================================================================ launchers
 hipError_t launch_smooth_quant(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                int64_t T, int64_t K, int n_mod, int8_t* q, float* x_scale,
-                               hipStream_t s) {
+                               int* zero_ints, int n_zero, hipStream_t s) {
     if (T >= kRowsPerWaveMinT) {
         const dim3 grid(static_cast<unsigned>((T + 3) / 4)), block(256);
         if (x_dt == DT::BF16)
             hipLaunchKernelGGL((k_smooth_quant_rows<bf16_t, 8>), grid, block, 0, s,
                                static_cast<const bf16_t*>(x), mod, inv_s, T, static_cast<int>(K),
-                               n_mod, q, x_scale);
+                               n_mod, q, x_scale, zero_ints, n_zero);
         else
             hipLaunchKernelGGL((k_smooth_quant_rows<float, 8>), grid, block, 0, s,
                                static_cast<const float*>(x), mod, inv_s, T, static_cast<int>(K),
-                               n_mod, q, x_scale);
+                               n_mod, q, x_scale, zero_ints, n_zero);
         return hipGetLastError();
     }
     const dim3 grid(static_cast<unsigned>(T)), block(256);
     if (x_dt == DT::BF16)
         hipLaunchKernelGGL(k_smooth_quant<bf16_t>, grid, block, 0, s,
                            static_cast<const bf16_t*>(x), mod, inv_s, static_cast<int>(K), n_mod,
-                           q, x_scale);
+                           q, x_scale, zero_ints, n_zero);
     else
         hipLaunchKernelGGL(k_smooth_quant<float>, grid, block, 0, s,
                            static_cast<const float*>(x), mod, inv_s, static_cast<int>(K), n_mod,
-                           q, x_scale);
+                           q, x_scale, zero_ints, n_zero);
     return hipGetLastError();
 }
 
 template <typename XT, typename LT>
 static void launch_down_t(const void* x, const int32_t* mod, const float* inv_s, const void* ld,
-                          int64_t T, int64_t K, int rank, int n_mod, int kslice, int nks,
-                          float* u, hipStream_t s) {
-    const dim3 grid(static_cast<unsigned>((T + kRowsDown - 1) / kRowsDown), nks), block(256);
+                          int64_t T, int64_t K, int rank, int n_mod, const Workspace& w,
+                          hipStream_t s) {
+    const dim3 grid(static_cast<unsigned>((T + kDownRows - 1) / kDownRows),
+                    static_cast<unsigned>(w.n_kslices)), block(256);
     hipLaunchKernelGGL((k_lowrank_down<XT, LT>), grid, block, 0, s, static_cast<const XT*>(x),
                        mod, inv_s, static_cast<const LT*>(ld), T, static_cast<int>(K), rank,
-                       n_mod, kslice, u);
+                       n_mod, w.kslice, w.n_kslices, w.u, w.u_part, w.tickets);
 }
 
 hipError_t launch_lowrank_down(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, DT lr_dt, int64_t T, int64_t K, int rank,
-                               int n_mod, int kslice, int n_kslices, float* u, hipStream_t s) {
+                               int n_mod, const Workspace& w, hipStream_t s) {
     if (x_dt == DT::BF16) {
-        if (lr_dt == DT::BF16) launch_down_t<bf16_t, bf16_t>(x, mod, inv_s, l_down, T, K, rank, n_mod, kslice, n_kslices, u, s);
-        else launch_down_t<bf16_t, float>(x, mod, inv_s, l_down, T, K, rank, n_mod, kslice, n_kslices, u, s);
+        if (lr_dt == DT::BF16) launch_down_t<bf16_t, bf16_t>(x, mod, inv_s, l_down, T, K, rank, n_mod, w, s);
+        else launch_down_t<bf16_t, float>(x, mod, inv_s, l_down, T, K, rank, n_mod, w, s);
     } else {
-        if (lr_dt == DT::BF16) launch_down_t<float, bf16_t>(x, mod, inv_s, l_down, T, K, rank, n_mod, kslice, n_kslices, u, s);
-        else launch_down_t<float, float>(x, mod, inv_s, l_down, T, K, rank, n_mod, kslice, n_kslices, u, s);
+        if (lr_dt == DT::BF16) launch_down_t<float, bf16_t>(x, mod, inv_s, l_down, T, K, rank, n_mod, w, s);
+        else launch_down_t<float, float>(x, mod, inv_s, l_down, T, K, rank, n_mod, w, s);
     }
     return hipGetLastError();
+}
+
+template <typename YT, typename LT>
+static void launch_gemm_small_t(const int8_t* q, const float* x_scale, const int8_t* wq,
+                                const float* w_scale, int64_t T, int64_t K, int64_t N,
+                                const int32_t* mod, const float* u, int rank, int n_mod,
+                                const void* r_up, int32_t* acc, void* y, hipStream_t s) {
+    hipLaunchKernelGGL((k_gemm_small<YT, LT>), dim3(static_cast<unsigned>(N / 16)), dim3(256), 0, s,
+                       q, wq, x_scale, w_scale, static_cast<int>(T), static_cast<int>(K),
+                       static_cast<int>(N), mod, u, rank, n_mod, static_cast<const LT*>(r_up), acc,
+                       static_cast<YT*>(y));
 }
 
 template <typename YT, typename LT, bool CMC, bool ACC>
@@ -1278,6 +1448,17 @@ hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        const int32_t* mod, const float* u, int rank, int n_mod,
                        const void* r_up, DT lr_dt, bool cmc, int32_t* acc, void* y, DT y_dt,
                        hipStream_t s) {
+    if (T <= kSmallMaxT && K % 64 == 0) {
+        const float* uu = cmc ? u : nullptr;
+        if (y_dt == DT::BF16) {
+            if (lr_dt == DT::BF16) launch_gemm_small_t<bf16_t, bf16_t>(q, x_scale, wq, w_scale, T, K, N, mod, uu, rank, n_mod, r_up, acc, y, s);
+            else launch_gemm_small_t<bf16_t, float>(q, x_scale, wq, w_scale, T, K, N, mod, uu, rank, n_mod, r_up, acc, y, s);
+        } else {
+            if (lr_dt == DT::BF16) launch_gemm_small_t<float, bf16_t>(q, x_scale, wq, w_scale, T, K, N, mod, uu, rank, n_mod, r_up, acc, y, s);
+            else launch_gemm_small_t<float, float>(q, x_scale, wq, w_scale, T, K, N, mod, uu, rank, n_mod, r_up, acc, y, s);
+        }
+        return hipGetLastError();
+    }
 #define MASQ_GEMM(YT, LT, C, A) launch_gemm_t<YT, LT, C, A>(q, x_scale, wq, w_scale, T, K, N, mod, u, rank, n_mod, r_up, acc, y, s)
     // the int32 accumulator output exists only for the plain product (no
     // compensation); it is a separate instantiation because storing the

@@ -165,6 +165,12 @@ _EDGE = {
     "rank0": dict(T=70, K=64, N=64, r=0, M=2, act="f32", lr="f32"),
     "single_modality": dict(T=70, K=64, N=64, r=16, M=1, act="bf16", lr="bf16"),
     "four_modalities": dict(T=260, K=128, N=96, r=16, M=4, act="bf16", lr="bf16"),
+    # small batches split the down-projection along k (ragged last slice)
+    "sliced_down_ragged_k": dict(T=40, K=1552, N=160, r=32, M=3, act="bf16", lr="bf16"),
+    "sliced_down_rank128": dict(T=20, K=1024, N=96, r=128, M=2, act="bf16", lr="bf16"),
+    "sliced_down_fp32": dict(T=9, K=2064, N=48, r=16, M=3, act="f32", lr="f32"),
+    "decode_t16_k4096": dict(T=16, K=4096, N=512, r=64, M=2, act="bf16", lr="bf16"),
+    "decode_t5_alternating": dict(T=5, K=1024, N=272, r=64, M=3, act="bf16", lr="bf16"),
 }
 
 
