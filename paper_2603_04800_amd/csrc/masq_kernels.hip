@@ -373,7 +373,7 @@ template <typename XT> struct DownK<XT, float> {   // fp32 factors: fp32 MFMA
 
 // The 16 x rc block of u (rank columns c0..c0+rc) over k in [kb, ke), summed
 // over the modalities present, written as red-reduced fp32 to out(row, col).
-template <typename XT, typename LT, typename Out>
+template <int NW, typename XT, typename LT, typename Out>
 __device__ __forceinline__ void down_group(const XT* x, const float* inv_s, const LT* l_down,
                                            int64_t row0, int64_t T, int K, int r, int n_mod,
                                            int kb, int ke, int c0, const int* smod,
@@ -384,7 +384,7 @@ __device__ __forceinline__ void down_group(const XT* x, const float* inv_s, cons
     const int ncb = rc >> 4;
     constexpr int step = DownK<XT, LT>::kStep;
     const int span = ke - kb;
-    const int q = ((span + 4 * step - 1) / (4 * step)) * step;   // k per wave, step-aligned
+    const int q = ((span + NW * step - 1) / (NW * step)) * step;  // k per wave, step-aligned
     const int wkb = min(ke, kb + wave * q);
     const int wke = min(ke, wkb + q);
     v4f acc[4];
@@ -403,9 +403,12 @@ __device__ __forceinline__ void down_group(const XT* x, const float* inv_s, cons
         for (int i = 0; i < 4; ++i) red[wave][4 * (lane >> 4) + i][16 * j + (lane & 15)] = acc[j][i];
     }
     __syncthreads();
-    for (int idx = tid; idx < kRowsDown * rc; idx += 256) {
+    for (int idx = tid; idx < kRowsDown * rc; idx += 64 * NW) {
         const int row = idx / rc, col = idx - row * rc;
-        out(row, c0 + col, ((red[0][row][col] + red[1][row][col]) + red[2][row][col]) + red[3][row][col]);
+        float v = red[0][row][col];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) v += red[w][row][col];       // fixed order
+        out(row, c0 + col, v);
     }
     __syncthreads();
 }
@@ -427,8 +430,10 @@ __device__ __forceinline__ unsigned tile_presence(const int* smod) {
 // on tickets[tile], cleared beforehand by the quantisation kernel) adds the
 // partials in slice order, so the result does not depend on timing.  Tiles
 // without non-text rows are skipped (their u rows are never read).
+constexpr int kDownWaves = 8;
+
 template <typename XT, typename LT>
-__global__ __launch_bounds__(256) void k_lowrank_down(const XT* __restrict__ x,
+__global__ __launch_bounds__(64 * kDownWaves) void k_lowrank_down(const XT* __restrict__ x,
                                                       const int32_t* __restrict__ mod,
                                                       const float* __restrict__ inv_s,
                                                       const LT* __restrict__ l_down, int64_t T,
@@ -437,7 +442,7 @@ __global__ __launch_bounds__(256) void k_lowrank_down(const XT* __restrict__ x,
                                                       float* __restrict__ u_part,
                                                       int* __restrict__ tickets) {
     __shared__ int smod[kRowsDown];
-    __shared__ float red[4][kRowsDown][64];
+    __shared__ float red[kDownWaves][kRowsDown][64];
     __shared__ int last;
     const int tid = threadIdx.x;
     const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kRowsDown;
@@ -453,11 +458,11 @@ __global__ __launch_bounds__(256) void k_lowrank_down(const XT* __restrict__ x,
     if (!present) return;                                            // uniform per tile
     float* out = n_kslices > 1 ? u_part + static_cast<int64_t>(s) * T * r : u;
     for (int c0 = 0; c0 < r; c0 += 64)
-        down_group<XT, LT>(x, inv_s, l_down, row0, T, K, r, n_mod, kb, ke, c0, smod, present, red,
-                           [&](int row, int col, float v) {
-                               const int64_t t = row0 + row;
-                               if (t < T) out[t * r + col] = v;
-                           });
+        down_group<kDownWaves, XT, LT>(x, inv_s, l_down, row0, T, K, r, n_mod, kb, ke, c0, smod,
+                                       present, red, [&](int row, int col, float v) {
+                                           const int64_t t = row0 + row;
+                                           if (t < T) out[t * r + col] = v;
+                                       });
     if (n_kslices == 1) return;
 
     __threadfence();                 // this slice's partials are visible device-wide ...
@@ -470,7 +475,7 @@ __global__ __launch_bounds__(256) void k_lowrank_down(const XT* __restrict__ x,
     // are loaded together and added in slice order
     const int rows = static_cast<int>(min<int64_t>(kDownRows, T - row0));
     const int64_t slice = T * r;
-    for (int idx = 4 * tid; idx < rows * r; idx += 4 * 256) {
+    for (int idx = 4 * tid; idx < rows * r; idx += 4 * 64 * kDownWaves) {
         const int64_t e = row0 * r + idx;
         v4f v = *reinterpret_cast<const v4f*>(u_part + e);
         for (int q0 = 1; q0 < n_kslices; q0 += 8) {
@@ -509,8 +514,8 @@ __global__ __launch_bounds__(256) void k_lowrank_comp(const XT* __restrict__ x,
     const unsigned present = tile_presence(smod);
     if (!present) return;
     for (int c0 = 0; c0 < r; c0 += 64)
-        down_group<XT, LT>(x, inv_s, l_down, row0, T, K, r, n_mod, 0, K, c0, smod, present, red,
-                           [&](int row, int col, float v) { su[row][col] = v; });
+        down_group<4, XT, LT>(x, inv_s, l_down, row0, T, K, r, n_mod, 0, K, c0, smod, present, red,
+                              [&](int row, int col, float v) { su[row][col] = v; });
     for (int o = threadIdx.x; o < N; o += 256) {
         for (int i = 0; i < kRowsDown; ++i) {
             const int m = smod[i];
@@ -642,26 +647,48 @@ template <> struct Cmc<float> {           // fp32 operands, v_mfma_f32_32x32x2f3
     static constexpr int kUBytes = kTileM * 256;       // 64 floats per row
     static constexpr int kRBytes = kTileN * 256;
 
+    // 16-byte pieces, 8 per thread in flight: slot idx -> row idx / 16,
+    // piece idx % 16 (pieces past the chunk's rc / 4 are skipped)
     static __device__ __forceinline__ void stage_u(uint8_t* base, const int* s_mod, const float* u,
                                                    int64_t row0, int64_t T, int r, int c0,
                                                    int tid) {
         float* su = reinterpret_cast<float*>(base);
-        const int rc = min(64, r - c0);
-        for (int idx = tid; idx < kTileM * rc; idx += 256) {
-            const int row = idx / rc, k = idx - row * rc;
-            const int64_t t = row0 + row;
-            su[row * 64 + k] = (t < T && s_mod[row] > 0) ? u[t * r + c0 + k] : 0.f;
+        const int nq = min(64, r - c0) >> 2;
+        for (int b = 0; b < kTileM * 16; b += 256 * 8) {
+            v4f v[8];
+#pragma unroll
+            for (int it = 0; it < 8; ++it) {
+                const int idx = b + tid + 256 * it, row = idx >> 4, pc = min(idx & 15, nq - 1);
+                const int64_t t = min(row0 + row, T - 1);
+                v[it] = *reinterpret_cast<const v4f*>(u + t * r + c0 + 4 * pc);
+            }
+#pragma unroll
+            for (int it = 0; it < 8; ++it) {
+                const int idx = b + tid + 256 * it, row = idx >> 4, pc = idx & 15;
+                if (pc >= nq) continue;
+                const bool live = row0 + row < T && s_mod[row] > 0;
+                *reinterpret_cast<v4f*>(su + row * 64 + 4 * pc) = live ? v[it] : v4f{0.f, 0.f, 0.f, 0.f};
+            }
         }
     }
 
     static __device__ __forceinline__ void stage_r(uint8_t* base, const float* rm, int col0, int N,
                                                    int r, int c0, int tid) {
         float* sr = reinterpret_cast<float*>(base);
-        const int rc = min(64, r - c0);
-        for (int idx = tid; idx < kTileN * rc; idx += 256) {
-            const int row = idx / rc, k = idx - row * rc;
-            const int col = min(col0 + row, N - 1);
-            sr[row * 64 + k] = rm[static_cast<int64_t>(col) * r + c0 + k];
+        const int nq = min(64, r - c0) >> 2;
+        for (int b = 0; b < kTileN * 16; b += 256 * 8) {
+            v4f v[8];
+#pragma unroll
+            for (int it = 0; it < 8; ++it) {
+                const int idx = b + tid + 256 * it, row = idx >> 4, pc = min(idx & 15, nq - 1);
+                const int col = min(col0 + row, N - 1);
+                v[it] = *reinterpret_cast<const v4f*>(rm + static_cast<int64_t>(col) * r + c0 + 4 * pc);
+            }
+#pragma unroll
+            for (int it = 0; it < 8; ++it) {
+                const int idx = b + tid + 256 * it, row = idx >> 4, pc = idx & 15;
+                if (pc < nq) *reinterpret_cast<v4f*>(sr + row * 64 + 4 * pc) = v[it];
+            }
         }
     }
 
@@ -1365,7 +1392,8 @@ __global__ __launch_bounds__(256) void k_gemm_small(
 hipError_t launch_smooth_quant(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                int64_t T, int64_t K, int n_mod, int8_t* q, float* x_scale,
                                int* zero_ints, int n_zero, hipStream_t s) {
-    if (T >= kRowsPerWaveMinT) {
+    // a wave per row for large batches whose rows fit its register cache
+    if (T >= kRowsPerWaveMinT && K <= 64 * 8 * 8) {
         const dim3 grid(static_cast<unsigned>((T + 3) / 4)), block(256);
         if (x_dt == DT::BF16)
             hipLaunchKernelGGL((k_smooth_quant_rows<bf16_t, 8>), grid, block, 0, s,
@@ -1394,7 +1422,7 @@ static void launch_down_t(const void* x, const int32_t* mod, const float* inv_s,
                           int64_t T, int64_t K, int rank, int n_mod, const Workspace& w,
                           hipStream_t s) {
     const dim3 grid(static_cast<unsigned>((T + kDownRows - 1) / kDownRows),
-                    static_cast<unsigned>(w.n_kslices)), block(256);
+                    static_cast<unsigned>(w.n_kslices)), block(64 * kDownWaves);
     hipLaunchKernelGGL((k_lowrank_down<XT, LT>), grid, block, 0, s, static_cast<const XT*>(x),
                        mod, inv_s, static_cast<const LT*>(ld), T, static_cast<int>(K), rank,
                        n_mod, w.kslice, w.n_kslices, w.u, w.u_part, w.tickets);
