@@ -18,7 +18,8 @@ static size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255);
 static void plan_kslices(int64_t T, int64_t K, int& n_kslices, int& kslice) {
     const int64_t tiles = T > 0 ? (T + kDownRows - 1) / kDownRows : 1;
     const int64_t steps = (K + kDownStep - 1) / kDownStep;
-    int64_t want = tiles <= 16 ? (512 + tiles - 1) / tiles : 1;
+    int64_t want = small_path(T, K) ? kSmallSlices
+                                    : (tiles <= 16 ? (512 + tiles - 1) / tiles : 1);
     want = want < 1 ? 1 : (want > steps ? steps : want);
     const int64_t per = (steps + want - 1) / want;          // steps per slice
     kslice = static_cast<int>(per * kDownStep);
@@ -48,8 +49,9 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
         w.u = reinterpret_cast<float*>(carve(ur));
         if (w.n_kslices > 1) {
             w.u_part = reinterpret_cast<float*>(carve(ur * static_cast<size_t>(w.n_kslices)));
-            w.tickets = reinterpret_cast<int*>(
-                carve(static_cast<size_t>((T + kDownRows - 1) / kDownRows) * sizeof(int)));
+            if (!small_path(T, K))    // the small-batch GEMM adds the partials itself
+                w.tickets = reinterpret_cast<int*>(
+                    carve(static_cast<size_t>((T + kDownRows - 1) / kDownRows) * sizeof(int)));
         }
     }
     w.bytes = off;
@@ -119,7 +121,12 @@ masq_status fused_stage(const Fused& a, int stage) {
         masq::plan_workspace(a.workspace, a.T, a.c_in, a.c_out, a.rank, a.n_mod);
     hipStream_t s = static_cast<hipStream_t>(a.stream);
     (void)hipGetLastError();
-    if (stage & 1) {
+    if ((stage & 1) && masq::small_path(a.T, a.c_in)) {
+        st = from_hip(masq::launch_stage1_small(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
+                                                a.l_down, to_dt(a.lr_dt), a.T, a.c_in, a.rank,
+                                                a.n_mod, cmc, w, s));
+        if (st != MASQ_OK) return st;
+    } else if (stage & 1) {
         const int n_tickets = w.tickets ? static_cast<int>((a.T + masq::kDownRows - 1) / masq::kDownRows) : 0;
         st = from_hip(masq::launch_smooth_quant(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                 a.T, a.c_in, a.n_mod, w.q, w.x_scale,
@@ -134,8 +141,9 @@ masq_status fused_stage(const Fused& a, int stage) {
     }
     if (stage & 2) {
         st = from_hip(masq::launch_gemm(w.q, w.x_scale, a.wq, a.w_scale, a.T, a.c_in, a.c_out,
-                                        a.modality, w.u, a.rank, a.n_mod, a.r_up, to_dt(a.lr_dt),
-                                        cmc, nullptr, a.y, to_dt(a.y_dt), s));
+                                        a.modality, w.u, w.u_part, w.n_kslices, a.rank, a.n_mod,
+                                        a.r_up, to_dt(a.lr_dt), cmc, nullptr, a.y, to_dt(a.y_dt),
+                                        s));
     }
     return st;
 }
@@ -193,7 +201,7 @@ masq_status masq_w8a8_gemm(const int8_t* q, const float* x_scale, const int8_t* 
     if (T == 0) return MASQ_OK;
     (void)hipGetLastError();
     return from_hip(masq::launch_gemm(q, x_scale, wq, w_scale, T, c_in, c_out, nullptr, nullptr,
-                                      0, 1, nullptr, DT::BF16, false, acc, y, to_dt(y_dt),
+                                      nullptr, 1, 0, 1, nullptr, DT::BF16, false, acc, y, to_dt(y_dt),
                                       static_cast<hipStream_t>(stream)));
 }
 

@@ -16,6 +16,12 @@ constexpr int kRowsDown = 16;     // rows per down-projection tile
 constexpr int kDownRows = kRowsDown;
 constexpr int kDownStep = 512;    // k granularity of a down-projection slice (128 per wave)
 constexpr int kMaxRank = 256;
+constexpr int kSmallMaxT = 16;    // batches this small use the Wq-streaming GEMM
+constexpr int kSmallSlices = 8;   // down-projection k slices summed by that GEMM
+
+// The small-batch path: the Wq-streaming GEMM, which also adds the
+// down-projection's k-slice partials itself.
+inline bool small_path(int64_t T, int64_t K) { return T <= kSmallMaxT && K % 64 == 0; }
 constexpr int64_t kRowsPerWaveMinT = 256;   // batches this large quantise one row per wave
 
 enum class DT : int { F32 = 0, BF16 = 1 };
@@ -60,11 +66,19 @@ hipError_t launch_lowrank_down(const void* x, DT x_dt, const int32_t* mod, const
                                const void* l_down, DT lr_dt, int64_t T, int64_t K, int rank,
                                int n_mod, const Workspace& w, hipStream_t s);
 
+// Stage 1 of the small-batch path (small_path): quantisation of every row
+// and the k-sliced down-projection (partials) in one launch.
+hipError_t launch_stage1_small(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
+                               const void* l_down, DT lr_dt, int64_t T, int64_t K, int rank,
+                               int n_mod, bool cmc, const Workspace& w, hipStream_t s);
+
+// u: the down-projection; on the small-batch path (small_path) with
+// n_kslices > 1 the GEMM adds the slice partials u_part itself.
 hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        const float* w_scale, int64_t T, int64_t K, int64_t N,
-                       const int32_t* mod, const float* u, int rank, int n_mod,
-                       const void* r_up, DT lr_dt, bool cmc, int32_t* acc, void* y, DT y_dt,
-                       hipStream_t s);
+                       const int32_t* mod, const float* u, const float* u_part, int n_kslices,
+                       int rank, int n_mod, const void* r_up, DT lr_dt, bool cmc, int32_t* acc,
+                       void* y, DT y_dt, hipStream_t s);
 
 hipError_t launch_lowrank_comp(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, const void* r_up, DT lr_dt, int64_t T,

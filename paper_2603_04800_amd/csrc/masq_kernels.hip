@@ -104,36 +104,33 @@ __device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
 // absmax and the quantisation; a longer row streams its remainder twice.
 constexpr int kSqChunks = 10;
 
-template <typename XT>
-__global__ __launch_bounds__(256) void k_smooth_quant(const XT* __restrict__ x,
-                                                      const int32_t* __restrict__ mod,
-                                                      const float* __restrict__ inv_s, int K,
-                                                      int n_mod, int8_t* __restrict__ q,
-                                                      float* __restrict__ x_scale,
-                                                      int* __restrict__ zero_ints, int n_zero) {
-    __shared__ float red[4];
-    const int64_t t = blockIdx.x;
-    if (blockIdx.x == 0)
-        for (int i = threadIdx.x; i < n_zero; i += 256) zero_ints[i] = 0;
+// Row t quantised by a workgroup of NT threads keeping NT x 8 x NCH elements
+// of the row in registers.
+template <typename XT, int NT, int NCH>
+__device__ __forceinline__ void sq_row(const XT* __restrict__ x, const int32_t* __restrict__ mod,
+                                       const float* __restrict__ inv_s, int K, int n_mod,
+                                       int8_t* __restrict__ q, float* __restrict__ x_scale,
+                                       int64_t t) {
+    __shared__ float red[NT / 64];
     const int m = sane_mod(mod[t], n_mod);
     const XT* xr = x + t * static_cast<int64_t>(K);
     const float* sr = inv_s + static_cast<int64_t>(m) * K;
     int8_t* qr = q + t * static_cast<int64_t>(K);
     const int nv = K >> 3;
 
-    float xs[kSqChunks][8];
+    float xs[NCH][8];
     float amax = 0.f;
     {
-        float xv[kSqChunks][8], sv[kSqChunks][8];
+        float xv[NCH][8], sv[NCH][8];
 #pragma unroll
-        for (int c = 0; c < kSqChunks; ++c) {
-            const int v = min(static_cast<int>(threadIdx.x) + 256 * c, nv - 1);   // clamped
+        for (int c = 0; c < NCH; ++c) {
+            const int v = min(static_cast<int>(threadIdx.x) + NT * c, nv - 1);   // clamped
             Elem<XT>::load8(xr + 8 * v, xv[c]);
             load8_f32(sr + 8 * v, sv[c]);
         }
 #pragma unroll
-        for (int c = 0; c < kSqChunks; ++c) {
-            const bool in = static_cast<int>(threadIdx.x) + 256 * c < nv;
+        for (int c = 0; c < NCH; ++c) {
+            const bool in = static_cast<int>(threadIdx.x) + NT * c < nv;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 xs[c][j] = xv[c][j] * sv[c][j];
@@ -141,7 +138,7 @@ __global__ __launch_bounds__(256) void k_smooth_quant(const XT* __restrict__ x,
             }
         }
     }
-    for (int v = threadIdx.x + 256 * kSqChunks; v < nv; v += 256) {
+    for (int v = threadIdx.x + NT * NCH; v < nv; v += NT) {
         float xv[8], sv[8];
         Elem<XT>::load8(xr + 8 * v, xv);
         load8_f32(sr + 8 * v, sv);
@@ -151,7 +148,9 @@ __global__ __launch_bounds__(256) void k_smooth_quant(const XT* __restrict__ x,
     amax = wave_max(amax);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = amax;
     __syncthreads();
-    amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    amax = red[0];
+#pragma unroll
+    for (int w = 1; w < NT / 64; ++w) amax = fmaxf(amax, red[w]);
 
     const bool nz = amax > 0.f;
     const float dx = nz ? amax / 127.0f : 0.f;     // correctly rounded
@@ -172,11 +171,11 @@ __global__ __launch_bounds__(256) void k_smooth_quant(const XT* __restrict__ x,
         *reinterpret_cast<v2i*>(qr + 8 * v) = out;
     };
 #pragma unroll
-    for (int c = 0; c < kSqChunks; ++c) {
-        const int v = static_cast<int>(threadIdx.x) + 256 * c;
+    for (int c = 0; c < NCH; ++c) {
+        const int v = static_cast<int>(threadIdx.x) + NT * c;
         if (v < nv) put8(v, xs[c]);
     }
-    for (int v = threadIdx.x + 256 * kSqChunks; v < nv; v += 256) {
+    for (int v = threadIdx.x + NT * NCH; v < nv; v += NT) {
         float xv[8], sv[8], val[8];
         Elem<XT>::load8(xr + 8 * v, xv);
         load8_f32(sr + 8 * v, sv);
@@ -184,6 +183,18 @@ __global__ __launch_bounds__(256) void k_smooth_quant(const XT* __restrict__ x,
         for (int j = 0; j < 8; ++j) val[j] = xv[j] * sv[j];
         put8(v, val);
     }
+}
+
+template <typename XT>
+__global__ __launch_bounds__(256) void k_smooth_quant(const XT* __restrict__ x,
+                                                      const int32_t* __restrict__ mod,
+                                                      const float* __restrict__ inv_s, int K,
+                                                      int n_mod, int8_t* __restrict__ q,
+                                                      float* __restrict__ x_scale,
+                                                      int* __restrict__ zero_ints, int n_zero) {
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < n_zero; i += 256) zero_ints[i] = 0;
+    sq_row<XT, 256, kSqChunks>(x, mod, inv_s, K, n_mod, q, x_scale, blockIdx.x);
 }
 
 __device__ __forceinline__ void split_bf16x8(const float (&v)[8], v4i& hi, v4i& lo) {
@@ -433,20 +444,17 @@ __device__ __forceinline__ unsigned tile_presence(const int* smod) {
 constexpr int kDownWaves = 8;
 
 template <typename XT, typename LT>
-__global__ __launch_bounds__(64 * kDownWaves) void k_lowrank_down(const XT* __restrict__ x,
-                                                      const int32_t* __restrict__ mod,
-                                                      const float* __restrict__ inv_s,
-                                                      const LT* __restrict__ l_down, int64_t T,
-                                                      int K, int r, int n_mod, int kslice,
-                                                      int n_kslices, float* __restrict__ u,
-                                                      float* __restrict__ u_part,
-                                                      int* __restrict__ tickets) {
+__device__ __forceinline__ void down_tile(const XT* __restrict__ x, const int32_t* __restrict__ mod,
+                                          const float* __restrict__ inv_s,
+                                          const LT* __restrict__ l_down, int64_t T, int K, int r,
+                                          int n_mod, int kslice, int n_kslices,
+                                          float* __restrict__ u, float* __restrict__ u_part,
+                                          int* __restrict__ tickets, int tile, int s) {
     __shared__ int smod[kRowsDown];
     __shared__ float red[kDownWaves][kRowsDown][64];
     __shared__ int last;
     const int tid = threadIdx.x;
-    const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kRowsDown;
-    const int s = blockIdx.y;
+    const int64_t row0 = static_cast<int64_t>(tile) * kRowsDown;
     const int kb = s * kslice;
     const int ke = min(K, kb + kslice);
     if (tid < kRowsDown) {
@@ -463,11 +471,11 @@ __global__ __launch_bounds__(64 * kDownWaves) void k_lowrank_down(const XT* __re
                                            const int64_t t = row0 + row;
                                            if (t < T) out[t * r + col] = v;
                                        });
-    if (n_kslices == 1) return;
+    if (n_kslices == 1 || tickets == nullptr) return;   // the consumer adds the partials
 
     __threadfence();                 // this slice's partials are visible device-wide ...
     __syncthreads();
-    if (tid == 0) last = atomicAdd(&tickets[blockIdx.x], 1) == n_kslices - 1;
+    if (tid == 0) last = atomicAdd(&tickets[tile], 1) == n_kslices - 1;
     __syncthreads();
     if (!last) return;
     __threadfence();                 // ... before the last arrival reads them all
@@ -490,6 +498,36 @@ __global__ __launch_bounds__(64 * kDownWaves) void k_lowrank_down(const XT* __re
                 if (q0 + k < n_kslices) v += part[k];
         }
         *reinterpret_cast<v4f*>(u + e) = v;
+    }
+}
+
+template <typename XT, typename LT>
+__global__ __launch_bounds__(64 * kDownWaves) void k_lowrank_down(const XT* __restrict__ x,
+                                                      const int32_t* __restrict__ mod,
+                                                      const float* __restrict__ inv_s,
+                                                      const LT* __restrict__ l_down, int64_t T,
+                                                      int K, int r, int n_mod, int kslice,
+                                                      int n_kslices, float* __restrict__ u,
+                                                      float* __restrict__ u_part,
+                                                      int* __restrict__ tickets) {
+    down_tile<XT, LT>(x, mod, inv_s, l_down, T, K, r, n_mod, kslice, n_kslices, u, u_part, tickets,
+                      blockIdx.x, blockIdx.y);
+}
+
+// Stage 1 of the small-batch path in one launch: workgroups [0, T) quantise
+// one row each, workgroups [T, T + n_kslices) compute one k slice of the
+// down-projection (partials left for the GEMM to add).
+template <typename XT, typename LT>
+__global__ __launch_bounds__(64 * kDownWaves) void k_stage1_small(
+    const XT* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
+    const LT* __restrict__ l_down, int T, int K, int r, int n_mod, int kslice, int n_kslices,
+    int8_t* __restrict__ q, float* __restrict__ x_scale, float* __restrict__ u,
+    float* __restrict__ u_part) {
+    if (static_cast<int>(blockIdx.x) < T) {
+        sq_row<XT, 64 * kDownWaves, kSqChunks / 2>(x, mod, inv_s, K, n_mod, q, x_scale, blockIdx.x);
+    } else if (l_down != nullptr) {
+        down_tile<XT, LT>(x, mod, inv_s, l_down, T, K, r, n_mod, kslice, n_kslices, u, u_part,
+                          nullptr, 0, blockIdx.x - T);
     }
 }
 
@@ -1317,16 +1355,16 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dma(
 // per-wave int32 partials are added in a fixed order in LDS (exact), then
 // each thread finishes one (token, channel): dequantisation, the rank-r
 // compensation u L2^m in fp32 for non-text tokens, and the store.
-constexpr int kSmallMaxT = 16;
 constexpr int kSmallDepth = 16;
 
 template <typename YT, typename LT>
 __global__ __launch_bounds__(256) void k_gemm_small(
     const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
     const float* __restrict__ w_scale, int T, int K, int N, const int32_t* __restrict__ mod,
-    const float* __restrict__ u, int r, int n_mod, const LT* __restrict__ r_up,
-    int32_t* __restrict__ acc_out, YT* __restrict__ y) {
+    const float* __restrict__ u, const float* __restrict__ u_part, int n_kslices, int r,
+    int n_mod, const LT* __restrict__ r_up, int32_t* __restrict__ acc_out, YT* __restrict__ y) {
     __shared__ int part[4][16][16];
+    __shared__ float su[kSmallMaxT][kMaxRank];     // u rows of the batch
     const int tid = threadIdx.x, lane = tid & 63;
     // wave-uniform k range (scalar registers), so the loop below branches on
     // it: MFMA instructions ignore EXEC and must not sit under a lane mask
@@ -1361,6 +1399,26 @@ __global__ __launch_bounds__(256) void k_gemm_small(
     // acc[e]: token 4 (lane / 16) + e, channel col0 + lane % 16
 #pragma unroll
     for (int e = 0; e < 4; ++e) part[wave][4 * (lane >> 4) + e][lane & 15] = acc[e];
+    // u of the batch's rows into LDS, adding the k-slice partials in slice
+    // order when the down-projection left them separate
+    if (u != nullptr) {
+        const bool parts = u_part != nullptr && n_kslices > 1;
+        const float* src = parts ? u_part : u;
+        const int slices = parts ? n_kslices : 1;
+        for (int idx = 4 * tid; idx < T * r; idx += 4 * 256) {       // T r % 16 == 0
+            v4f p[kSmallSlices];
+#pragma unroll
+            for (int q = 0; q < kSmallSlices; ++q)                       // all loads in flight
+                p[q] = *reinterpret_cast<const v4f*>(
+                    src + static_cast<int64_t>(min(q, slices - 1)) * T * r + idx);
+            v4f v = p[0];
+#pragma unroll
+            for (int q = 1; q < kSmallSlices; ++q)
+                if (q < slices) v += p[q];                               // slice order
+            const int tt = idx / r, c = idx - tt * r;
+            *reinterpret_cast<v4f*>(&su[tt][c]) = v;
+        }
+    }
     __syncthreads();
     const int t = tid >> 4, o = tid & 15;
     if (t >= T) return;
@@ -1371,12 +1429,12 @@ __global__ __launch_bounds__(256) void k_gemm_small(
     float v = (static_cast<float>(a) * x_scale[t]) * w_scale[ch];
     const int m = (u != nullptr) ? sane_mod(mod[t], n_mod) : 0;
     if (m > 0) {
-        const float* ur = u + static_cast<int64_t>(t) * r;
         const LT* rr = r_up + (static_cast<int64_t>(m - 1) * N + ch) * r;
         float c = 0.f;
         for (int k0 = 0; k0 < r; k0 += 8) {
             float uv[8], rv[8];
-            load8_f32(ur + k0, uv);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) uv[k] = su[t][k0 + k];
             Elem<LT>::load8(rr + k0, rv);
 #pragma unroll
             for (int k = 0; k < 8; ++k) c = fmaf(uv[k], rv[k], c);
@@ -1441,15 +1499,40 @@ hipError_t launch_lowrank_down(const void* x, DT x_dt, const int32_t* mod, const
     return hipGetLastError();
 }
 
+template <typename XT, typename LT>
+static void launch_stage1_small_t(const void* x, const int32_t* mod, const float* inv_s,
+                                  const void* ld, int64_t T, int64_t K, int rank, int n_mod,
+                                  bool cmc, const Workspace& w, hipStream_t s) {
+    const unsigned blocks = static_cast<unsigned>(T + (cmc ? w.n_kslices : 0));
+    hipLaunchKernelGGL((k_stage1_small<XT, LT>), dim3(blocks), dim3(64 * kDownWaves), 0, s,
+                       static_cast<const XT*>(x), mod, inv_s, cmc ? static_cast<const LT*>(ld) : nullptr,
+                       static_cast<int>(T), static_cast<int>(K), rank, n_mod, w.kslice, w.n_kslices,
+                       w.q, w.x_scale, w.u, w.u_part);
+}
+
+hipError_t launch_stage1_small(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
+                               const void* l_down, DT lr_dt, int64_t T, int64_t K, int rank,
+                               int n_mod, bool cmc, const Workspace& w, hipStream_t s) {
+    if (x_dt == DT::BF16) {
+        if (lr_dt == DT::BF16) launch_stage1_small_t<bf16_t, bf16_t>(x, mod, inv_s, l_down, T, K, rank, n_mod, cmc, w, s);
+        else launch_stage1_small_t<bf16_t, float>(x, mod, inv_s, l_down, T, K, rank, n_mod, cmc, w, s);
+    } else {
+        if (lr_dt == DT::BF16) launch_stage1_small_t<float, bf16_t>(x, mod, inv_s, l_down, T, K, rank, n_mod, cmc, w, s);
+        else launch_stage1_small_t<float, float>(x, mod, inv_s, l_down, T, K, rank, n_mod, cmc, w, s);
+    }
+    return hipGetLastError();
+}
+
 template <typename YT, typename LT>
 static void launch_gemm_small_t(const int8_t* q, const float* x_scale, const int8_t* wq,
                                 const float* w_scale, int64_t T, int64_t K, int64_t N,
-                                const int32_t* mod, const float* u, int rank, int n_mod,
-                                const void* r_up, int32_t* acc, void* y, hipStream_t s) {
+                                const int32_t* mod, const float* u, const float* u_part,
+                                int n_kslices, int rank, int n_mod, const void* r_up, int32_t* acc,
+                                void* y, hipStream_t s) {
     hipLaunchKernelGGL((k_gemm_small<YT, LT>), dim3(static_cast<unsigned>(N / 16)), dim3(256), 0, s,
                        q, wq, x_scale, w_scale, static_cast<int>(T), static_cast<int>(K),
-                       static_cast<int>(N), mod, u, rank, n_mod, static_cast<const LT*>(r_up), acc,
-                       static_cast<YT*>(y));
+                       static_cast<int>(N), mod, u, u_part, n_kslices, rank, n_mod,
+                       static_cast<const LT*>(r_up), acc, static_cast<YT*>(y));
 }
 
 template <typename YT, typename LT, bool CMC, bool ACC>
@@ -1473,18 +1556,20 @@ static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* w
 
 hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        const float* w_scale, int64_t T, int64_t K, int64_t N,
-                       const int32_t* mod, const float* u, int rank, int n_mod,
-                       const void* r_up, DT lr_dt, bool cmc, int32_t* acc, void* y, DT y_dt,
-                       hipStream_t s) {
-    if (T <= kSmallMaxT && K % 64 == 0) {
+                       const int32_t* mod, const float* u, const float* u_part, int n_kslices,
+                       int rank, int n_mod, const void* r_up, DT lr_dt, bool cmc, int32_t* acc,
+                       void* y, DT y_dt, hipStream_t s) {
+    if (small_path(T, K)) {
         const float* uu = cmc ? u : nullptr;
+#define MASQ_SMALL(YT, LT) launch_gemm_small_t<YT, LT>(q, x_scale, wq, w_scale, T, K, N, mod, uu, u_part, n_kslices, rank, n_mod, r_up, acc, y, s)
         if (y_dt == DT::BF16) {
-            if (lr_dt == DT::BF16) launch_gemm_small_t<bf16_t, bf16_t>(q, x_scale, wq, w_scale, T, K, N, mod, uu, rank, n_mod, r_up, acc, y, s);
-            else launch_gemm_small_t<bf16_t, float>(q, x_scale, wq, w_scale, T, K, N, mod, uu, rank, n_mod, r_up, acc, y, s);
+            if (lr_dt == DT::BF16) MASQ_SMALL(bf16_t, bf16_t);
+            else MASQ_SMALL(bf16_t, float);
         } else {
-            if (lr_dt == DT::BF16) launch_gemm_small_t<float, bf16_t>(q, x_scale, wq, w_scale, T, K, N, mod, uu, rank, n_mod, r_up, acc, y, s);
-            else launch_gemm_small_t<float, float>(q, x_scale, wq, w_scale, T, K, N, mod, uu, rank, n_mod, r_up, acc, y, s);
+            if (lr_dt == DT::BF16) MASQ_SMALL(float, bf16_t);
+            else MASQ_SMALL(float, float);
         }
+#undef MASQ_SMALL
         return hipGetLastError();
     }
 #define MASQ_GEMM(YT, LT, C, A) launch_gemm_t<YT, LT, C, A>(q, x_scale, wq, w_scale, T, K, N, mod, u, rank, n_mod, r_up, acc, y, s)
