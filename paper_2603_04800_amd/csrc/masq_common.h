@@ -17,7 +17,7 @@ constexpr int kDownRows = kRowsDown;
 constexpr int kDownStep = 512;    // k granularity of a down-projection slice (128 per wave)
 constexpr int kMaxRank = 256;
 constexpr int kSmallMaxT = 16;    // batches this small use the Wq-streaming GEMM
-constexpr int kSmallSlices = 8;   // down-projection k slices summed by that GEMM
+constexpr int kSmallSlices = 32;  // down-projection k slices summed by that GEMM
 
 // The small-batch path: the Wq-streaming GEMM, which also adds the
 // down-projection's k-slice partials itself.

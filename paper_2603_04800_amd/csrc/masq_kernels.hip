@@ -1406,15 +1406,17 @@ __global__ __launch_bounds__(256) void k_gemm_small(
         const float* src = parts ? u_part : u;
         const int slices = parts ? n_kslices : 1;
         for (int idx = 4 * tid; idx < T * r; idx += 4 * 256) {       // T r % 16 == 0
-            v4f p[kSmallSlices];
+            v4f v = {0.f, 0.f, 0.f, 0.f};
+            for (int q0 = 0; q0 < slices; q0 += 8) {
+                v4f p[8];
 #pragma unroll
-            for (int q = 0; q < kSmallSlices; ++q)                       // all loads in flight
-                p[q] = *reinterpret_cast<const v4f*>(
-                    src + static_cast<int64_t>(min(q, slices - 1)) * T * r + idx);
-            v4f v = p[0];
+                for (int q = 0; q < 8; ++q)                              // 8 loads in flight
+                    p[q] = *reinterpret_cast<const v4f*>(
+                        src + static_cast<int64_t>(min(q0 + q, slices - 1)) * T * r + idx);
 #pragma unroll
-            for (int q = 1; q < kSmallSlices; ++q)
-                if (q < slices) v += p[q];                               // slice order
+                for (int q = 0; q < 8; ++q)
+                    if (q0 + q < slices) v = (q0 + q == 0) ? p[q] : v + p[q];   // slice order
+            }
             const int tt = idx / r, c = idx - tt * r;
             *reinterpret_cast<v4f*>(&su[tt][c]) = v;
         }
