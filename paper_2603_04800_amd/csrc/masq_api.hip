@@ -126,6 +126,11 @@ masq_status fused_stage(const Fused& a, int stage) {
                                                 a.l_down, to_dt(a.lr_dt), a.T, a.c_in, a.rank,
                                                 a.n_mod, cmc, w, s));
         if (st != MASQ_OK) return st;
+    } else if ((stage & 1) && cmc && masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt))) {
+        st = from_hip(masq::launch_stage1_fused(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
+                                                a.l_down, a.T, a.c_in, a.rank, a.n_mod, w.q,
+                                                w.x_scale, w.u, s));
+        if (st != MASQ_OK) return st;
     } else if (stage & 1) {
         const int n_tickets = w.tickets ? static_cast<int>((a.T + masq::kDownRows - 1) / masq::kDownRows) : 0;
         st = from_hip(masq::launch_smooth_quant(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,

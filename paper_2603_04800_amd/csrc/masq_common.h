@@ -66,6 +66,15 @@ hipError_t launch_lowrank_down(const void* x, DT x_dt, const int32_t* mod, const
                                const void* l_down, DT lr_dt, int64_t T, int64_t K, int rank,
                                int n_mod, const Workspace& w, hipStream_t s);
 
+// Stage 1 in one kernel for bf16 factors and rank <= 64 (fused_stage1_ok):
+// smoothing, quantisation and the down-projection, reading each row once.
+inline bool fused_stage1_ok(int64_t T, int64_t K, int rank, DT lr_dt) {
+    return !small_path(T, K) && lr_dt == DT::BF16 && rank > 0 && rank <= 64;
+}
+hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
+                               const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
+                               int8_t* q, float* x_scale, float* u, hipStream_t s);
+
 // Stage 1 of the small-batch path (small_path): quantisation of every row
 // and the k-sliced down-projection (partials) in one launch.
 hipError_t launch_stage1_small(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,

@@ -531,6 +531,171 @@ __global__ __launch_bounds__(64 * kDownWaves) void k_stage1_small(
     }
 }
 
+// ================================================================ fused stage 1
+// Smoothing, per-token quantisation and the down-projection in one kernel
+// (bf16 factors, rank <= 64, batches above the small path).  A workgroup
+// takes 16 rows; its 8 waves split K.  Pass 1 streams the rows once: each
+// wave keeps the absmax of its part of every row and accumulates u on
+// bf16 MFMA (hi/lo split of the smoothed values, rows masked to each
+// non-text modality present).  Absmax and u are combined across waves in
+// LDS in a fixed order.  Pass 2 re-reads the wave's part (from cache) and
+// writes the int8 codes with the row's reciprocal scale.
+constexpr int kFuseWaves = 8;
+
+template <typename XT>
+__global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
+    const XT* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
+    const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod,
+    int8_t* __restrict__ q, float* __restrict__ x_scale, float* __restrict__ u) {
+    __shared__ int smod[kRowsDown];
+    __shared__ float samax[kFuseWaves][kRowsDown];
+    __shared__ float red[kFuseWaves][kRowsDown][64];
+    __shared__ float srq[kRowsDown];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kRowsDown;
+    if (tid < kRowsDown) {
+        const int64_t t = row0 + tid;
+        smod[tid] = t < T ? sane_mod(mod[t], n_mod) : 0;
+    }
+    __syncthreads();
+    // non-text modalities present in the tile, as a list (scalar registers:
+    // the MFMA loop below must branch on it, MFMA ignores EXEC)
+    const unsigned present = static_cast<unsigned>(
+        __builtin_amdgcn_readfirstlane(static_cast<int>(tile_presence(smod))));
+    int mods[3] = {0, 0, 0};
+    int np = 0;
+    for (int m = 1; m < n_mod; ++m)
+        if (present & (1u << m)) mods[np++] = m;
+    const int ncb = r >> 4;                                   // 16-column MFMA blocks (<= 4)
+
+    constexpr int kStep = 32, kU = 2;
+    const int per = ((K + kFuseWaves * kStep - 1) / (kFuseWaves * kStep)) * kStep;
+    const int kb = min(K, wave * per), ke = min(K, kb + per);
+    const int ar = lane & 15, kg = lane >> 4;
+    const int64_t t = row0 + ar;
+    const bool valid = t < T;
+    const int mrow = smod[ar];
+    const XT* xrow = x + (valid ? t : row0) * static_cast<int64_t>(K);
+    const float* srow = inv_s + static_cast<int64_t>(mrow) * K;
+
+    v4f acc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = v4f{0.f, 0.f, 0.f, 0.f};
+    float amax = 0.f;
+    const v4i zero = {0, 0, 0, 0};
+    for (int k0 = kb; k0 < ke; k0 += kStep * kU) {
+        float xv[kU][8], sv[kU][8];
+        bool ok[kU];
+#pragma unroll
+        for (int uu = 0; uu < kU; ++uu) {
+            const int k = k0 + kStep * uu + 8 * kg;
+            ok[uu] = k < ke;
+            const int kc = ok[uu] ? k : ke - 8;
+            Elem<XT>::load8(xrow + kc, xv[uu]);
+            load8_f32(srow + kc, sv[uu]);
+        }
+        v4i hi[kU], lo[kU];
+#pragma unroll
+        for (int uu = 0; uu < kU; ++uu) {
+            float xs[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                xs[e] = xv[uu][e] * sv[uu][e];
+                if (valid && ok[uu]) amax = fmaxf(amax, fabsf(xs[e]));
+            }
+            split_bf16x8(xs, hi[uu], lo[uu]);
+        }
+        for (int p = 0; p < np; ++p) {                        // usually one modality
+            const bf16_t* lm = l_down + static_cast<int64_t>(mods[p] - 1) * r * K;
+            v4i bv[kU][4];
+#pragma unroll
+            for (int uu = 0; uu < kU; ++uu) {
+                const int k = k0 + kStep * uu + 8 * kg;
+                const int kc = ok[uu] ? k : ke - 8;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    bv[uu][j] = *reinterpret_cast<const v4i*>(
+                        lm + static_cast<int64_t>(16 * min(j, ncb - 1) + ar) * K + kc);
+            }
+            const bool mine = valid && mrow == mods[p];
+#pragma unroll
+            for (int uu = 0; uu < kU; ++uu) {
+                const bool use = mine && ok[uu];
+                const v4i h = use ? hi[uu] : zero, l = use ? lo[uu] : zero;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (j >= ncb) break;
+                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(v8bf, h), __builtin_bit_cast(v8bf, bv[uu][j]), acc[j], 0, 0, 0);
+                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(v8bf, l), __builtin_bit_cast(v8bf, bv[uu][j]), acc[j], 0, 0, 0);
+                }
+            }
+        }
+    }
+    // the four lanes of a row (lane % 16) hold its four k groups
+    amax = fmaxf(amax, __shfl_xor(amax, 16));
+    amax = fmaxf(amax, __shfl_xor(amax, 32));
+    if (lane < 16) samax[wave][lane] = amax;
+    if (np > 0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (j >= ncb) break;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) red[wave][4 * (lane >> 4) + i][16 * j + (lane & 15)] = acc[j][i];
+        }
+    }
+    __syncthreads();
+    if (tid < kRowsDown) {
+        float a = samax[0][tid];
+#pragma unroll
+        for (int w = 1; w < kFuseWaves; ++w) a = fmaxf(a, samax[w][tid]);
+        const bool nz = a > 0.f;
+        srq[tid] = nz ? 127.0f / a : 0.f;                     // correctly rounded
+        if (row0 + tid < T) x_scale[row0 + tid] = nz ? a / 127.0f : 0.f;
+    }
+    if (np > 0) {
+        for (int idx = tid; idx < kRowsDown * r; idx += 64 * kFuseWaves) {
+            const int row = idx / r, col = idx - row * r;
+            if (row0 + row >= T) continue;
+            float v = red[0][row][col];
+#pragma unroll
+            for (int w = 1; w < kFuseWaves; ++w) v += red[w][row][col];   // fixed order
+            u[(row0 + row) * r + col] = v;
+        }
+    }
+    __syncthreads();
+
+    // pass 2: lane -> row lane / 4, 16 consecutive elements at 16 (lane % 4)
+    const int qr = lane >> 2, qc = 16 * (lane & 3);
+    const int64_t tq = row0 + qr;
+    if (tq < T) {
+        const float rq = srq[qr];
+        const XT* xr2 = x + tq * static_cast<int64_t>(K);
+        const float* sr2 = inv_s + static_cast<int64_t>(smod[qr]) * K;
+        int8_t* qrow = q + tq * static_cast<int64_t>(K);
+        for (int k0 = kb; k0 < ke; k0 += 64) {
+            const int k = k0 + qc;
+            if (k >= ke) continue;
+            float xv[16], sv[16];
+            Elem<XT>::load8(xr2 + k, *reinterpret_cast<float(*)[8]>(xv));
+            Elem<XT>::load8(xr2 + k + 8, *reinterpret_cast<float(*)[8]>(xv + 8));
+            load8_f32(sr2 + k, *reinterpret_cast<float(*)[8]>(sv));
+            load8_f32(sr2 + k + 8, *reinterpret_cast<float(*)[8]>(sv + 8));
+            uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                float c = rintf((xv[e] * sv[e]) * rq);
+                c = fminf(fmaxf(c, -127.0f), 127.0f);
+                w[e >> 2] |= (static_cast<uint32_t>(static_cast<int32_t>(c)) & 0xFFu) << (8 * (e & 3));
+            }
+            *reinterpret_cast<v4i*>(qrow + k) = v4i{static_cast<int32_t>(w[0]), static_cast<int32_t>(w[1]),
+                                                    static_cast<int32_t>(w[2]), static_cast<int32_t>(w[3])};
+        }
+    }
+}
+
 // ================================================================ standalone CMC
 template <typename XT, typename LT, typename YT>
 __global__ __launch_bounds__(256) void k_lowrank_comp(const XT* __restrict__ x,
@@ -1498,6 +1663,21 @@ hipError_t launch_lowrank_down(const void* x, DT x_dt, const int32_t* mod, const
         if (lr_dt == DT::BF16) launch_down_t<float, bf16_t>(x, mod, inv_s, l_down, T, K, rank, n_mod, w, s);
         else launch_down_t<float, float>(x, mod, inv_s, l_down, T, K, rank, n_mod, w, s);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
+                               const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
+                               int8_t* q, float* x_scale, float* u, hipStream_t s) {
+    const dim3 grid(static_cast<unsigned>((T + kRowsDown - 1) / kRowsDown)), block(64 * kFuseWaves);
+    if (x_dt == DT::BF16)
+        hipLaunchKernelGGL(k_stage1_fused<bf16_t>, grid, block, 0, s, static_cast<const bf16_t*>(x),
+                           mod, inv_s, static_cast<const bf16_t*>(l_down), T, static_cast<int>(K),
+                           rank, n_mod, q, x_scale, u);
+    else
+        hipLaunchKernelGGL(k_stage1_fused<float>, grid, block, 0, s, static_cast<const float*>(x),
+                           mod, inv_s, static_cast<const bf16_t*>(l_down), T, static_cast<int>(K),
+                           rank, n_mod, q, x_scale, u);
     return hipGetLastError();
 }
 
