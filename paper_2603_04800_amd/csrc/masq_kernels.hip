@@ -756,24 +756,26 @@ template <> struct Cmc<bf16_t> {          // bf16 operands, v_mfma_f32_32x32x16_
     // All of a thread's global loads are issued before any is consumed (from
     // clamped, always valid addresses; unused values are replaced by zeros),
     // so the staging pays the memory latency once rather than per row.
+    template <int NT>
     static __device__ __forceinline__ void stage_u(uint8_t* su, const int* s_mod, const float* u,
                                                    int64_t row0, int64_t T, int r, int c0,
                                                    int tid) {
+        constexpr int kIt = 8 * 256 / NT, kRowStep = NT / 8;
         const int nch = min(64, r - c0) >> 3;
         const int ch = tid & 7;
         const int chc = min(ch, nch - 1);
-        v4f va[8], vb[8];
+        v4f va[kIt], vb[kIt];
 #pragma unroll
-        for (int it = 0; it < 8; ++it) {
-            const int row = (tid >> 3) + 32 * it;
+        for (int it = 0; it < kIt; ++it) {
+            const int row = (tid >> 3) + kRowStep * it;
             const int64_t t = min(row0 + row, T - 1);
             const float* src = u + t * r + c0 + 8 * chc;
             va[it] = *reinterpret_cast<const v4f*>(src);
             vb[it] = *reinterpret_cast<const v4f*>(src + 4);
         }
 #pragma unroll
-        for (int it = 0; it < 8; ++it) {
-            const int row = (tid >> 3) + 32 * it;
+        for (int it = 0; it < kIt; ++it) {
+            const int row = (tid >> 3) + kRowStep * it;
             const bool live = ch < nch && (row0 + row) < T && s_mod[row] > 0;
             const float uv[8] = {va[it].x, va[it].y, va[it].z, va[it].w,
                                  vb[it].x, vb[it].y, vb[it].z, vb[it].w};
@@ -786,21 +788,23 @@ template <> struct Cmc<bf16_t> {          // bf16 operands, v_mfma_f32_32x32x16_
         }
     }
 
+    template <int NT>
     static __device__ __forceinline__ void stage_r(uint8_t* sr, const bf16_t* rm, int col0, int N,
                                                    int r, int c0, int tid) {
+        constexpr int kIt = 8 * 256 / NT, kRowStep = NT / 8;
         const int nch = min(64, r - c0) >> 3;
         const int ch = tid & 7;
         const int chc = min(ch, nch - 1);
-        v4i pr[8];
+        v4i pr[kIt];
 #pragma unroll
-        for (int it = 0; it < 8; ++it) {
-            const int col = min(col0 + (tid >> 3) + 32 * it, N - 1);
+        for (int it = 0; it < kIt; ++it) {
+            const int col = min(col0 + (tid >> 3) + kRowStep * it, N - 1);
             pr[it] = *reinterpret_cast<const v4i*>(rm + static_cast<int64_t>(col) * r + c0 + 8 * chc);
         }
         const v4i zero = {0, 0, 0, 0};
 #pragma unroll
-        for (int it = 0; it < 8; ++it) {
-            const int row = (tid >> 3) + 32 * it;
+        for (int it = 0; it < kIt; ++it) {
+            const int row = (tid >> 3) + kRowStep * it;
             *reinterpret_cast<v4i*>(sr + row * 128 + ((ch ^ swz(row)) << 4)) = ch < nch ? pr[it] : zero;
         }
     }
@@ -852,22 +856,23 @@ template <> struct Cmc<float> {           // fp32 operands, v_mfma_f32_32x32x2f3
 
     // 16-byte pieces, 8 per thread in flight: slot idx -> row idx / 16,
     // piece idx % 16 (pieces past the chunk's rc / 4 are skipped)
+    template <int NT>
     static __device__ __forceinline__ void stage_u(uint8_t* base, const int* s_mod, const float* u,
                                                    int64_t row0, int64_t T, int r, int c0,
                                                    int tid) {
         float* su = reinterpret_cast<float*>(base);
         const int nq = min(64, r - c0) >> 2;
-        for (int b = 0; b < kTileM * 16; b += 256 * 8) {
+        for (int b = 0; b < kTileM * 16; b += NT * 8) {
             v4f v[8];
 #pragma unroll
             for (int it = 0; it < 8; ++it) {
-                const int idx = b + tid + 256 * it, row = idx >> 4, pc = min(idx & 15, nq - 1);
+                const int idx = b + tid + NT * it, row = idx >> 4, pc = min(idx & 15, nq - 1);
                 const int64_t t = min(row0 + row, T - 1);
                 v[it] = *reinterpret_cast<const v4f*>(u + t * r + c0 + 4 * pc);
             }
 #pragma unroll
             for (int it = 0; it < 8; ++it) {
-                const int idx = b + tid + 256 * it, row = idx >> 4, pc = idx & 15;
+                const int idx = b + tid + NT * it, row = idx >> 4, pc = idx & 15;
                 if (pc >= nq) continue;
                 const bool live = row0 + row < T && s_mod[row] > 0;
                 *reinterpret_cast<v4f*>(su + row * 64 + 4 * pc) = live ? v[it] : v4f{0.f, 0.f, 0.f, 0.f};
@@ -875,21 +880,22 @@ template <> struct Cmc<float> {           // fp32 operands, v_mfma_f32_32x32x2f3
         }
     }
 
+    template <int NT>
     static __device__ __forceinline__ void stage_r(uint8_t* base, const float* rm, int col0, int N,
                                                    int r, int c0, int tid) {
         float* sr = reinterpret_cast<float*>(base);
         const int nq = min(64, r - c0) >> 2;
-        for (int b = 0; b < kTileN * 16; b += 256 * 8) {
+        for (int b = 0; b < kTileN * 16; b += NT * 8) {
             v4f v[8];
 #pragma unroll
             for (int it = 0; it < 8; ++it) {
-                const int idx = b + tid + 256 * it, row = idx >> 4, pc = min(idx & 15, nq - 1);
+                const int idx = b + tid + NT * it, row = idx >> 4, pc = min(idx & 15, nq - 1);
                 const int col = min(col0 + row, N - 1);
                 v[it] = *reinterpret_cast<const v4f*>(rm + static_cast<int64_t>(col) * r + c0 + 4 * pc);
             }
 #pragma unroll
             for (int it = 0; it < 8; ++it) {
-                const int idx = b + tid + 256 * it, row = idx >> 4, pc = idx & 15;
+                const int idx = b + tid + NT * it, row = idx >> 4, pc = idx & 15;
                 if (pc < nq) *reinterpret_cast<v4f*>(sr + row * 64 + 4 * pc) = v[it];
             }
         }
@@ -943,19 +949,21 @@ __device__ __forceinline__ bool tile_coords(int tiles_m, int tiles_n, int& tm, i
 
 // Shared LDS of both GEMM kernels: the K stages during the main loop, then
 // the compensation pieces in the epilogue.
-// Row pitch of the per-wave output transpose buffer: 32 rows of 64 bf16
-// channels, padded by 16 bytes (rows stay 16-byte aligned for the 16-byte
-// reads; the column writes, one row per lane, then hit distinct banks).
-constexpr int kTrPitch = 144;
+// Per-wave output transpose buffer: 32 rows of TW bf16 channels (TW = 64
+// with 4 waves, 32 with 8), rows padded by 16 bytes (16-byte aligned rows
+// for the reads; the column writes, one row per lane, hit distinct banks).
+constexpr int tr_pitch(int tw) { return 2 * tw + 16; }
+constexpr int kTrBytes = 20480;       // max(4 x 32 x pitch(64), 8 x 32 x pitch(32))
 
 struct GemmSmem {
     uint8_t buf[2 * 65536];
     float dx[kTileM];
     float ws[kTileN];
     int mod[kTileM];
-    unsigned wpresent[4];     // per wave: bit m set if a row of modality m is in its 64 rows
-    uint8_t tr[4][32 * kTrPitch];
+    unsigned wpresent[8];     // per wave: bit m set if a row of modality m is in its rows
+    uint8_t tr[kTrBytes];
 };
+static_assert(4 * 32 * tr_pitch(64) <= kTrBytes && 8 * 32 * tr_pitch(32) <= kTrBytes, "tr");
 
 // Epilogue of a 256 x 256 tile whose int32 accumulators are in acc (this
 // wave's 128 x 128 quarter as 4 x 4 blocks of 32 x 32): optional int32 store,
@@ -982,23 +990,31 @@ __device__ __forceinline__ EpiPrefetch epi_prefetch(const float* __restrict__ x_
     return e;
 }
 
-template <typename YT, typename LT, bool CMC, bool ACC>
+// NWN waves along the channels (2: four waves of 128 x 128, 4: eight waves of
+// 128 x 64); NJ = 8 / NWN channel blocks of 32 per wave.
+template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2>
 __device__ __forceinline__ void gemm_epilogue(
-    v16i (&acc)[4][4], GemmSmem& sm, const EpiPrefetch& pf, int64_t T, int N, int64_t row0,
+    v16i (&acc)[4][8 / NWN], GemmSmem& sm, const EpiPrefetch& pf, int64_t T, int N, int64_t row0,
     int col0, const float* __restrict__ u, int r, int n_mod, const LT* __restrict__ r_up,
     int32_t* __restrict__ acc_out, YT* __restrict__ y) {
+    constexpr int NJ = 8 / NWN, NW = 2 * NWN, NT = 64 * NW;
+    constexpr int kWaveCols = 32 * NJ;                 // channels per wave
+    constexpr int TW = NJ == 4 ? 64 : 32;              // transpose unit width (channels)
+    constexpr int kPitch = tr_pitch(TW);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / NWN, wn = wave % NWN;
     // dx, ws, mod and wpresent lie outside the K-stage buffers, so they can be
     // written before the barrier; after it every wave is also done with the
     // K stages
-    sm.dx[tid] = pf.dx;
-    sm.ws[tid] = pf.ws;
+    if (tid < kTileM) {                        // threads past 256 carry no prefetch
+        sm.dx[tid] = pf.dx;
+        sm.ws[tid] = pf.ws;
+    }
     if constexpr (CMC) {
-        sm.mod[tid] = pf.mod;
+        if (tid < kTileM) sm.mod[tid] = pf.mod;
         unsigned wp = 0;
         for (int m = 1; m < n_mod; ++m)
-            if (__ballot(pf.mod == m) != 0ull) wp |= 1u << m;
+            if (__ballot(tid < kTileM && pf.mod == m) != 0ull) wp |= 1u << m;
         if (lane == 0) sm.wpresent[wave] = wp;
     }
     __syncthreads();
@@ -1011,19 +1027,21 @@ __device__ __forceinline__ void gemm_epilogue(
     const int n_chunks = (r + 63) >> 6;
     constexpr int kChunkBase = CMC ? Cmc<LT>::kUBytes : 0;
     if constexpr (CMC) {
-        present = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(
-            static_cast<int>(sm.wpresent[0] | sm.wpresent[1] | sm.wpresent[2] | sm.wpresent[3])));
+        unsigned pa = 0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) pa |= sm.wpresent[w];
+        present = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(pa)));
         n_present = __builtin_popcount(present);
         const int chunk_bytes = Cmc<LT>::kUBytes + n_present * Cmc<LT>::kRBytes;
         staged = n_chunks * chunk_bytes <= static_cast<int>(sizeof(sm.buf));
         if (n_present > 0 && staged && y != nullptr) {
             for (int c = 0; c < n_chunks; ++c) {
                 uint8_t* base = sm.buf + c * chunk_bytes;
-                Cmc<LT>::stage_u(base, sm.mod, u, row0, T, r, 64 * c, tid);
+                Cmc<LT>::template stage_u<NT>(base, sm.mod, u, row0, T, r, 64 * c, tid);
                 int p = 0;
                 for (int m = 1; m < n_mod; ++m) {
                     if (!(present & (1u << m))) continue;
-                    Cmc<LT>::stage_r(base + kChunkBase + p * Cmc<LT>::kRBytes,
+                    Cmc<LT>::template stage_r<NT>(base + kChunkBase + p * Cmc<LT>::kRBytes,
                                      r_up + static_cast<int64_t>(m - 1) * N * r, col0, N, r,
                                      64 * c, tid);
                     ++p;
@@ -1034,19 +1052,19 @@ __device__ __forceinline__ void gemm_epilogue(
     }
 
     // ---- accumulator layout: register e of a lane in block (i, j) holds token
-    // wm*128 + 32 i + (lane % 32) and channel wn*128 + 32 j + 8 (e / 4) +
+    // wm*128 + 32 i + (lane % 32) and channel wn*kWaveCols + 32 j + 8 (e / 4) +
     // 4 (lane / 32) + e % 4.  Loops over blocks are fully unrolled: the
     // accumulators are registers and must be indexed by constants.
     const bool interior = (row0 + kTileM <= T) && (col0 + kTileN <= N);
     auto tok_of = [&](int i) { return wm * 128 + i * 32 + (lane & 31); };
-    auto ch_of = [&](int j, int g) { return wn * 128 + j * 32 + 8 * g + 4 * (lane >> 5); };
+    auto ch_of = [&](int j, int g) { return wn * kWaveCols + j * 32 + 8 * g + 4 * (lane >> 5); };
 
     if constexpr (ACC) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int64_t tok = row0 + tok_of(i);
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < NJ; ++j)
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
                     const int ch = col0 + ch_of(j, g);
@@ -1086,33 +1104,37 @@ __device__ __forceinline__ void gemm_epilogue(
         load_ws(j, ws);
         return dequant_with(i, j, ws);
     };
-    // Stores of one token block (32 rows x 128 channels of this wave).  bf16
-    // output goes through a small per-wave LDS transpose so that every store
-    // instruction writes 8 whole 128-byte row pieces (the MFMA layout would
-    // give 32 rows x 16 bytes per instruction); LDS operations of one wave
-    // execute in order, so the buffer needs no further synchronisation.
-    auto store_rowblock = [&](const int i, const v16f (&ybs)[4]) __attribute__((always_inline)) {
+    // Stores of one token block (32 rows x kWaveCols channels of this wave).
+    // bf16 output goes through a small per-wave LDS transpose, TW channels
+    // at a time, so that every store instruction writes whole row pieces of
+    // 2 TW bytes (the MFMA layout would give 32 rows x 16 bytes per
+    // instruction); LDS operations of one wave execute in order, so the
+    // buffer needs no further synchronisation.
+    auto store_rowblock = [&](const int i, const v16f (&ybs)[NJ]) __attribute__((always_inline)) {
         const int64_t tok0 = row0 + wm * 128 + i * 32;
         if constexpr (sizeof(YT) == 2) {
-            uint8_t* scr = sm.tr[wave];
+            uint8_t* scr = sm.tr + wave * 32 * kPitch;
             const int rw = lane & 31, h = lane >> 5;
+            constexpr int kJper = TW / 32;                 // channel blocks per unit
+            constexpr int kLanesPerRow = TW / 8;           // 16-byte pieces per row
+            constexpr int kRowsPerRead = 64 / kLanesPerRow;
 #pragma unroll
-            for (int jp = 0; jp < 2; ++jp) {
+            for (int jp = 0; jp < NJ / kJper; ++jp) {
 #pragma unroll
-                for (int jj = 0; jj < 2; ++jj)
+                for (int jj = 0; jj < kJper; ++jj)
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
-                        const v16f& yb = ybs[2 * jp + jj];
+                        const v16f& yb = ybs[kJper * jp + jj];
                         v2i w;
                         w.x = static_cast<int32_t>(pack_bf16x2(yb[4 * g], yb[4 * g + 1]));
                         w.y = static_cast<int32_t>(pack_bf16x2(yb[4 * g + 2], yb[4 * g + 3]));
-                        *reinterpret_cast<v2i*>(scr + rw * kTrPitch + (jj * 32 + 8 * g + 4 * h) * 2) = w;
+                        *reinterpret_cast<v2i*>(scr + rw * kPitch + (jj * 32 + 8 * g + 4 * h) * 2) = w;
                     }
-                const int ch = col0 + wn * 128 + jp * 64 + (lane & 7) * 8;
+                const int ch = col0 + wn * kWaveCols + jp * TW + (lane % kLanesPerRow) * 8;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const int rr = k * 8 + (lane >> 3);
-                    const v4i d = *reinterpret_cast<const v4i*>(scr + rr * kTrPitch + (lane & 7) * 16);
+                for (int k = 0; k < 32 / kRowsPerRead; ++k) {
+                    const int rr = k * kRowsPerRead + lane / kLanesPerRow;
+                    const v4i d = *reinterpret_cast<const v4i*>(scr + rr * kPitch + (lane % kLanesPerRow) * 16);
                     const int64_t tok = tok0 + rr;
                     if (interior || (tok < T && ch < N))
                         *reinterpret_cast<v4i*>(y + tok * N + ch) = d;
@@ -1121,7 +1143,7 @@ __device__ __forceinline__ void gemm_epilogue(
         } else {
             const int64_t tok = tok0 + (lane & 31);
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < NJ; ++j)
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
                     const int ch = col0 + ch_of(j, g);
@@ -1134,14 +1156,14 @@ __device__ __forceinline__ void gemm_epilogue(
     };
 
     if (!CMC || n_present == 0) {
-        v4f wsv[4][4];                       // the wave's 128 channel scales, read once
+        v4f wsv[NJ][4];                      // the wave's channel scales, read once
 #pragma unroll
-        for (int j = 0; j < 4; ++j) load_ws(j, wsv[j]);
+        for (int j = 0; j < NJ; ++j) load_ws(j, wsv[j]);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            v16f ybs[4];
+            v16f ybs[NJ];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) ybs[j] = dequant_with(i, j, wsv[j]);
+            for (int j = 0; j < NJ; ++j) ybs[j] = dequant_with(i, j, wsv[j]);
             store_rowblock(i, ybs);
         }
         return;
@@ -1152,8 +1174,8 @@ __device__ __forceinline__ void gemm_epilogue(
             // Fast path: the present modalities lie side by side along the
             // rank dimension (slot p holds modality mods[p], r / 16 k steps
             // of 16 each).  Per token block, the compensation of its four
-            // channel blocks runs as four independent MFMA chains from zero
-            // and is added to the dequantised values.
+            // channel blocks runs as four independent MFMA chains that
+            // accumulate onto the dequantised values.
             int mods[2] = {0, 0};
             {
                 int p = 0;
@@ -1166,11 +1188,9 @@ __device__ __forceinline__ void gemm_epilogue(
             for (int i = 0; i < 4; ++i) {
                 const int trow = tok_of(i);
                 const int tm_ = sm.mod[trow];
-                v16f c[4];
+                v16f ybs[NJ];
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) c[j][e] = 0.f;
+                for (int j = 0; j < NJ; ++j) ybs[j] = dequant(i, j);
 #pragma unroll
                 for (int kk = 0; kk < 8; ++kk) {
                     const int p = kk >> 2, ks = kk & 3;
@@ -1188,20 +1208,13 @@ __device__ __forceinline__ void gemm_epilogue(
                     }
                     const uint8_t* sr = sm.buf + kChunkBase + p * Cmc<LT>::kRBytes;
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int crow = wn * 128 + j * 32 + (lane & 31);
+                    for (int j = 0; j < NJ; ++j) {
+                        const int crow = wn * kWaveCols + j * 32 + (lane & 31);
                         const v8bf bj = __builtin_bit_cast(
                             v8bf, *reinterpret_cast<const v4i*>(sr + crow * 128 + ((cc ^ swz(crow)) << 4)));
-                        c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bj, __builtin_bit_cast(v8bf, h), c[j], 0, 0, 0);
-                        c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bj, __builtin_bit_cast(v8bf, l), c[j], 0, 0, 0);
+                        ybs[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bj, __builtin_bit_cast(v8bf, h), ybs[j], 0, 0, 0);
+                        ybs[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bj, __builtin_bit_cast(v8bf, l), ybs[j], 0, 0, 0);
                     }
-                }
-                v16f ybs[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    ybs[j] = dequant(i, j);
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) ybs[j][e] += c[j][e];
                 }
                 store_rowblock(i, ybs);
             }
@@ -1216,12 +1229,12 @@ __device__ __forceinline__ void gemm_epilogue(
         for (int i = 0; i < 4; ++i) {
             const int trow = tok_of(i);
             const int tm_ = sm.mod[trow];
-            v16f ybs[4];
+            v16f ybs[NJ];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < NJ; ++j) {
                 v16f& yb = ybs[j];
                 yb = dequant(i, j);
-                const int crow = wn * 128 + j * 32 + (lane & 31);
+                const int crow = wn * kWaveCols + j * 32 + (lane & 31);
                 const int chunk_bytes = Cmc<LT>::kUBytes + n_present * Cmc<LT>::kRBytes;
                 for (int c = 0; c < n_chunks; ++c) {
                     int p = 0;
@@ -1384,8 +1397,10 @@ __device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_addr) {
 #define MASQ_WAIT_VMCNT_LGKM0(n) \
     __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (0 << 8))
 
-template <typename YT, typename LT, bool CMC, bool ACC>
-__global__ __launch_bounds__(256, 1) void k_gemm_dma(
+// NWN waves along the channels: 2 (four waves of 128 x 128, one per SIMD)
+// or 4 (eight waves of 128 x 64, two per SIMD).
+template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2>
+__global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
     const float* __restrict__ w_scale, int64_t T, int K, int N, int tiles_m, int tiles_n,
     const int32_t* __restrict__ mod, const float* __restrict__ u, int r, int n_mod,
@@ -1396,32 +1411,37 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dma(
     if (!tile_coords(tiles_m, tiles_n, tm, tn)) return;
     const int64_t row0 = static_cast<int64_t>(tm) * kTileM;
     const int col0 = tn * kTileN;
+    constexpr int NJ = 8 / NWN, NW = 2 * NWN;
+    constexpr int kRowsPerWave = kTileM / NW;           // DMA rows of A and of B per wave
+    constexpr int kDmaPerStage = 2 * kRowsPerWave / 16; // DMA instructions per thread per stage
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / NWN, wn = wave % NWN;
 
-    v16i acc[4][4];
+    v16i acc[4][NJ];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = v16i{0};
+        for (int j = 0; j < NJ; ++j) acc[i][j] = v16i{0};
 
     const EpiPrefetch pf = epi_prefetch(x_scale, w_scale, mod, CMC, T, N, row0, col0, n_mod);
 
-    // Wave w loads rows [64 w, 64 w + 64) of the A and of the B tile, 16 rows
-    // per instruction; lane i covers row 16 j + i / 4 at LDS chunk i % 4,
-    // which holds logical chunk (i % 4) ^ swz4(row).  Rows past T or N are
-    // clamped into the matrix; their results are discarded.
-    const int8_t* src[8];                 // [0..3]: A rows, [4..7]: B rows
-    uint32_t dst_off[8];
+    // Wave w loads rows [w R, w R + R) of the A and of the B tile (R =
+    // kRowsPerWave), 16 rows per instruction; lane i covers row 16 j + i / 4
+    // at LDS chunk i % 4, which holds logical chunk (i % 4) ^ swz4(row).
+    // Rows past T or N are clamped into the matrix; their results are
+    // discarded.
+    constexpr int kH = kDmaPerStage / 2;
+    const int8_t* src[kDmaPerStage];      // [0, kH): A rows, [kH, 2 kH): B rows
+    uint32_t dst_off[kDmaPerStage];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int row = wave * 64 + 16 * j + (lane >> 2);
+    for (int j = 0; j < kH; ++j) {
+        const int row = wave * kRowsPerWave + 16 * j + (lane >> 2);
         const int chunk = (lane & 3) ^ swz4(row);
         src[j] = A + min(row0 + row, T - 1) * K + 16 * chunk;
-        src[4 + j] = B + static_cast<int64_t>(min(col0 + row, N - 1)) * K + 16 * chunk;
+        src[kH + j] = B + static_cast<int64_t>(min(col0 + row, N - 1)) * K + 16 * chunk;
         dst_off[j] = static_cast<uint32_t>(
-            __builtin_amdgcn_readfirstlane((wave * 64 + 16 * j) * kDmaStageK));
-        dst_off[4 + j] = kTileM * kDmaStageK + dst_off[j];
+            __builtin_amdgcn_readfirstlane((wave * kRowsPerWave + 16 * j) * kDmaStageK));
+        dst_off[kH + j] = kTileM * kDmaStageK + dst_off[j];
     }
     const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sm.buf));
     auto issue_one = [&](int st, int q) __attribute__((always_inline)) {
@@ -1430,41 +1450,42 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dma(
     };
     auto issue = [&](int st) __attribute__((always_inline)) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q) issue_one(st, q);
+        for (int q = 0; q < kDmaPerStage; ++q) issue_one(st, q);
     };
     // fragment f of one 32-byte k step (f < 4: token block f of the q rows,
     // f >= 4: channel block f - 4 of the Wq rows)
-    auto read_frag = [&](int st, int ks, int f, v4i (&fa)[4], v4i (&fb)[4]) __attribute__((always_inline)) {
+    auto read_frag = [&](int st, int ks, int f, v4i (&fa)[4], v4i (&fb)[NJ]) __attribute__((always_inline)) {
         const uint8_t* sa = sm.buf + (st % kDmaStages) * kDmaStageBytes;
         const int c = 2 * ks + (lane >> 5);
         if (f < 4) {
             const int row = wm * 128 + f * 32 + (lane & 31);
             fa[f] = *reinterpret_cast<const v4i*>(sa + row * kDmaStageK + ((c ^ swz4(row)) << 4));
         } else {
-            const int row = wn * 128 + (f - 4) * 32 + (lane & 31);
+            const int row = wn * 32 * NJ + (f - 4) * 32 + (lane & 31);
             fb[f - 4] = *reinterpret_cast<const v4i*>(sa + kTileM * kDmaStageK + row * kDmaStageK +
                                                       ((c ^ swz4(row)) << 4));
         }
     };
-    // 16 MFMAs of one k step.  Interleaved with them, in a fixed order (each
-    // step is fenced against compiler reordering): two fragment reads of the
-    // next k step (st_next, ks_next) after each of the first four MFMAs, and
-    // with DMA one of stage dma_st's 8 loads after every second MFMA, so the
-    // LDS and vector-memory pipelines work while the matrix cores do.
-    auto mfma16 = [&](const v4i (&fa)[4], const v4i (&fb)[4], auto with_reads, int st_next,
-                      int ks_next, v4i (&na)[4], v4i (&nb)[4], auto with_dma, int dma_st)
-                      __attribute__((always_inline)) {
+    // The 4 NJ MFMAs of one k step.  Interleaved with them, in a fixed order
+    // (each step is fenced against compiler reordering): two fragment reads
+    // of the next k step (st_next, ks_next) after each of the first MFMAs,
+    // and with DMA one of stage dma_st's loads after every second MFMA, so
+    // the LDS and vector-memory pipelines work while the matrix cores do.
+    constexpr int kFrags = 4 + NJ;
+    auto mfma_group = [&](const v4i (&fa)[4], const v4i (&fb)[NJ], auto with_reads, int st_next,
+                          int ks_next, v4i (&na)[4], v4i (&nb)[NJ], auto with_dma, int dma_st)
+                          __attribute__((always_inline)) {
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            acc[q >> 2][q & 3] =
-                __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[q & 3], fa[q >> 2], acc[q >> 2][q & 3], 0, 0, 0);
+        for (int q = 0; q < 4 * NJ; ++q) {
+            acc[q / NJ][q % NJ] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[q % NJ], fa[q / NJ],
+                                                                        acc[q / NJ][q % NJ], 0, 0, 0);
             if constexpr (decltype(with_reads)::value)
-                if (q < 4) {
+                if (2 * q < kFrags) {
                     read_frag(st_next, ks_next, 2 * q, na, nb);
                     read_frag(st_next, ks_next, 2 * q + 1, na, nb);
                 }
             if constexpr (decltype(with_dma)::value)
-                if (q & 1) issue_one(dma_st, q >> 1);
+                if ((q & 1) && (q >> 1) < kDmaPerStage) issue_one(dma_st, q >> 1);
             MASQ_SCHED_FENCE();
         }
     };
@@ -1472,8 +1493,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dma(
     // once at most those of the `younger` later stages are in flight, and its
     // LDS reads of the buffer about to be refilled are complete
     auto publish = [&](int younger) __attribute__((always_inline)) {
-        if (younger >= 2) MASQ_WAIT_VMCNT_LGKM0(16);
-        else if (younger == 1) MASQ_WAIT_VMCNT_LGKM0(8);
+        if (younger >= 2) MASQ_WAIT_VMCNT_LGKM0(2 * kDmaPerStage);
+        else if (younger == 1) MASQ_WAIT_VMCNT_LGKM0(kDmaPerStage);
         else MASQ_WAIT_VMCNT_LGKM0(0);
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
@@ -1490,26 +1511,26 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dma(
     using no = std::false_type;
     const int nk = K / kDmaStageK;
     for (int st = 0; st < kDmaStages - 1 && st < nk; ++st) issue(st);
-    v4i fa0[4], fb0[4], fa1[4], fb1[4];
+    v4i fa0[4], fb0[NJ], fa1[4], fb1[NJ];
     auto body = [&](int kt, auto with_dma, auto with_next) __attribute__((always_inline)) {
         MASQ_SCHED_FENCE();
-        mfma16(fa0, fb0, yes{}, kt, 1, fa1, fb1, with_dma, kt + kDmaStages - 1);
+        mfma_group(fa0, fb0, yes{}, kt, 1, fa1, fb1, with_dma, kt + kDmaStages - 1);
         if constexpr (decltype(with_next)::value) {
             publish(min(nk - 2 - kt, 2));
             MASQ_SCHED_FENCE();
-            mfma16(fa1, fb1, yes{}, kt + 1, 0, fa0, fb0, no{}, 0);
+            mfma_group(fa1, fb1, yes{}, kt + 1, 0, fa0, fb0, no{}, 0);
         } else {
-            mfma16(fa1, fb1, no{}, 0, 0, fa0, fb0, no{}, 0);
+            mfma_group(fa1, fb1, no{}, 0, 0, fa0, fb0, no{}, 0);
         }
     };
     publish(min(nk - 1, 2));
 #pragma unroll
-    for (int f = 0; f < 8; ++f) read_frag(0, 0, f, fa0, fb0);
+    for (int f = 0; f < kFrags; ++f) read_frag(0, 0, f, fa0, fb0);
     int kt = 0;
     for (; kt + kDmaStages - 1 < nk; ++kt) body(kt, yes{}, yes{});
     for (; kt + 1 < nk; ++kt) body(kt, no{}, yes{});
     body(kt, no{}, no{});
-    gemm_epilogue<YT, LT, CMC, ACC>(acc, sm, pf, T, N, row0, col0, u, r, n_mod, r_up, acc_out, y);
+    gemm_epilogue<YT, LT, CMC, ACC, NWN>(acc, sm, pf, T, N, row0, col0, u, r, n_mod, r_up, acc_out, y);
 }
 
 // ================================================================ small-batch GEMM
@@ -1614,6 +1635,10 @@ __global__ __launch_bounds__(256) void k_gemm_small(
 }  // namespace
 
 // ================================================================ launchers
+// Waves along the channels of the 256 x 256 GEMM workgroup (2: four waves of
+// 128 x 128; 4: eight waves of 128 x 64, two per SIMD).
+constexpr int kGemmWavesN = 4;
+
 hipError_t launch_smooth_quant(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                int64_t T, int64_t K, int n_mod, int8_t* q, float* x_scale,
                                int* zero_ints, int n_zero, hipStream_t s) {
@@ -1727,9 +1752,10 @@ static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* w
     const int nt = tiles_m * tiles_n;
     const dim3 grid(8 * ((nt + 7) / 8)), block(256);
     if (K % kDmaStageK == 0)
-        hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC>), grid, block, 0, s, q, wq, x_scale, w_scale,
-                           T, static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
-                           rank, n_mod, static_cast<const LT*>(r_up), acc, static_cast<YT*>(y));
+        hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN>), grid, dim3(128 * kGemmWavesN),
+                           0, s, q, wq, x_scale, w_scale, T, static_cast<int>(K), static_cast<int>(N),
+                           tiles_m, tiles_n, mod, u, rank, n_mod, static_cast<const LT*>(r_up), acc,
+                           static_cast<YT*>(y));
     else
         hipLaunchKernelGGL((k_gemm<YT, LT, CMC, ACC>), grid, block, 0, s, q, wq, x_scale, w_scale, T,
                            static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
