@@ -41,12 +41,15 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
     w.q = reinterpret_cast<int8_t*>(carve(static_cast<size_t>(T) * static_cast<size_t>(K)));
     w.x_scale = reinterpret_cast<float*>(carve(static_cast<size_t>(T) * sizeof(float)));
     w.u = nullptr;
+    w.u_hl = nullptr;
     w.u_part = nullptr;
     w.tickets = nullptr;
     if (rank > 0 && n_mod > 1) {
         plan_kslices(T, K, w.n_kslices, w.kslice);
         const size_t ur = static_cast<size_t>(T) * static_cast<size_t>(rank) * sizeof(float);
         w.u = reinterpret_cast<float*>(carve(ur));
+        if (rank <= 64 && !small_path(T, K))
+            w.u_hl = carve(static_cast<size_t>(T) * 256);
         if (w.n_kslices > 1) {
             w.u_part = reinterpret_cast<float*>(carve(ur * static_cast<size_t>(w.n_kslices)));
             if (!small_path(T, K))    // the small-batch GEMM adds the partials itself
@@ -129,7 +132,7 @@ masq_status fused_stage(const Fused& a, int stage) {
     } else if ((stage & 1) && cmc && masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt))) {
         st = from_hip(masq::launch_stage1_fused(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                 a.l_down, a.T, a.c_in, a.rank, a.n_mod, w.q,
-                                                w.x_scale, w.u, s));
+                                                w.x_scale, w.u, w.u_hl, s));
         if (st != MASQ_OK) return st;
     } else if (stage & 1) {
         const int n_tickets = w.tickets ? static_cast<int>((a.T + masq::kDownRows - 1) / masq::kDownRows) : 0;
@@ -145,8 +148,12 @@ masq_status fused_stage(const Fused& a, int stage) {
         }
     }
     if (stage & 2) {
+        // the hi/lo rows of u exist when the fused stage 1 wrote them
+        const bool hl = cmc && !masq::small_path(a.T, a.c_in) &&
+                        masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt));
         st = from_hip(masq::launch_gemm(w.q, w.x_scale, a.wq, a.w_scale, a.T, a.c_in, a.c_out,
-                                        a.modality, w.u, w.u_part, w.n_kslices, a.rank, a.n_mod,
+                                        a.modality, w.u, hl ? w.u_hl : nullptr, w.u_part,
+                                        w.n_kslices, a.rank, a.n_mod,
                                         a.r_up, to_dt(a.lr_dt), cmc, nullptr, a.y, to_dt(a.y_dt),
                                         s));
     }
@@ -206,7 +213,7 @@ masq_status masq_w8a8_gemm(const int8_t* q, const float* x_scale, const int8_t* 
     if (T == 0) return MASQ_OK;
     (void)hipGetLastError();
     return from_hip(masq::launch_gemm(q, x_scale, wq, w_scale, T, c_in, c_out, nullptr, nullptr,
-                                      nullptr, 1, 0, 1, nullptr, DT::BF16, false, acc, y, to_dt(y_dt),
+                                      nullptr, nullptr, 1, 0, 1, nullptr, DT::BF16, false, acc, y, to_dt(y_dt),
                                       static_cast<hipStream_t>(stream)));
 }
 

@@ -47,6 +47,7 @@ struct Workspace {
     int8_t* q;
     float* x_scale;
     float* u;          // [T][rank] fp32 down-projection u = (x S^-1) L1
+    uint8_t* u_hl;     // [T][256 B] u as bf16 hi | lo rows (rank <= 64, large batches)
     float* u_part;     // [n_kslices][T][rank] fp32 partial sums over k slices (n_kslices > 1)
     int* tickets;      // [ceil(T / kDownRows)] arrival counters of the slice workgroups
     int n_kslices;
@@ -73,7 +74,8 @@ inline bool fused_stage1_ok(int64_t T, int64_t K, int rank, DT lr_dt) {
 }
 hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
-                               int8_t* q, float* x_scale, float* u, hipStream_t s);
+                               int8_t* q, float* x_scale, float* u, uint8_t* u_hl,
+                               hipStream_t s);
 
 // Stage 1 of the small-batch path (small_path): quantisation of every row
 // and the k-sliced down-projection (partials) in one launch.
@@ -82,10 +84,12 @@ hipError_t launch_stage1_small(const void* x, DT x_dt, const int32_t* mod, const
                                int n_mod, bool cmc, const Workspace& w, hipStream_t s);
 
 // u: the down-projection; on the small-batch path (small_path) with
-// n_kslices > 1 the GEMM adds the slice partials u_part itself.
+// n_kslices > 1 the GEMM adds the slice partials u_part itself.  u_hl
+// (optional): u as bf16 hi/lo rows, written by the fused stage 1.
 hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        const float* w_scale, int64_t T, int64_t K, int64_t N,
-                       const int32_t* mod, const float* u, const float* u_part, int n_kslices,
+                       const int32_t* mod, const float* u, const uint8_t* u_hl,
+                       const float* u_part, int n_kslices,
                        int rank, int n_mod, const void* r_up, DT lr_dt, bool cmc, int32_t* acc,
                        void* y, DT y_dt, hipStream_t s);
 

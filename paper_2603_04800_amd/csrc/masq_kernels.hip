@@ -546,7 +546,8 @@ template <typename XT>
 __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
     const XT* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
     const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod,
-    int8_t* __restrict__ q, float* __restrict__ x_scale, float* __restrict__ u) {
+    int8_t* __restrict__ q, float* __restrict__ x_scale, float* __restrict__ u,
+    uint8_t* __restrict__ u_hl) {
     __shared__ int smod[kRowsDown];
     __shared__ float samax[kFuseWaves][kRowsDown];
     __shared__ float red[kFuseWaves][kRowsDown][64];
@@ -655,14 +656,36 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
         srq[tid] = nz ? 127.0f / a : 0.f;                     // correctly rounded
         if (row0 + tid < T) x_scale[row0 + tid] = nz ? a / 127.0f : 0.f;
     }
-    if (np > 0) {
-        for (int idx = tid; idx < kRowsDown * r; idx += 64 * kFuseWaves) {
-            const int row = idx / r, col = idx - row * r;
-            if (row0 + row >= T) continue;
-            float v = red[0][row][col];
+    // u (fp32; written when the tile has non-text rows) and its bf16 hi/lo
+    // rows [hi 64 | lo 64] for the GEMM epilogue (text rows and columns past
+    // r zero there): thread (row, g) sums columns 8 g .. 8 g + 7 over the
+    // waves in a fixed order
+    if (tid < kRowsDown * 8 && (np > 0 || u_hl != nullptr)) {
+        const int row = tid >> 3, g = tid & 7;
+        const int64_t t = row0 + row;
+        if (t < T) {
+            float v[8];
 #pragma unroll
-            for (int w = 1; w < kFuseWaves; ++w) v += red[w][row][col];   // fixed order
-            u[(row0 + row) * r + col] = v;
+            for (int e = 0; e < 8; ++e) v[e] = 0.f;
+            if (np > 0 && 8 * g < r) {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    v4f a = *reinterpret_cast<const v4f*>(&red[0][row][8 * g + 4 * h]);
+#pragma unroll
+                    for (int w = 1; w < kFuseWaves; ++w)
+                        a += *reinterpret_cast<const v4f*>(&red[w][row][8 * g + 4 * h]);
+                    v[4 * h] = a.x; v[4 * h + 1] = a.y; v[4 * h + 2] = a.z; v[4 * h + 3] = a.w;
+                    *reinterpret_cast<v4f*>(u + t * r + 8 * g + 4 * h) = a;
+                }
+            }
+            if (u_hl != nullptr) {
+                v4i hi, lo;
+                split_bf16x8(v, hi, lo);
+                const v4i zero = {0, 0, 0, 0};
+                const bool live = smod[row] > 0;
+                *reinterpret_cast<v4i*>(u_hl + t * 256 + 16 * g) = live ? hi : zero;
+                *reinterpret_cast<v4i*>(u_hl + t * 256 + 128 + 16 * g) = live ? lo : zero;
+            }
         }
     }
     __syncthreads();
@@ -959,7 +982,8 @@ struct GemmSmem {
     uint8_t buf[2 * 65536];
     float dx[kTileM];
     float ws[kTileN];
-    int mod[kTileM];
+    int mod[kTileM];          // modality of each row (invalid ids read as text)
+    int rawmod[kTileM];       // modality ids as given (LDS-DMA target)
     unsigned wpresent[8];     // per wave: bit m set if a row of modality m is in its rows
     uint8_t tr[kTrBytes];
 };
@@ -990,13 +1014,24 @@ __device__ __forceinline__ EpiPrefetch epi_prefetch(const float* __restrict__ x_
     return e;
 }
 
+// State handed over by the DMA kernel: the per-row operands are in LDS
+// already, the modalities present are known, and with pre the fast-path
+// compensation operands sit at the given byte offsets of the K buffers.
+struct EpiDma {
+    unsigned present;
+    bool pre;
+    int off_uh, off_ul, off_r[2];
+};
+
 // NWN waves along the channels (2: four waves of 128 x 128, 4: eight waves of
-// 128 x 64); NJ = 8 / NWN channel blocks of 32 per wave.
-template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2>
+// 128 x 64); NJ = 8 / NWN channel blocks of 32 per wave.  DMA: called from
+// the DMA kernel (state in ed; pf unused), else the per-thread operands pf
+// are written to LDS here.
+template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2, bool DMA = false>
 __device__ __forceinline__ void gemm_epilogue(
     v16i (&acc)[4][8 / NWN], GemmSmem& sm, const EpiPrefetch& pf, int64_t T, int N, int64_t row0,
     int col0, const float* __restrict__ u, int r, int n_mod, const LT* __restrict__ r_up,
-    int32_t* __restrict__ acc_out, YT* __restrict__ y) {
+    int32_t* __restrict__ acc_out, YT* __restrict__ y, const EpiDma& ed = EpiDma{}) {
     constexpr int NJ = 8 / NWN, NW = 2 * NWN, NT = 64 * NW;
     constexpr int kWaveCols = 32 * NJ;                 // channels per wave
     constexpr int TW = NJ == 4 ? 64 : 32;              // transpose unit width (channels)
@@ -1006,16 +1041,18 @@ __device__ __forceinline__ void gemm_epilogue(
     // dx, ws, mod and wpresent lie outside the K-stage buffers, so they can be
     // written before the barrier; after it every wave is also done with the
     // K stages
-    if (tid < kTileM) {                        // threads past 256 carry no prefetch
-        sm.dx[tid] = pf.dx;
-        sm.ws[tid] = pf.ws;
-    }
-    if constexpr (CMC) {
-        if (tid < kTileM) sm.mod[tid] = pf.mod;
-        unsigned wp = 0;
-        for (int m = 1; m < n_mod; ++m)
-            if (__ballot(tid < kTileM && pf.mod == m) != 0ull) wp |= 1u << m;
-        if (lane == 0) sm.wpresent[wave] = wp;
+    if constexpr (!DMA) {
+        if (tid < kTileM) {                    // threads past 256 carry no prefetch
+            sm.dx[tid] = pf.dx;
+            sm.ws[tid] = pf.ws;
+        }
+        if constexpr (CMC) {
+            if (tid < kTileM) sm.mod[tid] = pf.mod;
+            unsigned wp = 0;
+            for (int m = 1; m < n_mod; ++m)
+                if (__ballot(tid < kTileM && pf.mod == m) != 0ull) wp |= 1u << m;
+            if (lane == 0) sm.wpresent[wave] = wp;
+        }
     }
     __syncthreads();
 
@@ -1026,15 +1063,27 @@ __device__ __forceinline__ void gemm_epilogue(
     unsigned present = 0;
     const int n_chunks = (r + 63) >> 6;
     constexpr int kChunkBase = CMC ? Cmc<LT>::kUBytes : 0;
+    // LDS byte offsets of the fast path's u hi, u lo and L2 pieces
+    int off_uh = 0, off_ul = kTileM * 128, off_r0 = kChunkBase, off_r1 = kChunkBase + (CMC ? Cmc<LT>::kRBytes : 0);
     if constexpr (CMC) {
-        unsigned pa = 0;
+        if constexpr (DMA) {
+            present = ed.present;
+        } else {
+            unsigned pa = 0;
 #pragma unroll
-        for (int w = 0; w < NW; ++w) pa |= sm.wpresent[w];
-        present = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(pa)));
+            for (int w = 0; w < NW; ++w) pa |= sm.wpresent[w];
+            present = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(pa)));
+        }
         n_present = __builtin_popcount(present);
         const int chunk_bytes = Cmc<LT>::kUBytes + n_present * Cmc<LT>::kRBytes;
         staged = n_chunks * chunk_bytes <= static_cast<int>(sizeof(sm.buf));
-        if (n_present > 0 && staged && y != nullptr) {
+        if (DMA && ed.pre) {
+            staged = true;
+            off_uh = ed.off_uh;
+            off_ul = ed.off_ul;
+            off_r0 = ed.off_r[0];
+            off_r1 = ed.off_r[1];
+        } else if (n_present > 0 && staged && y != nullptr) {
             for (int c = 0; c < n_chunks; ++c) {
                 uint8_t* base = sm.buf + c * chunk_bytes;
                 Cmc<LT>::template stage_u<NT>(base, sm.mod, u, row0, T, r, 64 * c, tid);
@@ -1199,14 +1248,14 @@ __device__ __forceinline__ void gemm_epilogue(
                     const int off = trow * 128 + ((cc ^ swz(trow)) << 4);
                     // text rows are zero in the staged u; a second modality
                     // present needs each slot masked to its own rows
-                    v4i h = *reinterpret_cast<const v4i*>(sm.buf + off);
-                    v4i l = *reinterpret_cast<const v4i*>(sm.buf + kTileM * 128 + off);
+                    v4i h = *reinterpret_cast<const v4i*>(sm.buf + off_uh + off);
+                    v4i l = *reinterpret_cast<const v4i*>(sm.buf + off_ul + off);
                     if (n_present > 1) {
                         const bool live = tm_ == mods[p];
                         h = live ? h : zero4;
                         l = live ? l : zero4;
                     }
-                    const uint8_t* sr = sm.buf + kChunkBase + p * Cmc<LT>::kRBytes;
+                    const uint8_t* sr = sm.buf + (p == 0 ? off_r0 : off_r1);
 #pragma unroll
                     for (int j = 0; j < NJ; ++j) {
                         const int crow = wn * kWaveCols + j * 32 + (lane & 31);
@@ -1397,16 +1446,32 @@ __device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_addr) {
 #define MASQ_WAIT_VMCNT_LGKM0(n) \
     __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (0 << 8))
 
+// One 4-byte lane of an LDS-DMA load: lane i writes LDS address m0 + 4 i.
+__device__ __forceinline__ void lds_dma4(const void* src, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+                 :: "v"(src), "s"(lds_addr) : "memory", "m0");
+}
+
 // NWN waves along the channels: 2 (four waves of 128 x 128, one per SIMD)
 // or 4 (eight waves of 128 x 64, two per SIMD).
+//
+// The per-row and per-channel epilogue operands (x scales, channel scales,
+// modality ids) reach LDS by DMA ahead of the first K stage.  When the
+// compensation takes the fast path (bf16 factors, rank <= 64, one or two
+// non-text modalities in the tile, u given as bf16 hi/lo rows in u_hl), its
+// LDS operands -- u hi, u lo and the L2 rows of each modality present, 32 KB
+// each -- are copied by DMA into the K buffers after the loop, with no
+// conversion in the epilogue.
 template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2>
 __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
     const float* __restrict__ w_scale, int64_t T, int K, int N, int tiles_m, int tiles_n,
-    const int32_t* __restrict__ mod, const float* __restrict__ u, int r, int n_mod,
-    const LT* __restrict__ r_up, int32_t* __restrict__ acc_out, YT* __restrict__ y) {
+    const int32_t* __restrict__ mod, const float* __restrict__ u, const uint8_t* __restrict__ u_hl,
+    int r, int n_mod, const LT* __restrict__ r_up, int32_t* __restrict__ acc_out,
+    YT* __restrict__ y) {
     __shared__ __attribute__((aligned(16))) GemmSmem sm;
     static_assert(kDmaStages * kDmaStageBytes <= static_cast<int>(sizeof(GemmSmem::buf)), "LDS");
+    static_assert(kDmaStageBytes == kTileM * 128, "an epilogue operand fills one K stage buffer");
     int tm, tn;
     if (!tile_coords(tiles_m, tiles_n, tm, tn)) return;
     const int64_t row0 = static_cast<int64_t>(tm) * kTileM;
@@ -1416,6 +1481,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     constexpr int kDmaPerStage = 2 * kRowsPerWave / 16; // DMA instructions per thread per stage
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / NWN, wn = wave % NWN;
+    const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sm.buf));
 
     v16i acc[4][NJ];
 #pragma unroll
@@ -1423,7 +1489,28 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
 #pragma unroll
         for (int j = 0; j < NJ; ++j) acc[i][j] = v16i{0};
 
-    const EpiPrefetch pf = epi_prefetch(x_scale, w_scale, mod, CMC, T, N, row0, col0, n_mod);
+    // per-row operands: 64 entries per instruction, piece c of the 12 (x
+    // scales, channel scales, modality ids; 4 each) issued by wave c % NW;
+    // indices past T or N are clamped (their results are discarded)
+    {
+        constexpr int kPieces = CMC ? 12 : 8;
+        for (int c = wave; c < kPieces; c += NW) {
+            const int part = c & 3, e = 64 * part + lane;
+            const void* src;
+            uint32_t dst;
+            if (c < 4) {
+                src = x_scale + min(row0 + e, T - 1);
+                dst = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&sm.dx[64 * part]));
+            } else if (c < 8) {
+                src = w_scale + min(col0 + e, N - 1);
+                dst = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&sm.ws[64 * part]));
+            } else {
+                src = mod + min(row0 + e, T - 1);
+                dst = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&sm.rawmod[64 * part]));
+            }
+            lds_dma4(src, static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(dst))));
+        }
+    }
 
     // Wave w loads rows [w R, w R + R) of the A and of the B tile (R =
     // kRowsPerWave), 16 rows per instruction; lane i covers row 16 j + i / 4
@@ -1443,7 +1530,6 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
             __builtin_amdgcn_readfirstlane((wave * kRowsPerWave + 16 * j) * kDmaStageK));
         dst_off[kH + j] = kTileM * kDmaStageK + dst_off[j];
     }
-    const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sm.buf));
     auto issue_one = [&](int st, int q) __attribute__((always_inline)) {
         const uint32_t sbase = lds0 + (st % kDmaStages) * kDmaStageBytes;
         lds_dma16(src[q] + st * kDmaStageK, sbase + dst_off[q]);
@@ -1505,13 +1591,57 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     // that publishes stage kt + 1 sits between the two MFMA groups of stage
     // kt.  The DMA of stage kt + 3 refills the buffer of stage kt - 1, which
     // every wave finished reading before the previous barrier.  The loop is
-    // split into three uniform phases (DMA still to issue / none / last
-    // stage) so that each body has a single shape.
+    // split into uniform phases (DMA still to issue / none / last stage) so
+    // that each body has a single shape.
     using yes = std::true_type;
     using no = std::false_type;
     const int nk = K / kDmaStageK;
     for (int st = 0; st < kDmaStages - 1 && st < nk; ++st) issue(st);
     v4i fa0[4], fb0[NJ], fa1[4], fb1[NJ];
+    publish(min(nk - 1, 2));
+
+    // The per-row operands have landed (they precede stage 0 in every wave's
+    // queue).  Modalities present in the tile, as scalars.
+    unsigned present = 0;
+    int mods[2] = {0, 0};
+    bool pre = false;
+    if constexpr (CMC) {
+        if (tid < kTileM) sm.mod[tid] = sane_mod(sm.rawmod[tid], n_mod);   // read after a barrier
+        const v4i m4 = *reinterpret_cast<const v4i*>(&sm.rawmod[4 * lane]);
+        const int s0 = sane_mod(m4.x, n_mod), s1 = sane_mod(m4.y, n_mod);
+        const int s2 = sane_mod(m4.z, n_mod), s3 = sane_mod(m4.w, n_mod);
+        for (int m = 1; m < n_mod; ++m)
+            if (__ballot(s0 == m || s1 == m || s2 == m || s3 == m) != 0ull) present |= 1u << m;
+        present = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(present)));
+        int p = 0;
+        for (int m = 1; m < n_mod && p < 2; ++m)
+            if (present & (1u << m)) mods[p++] = m;
+        const int np = __builtin_popcount(present);
+        pre = sizeof(LT) == 2 && u_hl != nullptr && r <= 64 && np >= 1 && np <= 2 && y != nullptr;
+    }
+    // compensation operand v (0: u hi, 1: u lo, 2 + p: L2 rows of mods[p])
+    // into K buffer v, 128-byte rows: lane i covers row 8 q + i / 8 of this
+    // wave's share at LDS chunk i % 8, which holds logical chunk
+    // (i % 8) ^ swz(row)
+    auto issue_extra = [&](int v) __attribute__((always_inline)) {
+        const uint32_t sbase = lds0 + v * kDmaStageBytes;
+        const LT* rm = r_up + static_cast<int64_t>(max((v == 2 ? mods[0] : mods[1]) - 1, 0)) * N * r;
+#pragma unroll
+        for (int q = 0; q < kDmaPerStage; ++q) {
+            const int rw = wave * kRowsPerWave + 8 * q;
+            const int row = rw + (lane >> 3);
+            const int lc = (lane & 7) ^ swz(row);
+            const uint8_t* sp =
+                v < 2 ? u_hl + min(row0 + row, T - 1) * 256 + 128 * v + 16 * lc
+                      : reinterpret_cast<const uint8_t*>(
+                            rm + static_cast<int64_t>(min(col0 + row, N - 1)) * r) +
+                            16 * min(lc, (r >> 3) - 1);
+            lds_dma16(sp, sbase + static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(rw * 128)));
+        }
+    };
+
+#pragma unroll
+    for (int f = 0; f < kFrags; ++f) read_frag(0, 0, f, fa0, fb0);
     auto body = [&](int kt, auto with_dma, auto with_next) __attribute__((always_inline)) {
         MASQ_SCHED_FENCE();
         mfma_group(fa0, fb0, yes{}, kt, 1, fa1, fb1, with_dma, kt + kDmaStages - 1);
@@ -1523,14 +1653,31 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
             mfma_group(fa1, fb1, no{}, 0, 0, fa0, fb0, no{}, 0);
         }
     };
-    publish(min(nk - 1, 2));
-#pragma unroll
-    for (int f = 0; f < kFrags; ++f) read_frag(0, 0, f, fa0, fb0);
     int kt = 0;
     for (; kt + kDmaStages - 1 < nk; ++kt) body(kt, yes{}, yes{});
     for (; kt + 1 < nk; ++kt) body(kt, no{}, yes{});
     body(kt, no{}, no{});
-    gemm_epilogue<YT, LT, CMC, ACC, NWN>(acc, sm, pf, T, N, row0, col0, u, r, n_mod, r_up, acc_out, y);
+
+    EpiDma ed{};
+    ed.present = present;
+    ed.pre = pre;
+    if constexpr (CMC) {
+        if (pre) {
+            // the K buffers are free once every wave is past its last reads
+            __syncthreads();
+            issue_extra(0);
+            issue_extra(1);
+            issue_extra(2);
+            if (mods[1] != 0) issue_extra(3);
+            ed.off_uh = 0;
+            ed.off_ul = kDmaStageBytes;
+            ed.off_r[0] = 2 * kDmaStageBytes;
+            ed.off_r[1] = 3 * kDmaStageBytes;
+        }
+    }
+    MASQ_WAIT_VMCNT_LGKM0(0);
+    gemm_epilogue<YT, LT, CMC, ACC, NWN, true>(acc, sm, EpiPrefetch{}, T, N, row0, col0, u, r, n_mod,
+                                               r_up, acc_out, y, ed);
 }
 
 // ================================================================ small-batch GEMM
@@ -1693,16 +1840,17 @@ hipError_t launch_lowrank_down(const void* x, DT x_dt, const int32_t* mod, const
 
 hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
-                               int8_t* q, float* x_scale, float* u, hipStream_t s) {
+                               int8_t* q, float* x_scale, float* u, uint8_t* u_hl,
+                               hipStream_t s) {
     const dim3 grid(static_cast<unsigned>((T + kRowsDown - 1) / kRowsDown)), block(64 * kFuseWaves);
     if (x_dt == DT::BF16)
         hipLaunchKernelGGL(k_stage1_fused<bf16_t>, grid, block, 0, s, static_cast<const bf16_t*>(x),
                            mod, inv_s, static_cast<const bf16_t*>(l_down), T, static_cast<int>(K),
-                           rank, n_mod, q, x_scale, u);
+                           rank, n_mod, q, x_scale, u, u_hl);
     else
         hipLaunchKernelGGL(k_stage1_fused<float>, grid, block, 0, s, static_cast<const float*>(x),
                            mod, inv_s, static_cast<const bf16_t*>(l_down), T, static_cast<int>(K),
-                           rank, n_mod, q, x_scale, u);
+                           rank, n_mod, q, x_scale, u, u_hl);
     return hipGetLastError();
 }
 
@@ -1745,8 +1893,8 @@ static void launch_gemm_small_t(const int8_t* q, const float* x_scale, const int
 template <typename YT, typename LT, bool CMC, bool ACC>
 static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* wq,
                           const float* w_scale, int64_t T, int64_t K, int64_t N,
-                          const int32_t* mod, const float* u, int rank, int n_mod,
-                          const void* r_up, int32_t* acc, void* y, hipStream_t s) {
+                          const int32_t* mod, const float* u, const uint8_t* u_hl, int rank,
+                          int n_mod, const void* r_up, int32_t* acc, void* y, hipStream_t s) {
     const int tiles_m = static_cast<int>((T + kTileM - 1) / kTileM);
     const int tiles_n = static_cast<int>((N + kTileN - 1) / kTileN);
     const int nt = tiles_m * tiles_n;
@@ -1754,8 +1902,8 @@ static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* w
     if (K % kDmaStageK == 0)
         hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN>), grid, dim3(128 * kGemmWavesN),
                            0, s, q, wq, x_scale, w_scale, T, static_cast<int>(K), static_cast<int>(N),
-                           tiles_m, tiles_n, mod, u, rank, n_mod, static_cast<const LT*>(r_up), acc,
-                           static_cast<YT*>(y));
+                           tiles_m, tiles_n, mod, u, u_hl, rank, n_mod, static_cast<const LT*>(r_up),
+                           acc, static_cast<YT*>(y));
     else
         hipLaunchKernelGGL((k_gemm<YT, LT, CMC, ACC>), grid, block, 0, s, q, wq, x_scale, w_scale, T,
                            static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
@@ -1764,9 +1912,9 @@ static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* w
 
 hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        const float* w_scale, int64_t T, int64_t K, int64_t N,
-                       const int32_t* mod, const float* u, const float* u_part, int n_kslices,
-                       int rank, int n_mod, const void* r_up, DT lr_dt, bool cmc, int32_t* acc,
-                       void* y, DT y_dt, hipStream_t s) {
+                       const int32_t* mod, const float* u, const uint8_t* u_hl,
+                       const float* u_part, int n_kslices, int rank, int n_mod, const void* r_up,
+                       DT lr_dt, bool cmc, int32_t* acc, void* y, DT y_dt, hipStream_t s) {
     if (small_path(T, K)) {
         const float* uu = cmc ? u : nullptr;
 #define MASQ_SMALL(YT, LT) launch_gemm_small_t<YT, LT>(q, x_scale, wq, w_scale, T, K, N, mod, uu, u_part, n_kslices, rank, n_mod, r_up, acc, y, s)
@@ -1780,7 +1928,7 @@ hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
 #undef MASQ_SMALL
         return hipGetLastError();
     }
-#define MASQ_GEMM(YT, LT, C, A) launch_gemm_t<YT, LT, C, A>(q, x_scale, wq, w_scale, T, K, N, mod, u, rank, n_mod, r_up, acc, y, s)
+#define MASQ_GEMM(YT, LT, C, A) launch_gemm_t<YT, LT, C, A>(q, x_scale, wq, w_scale, T, K, N, mod, u, u_hl, rank, n_mod, r_up, acc, y, s)
     // the int32 accumulator output exists only for the plain product (no
     // compensation); it is a separate instantiation because storing the
     // accumulators as well raises the epilogue's register pressure

@@ -174,6 +174,13 @@ _EDGE = {
     # grids with few tiles split K across workgroups (raw int32 slices added exactly)
     "splitk_bf16": dict(T=300, K=2048, N=512, r=64, M=3, act="bf16", lr="bf16"),
     "splitk_fp32_ragged": dict(T=260, K=1600, N=272, r=16, M=2, act="f32", lr="f32"),
+    # the compensation operands loaded as extra stages of the K ring: the
+    # shortest ring (four 64-byte stages), ranks below 64, mixed tiles
+    "ring_tail_k256_rank16": dict(T=520, K=256, N=272, r=16, M=2, act="bf16", lr="bf16",
+                                  layout="runs"),
+    "ring_tail_k320_rank32": dict(T=300, K=320, N=256, r=32, M=3, act="bf16", lr="bf16"),
+    "ring_tail_k512_rank48_f32_out": dict(T=400, K=512, N=336, r=48, M=3, act="f32", lr="bf16",
+                                          layout="runs"),
 }
 
 
@@ -204,11 +211,12 @@ def test_empty_batch_is_a_noop(ops):
     assert y.shape == (0, 32)
 
 
-def test_invalid_modality_ids_read_as_text(ops):
+@pytest.mark.parametrize("K,r", [(128, 16), (512, 64)])
+def test_invalid_modality_ids_read_as_text(ops, K, r):
     """Ids outside [0, n_mod) are documented to be read as text: the layer then
     equals the oracle run with those ids replaced by 0 (text rows exact)."""
     from paper_2603_04800_amd import workload
-    L = _random_layer(300, 128, 96, 16, 3, "bf16", "bf16")
+    L = _random_layer(300, K, 96, r, 3, "bf16", "bf16")
     bad = np.array([0, 5, 17, 100, 257, 299])
     mod_gpu = L["modality"].copy()
     mod_gpu[bad] = np.array([3, -1, 4, 1 << 20, -(1 << 30), 7], np.int32)
