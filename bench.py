@@ -250,6 +250,20 @@ def cpu_baseline(layers, min_seconds=10.0, max_runs=64):
                       f"through oracle.inference.linear (fp64), {runs} runs, {dt:.1f} s total"}
 
 
+def gemm_kernel_label(layers) -> str:
+    """Name of the stage-2 kernel(s) the layers dispatch to: batches of at
+    most 16 tokens with K % 64 == 0 take the weight-streaming kernel, other
+    K % 64 == 0 shapes the LDS-DMA tile kernel, the rest the general-K one."""
+    names = []
+    for L in layers:
+        T, K = L["x"].shape
+        n = ("k_gemm_small" if T <= 16 and K % 64 == 0
+             else "k_gemm_dma" if K % 64 == 0 else "k_gemm")
+        if n not in names:
+            names.append(n)
+    return " + ".join(names) + " (stage 2: int8 GEMM + dequant + compensation)"
+
+
 def gemm_bytes(L) -> int:
     """Bytes the stage-2 kernel must move at least: q codes, Wq, scales, the
     rank-r rows u, the factors of the non-text modalities present, modality
@@ -358,7 +372,7 @@ def main():
     src_hash = kernel_source_hash()
     traffic = traffic_from_profiles(cfg.name, src_hash)
     roof.update({
-        "kernel": "k_gemm_dma (stage 2: int8 GEMM + dequant + compensation)",
+        "kernel": gemm_kernel_label(layers),
         "traffic": traffic,
         "gemm_ms": round(gemm_ms, 5),
         "ops_per_step": int(ops), "algorithmic_bytes_per_step": int(gbytes),
