@@ -27,7 +27,6 @@ static void plan_kslices(int64_t T, int64_t K, int& n_kslices, int& kslice) {
 }
 
 Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, int n_mod) {
-    (void)N;
     Workspace w{};
     w.kslice = static_cast<int>(K);
     w.n_kslices = 1;
@@ -44,6 +43,15 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
     w.u_hl = nullptr;
     w.u_part = nullptr;
     w.tickets = nullptr;
+    w.dec_part = nullptr;
+    w.dec_tickets = nullptr;
+    w.dec_ns = w.dec_sp = w.dec_groups = 0;
+    if (small_path(T, K) && T > 0 && N > 0) {
+        plan_decode(K, N, w.dec_ns, w.dec_sp, w.dec_groups);
+        w.dec_part = reinterpret_cast<int32_t*>(carve(static_cast<size_t>(w.dec_ns) * kSmallMaxT *
+                                                      static_cast<size_t>(N) * sizeof(int32_t)));
+        w.dec_tickets = reinterpret_cast<int*>(carve(static_cast<size_t>(w.dec_groups) * sizeof(int)));
+    }
     if (rank > 0 && n_mod > 1) {
         plan_kslices(T, K, w.n_kslices, w.kslice);
         const size_t ur = static_cast<size_t>(T) * static_cast<size_t>(rank) * sizeof(float);
@@ -152,7 +160,8 @@ masq_status fused_stage(const Fused& a, int stage) {
         const bool hl = cmc && !masq::small_path(a.T, a.c_in) &&
                         masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt));
         st = from_hip(masq::launch_gemm(w.q, w.x_scale, a.wq, a.w_scale, a.T, a.c_in, a.c_out,
-                                        a.modality, w.u, hl ? w.u_hl : nullptr, w.u_part,
+                                        a.modality, w.u, hl ? w.u_hl : nullptr, w.dec_part,
+                                        w.dec_tickets, w.u_part,
                                         w.n_kslices, a.rank, a.n_mod,
                                         a.r_up, to_dt(a.lr_dt), cmc, nullptr, a.y, to_dt(a.y_dt),
                                         s));
@@ -213,7 +222,7 @@ masq_status masq_w8a8_gemm(const int8_t* q, const float* x_scale, const int8_t* 
     if (T == 0) return MASQ_OK;
     (void)hipGetLastError();
     return from_hip(masq::launch_gemm(q, x_scale, wq, w_scale, T, c_in, c_out, nullptr, nullptr,
-                                      nullptr, nullptr, 1, 0, 1, nullptr, DT::BF16, false, acc, y, to_dt(y_dt),
+                                      nullptr, nullptr, nullptr, nullptr, 1, 0, 1, nullptr, DT::BF16, false, acc, y, to_dt(y_dt),
                                       static_cast<hipStream_t>(stream)));
 }
 

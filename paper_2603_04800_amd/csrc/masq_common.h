@@ -17,11 +17,27 @@ constexpr int kDownRows = kRowsDown;
 constexpr int kDownStep = 512;    // k granularity of a down-projection slice (128 per wave)
 constexpr int kMaxRank = 256;
 constexpr int kSmallMaxT = 16;    // batches this small use the Wq-streaming GEMM
-constexpr int kSmallSlices = 32;  // down-projection k slices summed by that GEMM
+constexpr int kSmallSlices = 32;  // down-projection k slices (at most; >= 512 columns each) summed by that GEMM
+constexpr int kUBatch = 16;        // slice partials of u a thread keeps in flight when adding them
 
 // The small-batch path: the Wq-streaming GEMM, which also adds the
 // down-projection's k-slice partials itself.
 inline bool small_path(int64_t T, int64_t K) { return T <= kSmallMaxT && K % 64 == 0; }
+
+// Decode GEMM of the fused small-batch path: a workgroup covers kDecCh output
+// channels and one k slice of at most kDecSteps 64-byte steps (its waves hold
+// every Wq step of the slice in registers).  ns slices of sp steps (the last
+// may be shorter, none is empty), ngroups channel groups.
+constexpr int kDecSteps = 40;
+constexpr int kDecCh = 64;
+constexpr int kDecMaxSlices = 8;    // longer rows (K > 8 * 40 * 64) take the single-pass GEMM
+inline void plan_decode(int64_t K, int64_t N, int& ns, int& sp, int& ngroups) {
+    const int64_t nsteps = K / 64;
+    const int64_t ns0 = (nsteps + kDecSteps - 1) / kDecSteps;
+    sp = static_cast<int>((nsteps + ns0 - 1) / ns0);
+    ns = static_cast<int>((nsteps + sp - 1) / sp);
+    ngroups = static_cast<int>((N + kDecCh - 1) / kDecCh);
+}
 constexpr int64_t kRowsPerWaveMinT = 256;   // batches this large quantise one row per wave
 
 enum class DT : int { F32 = 0, BF16 = 1 };
@@ -50,6 +66,9 @@ struct Workspace {
     uint8_t* u_hl;     // [T][256 B] u as bf16 hi | lo rows (rank <= 64, large batches)
     float* u_part;     // [n_kslices][T][rank] fp32 partial sums over k slices (n_kslices > 1)
     int* tickets;      // [ceil(T / kDownRows)] arrival counters of the slice workgroups
+    int32_t* dec_part; // small-batch path: [ns][kSmallMaxT][N] int32 partial sums per k slice
+    int* dec_tickets;  // small-batch path: [ngroups] arrival counters (zeroed by stage 1)
+    int dec_ns, dec_sp, dec_groups;   // plan_decode of the small-batch path
     int n_kslices;
     int kslice;
     size_t bytes;
@@ -85,11 +104,13 @@ hipError_t launch_stage1_small(const void* x, DT x_dt, const int32_t* mod, const
 
 // u: the down-projection; on the small-batch path (small_path) with
 // n_kslices > 1 the GEMM adds the slice partials u_part itself.  u_hl
-// (optional): u as bf16 hi/lo rows, written by the fused stage 1.
+// (optional): u as bf16 hi/lo rows, written by the fused stage 1.  dec_part /
+// dec_tickets (optional, small-batch path): workspace of the k-sliced decode
+// GEMM; without them the single-pass small-batch GEMM runs.
 hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        const float* w_scale, int64_t T, int64_t K, int64_t N,
                        const int32_t* mod, const float* u, const uint8_t* u_hl,
-                       const float* u_part, int n_kslices,
+                       int32_t* dec_part, int* dec_tickets, const float* u_part, int n_kslices,
                        int rank, int n_mod, const void* r_up, DT lr_dt, bool cmc, int32_t* acc,
                        void* y, DT y_dt, hipStream_t s);
 

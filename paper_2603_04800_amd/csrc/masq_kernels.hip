@@ -516,13 +516,16 @@ __global__ __launch_bounds__(64 * kDownWaves) void k_lowrank_down(const XT* __re
 
 // Stage 1 of the small-batch path in one launch: workgroups [0, T) quantise
 // one row each, workgroups [T, T + n_kslices) compute one k slice of the
-// down-projection (partials left for the GEMM to add).
+// down-projection (partials left for the GEMM to add).  Workgroup 0 also
+// clears zero_ints (the decode GEMM's arrival counters).
 template <typename XT, typename LT>
 __global__ __launch_bounds__(64 * kDownWaves) void k_stage1_small(
     const XT* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
     const LT* __restrict__ l_down, int T, int K, int r, int n_mod, int kslice, int n_kslices,
     int8_t* __restrict__ q, float* __restrict__ x_scale, float* __restrict__ u,
-    float* __restrict__ u_part) {
+    float* __restrict__ u_part, int* __restrict__ zero_ints, int n_zero) {
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < n_zero; i += blockDim.x) zero_ints[i] = 0;
     if (static_cast<int>(blockIdx.x) < T) {
         sq_row<XT, 64 * kDownWaves, kSqChunks / 2>(x, mod, inv_s, K, n_mod, q, x_scale, blockIdx.x);
     } else if (l_down != nullptr) {
@@ -1690,6 +1693,59 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
 // compensation u L2^m in fp32 for non-text tokens, and the store.
 constexpr int kSmallDepth = 16;
 
+// u of a small batch's rows into LDS (256 threads), adding the k-slice
+// partials in slice order when the down-projection left them separate.
+__device__ __forceinline__ void small_u_rows(float (&su)[kSmallMaxT][kMaxRank],
+                                             const float* __restrict__ u,
+                                             const float* __restrict__ u_part, int n_kslices,
+                                             int T, int r, int tid) {
+    const bool parts = u_part != nullptr && n_kslices > 1;
+    const float* src = parts ? u_part : u;
+    const int slices = parts ? n_kslices : 1;
+    for (int idx = 4 * tid; idx < T * r; idx += 4 * 256) {       // T r % 16 == 0
+        v4f v = {0.f, 0.f, 0.f, 0.f};
+        for (int q0 = 0; q0 < slices; q0 += kUBatch) {
+            v4f p[kUBatch];
+#pragma unroll
+            for (int q = 0; q < kUBatch; ++q)                        // a batch in flight
+                p[q] = *reinterpret_cast<const v4f*>(
+                    src + static_cast<int64_t>(min(q0 + q, slices - 1)) * T * r + idx);
+#pragma unroll
+            for (int q = 0; q < kUBatch; ++q)
+                if (q0 + q < slices) v = (q0 + q == 0) ? p[q] : v + p[q];   // slice order
+        }
+        const int tt = idx / r, c = idx - tt * r;
+        *reinterpret_cast<v4f*>(&su[tt][c]) = v;
+    }
+}
+
+// Dequantisation, compensation (u rows in su) and store of one output of a
+// small batch: token t, channel ch, int32 accumulator a.
+template <typename YT, typename LT>
+__device__ __forceinline__ void small_output(const float (&su)[kSmallMaxT][kMaxRank], int a, int t,
+                                             int ch, int N, const float* __restrict__ x_scale,
+                                             const float* __restrict__ w_scale,
+                                             const int32_t* __restrict__ mod, bool cmc, int r,
+                                             int n_mod, const LT* __restrict__ r_up,
+                                             YT* __restrict__ y) {
+    float v = (static_cast<float>(a) * x_scale[t]) * w_scale[ch];
+    const int m = cmc ? sane_mod(mod[t], n_mod) : 0;
+    if (m > 0) {
+        const LT* rr = r_up + (static_cast<int64_t>(m - 1) * N + ch) * r;
+        float c = 0.f;
+        for (int k0 = 0; k0 < r; k0 += 8) {
+            float uv[8], rv[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) uv[k] = su[t][k0 + k];
+            Elem<LT>::load8(rr + k0, rv);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) c = fmaf(uv[k], rv[k], c);
+        }
+        v += c;
+    }
+    Elem<YT>::store1(y + static_cast<int64_t>(t) * N + ch, v);
+}
+
 template <typename YT, typename LT>
 __global__ __launch_bounds__(256) void k_gemm_small(
     const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
@@ -1732,28 +1788,7 @@ __global__ __launch_bounds__(256) void k_gemm_small(
     // acc[e]: token 4 (lane / 16) + e, channel col0 + lane % 16
 #pragma unroll
     for (int e = 0; e < 4; ++e) part[wave][4 * (lane >> 4) + e][lane & 15] = acc[e];
-    // u of the batch's rows into LDS, adding the k-slice partials in slice
-    // order when the down-projection left them separate
-    if (u != nullptr) {
-        const bool parts = u_part != nullptr && n_kslices > 1;
-        const float* src = parts ? u_part : u;
-        const int slices = parts ? n_kslices : 1;
-        for (int idx = 4 * tid; idx < T * r; idx += 4 * 256) {       // T r % 16 == 0
-            v4f v = {0.f, 0.f, 0.f, 0.f};
-            for (int q0 = 0; q0 < slices; q0 += 8) {
-                v4f p[8];
-#pragma unroll
-                for (int q = 0; q < 8; ++q)                              // 8 loads in flight
-                    p[q] = *reinterpret_cast<const v4f*>(
-                        src + static_cast<int64_t>(min(q0 + q, slices - 1)) * T * r + idx);
-#pragma unroll
-                for (int q = 0; q < 8; ++q)
-                    if (q0 + q < slices) v = (q0 + q == 0) ? p[q] : v + p[q];   // slice order
-            }
-            const int tt = idx / r, c = idx - tt * r;
-            *reinterpret_cast<v4f*>(&su[tt][c]) = v;
-        }
-    }
+    if (u != nullptr) small_u_rows(su, u, u_part, n_kslices, T, r, tid);
     __syncthreads();
     const int t = tid >> 4, o = tid & 15;
     if (t >= T) return;
@@ -1761,22 +1796,223 @@ __global__ __launch_bounds__(256) void k_gemm_small(
     const int ch = col0 + o;
     if (acc_out != nullptr) acc_out[static_cast<int64_t>(t) * N + ch] = a;
     if (y == nullptr) return;
-    float v = (static_cast<float>(a) * x_scale[t]) * w_scale[ch];
-    const int m = (u != nullptr) ? sane_mod(mod[t], n_mod) : 0;
-    if (m > 0) {
-        const LT* rr = r_up + (static_cast<int64_t>(m - 1) * N + ch) * r;
-        float c = 0.f;
-        for (int k0 = 0; k0 < r; k0 += 8) {
-            float uv[8], rv[8];
-#pragma unroll
-            for (int k = 0; k < 8; ++k) uv[k] = su[t][k0 + k];
-            Elem<LT>::load8(rr + k0, rv);
-#pragma unroll
-            for (int k = 0; k < 8; ++k) c = fmaf(uv[k], rv[k], c);
-        }
-        v += c;
+    small_output<YT, LT>(su, a, t, ch, N, x_scale, w_scale, mod, u != nullptr, r, n_mod, r_up, y);
+}
+
+// ---------------------------------------------------------------- decode GEMM
+// The fused layer's small-batch GEMM.  At most 16 tokens make the layer a
+// stream of Wq from HBM, so the kernel is shaped to keep as many Wq bytes in
+// flight as it can: a workgroup covers kDecCh output channels (16 per wave)
+// and one k slice of sp <= kDecSteps 64-byte steps, and each wave issues all
+// of its slice's Wq loads at once into registers.  The slice of q goes to
+// LDS by DMA queued ahead of those loads (vector-memory loads complete in
+// issue order, so waiting for q does not wait for Wq).  The int32 partial
+// sums of each slice go to the workspace; the last workgroup of a channel
+// group to arrive adds the slices in slice order and finishes the outputs
+// like the single-pass kernel (dequantisation, compensation, store).
+template <typename YT, typename LT>
+__global__ __launch_bounds__(256, 2) void k_gemm_decode(
+    const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
+    const float* __restrict__ w_scale, int T, int K, int N, int ns, int sp,
+    const int32_t* __restrict__ mod, const float* __restrict__ u,
+    const float* __restrict__ u_part, int n_kslices, int r, int n_mod,
+    const LT* __restrict__ r_up, int32_t* __restrict__ part, int* __restrict__ tickets,
+    YT* __restrict__ y) {
+    __shared__ __attribute__((aligned(16))) uint8_t sq[kDecSteps * 1024];
+    __shared__ float su[kSmallMaxT][kMaxRank];
+    __shared__ int s_last;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = blockIdx.x / ns, sl = blockIdx.x - g * ns;        // channel group, k slice
+    const int st0 = sl * sp;
+    const int S = min(sp, (K >> 6) - st0);                         // steps of this slice, >= 1
+    const int cb = g * kDecCh + 16 * wave;                         // the wave's first channel
+    const bool active = cb < N;
+
+    // q slice into LDS: step j as 16 rows x 64 bytes, row t's piece p at
+    // position p ^ swz4(t); rows past T repeat row T - 1 (results discarded)
+    const uint32_t sq0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sq));
+    {
+        const int t = lane >> 2, p = (lane & 3) ^ swz4(lane >> 2);
+        const int8_t* qa = A + static_cast<int64_t>(min(t, T - 1)) * K +
+                           static_cast<int64_t>(st0) * 64 + 16 * p;
+        for (int j = wave; j < S; j += 4) lds_dma16(qa + 64 * j, sq0 + j * 1024);
     }
-    Elem<YT>::store1(y + static_cast<int64_t>(t) * N + ch, v);
+    // every Wq step of the slice (steps past S repeat step S - 1 and are not
+    // used; a wave past N reads the last channel block and stores nothing)
+    v4i fb[kDecSteps];
+    {
+        const int8_t* bp = B + static_cast<int64_t>(min(cb, N - 16) + (lane & 15)) * K +
+                           static_cast<int64_t>(st0) * 64 + 16 * (lane >> 4);
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int j = 0; j < kDecSteps; ++j)
+            fb[j] = *reinterpret_cast<const v4i*>(bp + 64 * min(j, S - 1));
+        asm volatile("" ::: "memory");
+    }
+    // this wave's q loads are the ones older than its kDecSteps Wq loads;
+    // the barrier publishes every wave's share
+    MASQ_WAIT_VMCNT_LGKM0(kDecSteps);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    v4i acc = {0, 0, 0, 0};
+    {
+        const int rt = lane & 15;
+        const uint8_t* rd = sq + rt * 64 + (((lane >> 4) ^ swz4(rt)) << 4);
+        const v4i zero = {0, 0, 0, 0};
+#pragma unroll
+        for (int j = 0; j < kDecSteps; ++j) {
+            // steps past S multiply zeros (MFMA does not branch on lanes)
+            v4i fa = *reinterpret_cast<const v4i*>(rd + min(j, S - 1) * 1024);
+            fa = j < S ? fa : zero;
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa, fb[j], acc, 0, 0, 0);
+        }
+    }
+    // Hand-over of the partials without cache maintenance: they are written
+    // and read only by agent-scope atomic accesses, which the XCD-local L2
+    // does not hold back, and every store has completed (vmcnt 0) before the
+    // workgroup's arrival is counted.  (A device-scope fence would write
+    // back the whole L2 of the XCD, once per workgroup.)
+    // acc[e]: token 4 (lane / 16) + e, channel cb + lane % 16
+    if (active) {
+        int32_t* pp = part + static_cast<int64_t>(sl) * kSmallMaxT * N + cb + (lane & 15);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int t = 4 * (lane >> 4) + e;
+            if (t < T)
+                __hip_atomic_store(pp + static_cast<int64_t>(t) * N, acc[e], __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    MASQ_WAIT_VMCNT_LGKM0(0);
+    __syncthreads();
+    if (tid == 0)
+        s_last = __hip_atomic_fetch_add(&tickets[g], 1, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT) == ns - 1;
+    __syncthreads();
+    if (!s_last) return;
+    if (tid == 0)                       // ready for the next launch
+        __hip_atomic_store(&tickets[g], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+    // Everything the outputs need is loaded before any of it is used: the
+    // slice partials of the thread's outputs (slices past ns re-read slice
+    // ns - 1 and are not added), their scales and modality ids, the L2 rows
+    // of the group's channels for every non-text modality (into the q
+    // buffer, free now, slot (m - 1) kDecCh + o, when they fit in
+    // kRStage bytes) and the u rows of the batch.
+    constexpr int kOut = kSmallMaxT * kDecCh / 256;
+    constexpr int kRStage = 16384;
+    constexpr int kRPieces = kRStage / 16 / 256;                       // per thread
+    const bool cmc = u != nullptr;
+    int pv[kOut][kDecMaxSlices], mv[kOut];
+    float dxv[kOut], dwv[kOut];
+#pragma unroll
+    for (int i = 0; i < kOut; ++i) {
+        const int idx = tid + 256 * i;
+        const int t = min(idx / kDecCh, T - 1), ch = min(g * kDecCh + idx % kDecCh, N - 1);
+        int32_t* pa = part + static_cast<int64_t>(t) * N + ch;
+#pragma unroll
+        for (int q = 0; q < kDecMaxSlices; ++q)
+            pv[i][q] = __hip_atomic_load(pa + static_cast<int64_t>(min(q, ns - 1)) * kSmallMaxT * N,
+                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        dxv[i] = x_scale[t];
+        dwv[i] = w_scale[ch];
+        mv[i] = cmc ? sane_mod(mod[t], n_mod) : 0;
+    }
+    const int row_bytes = r * static_cast<int>(sizeof(LT));
+    const bool staged = cmc && (n_mod - 1) * kDecCh * row_bytes <= kRStage;
+    const int per_row = row_bytes >> 4;                                // 16-byte pieces per row
+    const int pieces = staged ? (n_mod - 1) * kDecCh * per_row : 0;
+    v4i rpc[kRPieces];
+#pragma unroll
+    for (int k = 0; k < kRPieces; ++k) {
+        const int i = min(tid + 256 * k, max(pieces - 1, 0));
+        const int row = i / max(per_row, 1), pc = i - row * max(per_row, 1);
+        const int mm = row / kDecCh, o = row - mm * kDecCh;
+        const int ch = min(g * kDecCh + o, N - 1);
+        if (tid + 256 * k < pieces)
+            rpc[k] = *reinterpret_cast<const v4i*>(
+                reinterpret_cast<const uint8_t*>(r_up + (static_cast<int64_t>(mm) * N + ch) * r) +
+                16 * pc);
+    }
+    // u rows: one v4f of T x r per thread, the k slices in batches of kUB
+    // (the first issued with the loads above), when the batch is small
+    // enough; else the general loop
+    const bool u_fast = cmc && T * r <= 4 * 256;
+    const int uslices = (u_part != nullptr && n_kslices > 1) ? n_kslices : 1;
+    const float* usrc = uslices > 1 ? u_part : u;
+    constexpr int kUB = kUBatch;
+    v4f up[kUB];
+    if (u_fast && 4 * tid < T * r) {
+#pragma unroll
+        for (int q = 0; q < kUB; ++q)
+            if (q < uslices)
+                up[q] = *reinterpret_cast<const v4f*>(usrc + static_cast<int64_t>(q) * T * r + 4 * tid);
+    }
+#pragma unroll
+    for (int k = 0; k < kRPieces; ++k) {
+        const int i = tid + 256 * k;
+        if (i < pieces) {
+            const int row = i / per_row, pc = i - row * per_row;
+            *reinterpret_cast<v4i*>(sq + row * row_bytes + 16 * pc) = rpc[k];
+        }
+    }
+    if (u_fast) {
+        if (4 * tid < T * r) {
+            v4f v = up[0];
+#pragma unroll
+            for (int q = 1; q < kUB; ++q)
+                if (q < uslices) v = v + up[q];                     // slice order
+            for (int q0 = kUB; q0 < uslices; q0 += kUB) {
+#pragma unroll
+                for (int q = 0; q < kUB; ++q)
+                    if (q0 + q < uslices)
+                        up[q] = *reinterpret_cast<const v4f*>(
+                            usrc + static_cast<int64_t>(q0 + q) * T * r + 4 * tid);
+#pragma unroll
+                for (int q = 0; q < kUB; ++q)
+                    if (q0 + q < uslices) v = v + up[q];
+            }
+            const int tt = (4 * tid) / r, c = 4 * tid - tt * r;
+            *reinterpret_cast<v4f*>(&su[tt][c]) = v;
+        }
+    } else if (cmc) {
+        small_u_rows(su, u, u_part, n_kslices, T, r, tid);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kOut; ++i) {
+        const int idx = tid + 256 * i;
+        const int t = idx / kDecCh, o = idx % kDecCh, ch = g * kDecCh + o;
+        if (t >= T || ch >= N) continue;
+        int a = pv[i][0];
+#pragma unroll
+        for (int q = 1; q < kDecMaxSlices; ++q) a += q < ns ? pv[i][q] : 0;
+        float v = (static_cast<float>(a) * dxv[i]) * dwv[i];
+        const int m = mv[i];
+        if (m > 0) {
+            float c = 0.f;
+            if (staged) {
+                const LT* rr = reinterpret_cast<const LT*>(sq + ((m - 1) * kDecCh + o) * row_bytes);
+                for (int k0 = 0; k0 < r; k0 += 8) {
+                    float rv[8];
+                    Elem<LT>::load8(rr + k0, rv);
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) c = fmaf(su[t][k0 + k], rv[k], c);
+                }
+            } else {
+                const LT* rr = r_up + (static_cast<int64_t>(m - 1) * N + ch) * r;
+                for (int k0 = 0; k0 < r; k0 += 8) {
+                    float rv[8];
+                    Elem<LT>::load8(rr + k0, rv);
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) c = fmaf(su[t][k0 + k], rv[k], c);
+                }
+            }
+            v += c;
+        }
+        Elem<YT>::store1(y + static_cast<int64_t>(t) * N + ch, v);
+    }
 }
 
 }  // namespace
@@ -1862,7 +2098,8 @@ static void launch_stage1_small_t(const void* x, const int32_t* mod, const float
     hipLaunchKernelGGL((k_stage1_small<XT, LT>), dim3(blocks), dim3(64 * kDownWaves), 0, s,
                        static_cast<const XT*>(x), mod, inv_s, cmc ? static_cast<const LT*>(ld) : nullptr,
                        static_cast<int>(T), static_cast<int>(K), rank, n_mod, w.kslice, w.n_kslices,
-                       w.q, w.x_scale, w.u, w.u_part);
+                       w.q, w.x_scale, w.u, w.u_part, w.dec_tickets,
+                       w.dec_tickets ? w.dec_groups : 0);
 }
 
 hipError_t launch_stage1_small(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
@@ -1876,6 +2113,20 @@ hipError_t launch_stage1_small(const void* x, DT x_dt, const int32_t* mod, const
         else launch_stage1_small_t<float, float>(x, mod, inv_s, l_down, T, K, rank, n_mod, cmc, w, s);
     }
     return hipGetLastError();
+}
+
+template <typename YT, typename LT>
+static void launch_gemm_decode_t(const int8_t* q, const float* x_scale, const int8_t* wq,
+                                 const float* w_scale, int64_t T, int64_t K, int64_t N,
+                                 const int32_t* mod, const float* u, const float* u_part,
+                                 int n_kslices, int rank, int n_mod, const void* r_up,
+                                 int32_t* part, int* tickets, void* y, hipStream_t s) {
+    int ns, sp, ngroups;
+    plan_decode(K, N, ns, sp, ngroups);
+    hipLaunchKernelGGL((k_gemm_decode<YT, LT>), dim3(static_cast<unsigned>(ngroups * ns)), dim3(256),
+                       0, s, q, wq, x_scale, w_scale, static_cast<int>(T), static_cast<int>(K),
+                       static_cast<int>(N), ns, sp, mod, u, u_part, n_kslices, rank, n_mod,
+                       static_cast<const LT*>(r_up), part, tickets, static_cast<YT*>(y));
 }
 
 template <typename YT, typename LT>
@@ -1913,8 +2164,25 @@ static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* w
 hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        const float* w_scale, int64_t T, int64_t K, int64_t N,
                        const int32_t* mod, const float* u, const uint8_t* u_hl,
-                       const float* u_part, int n_kslices, int rank, int n_mod, const void* r_up,
-                       DT lr_dt, bool cmc, int32_t* acc, void* y, DT y_dt, hipStream_t s) {
+                       int32_t* dec_part, int* dec_tickets, const float* u_part, int n_kslices,
+                       int rank, int n_mod, const void* r_up, DT lr_dt, bool cmc, int32_t* acc,
+                       void* y, DT y_dt, hipStream_t s) {
+    int dns = 0, dsp = 0, dng = 0;
+    if (small_path(T, K)) plan_decode(K, N, dns, dsp, dng);
+    if (small_path(T, K) && dec_part != nullptr && dec_tickets != nullptr && acc == nullptr &&
+        dns <= kDecMaxSlices) {
+        const float* uu = cmc ? u : nullptr;
+#define MASQ_DEC(YT, LT) launch_gemm_decode_t<YT, LT>(q, x_scale, wq, w_scale, T, K, N, mod, uu, u_part, n_kslices, rank, n_mod, r_up, dec_part, dec_tickets, y, s)
+        if (y_dt == DT::BF16) {
+            if (lr_dt == DT::BF16) MASQ_DEC(bf16_t, bf16_t);
+            else MASQ_DEC(bf16_t, float);
+        } else {
+            if (lr_dt == DT::BF16) MASQ_DEC(float, bf16_t);
+            else MASQ_DEC(float, float);
+        }
+#undef MASQ_DEC
+        return hipGetLastError();
+    }
     if (small_path(T, K)) {
         const float* uu = cmc ? u : nullptr;
 #define MASQ_SMALL(YT, LT) launch_gemm_small_t<YT, LT>(q, x_scale, wq, w_scale, T, K, N, mod, uu, u_part, n_kslices, rank, n_mod, r_up, acc, y, s)

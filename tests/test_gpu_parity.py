@@ -171,6 +171,11 @@ _EDGE = {
     "sliced_down_fp32": dict(T=9, K=2064, N=48, r=16, M=3, act="f32", lr="f32"),
     "decode_t16_k4096": dict(T=16, K=4096, N=512, r=64, M=2, act="bf16", lr="bf16"),
     "decode_t5_alternating": dict(T=5, K=1024, N=272, r=64, M=3, act="bf16", lr="bf16"),
+    # k-sliced decode GEMM: ragged last slice, a partial last channel group
+    "decode_t7_k2624_n208_two_slices": dict(T=7, K=2624, N=208, r=32, M=3, act="bf16",
+                                            lr="bf16"),
+    "decode_t16_k5184_fp32_three_slices": dict(T=16, K=5184, N=96, r=16, M=2, act="f32",
+                                               lr="f32"),
     # grids with few tiles split K across workgroups (raw int32 slices added exactly)
     "splitk_bf16": dict(T=300, K=2048, N=512, r=64, M=3, act="bf16", lr="bf16"),
     "splitk_fp32_ragged": dict(T=260, K=1600, N=272, r=16, M=2, act="f32", lr="f32"),
