@@ -544,29 +544,34 @@ __global__ __launch_bounds__(64 * kDownWaves) void k_stage1_small(
 // LDS in a fixed order.  Pass 2 re-reads the wave's part (from cache) and
 // writes the int8 codes with the row's reciprocal scale.
 constexpr int kFuseWaves = 8;
+constexpr int kFuseWideMinT = 8192;    // batches from this size take 32 rows per workgroup
 
-template <typename XT>
+template <typename XT, int RG>
 __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
     const XT* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
     const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod,
     int8_t* __restrict__ q, float* __restrict__ x_scale, float* __restrict__ u,
     uint8_t* __restrict__ u_hl) {
-    __shared__ int smod[kRowsDown];
-    __shared__ float samax[kFuseWaves][kRowsDown];
-    __shared__ float red[kFuseWaves][kRowsDown][64];
-    __shared__ float srq[kRowsDown];
+    constexpr int kRows = 16 * RG;                 // RG groups of 16 rows share each L1 fragment
+    __shared__ int smod[kRows];
+    __shared__ float samax[kFuseWaves][kRows];
+    __shared__ float red[kFuseWaves][kRows][64];
+    __shared__ float srq[kRows];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kRowsDown;
-    if (tid < kRowsDown) {
+    const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kRows;
+    if (tid < kRows) {
         const int64_t t = row0 + tid;
         smod[tid] = t < T ? sane_mod(mod[t], n_mod) : 0;
     }
     __syncthreads();
     // non-text modalities present in the tile, as a list (scalar registers:
     // the MFMA loop below must branch on it, MFMA ignores EXEC)
-    const unsigned present = static_cast<unsigned>(
-        __builtin_amdgcn_readfirstlane(static_cast<int>(tile_presence(smod))));
+    unsigned pres = 0;
+#pragma unroll
+    for (int i = 0; i < kRows; ++i)
+        if (smod[i] > 0) pres |= 1u << smod[i];
+    const unsigned present = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(pres)));
     int mods[3] = {0, 0, 0};
     int np = 0;
     for (int m = 1; m < n_mod; ++m)
@@ -577,39 +582,55 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
     const int per = ((K + kFuseWaves * kStep - 1) / (kFuseWaves * kStep)) * kStep;
     const int kb = min(K, wave * per), ke = min(K, kb + per);
     const int ar = lane & 15, kg = lane >> 4;
-    const int64_t t = row0 + ar;
-    const bool valid = t < T;
-    const int mrow = smod[ar];
-    const XT* xrow = x + (valid ? t : row0) * static_cast<int64_t>(K);
-    const float* srow = inv_s + static_cast<int64_t>(mrow) * K;
-
-    v4f acc[4];
+    bool valid[RG];
+    int mrow[RG];
+    const XT* xrow[RG];
+    const float* srow[RG];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[j] = v4f{0.f, 0.f, 0.f, 0.f};
-    float amax = 0.f;
+    for (int g = 0; g < RG; ++g) {
+        const int64_t t = row0 + 16 * g + ar;
+        valid[g] = t < T;
+        mrow[g] = smod[16 * g + ar];
+        xrow[g] = x + (valid[g] ? t : row0) * static_cast<int64_t>(K);
+        srow[g] = inv_s + static_cast<int64_t>(mrow[g]) * K;
+    }
+
+    v4f acc[RG][4];
+    float amax[RG];
+#pragma unroll
+    for (int g = 0; g < RG; ++g) {
+        amax[g] = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[g][j] = v4f{0.f, 0.f, 0.f, 0.f};
+    }
     const v4i zero = {0, 0, 0, 0};
     for (int k0 = kb; k0 < ke; k0 += kStep * kU) {
-        float xv[kU][8], sv[kU][8];
+        float xv[RG][kU][8], sv[RG][kU][8];
         bool ok[kU];
 #pragma unroll
         for (int uu = 0; uu < kU; ++uu) {
             const int k = k0 + kStep * uu + 8 * kg;
             ok[uu] = k < ke;
             const int kc = ok[uu] ? k : ke - 8;
-            Elem<XT>::load8(xrow + kc, xv[uu]);
-            load8_f32(srow + kc, sv[uu]);
-        }
-        v4i hi[kU], lo[kU];
 #pragma unroll
-        for (int uu = 0; uu < kU; ++uu) {
-            float xs[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                xs[e] = xv[uu][e] * sv[uu][e];
-                if (valid && ok[uu]) amax = fmaxf(amax, fabsf(xs[e]));
+            for (int g = 0; g < RG; ++g) {
+                Elem<XT>::load8(xrow[g] + kc, xv[g][uu]);
+                load8_f32(srow[g] + kc, sv[g][uu]);
             }
-            split_bf16x8(xs, hi[uu], lo[uu]);
         }
+        v4i hi[RG][kU], lo[RG][kU];
+#pragma unroll
+        for (int g = 0; g < RG; ++g)
+#pragma unroll
+            for (int uu = 0; uu < kU; ++uu) {
+                float xs[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    xs[e] = xv[g][uu][e] * sv[g][uu][e];
+                    if (valid[g] && ok[uu]) amax[g] = fmaxf(amax[g], fabsf(xs[e]));
+                }
+                split_bf16x8(xs, hi[g][uu], lo[g][uu]);
+            }
         for (int p = 0; p < np; ++p) {                        // usually one modality
             const bf16_t* lm = l_down + static_cast<int64_t>(mods[p] - 1) * r * K;
             v4i bv[kU][4];
@@ -622,36 +643,46 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
                     bv[uu][j] = *reinterpret_cast<const v4i*>(
                         lm + static_cast<int64_t>(16 * min(j, ncb - 1) + ar) * K + kc);
             }
-            const bool mine = valid && mrow == mods[p];
 #pragma unroll
-            for (int uu = 0; uu < kU; ++uu) {
-                const bool use = mine && ok[uu];
-                const v4i h = use ? hi[uu] : zero, l = use ? lo[uu] : zero;
+            for (int g = 0; g < RG; ++g) {
+                const bool mine = valid[g] && mrow[g] == mods[p];
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    if (j >= ncb) break;
-                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(v8bf, h), __builtin_bit_cast(v8bf, bv[uu][j]), acc[j], 0, 0, 0);
-                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(v8bf, l), __builtin_bit_cast(v8bf, bv[uu][j]), acc[j], 0, 0, 0);
+                for (int uu = 0; uu < kU; ++uu) {
+                    const bool use = mine && ok[uu];
+                    const v4i h = use ? hi[g][uu] : zero, l = use ? lo[g][uu] : zero;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        if (j >= ncb) break;
+                        acc[g][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            __builtin_bit_cast(v8bf, h), __builtin_bit_cast(v8bf, bv[uu][j]), acc[g][j], 0, 0, 0);
+                        acc[g][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            __builtin_bit_cast(v8bf, l), __builtin_bit_cast(v8bf, bv[uu][j]), acc[g][j], 0, 0, 0);
+                    }
                 }
             }
         }
     }
     // the four lanes of a row (lane % 16) hold its four k groups
-    amax = fmaxf(amax, __shfl_xor(amax, 16));
-    amax = fmaxf(amax, __shfl_xor(amax, 32));
-    if (lane < 16) samax[wave][lane] = amax;
+#pragma unroll
+    for (int g = 0; g < RG; ++g) {
+        float a = amax[g];
+        a = fmaxf(a, __shfl_xor(a, 16));
+        a = fmaxf(a, __shfl_xor(a, 32));
+        if (lane < 16) samax[wave][16 * g + lane] = a;
+    }
     if (np > 0) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            if (j >= ncb) break;
+        for (int g = 0; g < RG; ++g)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) red[wave][4 * (lane >> 4) + i][16 * j + (lane & 15)] = acc[j][i];
-        }
+            for (int j = 0; j < 4; ++j) {
+                if (j >= ncb) break;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    red[wave][16 * g + 4 * (lane >> 4) + i][16 * j + (lane & 15)] = acc[g][j][i];
+            }
     }
     __syncthreads();
-    if (tid < kRowsDown) {
+    if (tid < kRows) {
         float a = samax[0][tid];
 #pragma unroll
         for (int w = 1; w < kFuseWaves; ++w) a = fmaxf(a, samax[w][tid]);
@@ -663,7 +694,8 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
     // rows [hi 64 | lo 64] for the GEMM epilogue (text rows and columns past
     // r zero there): thread (row, g) sums columns 8 g .. 8 g + 7 over the
     // waves in a fixed order
-    if (tid < kRowsDown * 8 && (np > 0 || u_hl != nullptr)) {
+    static_assert(kRows * 8 <= 64 * kFuseWaves, "one thread per (row, 8 columns)");
+    if (tid < kRows * 8 && (np > 0 || u_hl != nullptr)) {
         const int row = tid >> 3, g = tid & 7;
         const int64_t t = row0 + row;
         if (t < T) {
@@ -684,7 +716,6 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
             if (u_hl != nullptr) {
                 v4i hi, lo;
                 split_bf16x8(v, hi, lo);
-                const v4i zero = {0, 0, 0, 0};
                 const bool live = smod[row] > 0;
                 *reinterpret_cast<v4i*>(u_hl + t * 256 + 16 * g) = live ? hi : zero;
                 *reinterpret_cast<v4i*>(u_hl + t * 256 + 128 + 16 * g) = live ? lo : zero;
@@ -693,31 +724,42 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
     }
     __syncthreads();
 
-    // pass 2: lane -> row lane / 4, 16 consecutive elements at 16 (lane % 4)
-    const int qr = lane >> 2, qc = 16 * (lane & 3);
-    const int64_t tq = row0 + qr;
-    if (tq < T) {
-        const float rq = srq[qr];
-        const XT* xr2 = x + tq * static_cast<int64_t>(K);
-        const float* sr2 = inv_s + static_cast<int64_t>(smod[qr]) * K;
-        int8_t* qrow = q + tq * static_cast<int64_t>(K);
-        for (int k0 = kb; k0 < ke; k0 += 64) {
-            const int k = k0 + qc;
-            if (k >= ke) continue;
-            float xv[16], sv[16];
-            Elem<XT>::load8(xr2 + k, *reinterpret_cast<float(*)[8]>(xv));
-            Elem<XT>::load8(xr2 + k + 8, *reinterpret_cast<float(*)[8]>(xv + 8));
-            load8_f32(sr2 + k, *reinterpret_cast<float(*)[8]>(sv));
-            load8_f32(sr2 + k + 8, *reinterpret_cast<float(*)[8]>(sv + 8));
+    // pass 2: lane -> row 16 g + lane / 4 of each row group, 16 consecutive
+    // elements at 16 (lane % 4); the row groups' loads go out together
+    const int qc = 16 * (lane & 3);
+    for (int k0 = kb; k0 < ke; k0 += 64) {
+        const int k = k0 + qc;
+        float xv[RG][16], sv[RG][16];
+        bool live[RG];
+#pragma unroll
+        for (int g = 0; g < RG; ++g) {
+            const int qr = 16 * g + (lane >> 2);
+            const int64_t tq = row0 + qr;
+            live[g] = tq < T && k < ke;
+            const int64_t tl = live[g] ? tq : row0;
+            const int kl = live[g] ? k : kb;
+            const XT* xr2 = x + tl * static_cast<int64_t>(K);
+            const float* sr2 = inv_s + static_cast<int64_t>(smod[qr]) * K;
+            Elem<XT>::load8(xr2 + kl, *reinterpret_cast<float(*)[8]>(xv[g]));
+            Elem<XT>::load8(xr2 + kl + 8, *reinterpret_cast<float(*)[8]>(xv[g] + 8));
+            load8_f32(sr2 + kl, *reinterpret_cast<float(*)[8]>(sv[g]));
+            load8_f32(sr2 + kl + 8, *reinterpret_cast<float(*)[8]>(sv[g] + 8));
+        }
+#pragma unroll
+        for (int g = 0; g < RG; ++g) {
+            if (!live[g]) continue;
+            const int qr = 16 * g + (lane >> 2);
+            const float rq = srq[qr];
             uint32_t w[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-                float c = rintf((xv[e] * sv[e]) * rq);
+                float c = rintf((xv[g][e] * sv[g][e]) * rq);
                 c = fminf(fmaxf(c, -127.0f), 127.0f);
                 w[e >> 2] |= (static_cast<uint32_t>(static_cast<int32_t>(c)) & 0xFFu) << (8 * (e & 3));
             }
-            *reinterpret_cast<v4i*>(qrow + k) = v4i{static_cast<int32_t>(w[0]), static_cast<int32_t>(w[1]),
-                                                    static_cast<int32_t>(w[2]), static_cast<int32_t>(w[3])};
+            *reinterpret_cast<v4i*>(q + (row0 + qr) * static_cast<int64_t>(K) + k) =
+                v4i{static_cast<int32_t>(w[0]), static_cast<int32_t>(w[1]), static_cast<int32_t>(w[2]),
+                    static_cast<int32_t>(w[3])};
         }
     }
 }
@@ -2078,15 +2120,20 @@ hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const
                                const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
                                int8_t* q, float* x_scale, float* u, uint8_t* u_hl,
                                hipStream_t s) {
-    const dim3 grid(static_cast<unsigned>((T + kRowsDown - 1) / kRowsDown)), block(64 * kFuseWaves);
-    if (x_dt == DT::BF16)
-        hipLaunchKernelGGL(k_stage1_fused<bf16_t>, grid, block, 0, s, static_cast<const bf16_t*>(x),
-                           mod, inv_s, static_cast<const bf16_t*>(l_down), T, static_cast<int>(K),
-                           rank, n_mod, q, x_scale, u, u_hl);
-    else
-        hipLaunchKernelGGL(k_stage1_fused<float>, grid, block, 0, s, static_cast<const float*>(x),
-                           mod, inv_s, static_cast<const bf16_t*>(l_down), T, static_cast<int>(K),
-                           rank, n_mod, q, x_scale, u, u_hl);
+    // 32 rows per workgroup halve the L1 re-reads once the batch fills the
+    // chip at that size; smaller batches keep 16 rows for more workgroups
+    const bool wide = T >= kFuseWideMinT;
+    const int rows = wide ? 32 : 16;
+    const dim3 grid(static_cast<unsigned>((T + rows - 1) / rows)), block(64 * kFuseWaves);
+#define MASQ_F1(XT, RG) hipLaunchKernelGGL((k_stage1_fused<XT, RG>), grid, block, 0, s, \
+        static_cast<const XT*>(x), mod, inv_s, static_cast<const bf16_t*>(l_down), T, \
+        static_cast<int>(K), rank, n_mod, q, x_scale, u, u_hl)
+    if (x_dt == DT::BF16) {
+        if (wide) MASQ_F1(bf16_t, 2); else MASQ_F1(bf16_t, 1);
+    } else {
+        if (wide) MASQ_F1(float, 2); else MASQ_F1(float, 1);
+    }
+#undef MASQ_F1
     return hipGetLastError();
 }
 

@@ -181,6 +181,9 @@ _EDGE = {
     "splitk_fp32_ragged": dict(T=260, K=1600, N=272, r=16, M=2, act="f32", lr="f32"),
     # the compensation operands loaded as extra stages of the K ring: the
     # shortest ring (four 64-byte stages), ranks below 64, mixed tiles
+    # 32-row stage-1 workgroups (batches of 8192 tokens and more), ragged tail
+    "stage1_wide_ragged_t8200": dict(T=8200, K=128, N=32, r=64, M=3, act="bf16", lr="bf16",
+                                     layout="runs"),
     "ring_tail_k256_rank16": dict(T=520, K=256, N=272, r=16, M=2, act="bf16", lr="bf16",
                                   layout="runs"),
     "ring_tail_k320_rank32": dict(T=300, K=320, N=256, r=32, M=3, act="bf16", lr="bf16"),
