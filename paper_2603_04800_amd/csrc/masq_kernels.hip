@@ -81,6 +81,32 @@ template <> struct Elem<bf16_t> {
 
 __device__ __forceinline__ void load8_f32(const float* p, float (&v)[8]) { Elem<float>::load8(p, v); }
 
+// Eight elements as loaded (16 or 32 bytes), converted to fp32 only when
+// used, so that a software pipeline can keep the load in flight meanwhile.
+template <typename T> struct Raw8;
+template <> struct Raw8<bf16_t> {
+    v4i a;
+    __device__ __forceinline__ void load(const bf16_t* p) { a = *reinterpret_cast<const v4i*>(p); }
+    __device__ __forceinline__ void to_f32(float (&v)[8]) const {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[2 * j] = __uint_as_float(static_cast<uint32_t>(a[j]) << 16);
+            v[2 * j + 1] = __uint_as_float(static_cast<uint32_t>(a[j]) & 0xFFFF0000u);
+        }
+    }
+};
+template <> struct Raw8<float> {
+    v4f a, b;
+    __device__ __forceinline__ void load(const float* p) {
+        a = *reinterpret_cast<const v4f*>(p);
+        b = *reinterpret_cast<const v4f*>(p + 4);
+    }
+    __device__ __forceinline__ void to_f32(float (&v)[8]) const {
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    }
+};
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
@@ -604,44 +630,71 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
         for (int j = 0; j < 4; ++j) acc[g][j] = v4f{0.f, 0.f, 0.f, 0.f};
     }
     const v4i zero = {0, 0, 0, 0};
-    for (int k0 = kb; k0 < ke; k0 += kStep * kU) {
-        float xv[RG][kU][8], sv[RG][kU][8];
-        bool ok[kU];
+    // Pass 1 as a two-deep software pipeline (one row group): the loads of
+    // the next 64 columns (rows, smoothing factors, L1 rows of the first
+    // modality present) are issued before the current ones are used; the L1
+    // rows of further modalities are loaded in place.
+    struct Stage {
+        Raw8<XT> xr[RG][kU];
+        Raw8<float> sr[RG][kU];
+        v4i bv[kU][4];
+    };
+    const bf16_t* lm0 = l_down + static_cast<int64_t>(max(mods[0] - 1, 0)) * r * K;
+    auto issue = [&](int k0, Stage& S) __attribute__((always_inline)) {
 #pragma unroll
         for (int uu = 0; uu < kU; ++uu) {
             const int k = k0 + kStep * uu + 8 * kg;
-            ok[uu] = k < ke;
-            const int kc = ok[uu] ? k : ke - 8;
+            const int kc = k < ke ? k : ke - 8;
 #pragma unroll
             for (int g = 0; g < RG; ++g) {
-                Elem<XT>::load8(xrow[g] + kc, xv[g][uu]);
-                load8_f32(srow[g] + kc, sv[g][uu]);
+                S.xr[g][uu].load(xrow[g] + kc);
+                S.sr[g][uu].load(srow[g] + kc);
+            }
+            if (np > 0) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    S.bv[uu][j] = *reinterpret_cast<const v4i*>(
+                        lm0 + static_cast<int64_t>(16 * min(j, ncb - 1) + ar) * K + kc);
             }
         }
+    };
+    auto compute = [&](int k0, const Stage& S) __attribute__((always_inline)) {
+        bool ok[kU];
+#pragma unroll
+        for (int uu = 0; uu < kU; ++uu) ok[uu] = k0 + kStep * uu + 8 * kg < ke;
         v4i hi[RG][kU], lo[RG][kU];
 #pragma unroll
         for (int g = 0; g < RG; ++g)
 #pragma unroll
             for (int uu = 0; uu < kU; ++uu) {
-                float xs[8];
+                float xv[8], sv[8], xs[8];
+                S.xr[g][uu].to_f32(xv);
+                S.sr[g][uu].to_f32(sv);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    xs[e] = xv[g][uu][e] * sv[g][uu][e];
+                    xs[e] = xv[e] * sv[e];
                     if (valid[g] && ok[uu]) amax[g] = fmaxf(amax[g], fabsf(xs[e]));
                 }
                 split_bf16x8(xs, hi[g][uu], lo[g][uu]);
             }
         for (int p = 0; p < np; ++p) {                        // usually one modality
-            const bf16_t* lm = l_down + static_cast<int64_t>(mods[p] - 1) * r * K;
             v4i bv[kU][4];
+            if (p == 0) {
 #pragma unroll
-            for (int uu = 0; uu < kU; ++uu) {
-                const int k = k0 + kStep * uu + 8 * kg;
-                const int kc = ok[uu] ? k : ke - 8;
+                for (int uu = 0; uu < kU; ++uu)
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    bv[uu][j] = *reinterpret_cast<const v4i*>(
-                        lm + static_cast<int64_t>(16 * min(j, ncb - 1) + ar) * K + kc);
+                    for (int j = 0; j < 4; ++j) bv[uu][j] = S.bv[uu][j];
+            } else {
+                const bf16_t* lm = l_down + static_cast<int64_t>(mods[p] - 1) * r * K;
+#pragma unroll
+                for (int uu = 0; uu < kU; ++uu) {
+                    const int k = k0 + kStep * uu + 8 * kg;
+                    const int kc = ok[uu] ? k : ke - 8;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        bv[uu][j] = *reinterpret_cast<const v4i*>(
+                            lm + static_cast<int64_t>(16 * min(j, ncb - 1) + ar) * K + kc);
+                }
             }
 #pragma unroll
             for (int g = 0; g < RG; ++g) {
@@ -660,6 +713,26 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
                     }
                 }
             }
+        }
+    };
+    constexpr int kSpan = kStep * kU;
+    if constexpr (RG == 1) {
+        if (kb < ke) {
+            Stage A, B;
+            issue(kb, A);
+            for (int k0 = kb; k0 < ke; k0 += 2 * kSpan) {
+                if (k0 + kSpan < ke) issue(k0 + kSpan, B);
+                compute(k0, A);
+                if (k0 + kSpan >= ke) break;
+                if (k0 + 2 * kSpan < ke) issue(k0 + 2 * kSpan, A);
+                compute(k0 + kSpan, B);
+            }
+        }
+    } else {                          // two row groups: no registers for a second stage
+        for (int k0 = kb; k0 < ke; k0 += kSpan) {
+            Stage A;
+            issue(k0, A);
+            compute(k0, A);
         }
     }
     // the four lanes of a row (lane % 16) hold its four k groups
