@@ -52,6 +52,7 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
                                                       static_cast<size_t>(N) * sizeof(int32_t)));
         w.dec_tickets = reinterpret_cast<int*>(carve(static_cast<size_t>(w.dec_groups) * sizeof(int)));
     }
+    int n_down_tickets = 0;
     if (rank > 0 && n_mod > 1) {
         plan_kslices(T, K, w.n_kslices, w.kslice);
         const size_t ur = static_cast<size_t>(T) * static_cast<size_t>(rank) * sizeof(float);
@@ -61,10 +62,28 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
         if (w.n_kslices > 1) {
             w.u_part = reinterpret_cast<float*>(carve(ur * static_cast<size_t>(w.n_kslices)));
             if (!small_path(T, K))    // the small-batch GEMM adds the partials itself
-                w.tickets = reinterpret_cast<int*>(
-                    carve(static_cast<size_t>((T + kDownRows - 1) / kDownRows) * sizeof(int)));
+                n_down_tickets = static_cast<int>((T + kDownRows - 1) / kDownRows);
         }
     }
+    w.gk_splits = plan_gemm_splits(T, K, N);
+    const int n_gk_tickets = w.gk_splits > 1 ? static_cast<int>(((T + kTileM - 1) / kTileM) *
+                                                                 ((N + kTileN - 1) / kTileN))
+                                             : 0;
+    // the arrival counters of the down-projection and of the split GEMM lie
+    // side by side, so that stage 1 clears them in one go
+    w.tickets = nullptr;
+    w.gk_tickets = nullptr;
+    w.zero_base = nullptr;
+    w.n_zero = n_down_tickets + n_gk_tickets;
+    if (w.n_zero > 0) {
+        w.zero_base = reinterpret_cast<int*>(carve(static_cast<size_t>(w.n_zero) * sizeof(int)));
+        if (n_down_tickets > 0) w.tickets = w.zero_base;
+        if (n_gk_tickets > 0) w.gk_tickets = w.zero_base ? w.zero_base + n_down_tickets : nullptr;
+    }
+    w.gk_part = nullptr;
+    if (n_gk_tickets > 0)
+        w.gk_part = reinterpret_cast<int32_t*>(carve(static_cast<size_t>(n_gk_tickets) * w.gk_splits *
+                                                     kTileM * kTileN * sizeof(int32_t)));
     w.bytes = off;
     return w;
 }
@@ -140,13 +159,12 @@ masq_status fused_stage(const Fused& a, int stage) {
     } else if ((stage & 1) && cmc && masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt))) {
         st = from_hip(masq::launch_stage1_fused(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                 a.l_down, a.T, a.c_in, a.rank, a.n_mod, w.q,
-                                                w.x_scale, w.u, w.u_hl, s));
+                                                w.x_scale, w.u, w.u_hl, w.zero_base, w.n_zero, s));
         if (st != MASQ_OK) return st;
     } else if (stage & 1) {
-        const int n_tickets = w.tickets ? static_cast<int>((a.T + masq::kDownRows - 1) / masq::kDownRows) : 0;
         st = from_hip(masq::launch_smooth_quant(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                 a.T, a.c_in, a.n_mod, w.q, w.x_scale,
-                                                w.tickets, n_tickets, s));
+                                                w.zero_base, w.n_zero, s));
         if (st != MASQ_OK) return st;
         if (cmc) {
             st = from_hip(masq::launch_lowrank_down(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
@@ -161,7 +179,8 @@ masq_status fused_stage(const Fused& a, int stage) {
                         masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt));
         st = from_hip(masq::launch_gemm(w.q, w.x_scale, a.wq, a.w_scale, a.T, a.c_in, a.c_out,
                                         a.modality, w.u, hl ? w.u_hl : nullptr, w.dec_part,
-                                        w.dec_tickets, w.u_part,
+                                        w.dec_tickets, w.gk_splits, w.gk_part, w.gk_tickets,
+                                        w.u_part,
                                         w.n_kslices, a.rank, a.n_mod,
                                         a.r_up, to_dt(a.lr_dt), cmc, nullptr, a.y, to_dt(a.y_dt),
                                         s));
@@ -222,7 +241,8 @@ masq_status masq_w8a8_gemm(const int8_t* q, const float* x_scale, const int8_t* 
     if (T == 0) return MASQ_OK;
     (void)hipGetLastError();
     return from_hip(masq::launch_gemm(q, x_scale, wq, w_scale, T, c_in, c_out, nullptr, nullptr,
-                                      nullptr, nullptr, nullptr, nullptr, 1, 0, 1, nullptr, DT::BF16, false, acc, y, to_dt(y_dt),
+                                      nullptr, nullptr, nullptr, 1, nullptr, nullptr, nullptr, 1, 0,
+                                      1, nullptr, DT::BF16, false, acc, y, to_dt(y_dt),
                                       static_cast<hipStream_t>(stream)));
 }
 

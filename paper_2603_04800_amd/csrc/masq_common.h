@@ -24,6 +24,22 @@ constexpr int kUBatch = 16;        // slice partials of u a thread keeps in flig
 // down-projection's k-slice partials itself.
 inline bool small_path(int64_t T, int64_t K) { return T <= kSmallMaxT && K % 64 == 0; }
 
+// K split of the 256 x 256 tile GEMM for grids with few tiles (fused layer,
+// K % 64 == 0): S slices of at least 8 64-byte stages; each slice's int32
+// accumulators go to the workspace and the last slice of a tile to arrive
+// adds them and finishes the tile.
+constexpr int kSplitMaxTiles = 128;   // grids with at least this many tiles are not split
+constexpr int kSplitMax = 4;
+inline int plan_gemm_splits(int64_t T, int64_t K, int64_t N) {
+    if (T <= 0 || N <= 0 || small_path(T, K) || K % 64 != 0) return 1;
+    const int64_t tiles = ((T + kTileM - 1) / kTileM) * ((N + kTileN - 1) / kTileN);
+    if (tiles >= kSplitMaxTiles) return 1;
+    int64_t S = 256 / tiles;
+    if (S > kSplitMax) S = kSplitMax;
+    if (S > (K / 64) / 8) S = (K / 64) / 8;
+    return S < 1 ? 1 : static_cast<int>(S);
+}
+
 // Decode GEMM of the fused small-batch path: a workgroup covers kDecCh output
 // channels and one k slice of at most kDecSteps 64-byte steps (its waves hold
 // every Wq step of the slice in registers).  ns slices of sp steps (the last
@@ -69,6 +85,11 @@ struct Workspace {
     int32_t* dec_part; // small-batch path: [ns][kSmallMaxT][N] int32 partial sums per k slice
     int* dec_tickets;  // small-batch path: [ngroups] arrival counters (zeroed by stage 1)
     int dec_ns, dec_sp, dec_groups;   // plan_decode of the small-batch path
+    int gk_splits;     // plan_gemm_splits
+    int32_t* gk_part;  // [tiles][gk_splits][256 * 256] int32 slice accumulators (gk_splits > 1)
+    int* gk_tickets;   // [tiles] arrival counters (gk_splits > 1); follow `tickets` when both exist
+    int n_zero;        // ints from zero_base that stage 1 clears
+    int* zero_base;
     int n_kslices;
     int kslice;
     size_t bytes;
@@ -94,7 +115,7 @@ inline bool fused_stage1_ok(int64_t T, int64_t K, int rank, DT lr_dt) {
 hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
                                int8_t* q, float* x_scale, float* u, uint8_t* u_hl,
-                               hipStream_t s);
+                               int* zero_ints, int n_zero, hipStream_t s);
 
 // Stage 1 of the small-batch path (small_path): quantisation of every row
 // and the k-sliced down-projection (partials) in one launch.
@@ -110,7 +131,8 @@ hipError_t launch_stage1_small(const void* x, DT x_dt, const int32_t* mod, const
 hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        const float* w_scale, int64_t T, int64_t K, int64_t N,
                        const int32_t* mod, const float* u, const uint8_t* u_hl,
-                       int32_t* dec_part, int* dec_tickets, const float* u_part, int n_kslices,
+                       int32_t* dec_part, int* dec_tickets, int gk_splits, int32_t* gk_part,
+                       int* gk_tickets, const float* u_part, int n_kslices,
                        int rank, int n_mod, const void* r_up, DT lr_dt, bool cmc, int32_t* acc,
                        void* y, DT y_dt, hipStream_t s);
 

@@ -577,8 +577,10 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
     const XT* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
     const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod,
     int8_t* __restrict__ q, float* __restrict__ x_scale, float* __restrict__ u,
-    uint8_t* __restrict__ u_hl) {
+    uint8_t* __restrict__ u_hl, int* __restrict__ zero_ints, int n_zero) {
     constexpr int kRows = 16 * RG;                 // RG groups of 16 rows share each L1 fragment
+    if (blockIdx.x == 0)                           // arrival counters of stage 2
+        for (int i = threadIdx.x; i < n_zero; i += blockDim.x) zero_ints[i] = 0;
     __shared__ int smod[kRows];
     __shared__ float samax[kFuseWaves][kRows];
     __shared__ float red[kFuseWaves][kRows][64];
@@ -1103,8 +1105,10 @@ struct GemmSmem {
     int mod[kTileM];          // modality of each row (invalid ids read as text)
     int rawmod[kTileM];       // modality ids as given (LDS-DMA target)
     unsigned wpresent[8];     // per wave: bit m set if a row of modality m is in its rows
-    uint8_t tr[kTrBytes];
+    uint8_t tr[kTrBytes];     // 16-byte aligned (the transposes use 16-byte LDS accesses)
+    int last;                 // split K: this workgroup is the last slice of its tile to arrive
 };
+static_assert(offsetof(GemmSmem, tr) % 16 == 0, "tr alignment");
 static_assert(4 * 32 * tr_pitch(64) <= kTrBytes && 8 * 32 * tr_pitch(32) <= kTrBytes, "tr");
 
 // Epilogue of a 256 x 256 tile whose int32 accumulators are in acc (this
@@ -1580,18 +1584,28 @@ __device__ __forceinline__ void lds_dma4(const void* src, uint32_t lds_addr) {
 // LDS operands -- u hi, u lo and the L2 rows of each modality present, 32 KB
 // each -- are copied by DMA into the K buffers after the loop, with no
 // conversion in the epilogue.
-template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2>
+template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2, bool SPLIT = false>
 __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
     const float* __restrict__ w_scale, int64_t T, int K, int N, int tiles_m, int tiles_n,
     const int32_t* __restrict__ mod, const float* __restrict__ u, const uint8_t* __restrict__ u_hl,
     int r, int n_mod, const LT* __restrict__ r_up, int32_t* __restrict__ acc_out,
-    YT* __restrict__ y) {
+    YT* __restrict__ y, int S, int32_t* __restrict__ part, int* __restrict__ tickets) {
     __shared__ __attribute__((aligned(16))) GemmSmem sm;
     static_assert(kDmaStages * kDmaStageBytes <= static_cast<int>(sizeof(GemmSmem::buf)), "LDS");
     static_assert(kDmaStageBytes == kTileM * 128, "an epilogue operand fills one K stage buffer");
+    if constexpr (!SPLIT) S = 1;
     int tm, tn;
-    if (!tile_coords(tiles_m, tiles_n, tm, tn)) return;
+    if (!tile_coords(tiles_m, tiles_n * S, tm, tn)) return;
+    // split K: slice sl of S covers stages [kst0, kst0 + nk) of the tile
+    int sl = 0;
+    if constexpr (SPLIT) {
+        sl = tn % S;
+        tn /= S;
+    }
+    const int nk_all = K / kDmaStageK;
+    const int nk_slice = SPLIT ? (nk_all + S - 1) / S : nk_all;
+    const int kst0 = sl * nk_slice;
     const int64_t row0 = static_cast<int64_t>(tm) * kTileM;
     const int col0 = tn * kTileN;
     constexpr int NJ = 8 / NWN, NW = 2 * NWN;
@@ -1642,8 +1656,9 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     for (int j = 0; j < kH; ++j) {
         const int row = wave * kRowsPerWave + 16 * j + (lane >> 2);
         const int chunk = (lane & 3) ^ swz4(row);
-        src[j] = A + min(row0 + row, T - 1) * K + 16 * chunk;
-        src[kH + j] = B + static_cast<int64_t>(min(col0 + row, N - 1)) * K + 16 * chunk;
+        src[j] = A + min(row0 + row, T - 1) * K + kst0 * kDmaStageK + 16 * chunk;
+        src[kH + j] = B + static_cast<int64_t>(min(col0 + row, N - 1)) * K + kst0 * kDmaStageK +
+                      16 * chunk;
         dst_off[j] = static_cast<uint32_t>(
             __builtin_amdgcn_readfirstlane((wave * kRowsPerWave + 16 * j) * kDmaStageK));
         dst_off[kH + j] = kTileM * kDmaStageK + dst_off[j];
@@ -1713,7 +1728,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     // that each body has a single shape.
     using yes = std::true_type;
     using no = std::false_type;
-    const int nk = K / kDmaStageK;
+    const int nk = min(nk_slice, nk_all - kst0);             // >= 1 (plan_gemm_splits)
     for (int st = 0; st < kDmaStages - 1 && st < nk; ++st) issue(st);
     v4i fa0[4], fb0[NJ], fa1[4], fb1[NJ];
     publish(min(nk - 1, 2));
@@ -1775,6 +1790,51 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     for (; kt + kDmaStages - 1 < nk; ++kt) body(kt, yes{}, yes{});
     for (; kt + 1 < nk; ++kt) body(kt, no{}, yes{});
     body(kt, no{}, no{});
+
+    if constexpr (SPLIT) {
+        // Every slice writes its accumulators to its slot of the tile's
+        // workspace (value-major: each 16-byte store instruction covers 1 KB
+        // of consecutive bytes) with the agent-coherent cache policy (sc1),
+        // so the XCD-local L2 does not hold them back, and counts its arrival
+        // once the stores have completed; the last slice to arrive reads the
+        // others' slots with the same policy and adds them (exact in any
+        // order) before the epilogue.  No fence, no waiting on other
+        // workgroups.  Accesses go through a buffer descriptor that covers
+        // exactly the tile's S slots (raw, untyped: descriptor word 3 =
+        // 0x00020000 on this architecture).
+        constexpr int NT = 64 * NW, kV4 = 4 * NJ * 4;          // v4 groups per thread
+        constexpr int kSlot = kTileM * kTileN * 4;            // bytes per slice slot
+        constexpr int kPolicy = 16;                           // sc1
+        const int tile = tm * tiles_n + tn;
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            part + static_cast<int64_t>(tile) * S * (kTileM * kTileN), 0, S * kSlot, 0x00020000);
+#pragma unroll
+        for (int c = 0; c < kV4; ++c) {
+            const v16i& blk = acc[c / (4 * NJ)][(c / 4) % NJ];
+            const v4i v = {blk[4 * (c % 4)], blk[4 * (c % 4) + 1], blk[4 * (c % 4) + 2],
+                           blk[4 * (c % 4) + 3]};
+            __builtin_amdgcn_raw_buffer_store_b128(v, rs, sl * kSlot + (c * NT + tid) * 16, 0, kPolicy);
+        }
+        MASQ_WAIT_VMCNT_LGKM0(0);
+        __syncthreads();
+        if (tid == 0)
+            sm.last = __hip_atomic_fetch_add(&tickets[tile], 1, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT) == S - 1;
+        __syncthreads();
+        if (!sm.last) return;
+        if (tid == 0) __hip_atomic_store(&tickets[tile], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int s2 = 0; s2 < S; ++s2) {
+            if (s2 == sl) continue;
+#pragma unroll
+            for (int c = 0; c < kV4; ++c) {
+                const v4i v = __builtin_amdgcn_raw_buffer_load_b128(
+                    rs, s2 * kSlot + (c * NT + tid) * 16, 0, kPolicy);
+                v16i& blk = acc[c / (4 * NJ)][(c / 4) % NJ];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) blk[4 * (c % 4) + e] += v[e];
+            }
+        }
+    }
 
     EpiDma ed{};
     ed.present = present;
@@ -2192,7 +2252,7 @@ hipError_t launch_lowrank_down(const void* x, DT x_dt, const int32_t* mod, const
 hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
                                int8_t* q, float* x_scale, float* u, uint8_t* u_hl,
-                               hipStream_t s) {
+                               int* zero_ints, int n_zero, hipStream_t s) {
     // 32 rows per workgroup halve the L1 re-reads once the batch fills the
     // chip at that size; smaller batches keep 16 rows for more workgroups
     const bool wide = T >= kFuseWideMinT;
@@ -2200,7 +2260,7 @@ hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const
     const dim3 grid(static_cast<unsigned>((T + rows - 1) / rows)), block(64 * kFuseWaves);
 #define MASQ_F1(XT, RG) hipLaunchKernelGGL((k_stage1_fused<XT, RG>), grid, block, 0, s, \
         static_cast<const XT*>(x), mod, inv_s, static_cast<const bf16_t*>(l_down), T, \
-        static_cast<int>(K), rank, n_mod, q, x_scale, u, u_hl)
+        static_cast<int>(K), rank, n_mod, q, x_scale, u, u_hl, zero_ints, n_zero)
     if (x_dt == DT::BF16) {
         if (wide) MASQ_F1(bf16_t, 2); else MASQ_F1(bf16_t, 1);
     } else {
@@ -2265,17 +2325,28 @@ template <typename YT, typename LT, bool CMC, bool ACC>
 static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* wq,
                           const float* w_scale, int64_t T, int64_t K, int64_t N,
                           const int32_t* mod, const float* u, const uint8_t* u_hl, int rank,
-                          int n_mod, const void* r_up, int32_t* acc, void* y, hipStream_t s) {
+                          int n_mod, const void* r_up, int32_t* acc, void* y, int S,
+                          int32_t* part, int* tickets, hipStream_t s) {
     const int tiles_m = static_cast<int>((T + kTileM - 1) / kTileM);
     const int tiles_n = static_cast<int>((N + kTileN - 1) / kTileN);
     const int nt = tiles_m * tiles_n;
     const dim3 grid(8 * ((nt + 7) / 8)), block(256);
-    if (K % kDmaStageK == 0)
-        hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN>), grid, dim3(128 * kGemmWavesN),
-                           0, s, q, wq, x_scale, w_scale, T, static_cast<int>(K), static_cast<int>(N),
-                           tiles_m, tiles_n, mod, u, u_hl, rank, n_mod, static_cast<const LT*>(r_up),
-                           acc, static_cast<YT*>(y));
-    else
+    if (K % kDmaStageK == 0) {
+        if (part == nullptr || tickets == nullptr) S = 1;
+        const dim3 gridk(8 * ((nt * S + 7) / 8));
+        if (S > 1)
+            hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN, true>), gridk,
+                               dim3(128 * kGemmWavesN), 0, s, q, wq, x_scale, w_scale, T,
+                               static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
+                               u_hl, rank, n_mod, static_cast<const LT*>(r_up), acc,
+                               static_cast<YT*>(y), S, part, tickets);
+        else
+            hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN, false>), gridk,
+                               dim3(128 * kGemmWavesN), 0, s, q, wq, x_scale, w_scale, T,
+                               static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
+                               u_hl, rank, n_mod, static_cast<const LT*>(r_up), acc,
+                               static_cast<YT*>(y), 1, nullptr, nullptr);
+    } else
         hipLaunchKernelGGL((k_gemm<YT, LT, CMC, ACC>), grid, block, 0, s, q, wq, x_scale, w_scale, T,
                            static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
                            rank, n_mod, static_cast<const LT*>(r_up), acc, static_cast<YT*>(y));
@@ -2284,7 +2355,8 @@ static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* w
 hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        const float* w_scale, int64_t T, int64_t K, int64_t N,
                        const int32_t* mod, const float* u, const uint8_t* u_hl,
-                       int32_t* dec_part, int* dec_tickets, const float* u_part, int n_kslices,
+                       int32_t* dec_part, int* dec_tickets, int gk_splits, int32_t* gk_part,
+                       int* gk_tickets, const float* u_part, int n_kslices,
                        int rank, int n_mod, const void* r_up, DT lr_dt, bool cmc, int32_t* acc,
                        void* y, DT y_dt, hipStream_t s) {
     int dns = 0, dsp = 0, dng = 0;
@@ -2316,7 +2388,7 @@ hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
 #undef MASQ_SMALL
         return hipGetLastError();
     }
-#define MASQ_GEMM(YT, LT, C, A) launch_gemm_t<YT, LT, C, A>(q, x_scale, wq, w_scale, T, K, N, mod, u, u_hl, rank, n_mod, r_up, acc, y, s)
+#define MASQ_GEMM(YT, LT, C, A) launch_gemm_t<YT, LT, C, A>(q, x_scale, wq, w_scale, T, K, N, mod, u, u_hl, rank, n_mod, r_up, acc, y, gk_splits, gk_part, gk_tickets, s)
     // the int32 accumulator output exists only for the plain product (no
     // compensation); it is a separate instantiation because storing the
     // accumulators as well raises the epilogue's register pressure
