@@ -1057,6 +1057,32 @@ template <> struct Cmc<float> {           // fp32 operands, v_mfma_f32_32x32x2f3
         return yb;
     }
 
+    // the same for NJ channel blocks at once (rows brow[j] of the staged L2),
+    // reads of 8 k steps batched ahead of their MFMAs and the NJ independent
+    // accumulation chains interleaved
+    template <int NJ>
+    static __device__ __forceinline__ void from_lds_multi(const uint8_t* base_u, const uint8_t* base_r,
+                                                          int rc, int arow, const int (&brow)[NJ],
+                                                          bool live, int lane, v16f (&yb)[NJ]) {
+        const float* su = reinterpret_cast<const float*>(base_u);
+        const float* sr = reinterpret_cast<const float*>(base_r);
+        for (int k0 = 0; k0 < rc; k0 += 16) {                 // rc % 16 == 0
+            float av[8], bv[NJ][8];
+#pragma unroll
+            for (int st = 0; st < 8; ++st) {
+                const int k = k0 + 2 * st + (lane >> 5);
+                av[st] = live ? su[arow * 64 + k] : 0.f;
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) bv[j][st] = sr[brow[j] * 64 + k];
+            }
+#pragma unroll
+            for (int st = 0; st < 8; ++st)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+                    yb[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(bv[j][st], av[st], yb[j], 0, 0, 0);
+        }
+    }
+
     static __device__ __forceinline__ v16f from_global(const float* u, const float* rm, bool live,
                                                        int64_t t, int col, int r, int c0,
                                                        int lane, v16f yb) {
@@ -1385,6 +1411,38 @@ __device__ __forceinline__ void gemm_epilogue(
                             v8bf, *reinterpret_cast<const v4i*>(sr + crow * 128 + ((cc ^ swz(crow)) << 4)));
                         ybs[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bj, __builtin_bit_cast(v8bf, h), ybs[j], 0, 0, 0);
                         ybs[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bj, __builtin_bit_cast(v8bf, l), ybs[j], 0, 0, 0);
+                    }
+                }
+                store_rowblock(i, ybs);
+            }
+            return;
+        }
+    }
+
+    // fp32 factors, all pieces staged: the channel blocks of a token block
+    // advance together (independent MFMA chains, batched LDS reads)
+    if constexpr (CMC && sizeof(LT) == 4) {
+        if (staged) {
+            const int chunk_bytes = Cmc<LT>::kUBytes + n_present * Cmc<LT>::kRBytes;
+            int brow[NJ];
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) brow[j] = wn * kWaveCols + j * 32 + (lane & 31);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int trow = tok_of(i);
+                const int tm_ = sm.mod[trow];
+                v16f ybs[NJ];
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) ybs[j] = dequant(i, j);
+                for (int c = 0; c < n_chunks; ++c) {
+                    int p = 0;
+                    for (int m = 1; m < n_mod; ++m) {
+                        if (!(present & (1u << m))) continue;
+                        const uint8_t* base = sm.buf + c * chunk_bytes;
+                        Cmc<LT>::template from_lds_multi<NJ>(base, base + kChunkBase + p * Cmc<LT>::kRBytes,
+                                                             min(64, r - 64 * c), trow, brow,
+                                                             tm_ == m, lane, ybs);
+                        ++p;
                     }
                 }
                 store_rowblock(i, ybs);
