@@ -252,12 +252,13 @@ def cpu_baseline(layers, min_seconds=10.0, max_runs=64):
 
 def gemm_kernel_label(layers) -> str:
     """Name of the stage-2 kernel(s) the layers dispatch to: batches of at
-    most 16 tokens with K % 64 == 0 take the weight-streaming kernel, other
+    most 16 tokens with K % 64 == 0 take the k-sliced decode kernel (K up to
+    8 slices of 40 64-byte steps; longer rows the single-pass one), other
     K % 64 == 0 shapes the LDS-DMA tile kernel, the rest the general-K one."""
     names = []
     for L in layers:
         T, K = L["x"].shape
-        n = ("k_gemm_small" if T <= 16 and K % 64 == 0
+        n = (("k_gemm_decode" if K <= 8 * 40 * 64 else "k_gemm_small") if T <= 16 and K % 64 == 0
              else "k_gemm_dma" if K % 64 == 0 else "k_gemm")
         if n not in names:
             names.append(n)
