@@ -80,6 +80,14 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
         if (n_down_tickets > 0) w.tickets = w.zero_base;
         if (n_gk_tickets > 0) w.gk_tickets = w.zero_base ? w.zero_base + n_down_tickets : nullptr;
     }
+    w.dw_slices = w.dw_kslice = 0;
+    w.dw_part = nullptr;
+    if (rank > 0 && rank <= 64 && n_mod > 1 && !small_path(T, K) && T >= kDownWideMinT &&
+        K >= kDownWideMinK) {
+        plan_down_wide(T, K, w.dw_slices, w.dw_kslice);
+        w.dw_part = reinterpret_cast<float*>(carve(static_cast<size_t>(w.dw_slices) * T *
+                                                   static_cast<size_t>(rank) * sizeof(float)));
+    }
     w.gk_part = nullptr;
     if (n_gk_tickets > 0)
         w.gk_part = reinterpret_cast<int32_t*>(carve(static_cast<size_t>(n_gk_tickets) * w.gk_splits *
@@ -155,6 +163,17 @@ masq_status fused_stage(const Fused& a, int stage) {
         st = from_hip(masq::launch_stage1_small(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                 a.l_down, to_dt(a.lr_dt), a.T, a.c_in, a.rank,
                                                 a.n_mod, cmc, w, s));
+        if (st != MASQ_OK) return st;
+    } else if ((stage & 1) && cmc && masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt)) &&
+               w.dw_part != nullptr) {
+        // large batch: wide down-projection, then quantisation adding its partials
+        st = from_hip(masq::launch_down_wide(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth, a.l_down,
+                                             a.T, a.c_in, a.rank, a.n_mod, w, s));
+        if (st != MASQ_OK) return st;
+        const masq::UFinish fin{w.dw_part, w.dw_slices, a.rank, w.u, w.u_hl};
+        st = from_hip(masq::launch_smooth_quant(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
+                                                a.T, a.c_in, a.n_mod, w.q, w.x_scale,
+                                                w.zero_base, w.n_zero, s, &fin));
         if (st != MASQ_OK) return st;
     } else if ((stage & 1) && cmc && masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt))) {
         st = from_hip(masq::launch_stage1_fused(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,

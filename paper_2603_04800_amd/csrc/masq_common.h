@@ -24,6 +24,24 @@ constexpr int kUBatch = 16;        // slice partials of u a thread keeps in flig
 // down-projection's k-slice partials itself.
 inline bool small_path(int64_t T, int64_t K) { return T <= kSmallMaxT && K % 64 == 0; }
 
+// Stage 1 of large batches with long rows, bf16 factors, rank <= 64
+// (fused_stage1_ok): the down-projection runs over 128-row tiles and S k
+// slices of kslice columns (about 512 workgroups, slices of at least 256
+// columns); the quantisation kernel then adds the slices' partials into u.
+// (Shorter rows keep the fused stage 1, which reads each row once.)
+constexpr int64_t kDownWideMinT = 1024;
+constexpr int64_t kDownWideMinK = 8192;
+constexpr int kDownWideRows = 128;
+inline void plan_down_wide(int64_t T, int64_t K, int& S, int& kslice) {
+    const int64_t tiles = (T + kDownWideRows - 1) / kDownWideRows;
+    int64_t want = (512 + tiles - 1) / tiles;
+    const int64_t most = (K + 255) / 256;
+    if (want > most) want = most;
+    if (want < 1) want = 1;
+    kslice = static_cast<int>(((K + want - 1) / want + 63) / 64 * 64);
+    S = static_cast<int>((K + kslice - 1) / kslice);
+}
+
 // K split of the 256 x 256 tile GEMM for grids with few tiles (fused layer,
 // K % 64 == 0): S slices of at least 8 64-byte stages; each slice's int32
 // accumulators go to the workspace and the last slice of a tile to arrive
@@ -90,6 +108,8 @@ struct Workspace {
     int* gk_tickets;   // [tiles] arrival counters (gk_splits > 1); follow `tickets` when both exist
     int n_zero;        // ints from zero_base that stage 1 clears
     int* zero_base;
+    int dw_slices, dw_kslice;   // plan_down_wide (dw_part != nullptr)
+    float* dw_part;    // [dw_slices][T][rank] fp32 partials of the wide down-projection
     int n_kslices;
     int kslice;
     size_t bytes;
@@ -99,9 +119,22 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
 
 // zero_ints / n_zero: optional array the kernel clears on the way (the
 // down-projection's tickets, which must start at zero).
+// fin (optional): add the wide down-projection's slice partials into u (and
+// its bf16 hi/lo rows) while quantising.
+struct UFinish {
+    const float* part;   // [slices][T][r]
+    int slices, r;
+    float* u;
+    uint8_t* u_hl;       // may be null
+};
 hipError_t launch_smooth_quant(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                int64_t T, int64_t K, int n_mod, int8_t* q, float* x_scale,
-                               int* zero_ints, int n_zero, hipStream_t s);
+                               int* zero_ints, int n_zero, hipStream_t s,
+                               const UFinish* fin = nullptr);
+
+hipError_t launch_down_wide(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
+                            const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
+                            const Workspace& w, hipStream_t s);
 
 hipError_t launch_lowrank_down(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, DT lr_dt, int64_t T, int64_t K, int rank,

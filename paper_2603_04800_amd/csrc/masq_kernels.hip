@@ -211,15 +211,50 @@ __device__ __forceinline__ void sq_row(const XT* __restrict__ x, const int32_t* 
     }
 }
 
+// u of row t from the wide down-projection's slice partials (one wave, lane
+// k = rank column k < r <= 64): the slices added in slice order; also its
+// bf16 hi/lo row [hi 64 | lo 64] (zero for text rows and columns past r).
+__device__ __forceinline__ void finish_u_row(int64_t t, int64_t T, bool text, const float* part,
+                                             int slices, int r, float* u, uint8_t* u_hl,
+                                             int lane) {
+    const int k = lane;
+    float v = 0.f;                      // text rows: u = 0 (their partials are not written)
+    if (k < r && !text) {
+        const float* p = part + t * r + k;
+        const int64_t step = T * r;
+        v = p[0];
+        for (int s0 = 1; s0 < slices; s0 += 8) {
+            float pv[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) pv[q] = p[min(s0 + q, slices - 1) * step];
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                if (s0 + q < slices) v += pv[q];
+        }
+    }
+    if (k < r) u[t * r + k] = v;
+    if (u_hl != nullptr) {
+        const bool live = !text && k < r;
+        const uint32_t hb = f32_to_bf16(v);
+        const uint32_t lb = f32_to_bf16(v - __uint_as_float(hb << 16));
+        reinterpret_cast<uint16_t*>(u_hl + t * 256)[k] = static_cast<uint16_t>(live ? hb : 0u);
+        reinterpret_cast<uint16_t*>(u_hl + t * 256 + 128)[k] = static_cast<uint16_t>(live ? lb : 0u);
+    }
+}
+
 template <typename XT>
 __global__ __launch_bounds__(256) void k_smooth_quant(const XT* __restrict__ x,
                                                       const int32_t* __restrict__ mod,
                                                       const float* __restrict__ inv_s, int K,
                                                       int n_mod, int8_t* __restrict__ q,
                                                       float* __restrict__ x_scale,
-                                                      int* __restrict__ zero_ints, int n_zero) {
+                                                      int* __restrict__ zero_ints, int n_zero,
+                                                      int64_t T, UFinish fin) {
     if (blockIdx.x == 0)
         for (int i = threadIdx.x; i < n_zero; i += 256) zero_ints[i] = 0;
+    if (fin.part != nullptr && threadIdx.x < 64)
+        finish_u_row(blockIdx.x, T, sane_mod(mod[blockIdx.x], n_mod) == 0, fin.part, fin.slices,
+                     fin.r, fin.u, fin.u_hl, threadIdx.x);
     sq_row<XT, 256, kSqChunks>(x, mod, inv_s, K, n_mod, q, x_scale, blockIdx.x);
 }
 
@@ -238,6 +273,7 @@ __device__ __forceinline__ void split_bf16x8(const float (&v)[8], v4i& hi, v4i& 
 // to 64 * 8 * NC elements; longer rows stream their remainder twice.  Used
 // for large batches; k_smooth_quant (a whole workgroup per row) serves small
 // ones, where a row's latency matters more than the number of rows in flight.
+
 template <typename XT, int NC>
 __global__ __launch_bounds__(256) void k_smooth_quant_rows(const XT* __restrict__ x,
                                                            const int32_t* __restrict__ mod,
@@ -246,13 +282,14 @@ __global__ __launch_bounds__(256) void k_smooth_quant_rows(const XT* __restrict_
                                                            int8_t* __restrict__ q,
                                                            float* __restrict__ x_scale,
                                                            int* __restrict__ zero_ints,
-                                                           int n_zero) {
+                                                           int n_zero, UFinish fin) {
     if (blockIdx.x == 0)
         for (int i = threadIdx.x; i < n_zero; i += 256) zero_ints[i] = 0;
     const int lane = threadIdx.x & 63;
     const int64_t t = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
     if (t >= T) return;
     const int m = sane_mod(mod[t], n_mod);
+    if (fin.part != nullptr) finish_u_row(t, T, m == 0, fin.part, fin.slices, fin.r, fin.u, fin.u_hl, lane);
     const XT* xr = x + t * static_cast<int64_t>(K);
     const float* sr = inv_s + static_cast<int64_t>(m) * K;
     int8_t* qr = q + t * static_cast<int64_t>(K);
@@ -538,6 +575,147 @@ __global__ __launch_bounds__(64 * kDownWaves) void k_lowrank_down(const XT* __re
                                                       int* __restrict__ tickets) {
     down_tile<XT, LT>(x, mod, inv_s, l_down, T, K, r, n_mod, kslice, n_kslices, u, u_part, tickets,
                       blockIdx.x, blockIdx.y);
+}
+
+// Down-projection of large batches (bf16 factors, rank <= 64): u = (x S_m^-1)
+// L1^m of the non-text rows over 128-row tiles (each L1 fragment serves 128
+// rows) and k slices [s kslice, (s + 1) kslice); grid (ceil(T / 128), S).
+// Wave w takes rows 32 w .. 32 w + 31 of the tile (skipping out when none of
+// them is non-text) and accumulates on v_mfma_f32_32x32x16_bf16 with the L1
+// rows as operand A, the hi/lo split of the smoothed rows as operand B, so
+// that each lane ends up with one token and 16 rank columns.  The slice's
+// fp32 partials go to part[s]; the quantisation kernel adds the slices in
+// slice order.
+template <typename XT>
+__global__ __launch_bounds__(256, 2) void k_down_wide(const XT* __restrict__ x,
+                                                   const int32_t* __restrict__ mod,
+                                                   const float* __restrict__ inv_s,
+                                                   const bf16_t* __restrict__ l_down, int64_t T,
+                                                   int K, int r, int n_mod, int kslice,
+                                                   float* __restrict__ part) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int rl = lane & 31, kg = lane >> 5;
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * kDownWideRows + 32 * wave + rl;
+    const bool valid = t < T;
+    const int mrow = valid ? sane_mod(mod[t], n_mod) : 0;
+    unsigned pres = 0;
+    for (int m = 1; m < n_mod; ++m)
+        if (__ballot(valid && mrow == m) != 0ull) pres |= 1u << m;
+    const unsigned present = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(pres)));
+    if (present == 0) return;                                 // uniform: no non-text row here
+    int mods[3] = {0, 0, 0};
+    int np = 0;
+    for (int m = 1; m < n_mod; ++m)
+        if (present & (1u << m)) mods[np++] = m;
+    const int kb = blockIdx.y * kslice, ke = min(K, kb + kslice);
+    const XT* xrow = x + (valid ? t : 0) * static_cast<int64_t>(K);
+    const float* srow = inv_s + static_cast<int64_t>(mrow) * K;
+    const int nrb = (r + 31) >> 5;                            // 32-rank blocks (1 or 2)
+    v16f acc[2];
+    acc[0] = v16f{0.f};
+    acc[1] = v16f{0.f};
+    const v4i zero = {0, 0, 0, 0};
+    // two-deep software pipeline over rounds of kSteps 16-column MFMA steps:
+    // the next round's loads (rows, smoothing factors, L1 rows of the first
+    // modality present) are in flight while the current round is used
+    constexpr int kSteps = 2;
+    struct Stage {
+        Raw8<XT> xr[kSteps];
+        Raw8<float> sr[kSteps];
+        v4i bv[kSteps][2];
+    };
+    const bf16_t* lm0 = l_down + static_cast<int64_t>(mods[0] - 1) * r * K;
+    auto issue = [&](int k0, Stage& S) __attribute__((always_inline)) {
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st) {
+            const int k = k0 + 16 * st + 8 * kg;
+            const int kc = k < ke ? k : ke - 8;
+            S.xr[st].load(xrow + kc);
+            S.sr[st].load(srow + kc);
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb)
+                S.bv[st][rb] = *reinterpret_cast<const v4i*>(
+                    lm0 + static_cast<int64_t>(min(32 * rb + rl, r - 1)) * K + kc);
+        }
+    };
+    auto compute = [&](int k0, const Stage& S) __attribute__((always_inline)) {
+        bool ok[kSteps];
+        v4i hi[kSteps], lo[kSteps];
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st) {
+            ok[st] = k0 + 16 * st + 8 * kg < ke;
+            float xv[8], sv[8], xs[8];
+            S.xr[st].to_f32(xv);
+            S.sr[st].to_f32(sv);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) xs[e] = xv[e] * sv[e];
+            split_bf16x8(xs, hi[st], lo[st]);
+        }
+        for (int p = 0; p < np; ++p) {                        // usually one modality
+            v4i bv[kSteps][2];
+            if (p == 0) {
+#pragma unroll
+                for (int st = 0; st < kSteps; ++st) {
+                    bv[st][0] = S.bv[st][0];
+                    bv[st][1] = S.bv[st][1];
+                }
+            } else {
+                const bf16_t* lm = l_down + static_cast<int64_t>(mods[p] - 1) * r * K;
+#pragma unroll
+                for (int st = 0; st < kSteps; ++st) {
+                    const int k = k0 + 16 * st + 8 * kg;
+                    const int kc = ok[st] ? k : ke - 8;
+#pragma unroll
+                    for (int rb = 0; rb < 2; ++rb)
+                        bv[st][rb] = *reinterpret_cast<const v4i*>(
+                            lm + static_cast<int64_t>(min(32 * rb + rl, r - 1)) * K + kc);
+                }
+            }
+            const bool mine = valid && mrow == mods[p];
+#pragma unroll
+            for (int st = 0; st < kSteps; ++st) {
+                const bool use = mine && ok[st];
+                const v4i h = use ? hi[st] : zero, l = use ? lo[st] : zero;
+#pragma unroll
+                for (int rb = 0; rb < 2; ++rb) {
+                    if (rb >= nrb) break;
+                    // rank rows past r multiply zeros
+                    const v4i bb = (32 * rb + rl < r) ? bv[st][rb] : zero;
+                    acc[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(v8bf, bb), __builtin_bit_cast(v8bf, h), acc[rb], 0, 0, 0);
+                    acc[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(v8bf, bb), __builtin_bit_cast(v8bf, l), acc[rb], 0, 0, 0);
+                }
+            }
+        }
+    };
+    constexpr int kSpan = 16 * kSteps;
+    {
+        Stage A, B;
+        issue(kb, A);
+        for (int k0 = kb; k0 < ke; k0 += 2 * kSpan) {
+            if (k0 + kSpan < ke) issue(k0 + kSpan, B);
+            compute(k0, A);
+            if (k0 + kSpan >= ke) break;
+            if (k0 + 2 * kSpan < ke) issue(k0 + 2 * kSpan, A);
+            compute(k0 + kSpan, B);
+        }
+    }
+    // acc[rb][e]: token t, rank 32 rb + 8 (e / 4) + 4 kg + e % 4
+    if (!valid) return;
+    float* out = part + (static_cast<int64_t>(blockIdx.y) * T + t) * r;
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+        if (rb >= nrb) break;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int rk = 32 * rb + 8 * g + 4 * kg;
+            if (rk < r)
+                *reinterpret_cast<v4f*>(out + rk) =
+                    v4f{acc[rb][4 * g], acc[rb][4 * g + 1], acc[rb][4 * g + 2], acc[rb][4 * g + 3]};
+        }
+    }
 }
 
 // Stage 1 of the small-batch path in one launch: workgroups [0, T) quantise
@@ -2257,29 +2435,30 @@ constexpr int kGemmWavesN = 4;
 
 hipError_t launch_smooth_quant(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                int64_t T, int64_t K, int n_mod, int8_t* q, float* x_scale,
-                               int* zero_ints, int n_zero, hipStream_t s) {
+                               int* zero_ints, int n_zero, hipStream_t s, const UFinish* fin_in) {
+    const UFinish fin = fin_in ? *fin_in : UFinish{nullptr, 0, 0, nullptr, nullptr};
     // a wave per row for large batches whose rows fit its register cache
     if (T >= kRowsPerWaveMinT && K <= 64 * 8 * 8) {
         const dim3 grid(static_cast<unsigned>((T + 3) / 4)), block(256);
         if (x_dt == DT::BF16)
             hipLaunchKernelGGL((k_smooth_quant_rows<bf16_t, 8>), grid, block, 0, s,
                                static_cast<const bf16_t*>(x), mod, inv_s, T, static_cast<int>(K),
-                               n_mod, q, x_scale, zero_ints, n_zero);
+                               n_mod, q, x_scale, zero_ints, n_zero, fin);
         else
             hipLaunchKernelGGL((k_smooth_quant_rows<float, 8>), grid, block, 0, s,
                                static_cast<const float*>(x), mod, inv_s, T, static_cast<int>(K),
-                               n_mod, q, x_scale, zero_ints, n_zero);
+                               n_mod, q, x_scale, zero_ints, n_zero, fin);
         return hipGetLastError();
     }
     const dim3 grid(static_cast<unsigned>(T)), block(256);
     if (x_dt == DT::BF16)
         hipLaunchKernelGGL(k_smooth_quant<bf16_t>, grid, block, 0, s,
                            static_cast<const bf16_t*>(x), mod, inv_s, static_cast<int>(K), n_mod,
-                           q, x_scale, zero_ints, n_zero);
+                           q, x_scale, zero_ints, n_zero, T, fin);
     else
         hipLaunchKernelGGL(k_smooth_quant<float>, grid, block, 0, s,
                            static_cast<const float*>(x), mod, inv_s, static_cast<int>(K), n_mod,
-                           q, x_scale, zero_ints, n_zero);
+                           q, x_scale, zero_ints, n_zero, T, fin);
     return hipGetLastError();
 }
 
@@ -2304,6 +2483,22 @@ hipError_t launch_lowrank_down(const void* x, DT x_dt, const int32_t* mod, const
         if (lr_dt == DT::BF16) launch_down_t<float, bf16_t>(x, mod, inv_s, l_down, T, K, rank, n_mod, w, s);
         else launch_down_t<float, float>(x, mod, inv_s, l_down, T, K, rank, n_mod, w, s);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_down_wide(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
+                            const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
+                            const Workspace& w, hipStream_t s) {
+    const dim3 grid(static_cast<unsigned>((T + kDownWideRows - 1) / kDownWideRows),
+                    static_cast<unsigned>(w.dw_slices)), block(256);
+    if (x_dt == DT::BF16)
+        hipLaunchKernelGGL((k_down_wide<bf16_t>), grid, block, 0, s, static_cast<const bf16_t*>(x),
+                           mod, inv_s, static_cast<const bf16_t*>(l_down), T, static_cast<int>(K),
+                           rank, n_mod, w.dw_kslice, w.dw_part);
+    else
+        hipLaunchKernelGGL((k_down_wide<float>), grid, block, 0, s, static_cast<const float*>(x),
+                           mod, inv_s, static_cast<const bf16_t*>(l_down), T, static_cast<int>(K),
+                           rank, n_mod, w.dw_kslice, w.dw_part);
     return hipGetLastError();
 }
 

@@ -181,6 +181,12 @@ _EDGE = {
     "splitk_fp32_ragged": dict(T=260, K=1600, N=272, r=16, M=2, act="f32", lr="f32"),
     # the compensation operands loaded as extra stages of the K ring: the
     # shortest ring (four 64-byte stages), ranks below 64, mixed tiles
+    # wide down-projection (at least 1024 tokens, rows of 8192 and more):
+    # ragged last k slice, ranks below 64, fp32 activations
+    "down_wide_t1100_k8208_r32": dict(T=1100, K=8208, N=32, r=32, M=3, act="bf16", lr="bf16",
+                                      layout="runs"),
+    "down_wide_f32_t1030_k8192_r48": dict(T=1030, K=8192, N=16, r=48, M=2, act="f32",
+                                          lr="bf16"),
     # 32-row stage-1 workgroups (batches of 8192 tokens and more), ragged tail
     "stage1_wide_ragged_t8200": dict(T=8200, K=128, N=32, r=64, M=3, act="bf16", lr="bf16",
                                      layout="runs"),
