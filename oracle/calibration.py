@@ -9,7 +9,8 @@ C_in up to a few thousand:
   G1  R^m_i = max_t |x^m_{t,i}|                       (Sec. 4.1, range R^m)
   G2  w_i = max_j |w_{j,i}| over the output channels of input channel i
   G3  s^m_i = sqrt(R^m_i / w_i)                       (Sec. 4.2, MAS initial factors)
-  G4  Q(S_t W): per-output-channel symmetric int8     (eq. PTQ, Sec. 4.3)
+  G4  Q(S_t W): per-output-channel symmetric int8 (or 4-bit for W4A8)
+                                                      (eq. PTQ, Sec. 4.3; Tables 1-2)
   G5  dW = S_m W - Q(S_t W)                           (Sec. 4.3, residual)
   G6  P Lambda P^T = SVD((X_m S_m^-1)^T (X_m S_m^-1)), T = (P Lambda^1/2)^T
   G7  SVD(T dW) = U Sigma V^T, truncated to rank r
@@ -51,20 +52,22 @@ def smoothing_factor(r: np.ndarray, wmax: np.ndarray):
     return s32, inv
 
 
-def quantize_weight(w: np.ndarray, s32_text: np.ndarray):
-    """G4: Q(S_t W) with one symmetric scale per output channel.
+def quantize_weight(w: np.ndarray, s32_text: np.ndarray, bits: int = 8):
+    """G4: Q(S_t W) with one symmetric scale per output channel, b-bit codes
+    in [-(2^(b-1) - 1), 2^(b-1) - 1] (b = 8: W8A8; b = 4: the W4A8 setting).
 
     Returns codes wq [N][K] int8, scales w_scale [N] float32 and the
     dequantized weight wdq [K][N] fp64 (codes times the stored fp32 scale)."""
+    qmax = (1 << (bits - 1)) - 1
     ws = np.asarray(s32_text, np.float64)[:, None] * np.asarray(w, np.float64)   # [K][N]
     n = ws.shape[1]
     wq = np.zeros((n, ws.shape[0]), np.int8)
     scale = np.zeros(n, np.float32)
     for o in range(n):
         col = ws[:, o]
-        delta = np.max(np.abs(col)) / QMAX
+        delta = np.max(np.abs(col)) / qmax
         if delta > 0:
-            wq[o] = np.clip(np.rint(col / delta), -QMAX, QMAX).astype(np.int8)
+            wq[o] = np.clip(np.rint(col / delta), -qmax, qmax).astype(np.int8)
         scale[o] = np.float32(delta)
     wdq = wq.T.astype(np.float64) * scale.astype(np.float64)[None, :]
     return wq, scale, wdq
@@ -116,10 +119,13 @@ def cmc_factors(z: np.ndarray, dw: np.ndarray, rank: int, ridge: float = 1e-6):
 
 
 def calibrate(x, modality, w, n_mod: int, rank: int, lr_dtype: str = "f32",
-              base: str = "quantized", ridge: float = 1e-6, smoothing=None) -> dict:
+              base: str = "quantized", ridge: float = 1e-6, smoothing=None,
+              weight_bits: int = 8) -> dict:
     """All artifacts of one layer in the C library's layouts.
 
-    ``smoothing`` optionally overrides the per-modality factors s32 [M][K]."""
+    ``smoothing`` optionally overrides the per-modality factors s32 [M][K];
+    ``weight_bits`` = 4 gives the W4A8 setting (the residual dW and the CMC
+    factors are then taken against the 4-bit shared weight)."""
     x = np.asarray(x, np.float32)
     modality = np.asarray(modality)
     wmax = weight_range(w)
@@ -130,7 +136,7 @@ def calibrate(x, modality, w, n_mod: int, rank: int, lr_dtype: str = "f32",
     else:
         s32 = np.asarray(smoothing, np.float32)
     inv = (np.float32(1.0) / s32).astype(np.float32)
-    wq, w_scale, wdq = quantize_weight(w, s32[0])
+    wq, w_scale, wdq = quantize_weight(w, s32[0], weight_bits)
     k, n = x.shape[1], wq.shape[0]
     l_down = np.zeros((max(n_mod - 1, 0), rank, k))
     r_up = np.zeros((max(n_mod - 1, 0), n, rank))

@@ -51,17 +51,19 @@ def smoothing_factors(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod:
     return s32, inv
 
 
-def quantize_shared_weight(w: np.ndarray, s32_text: np.ndarray):
-    """Q(diag(s_t) W) per output channel -> (wq [N][K] int8, w_scale [N] f32).
+def quantize_shared_weight(w: np.ndarray, s32_text: np.ndarray, bits: int = 8):
+    """Q(diag(s_t) W) per output channel -> (wq [N][K] int8, w_scale [N] f32),
+    b-bit codes in [-(2^(b-1) - 1), 2^(b-1) - 1] (8, or 4 for W4A8).
 
     fp64 throughout: s32 * w is exact, the step is one correctly rounded
     division, codes round half to even (torch.round)."""
     import torch
+    qmax = (1 << (bits - 1)) - 1
     ws = torch.from_numpy(np.ascontiguousarray(w, np.float32)).double()
     ws.mul_(torch.from_numpy(np.asarray(s32_text, np.float32)).double()[:, None])
-    step = ws.abs().amax(dim=0) / QMAX
+    step = ws.abs().amax(dim=0) / qmax
     safe = torch.where(step > 0, step, torch.ones_like(step))
-    codes = torch.round(ws.div_(safe[None, :])).clamp_(-QMAX, QMAX)
+    codes = torch.round(ws.div_(safe[None, :])).clamp_(-qmax, qmax)
     codes[:, step == 0] = 0
     return codes.t().contiguous().to(torch.int8).numpy(), step.float().numpy()
 
@@ -155,7 +157,7 @@ def cmc_factors(z: np.ndarray, dw: np.ndarray, rank: int, ridge: float = 1e-6, s
 
 def calibrate_layer(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: int,
                     rank: int, lr_dtype: str = "bf16", ridge: float = 1e-6,
-                    seed: int = 0) -> dict:
+                    seed: int = 0, weight_bits: int = 8) -> dict:
     """All inference artifacts of one linear from calibration activations.
 
     x: [T][K] float32 calibration rows, modality: [T] ids, w: [K][N] float
@@ -164,7 +166,7 @@ def calibrate_layer(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: i
     modality = np.asarray(modality, np.int32)
     w = np.asarray(w, np.float32)
     s32, inv = smoothing_factors(x, modality, w, n_mod)
-    wq, w_scale = quantize_shared_weight(w, s32[0])
+    wq, w_scale = quantize_shared_weight(w, s32[0], weight_bits)
     k, n = w.shape
     l_down = np.zeros((max(n_mod - 1, 0), rank, k), np.float32)
     r_up = np.zeros((max(n_mod - 1, 0), n, rank), np.float32)
@@ -181,4 +183,4 @@ def calibrate_layer(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: i
         r_up = _to_bf16_values(r_up)
     return dict(inv_smooth=inv, s32=s32, wq=wq, w_scale=w_scale,
                 l_down=np.ascontiguousarray(l_down), r_up=np.ascontiguousarray(r_up),
-                rank=rank, n_mod=n_mod, lr_dtype=lr_dtype)
+                rank=rank, n_mod=n_mod, lr_dtype=lr_dtype, weight_bits=weight_bits)

@@ -214,10 +214,13 @@ def _small_layer(seed, T=(96, 80, 72), K=24, N=20, scales=(1.0, 30.0, 2.0)):
     return x, mod, w
 
 
-@pytest.mark.parametrize("base", ["quantized", "fp"])
-def test_full_rank_reconstructs_modality_smoothed_weight(base):
+@pytest.mark.parametrize("base,bits", [("quantized", 8), ("fp", 8), ("quantized", 4)])
+def test_full_rank_reconstructs_modality_smoothed_weight(base, bits):
+    """At full rank the compensation restores S_m W exactly on top of the
+    shared weight, whatever its bit width (8, or 4 in the W4A8 setting)."""
     x, mod, w = _small_layer(1)
-    art = cal.calibrate(x, mod, w, 3, rank=min(w.shape), lr_dtype="f64", base=base)
+    art = cal.calibrate(x, mod, w, 3, rank=min(w.shape), lr_dtype="f64", base=base,
+                        weight_bits=bits)
     base_w = art["wdq"] if base == "quantized" else art["s32"][0][:, None].astype(np.float64) * w
     for m in (1, 2):
         target = art["s32"][m][:, None].astype(np.float64) * w
@@ -275,6 +278,32 @@ def test_weight_quantizer_properties():
     assert np.all(np.abs(wq).max(axis=1) == 127)
     err = np.abs(wdq - ws)
     assert np.all(err <= scale[None, :].astype(np.float64) * 0.5 * (1 + 1e-6))
+
+
+def test_weight_quantizer_4bit_brute_force():
+    """The 4-bit shared weight of the W4A8 setting (Tables 1-2) under eq. PTQ:
+    per output channel the step is max |S_t W| / 7 and each code is the
+    ratio rounded half to even, clamped to [-7, 7]; checked element by
+    element with Python floats and round()."""
+    rng = np.random.default_rng(5)
+    K, N = 24, 7
+    w = rng.standard_normal((K, N))
+    w[3, 2] = 0.0
+    s32 = rng.uniform(0.3, 3.0, K).astype(np.float32)
+    wq, scale, wdq = cal.quantize_weight(w, s32, bits=4)
+    assert wq.dtype == np.int8 and wq.shape == (N, K)
+    for o in range(N):
+        col = [float(s32[i]) * float(w[i, o]) for i in range(K)]
+        step = max(abs(v) for v in col) / 7
+        assert scale[o] == np.float32(step)
+        for i in range(K):
+            assert int(wq[o, i]) == max(-7, min(7, round(col[i] / step)))
+    assert np.all(np.abs(wq).max(axis=1) == 7)
+    err = np.abs(wdq - s32[:, None].astype(np.float64) * w)
+    assert np.all(err <= scale[None, :].astype(np.float64) * 0.5 * (1 + 1e-6))
+    # a weight already on the 4-bit grid quantizes to itself
+    wq2, scale2, _ = cal.quantize_weight(wdq / s32[:, None].astype(np.float64), s32, bits=4)
+    assert np.array_equal(wq2, wq)
 
 
 def test_theorem2_eckart_young():
