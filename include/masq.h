@@ -149,6 +149,43 @@ masq_status masq_linear_stage2(const void* x, masq_dtype x_dt, const int32_t* mo
                                int32_t rank, int32_t n_mod, void* y, masq_dtype y_dt,
                                void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * 4-bit shared weight (W4A8, the low-bit setting of Tables 1-2).  Q(S_t W)
+ * is quantised per output channel to 4-bit codes (eq. PTQ with b = 4:
+ * codes in [-7, 7], w_scale[o] = max_i |(S_t W)[o][i]| / 7) and stored
+ * packed, two codes per byte: row o of wq4 is c_in / 2 bytes; the 4-byte
+ * word g of a row holds codes 8g .. 8g + 7, its byte b carrying code 8g + b
+ * in the low nibble and code 8g + b + 4 in the high nibble, two's
+ * complement.  The activations stay 8-bit.  Each entry point matches its
+ * int8 counterpart called with the unpacked codes as wq, bit for bit (the
+ * product of codes is still summed exactly in int32), with the same
+ * arguments, workspace (masq_linear_fused_workspace_bytes) and errors, and
+ * in addition: c_in must be a multiple of 64 (else MASQ_ERR_SHAPE); wq4
+ * must be 16-byte aligned (else MASQ_ERR_ALIGN).  The weight bytes read
+ * from memory halve, which is what bounds small batches.
+ */
+masq_status masq_w4a8_gemm(const int8_t* q, const float* x_scale, const uint8_t* wq4,
+                           const float* w_scale, int64_t T, int64_t c_in, int64_t c_out,
+                           int32_t* acc, void* y, masq_dtype y_dt, void* stream);
+masq_status masq_linear_fused_w4a8(const void* x, masq_dtype x_dt, const int32_t* modality,
+                                   const float* inv_smooth, const uint8_t* wq4,
+                                   const float* w_scale, const void* l_down, const void* r_up,
+                                   masq_dtype lr_dt, int64_t T, int64_t c_in, int64_t c_out,
+                                   int32_t rank, int32_t n_mod, void* y, masq_dtype y_dt,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+masq_status masq_linear_stage1_w4a8(const void* x, masq_dtype x_dt, const int32_t* modality,
+                                    const float* inv_smooth, const uint8_t* wq4,
+                                    const float* w_scale, const void* l_down, const void* r_up,
+                                    masq_dtype lr_dt, int64_t T, int64_t c_in, int64_t c_out,
+                                    int32_t rank, int32_t n_mod, void* y, masq_dtype y_dt,
+                                    void* workspace, size_t workspace_bytes, void* stream);
+masq_status masq_linear_stage2_w4a8(const void* x, masq_dtype x_dt, const int32_t* modality,
+                                    const float* inv_smooth, const uint8_t* wq4,
+                                    const float* w_scale, const void* l_down, const void* r_up,
+                                    masq_dtype lr_dt, int64_t T, int64_t c_in, int64_t c_out,
+                                    int32_t rank, int32_t n_mod, void* y, masq_dtype y_dt,
+                                    void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

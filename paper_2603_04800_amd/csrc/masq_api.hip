@@ -129,11 +129,13 @@ struct Fused {
     const int8_t* wq; const float* w_scale; const void* l_down; const void* r_up;
     masq_dtype lr_dt; int64_t T, c_in, c_out; int32_t rank, n_mod; void* y; masq_dtype y_dt;
     void* workspace; size_t workspace_bytes; void* stream;
+    bool w4;      // wq: packed 4-bit codes, [c_out][c_in / 2] bytes
 };
 
 masq_status validate_fused(const Fused& a) {
     masq_status st = check_dims(a.T, a.c_in, a.c_out, true);
     if (st != MASQ_OK) return st;
+    if (a.w4 && a.c_in % 64 != 0) return MASQ_ERR_SHAPE;
     if ((st = check_rank(a.rank, a.n_mod)) != MASQ_OK) return st;
     if (!valid_dt(a.x_dt) || !valid_dt(a.y_dt) || !valid_dt(a.lr_dt)) return MASQ_ERR_DTYPE;
     if (a.T == 0) return MASQ_OK;      // empty batch: nothing is read or written
@@ -202,7 +204,7 @@ masq_status fused_stage(const Fused& a, int stage) {
                                         w.u_part,
                                         w.n_kslices, a.rank, a.n_mod,
                                         a.r_up, to_dt(a.lr_dt), cmc, nullptr, a.y, to_dt(a.y_dt),
-                                        s));
+                                        s, a.w4));
     }
     return st;
 }
@@ -246,11 +248,12 @@ masq_status masq_smooth_quant(const void* x, masq_dtype x_dt, const int32_t* mod
                                               static_cast<hipStream_t>(stream)));
 }
 
-masq_status masq_w8a8_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
-                           const float* w_scale, int64_t T, int64_t c_in, int64_t c_out,
-                           int32_t* acc, void* y, masq_dtype y_dt, void* stream) {
+static masq_status gemm_call(const int8_t* q, const float* x_scale, const int8_t* wq,
+                             const float* w_scale, int64_t T, int64_t c_in, int64_t c_out,
+                             int32_t* acc, void* y, masq_dtype y_dt, void* stream, bool w4) {
     masq_status st = check_dims(T, c_in, c_out, true);
     if (st != MASQ_OK) return st;
+    if (w4 && c_in % 64 != 0) return MASQ_ERR_SHAPE;
     if (!valid_dt(y_dt)) return MASQ_ERR_DTYPE;
     if (T == 0) return MASQ_OK;
     if (!q || !x_scale || !wq || !w_scale || (!acc && !y)) return MASQ_ERR_NULL;
@@ -262,7 +265,20 @@ masq_status masq_w8a8_gemm(const int8_t* q, const float* x_scale, const int8_t* 
     return from_hip(masq::launch_gemm(q, x_scale, wq, w_scale, T, c_in, c_out, nullptr, nullptr,
                                       nullptr, nullptr, nullptr, 1, nullptr, nullptr, nullptr, 1, 0,
                                       1, nullptr, DT::BF16, false, acc, y, to_dt(y_dt),
-                                      static_cast<hipStream_t>(stream)));
+                                      static_cast<hipStream_t>(stream), w4));
+}
+
+masq_status masq_w8a8_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
+                           const float* w_scale, int64_t T, int64_t c_in, int64_t c_out,
+                           int32_t* acc, void* y, masq_dtype y_dt, void* stream) {
+    return gemm_call(q, x_scale, wq, w_scale, T, c_in, c_out, acc, y, y_dt, stream, false);
+}
+
+masq_status masq_w4a8_gemm(const int8_t* q, const float* x_scale, const uint8_t* wq4,
+                           const float* w_scale, int64_t T, int64_t c_in, int64_t c_out,
+                           int32_t* acc, void* y, masq_dtype y_dt, void* stream) {
+    return gemm_call(q, x_scale, reinterpret_cast<const int8_t*>(wq4), w_scale, T, c_in, c_out,
+                     acc, y, y_dt, stream, true);
 }
 
 masq_status masq_lowrank_comp(const void* x, masq_dtype x_dt, const int32_t* modality,
@@ -299,12 +315,27 @@ size_t masq_linear_fused_workspace_bytes(int64_t T, int64_t c_in, int64_t c_out,
         const int8_t *wq, const float *w_scale, const void *l_down, const void *r_up,        \
         masq_dtype lr_dt, int64_t T, int64_t c_in, int64_t c_out, int32_t rank, int32_t n_mod, \
         void *y, masq_dtype y_dt, void *workspace, size_t workspace_bytes, void *stream
-#define MASQ_FUSED_PACK                                                                      \
-    Fused { x, x_dt, modality, inv_smooth, wq, w_scale, l_down, r_up, lr_dt, T, c_in, c_out, \
-            rank, n_mod, y, y_dt, workspace, workspace_bytes, stream }
+#define MASQ_FUSED_ARGS_W4                                                                     \
+    const void *x, masq_dtype x_dt, const int32_t *modality, const float *inv_smooth,        \
+        const uint8_t *wq4, const float *w_scale, const void *l_down, const void *r_up,      \
+        masq_dtype lr_dt, int64_t T, int64_t c_in, int64_t c_out, int32_t rank, int32_t n_mod, \
+        void *y, masq_dtype y_dt, void *workspace, size_t workspace_bytes, void *stream
+#define MASQ_FUSED_PACK(W, FOUR)                                                             \
+    Fused { x, x_dt, modality, inv_smooth, W, w_scale, l_down, r_up, lr_dt, T, c_in, c_out,  \
+            rank, n_mod, y, y_dt, workspace, workspace_bytes, stream, FOUR }
+#define MASQ_W4 reinterpret_cast<const int8_t*>(wq4)
 
-masq_status masq_linear_fused(MASQ_FUSED_ARGS) { return fused_stage(MASQ_FUSED_PACK, 3); }
-masq_status masq_linear_stage1(MASQ_FUSED_ARGS) { return fused_stage(MASQ_FUSED_PACK, 1); }
-masq_status masq_linear_stage2(MASQ_FUSED_ARGS) { return fused_stage(MASQ_FUSED_PACK, 2); }
+masq_status masq_linear_fused(MASQ_FUSED_ARGS) { return fused_stage(MASQ_FUSED_PACK(wq, false), 3); }
+masq_status masq_linear_stage1(MASQ_FUSED_ARGS) { return fused_stage(MASQ_FUSED_PACK(wq, false), 1); }
+masq_status masq_linear_stage2(MASQ_FUSED_ARGS) { return fused_stage(MASQ_FUSED_PACK(wq, false), 2); }
+masq_status masq_linear_fused_w4a8(MASQ_FUSED_ARGS_W4) {
+    return fused_stage(MASQ_FUSED_PACK(MASQ_W4, true), 3);
+}
+masq_status masq_linear_stage1_w4a8(MASQ_FUSED_ARGS_W4) {
+    return fused_stage(MASQ_FUSED_PACK(MASQ_W4, true), 1);
+}
+masq_status masq_linear_stage2_w4a8(MASQ_FUSED_ARGS_W4) {
+    return fused_stage(MASQ_FUSED_PACK(MASQ_W4, true), 2);
+}
 
 }  // extern "C"

@@ -160,14 +160,15 @@ hipError_t launch_stage1_small(const void* x, DT x_dt, const int32_t* mod, const
 // n_kslices > 1 the GEMM adds the slice partials u_part itself.  u_hl
 // (optional): u as bf16 hi/lo rows, written by the fused stage 1.  dec_part /
 // dec_tickets (optional, small-batch path): workspace of the k-sliced decode
-// GEMM; without them the single-pass small-batch GEMM runs.
+// GEMM; without them the single-pass small-batch GEMM runs.  w4: wq holds
+// packed 4-bit codes ([N][K / 2] bytes, K % 64 == 0).
 hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        const float* w_scale, int64_t T, int64_t K, int64_t N,
                        const int32_t* mod, const float* u, const uint8_t* u_hl,
                        int32_t* dec_part, int* dec_tickets, int gk_splits, int32_t* gk_part,
                        int* gk_tickets, const float* u_part, int n_kslices,
                        int rank, int n_mod, const void* r_up, DT lr_dt, bool cmc, int32_t* acc,
-                       void* y, DT y_dt, hipStream_t s);
+                       void* y, DT y_dt, hipStream_t s, bool w4 = false);
 
 hipError_t launch_lowrank_comp(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, const void* r_up, DT lr_dt, int64_t T,

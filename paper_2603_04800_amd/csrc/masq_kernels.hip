@@ -123,6 +123,20 @@ __device__ __forceinline__ int sane_mod(int m, int n_mod) {
 // (or 16) consecutive rows read at one logical chunk land on distinct banks.
 __device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
 
+// 4-bit shared weight.  A row of K codes is packed two per byte, in 4-byte
+// words of 8 codes: byte b of the word holding codes 8g .. 8g + 7 carries
+// code 8g + b in its low nibble and code 8g + b + 4 in its high nibble
+// (two's complement).  Two packed words (16 codes) become one 16-byte int8
+// MFMA operand in k order, each code multiplied by 16: masking leaves every
+// nibble in the high half of its byte, so the int8 byte reads 16 c.  An int32
+// sum of such products is 16 times the true one and a multiple of 16, so an
+// arithmetic shift right by 4 recovers it exactly.  (|16 c q| <= 112 * 127:
+// any K below 2^31 / 14224 stays in range.)
+__device__ __forceinline__ v4i w4_operand(v2i p) {
+    constexpr int kHi = static_cast<int>(0xF0F0F0F0u);
+    return v4i{(p.x << 4) & kHi, p.x & kHi, (p.y << 4) & kHi, p.y & kHi};
+}
+
 // ================================================================ smoothing + quant
 // One workgroup per token row (small batches, where a row's latency
 // matters): the first 256 x 8 x kSqChunks elements of the row are loaded
@@ -1820,7 +1834,15 @@ __device__ __forceinline__ void lds_dma4(const void* src, uint32_t lds_addr) {
 // LDS operands -- u hi, u lo and the L2 rows of each modality present, 32 KB
 // each -- are copied by DMA into the K buffers after the loop, with no
 // conversion in the epilogue.
-template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2, bool SPLIT = false>
+//
+// W4: Wq holds packed 4-bit codes.  A stage's B tile is then 256 rows of 32
+// bytes (two 16-byte halves, the half at position p of row r holding
+// logical half p ^ ((r / 8) % 2), so that a wave's 8-byte fragment reads
+// spread over the banks); lane group h of a wave takes the codes of half h
+// (k chunks 2h and 2h + 1 of the stage, one per k step), and the q
+// fragments follow the same k order.
+template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2, bool SPLIT = false,
+          bool W4 = false>
 __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
     const float* __restrict__ w_scale, int64_t T, int K, int N, int tiles_m, int tiles_n,
@@ -1846,7 +1868,13 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     const int col0 = tn * kTileN;
     constexpr int NJ = 8 / NWN, NW = 2 * NWN;
     constexpr int kRowsPerWave = kTileM / NW;           // DMA rows of A and of B per wave
-    constexpr int kDmaPerStage = 2 * kRowsPerWave / 16; // DMA instructions per thread per stage
+    constexpr int kStepB = W4 ? kDmaStageK / 2 : kDmaStageK;   // B bytes per row and stage
+    constexpr int kDmaA = kRowsPerWave / 16;            // DMA instructions per thread per stage:
+    constexpr int kDmaB = kRowsPerWave * kStepB / 1024; //   A rows, B rows
+    constexpr int kDmaPerStage = kDmaA + kDmaB;
+    constexpr int kDmaExtra = kRowsPerWave / 8;         // per epilogue operand (128-byte rows)
+    static_assert(kDmaB >= 1 && kRowsPerWave * kStepB % 1024 == 0, "B rows per DMA");
+    using BRaw = std::conditional_t<W4, v2i, v4i>;      // a lane's B bytes of one k step
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / NWN, wn = wave % NWN;
     const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sm.buf));
@@ -1883,25 +1911,33 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     // Wave w loads rows [w R, w R + R) of the A and of the B tile (R =
     // kRowsPerWave), 16 rows per instruction; lane i covers row 16 j + i / 4
     // at LDS chunk i % 4, which holds logical chunk (i % 4) ^ swz4(row).
-    // Rows past T or N are clamped into the matrix; their results are
-    // discarded.
-    constexpr int kH = kDmaPerStage / 2;
-    const int8_t* src[kDmaPerStage];      // [0, kH): A rows, [kH, 2 kH): B rows
+    // (W4 B rows: 32 rows per instruction, lane i covers row 32 j + i / 2 at
+    // half i % 2.)  Rows past T or N are clamped into the matrix; their
+    // results are discarded.
+    const int8_t* src[kDmaPerStage];      // [0, kDmaA): A rows, then B rows
     uint32_t dst_off[kDmaPerStage];
 #pragma unroll
-    for (int j = 0; j < kH; ++j) {
+    for (int j = 0; j < kDmaA; ++j) {
         const int row = wave * kRowsPerWave + 16 * j + (lane >> 2);
         const int chunk = (lane & 3) ^ swz4(row);
         src[j] = A + min(row0 + row, T - 1) * K + kst0 * kDmaStageK + 16 * chunk;
-        src[kH + j] = B + static_cast<int64_t>(min(col0 + row, N - 1)) * K + kst0 * kDmaStageK +
-                      16 * chunk;
         dst_off[j] = static_cast<uint32_t>(
             __builtin_amdgcn_readfirstlane((wave * kRowsPerWave + 16 * j) * kDmaStageK));
-        dst_off[kH + j] = kTileM * kDmaStageK + dst_off[j];
+    }
+#pragma unroll
+    for (int j = 0; j < kDmaB; ++j) {
+        constexpr int kRowsPerDma = 1024 / kStepB;
+        const int lanes_per_row = kStepB / 16;
+        const int row = wave * kRowsPerWave + kRowsPerDma * j + lane / lanes_per_row;
+        const int piece = W4 ? ((lane & 1) ^ ((row >> 3) & 1)) : ((lane & 3) ^ swz4(row));
+        src[kDmaA + j] = B + static_cast<int64_t>(min(col0 + row, N - 1)) * (W4 ? K / 2 : K) +
+                         kst0 * kStepB + 16 * piece;
+        dst_off[kDmaA + j] = kTileM * kDmaStageK + static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(
+                                 (wave * kRowsPerWave + kRowsPerDma * j) * kStepB));
     }
     auto issue_one = [&](int st, int q) __attribute__((always_inline)) {
         const uint32_t sbase = lds0 + (st % kDmaStages) * kDmaStageBytes;
-        lds_dma16(src[q] + st * kDmaStageK, sbase + dst_off[q]);
+        lds_dma16(src[q] + st * (q < kDmaA ? kDmaStageK : kStepB), sbase + dst_off[q]);
     };
     auto issue = [&](int st) __attribute__((always_inline)) {
 #pragma unroll
@@ -1909,16 +1945,21 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     };
     // fragment f of one 32-byte k step (f < 4: token block f of the q rows,
     // f >= 4: channel block f - 4 of the Wq rows)
-    auto read_frag = [&](int st, int ks, int f, v4i (&fa)[4], v4i (&fb)[NJ]) __attribute__((always_inline)) {
+    auto read_frag = [&](int st, int ks, int f, v4i (&fa)[4], BRaw (&fb)[NJ]) __attribute__((always_inline)) {
         const uint8_t* sa = sm.buf + (st % kDmaStages) * kDmaStageBytes;
-        const int c = 2 * ks + (lane >> 5);
+        const int c = W4 ? 2 * (lane >> 5) + ks : 2 * ks + (lane >> 5);
         if (f < 4) {
             const int row = wm * 128 + f * 32 + (lane & 31);
             fa[f] = *reinterpret_cast<const v4i*>(sa + row * kDmaStageK + ((c ^ swz4(row)) << 4));
         } else {
             const int row = wn * 32 * NJ + (f - 4) * 32 + (lane & 31);
-            fb[f - 4] = *reinterpret_cast<const v4i*>(sa + kTileM * kDmaStageK + row * kDmaStageK +
-                                                      ((c ^ swz4(row)) << 4));
+            const uint8_t* sb = sa + kTileM * kDmaStageK;
+            if constexpr (W4)
+                fb[f - 4] = *reinterpret_cast<const v2i*>(
+                    sb + row * kStepB + 16 * ((lane >> 5) ^ ((row >> 3) & 1)) + 8 * ks);
+            else
+                fb[f - 4] = *reinterpret_cast<const v4i*>(sb + row * kDmaStageK +
+                                                          ((c ^ swz4(row)) << 4));
         }
     };
     // The 4 NJ MFMAs of one k step.  Interleaved with them, in a fixed order
@@ -1927,12 +1968,18 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     // and with DMA one of stage dma_st's loads after every second MFMA, so
     // the LDS and vector-memory pipelines work while the matrix cores do.
     constexpr int kFrags = 4 + NJ;
-    auto mfma_group = [&](const v4i (&fa)[4], const v4i (&fb)[NJ], auto with_reads, int st_next,
-                          int ks_next, v4i (&na)[4], v4i (&nb)[NJ], auto with_dma, int dma_st)
+    auto mfma_group = [&](const v4i (&fa)[4], const BRaw (&fb)[NJ], auto with_reads, int st_next,
+                          int ks_next, v4i (&na)[4], BRaw (&nb)[NJ], auto with_dma, int dma_st)
                           __attribute__((always_inline)) {
+        v4i ub[NJ];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            if constexpr (W4) ub[j] = w4_operand(fb[j]);
+            else ub[j] = fb[j];
+        }
 #pragma unroll
         for (int q = 0; q < 4 * NJ; ++q) {
-            acc[q / NJ][q % NJ] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[q % NJ], fa[q / NJ],
+            acc[q / NJ][q % NJ] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ub[q % NJ], fa[q / NJ],
                                                                         acc[q / NJ][q % NJ], 0, 0, 0);
             if constexpr (decltype(with_reads)::value)
                 if (2 * q < kFrags) {
@@ -1966,7 +2013,8 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     using no = std::false_type;
     const int nk = min(nk_slice, nk_all - kst0);             // >= 1 (plan_gemm_splits)
     for (int st = 0; st < kDmaStages - 1 && st < nk; ++st) issue(st);
-    v4i fa0[4], fb0[NJ], fa1[4], fb1[NJ];
+    v4i fa0[4], fa1[4];
+    BRaw fb0[NJ], fb1[NJ];
     publish(min(nk - 1, 2));
 
     // The per-row operands have landed (they precede stage 0 in every wave's
@@ -1996,7 +2044,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
         const uint32_t sbase = lds0 + v * kDmaStageBytes;
         const LT* rm = r_up + static_cast<int64_t>(max((v == 2 ? mods[0] : mods[1]) - 1, 0)) * N * r;
 #pragma unroll
-        for (int q = 0; q < kDmaPerStage; ++q) {
+        for (int q = 0; q < kDmaExtra; ++q) {
             const int rw = wave * kRowsPerWave + 8 * q;
             const int row = rw + (lane >> 3);
             const int lc = (lane & 7) ^ swz(row);
@@ -2026,6 +2074,14 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     for (; kt + kDmaStages - 1 < nk; ++kt) body(kt, yes{}, yes{});
     for (; kt + 1 < nk; ++kt) body(kt, no{}, yes{});
     body(kt, no{}, no{});
+    if constexpr (W4) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[i][j][e] >>= 4;     // exact: 16 x the sum
+    }
 
     if constexpr (SPLIT) {
         // Every slice writes its accumulators to its slot of the tile's
@@ -2157,7 +2213,7 @@ __device__ __forceinline__ void small_output(const float (&su)[kSmallMaxT][kMaxR
     Elem<YT>::store1(y + static_cast<int64_t>(t) * N + ch, v);
 }
 
-template <typename YT, typename LT>
+template <typename YT, typename LT, bool W4>
 __global__ __launch_bounds__(256) void k_gemm_small(
     const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
     const float* __restrict__ w_scale, int T, int K, int N, const int32_t* __restrict__ mod,
@@ -2175,15 +2231,21 @@ __global__ __launch_bounds__(256) void k_gemm_small(
     const int sb = min(nsteps, wave * per);
     const int se = min(nsteps, sb + per);
     // lane: row (token / channel) lane % 16, 16-byte k group lane / 16
+    // (W4: Wq rows of K / 2 packed bytes, 8 bytes a lane a step)
+    using BRaw = std::conditional_t<W4, v2i, v4i>;
+    constexpr int kStepB = W4 ? 32 : 64;
     const int8_t* ap = A + static_cast<int64_t>(min(lane & 15, T - 1)) * K + 16 * (lane >> 4);
-    const int8_t* bp = B + static_cast<int64_t>(col0 + (lane & 15)) * K + 16 * (lane >> 4);
+    const int8_t* bp = B + static_cast<int64_t>(col0 + (lane & 15)) * (W4 ? K / 2 : K) +
+                       (kStepB / 4) * (lane >> 4);
     auto step_addr = [&](int st) { return static_cast<int64_t>(min(st, nsteps - 1)) * 64; };
+    auto step_addr_b = [&](int st) { return static_cast<int64_t>(min(st, nsteps - 1)) * kStepB; };
     v4i acc = {0, 0, 0, 0};
-    v4i fa[kSmallDepth], fb[kSmallDepth];
+    v4i fa[kSmallDepth];
+    BRaw fb[kSmallDepth];
 #pragma unroll
     for (int d = 0; d < kSmallDepth; ++d) {
         fa[d] = *reinterpret_cast<const v4i*>(ap + step_addr(sb + d));
-        fb[d] = *reinterpret_cast<const v4i*>(bp + step_addr(sb + d));
+        fb[d] = *reinterpret_cast<const BRaw*>(bp + step_addr_b(sb + d));
     }
     const v4i zero = {0, 0, 0, 0};
     for (int st0 = sb; st0 < se; st0 += kSmallDepth) {
@@ -2191,10 +2253,17 @@ __global__ __launch_bounds__(256) void k_gemm_small(
         for (int d = 0; d < kSmallDepth; ++d) {
             // steps past the wave's range (last round) contribute zeros
             const bool in = st0 + d < se;
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(in ? fa[d] : zero, fb[d], acc, 0, 0, 0);
+            v4i b;
+            if constexpr (W4) b = w4_operand(fb[d]);
+            else b = fb[d];
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(in ? fa[d] : zero, b, acc, 0, 0, 0);
             fa[d] = *reinterpret_cast<const v4i*>(ap + step_addr(st0 + d + kSmallDepth));
-            fb[d] = *reinterpret_cast<const v4i*>(bp + step_addr(st0 + d + kSmallDepth));
+            fb[d] = *reinterpret_cast<const BRaw*>(bp + step_addr_b(st0 + d + kSmallDepth));
         }
+    }
+    if constexpr (W4) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[e] >>= 4;                   // exact: 16 x the sum
     }
     // acc[e]: token 4 (lane / 16) + e, channel col0 + lane % 16
 #pragma unroll
@@ -2221,7 +2290,9 @@ __global__ __launch_bounds__(256) void k_gemm_small(
 // sums of each slice go to the workspace; the last workgroup of a channel
 // group to arrive adds the slices in slice order and finishes the outputs
 // like the single-pass kernel (dequantisation, compensation, store).
-template <typename YT, typename LT>
+// W4: Wq holds packed 4-bit codes (K / 2 bytes a row, 8 bytes a lane a step,
+// unpacked into the MFMA operand in registers).
+template <typename YT, typename LT, bool W4>
 __global__ __launch_bounds__(256, 2) void k_gemm_decode(
     const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
     const float* __restrict__ w_scale, int T, int K, int N, int ns, int sp,
@@ -2251,14 +2322,17 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
     }
     // every Wq step of the slice (steps past S repeat step S - 1 and are not
     // used; a wave past N reads the last channel block and stores nothing)
-    v4i fb[kDecSteps];
+    using BRaw = std::conditional_t<W4, v2i, v4i>;
+    constexpr int kStepB = W4 ? 32 : 64;                           // Wq bytes per row and step
+    BRaw fb[kDecSteps];
     {
-        const int8_t* bp = B + static_cast<int64_t>(min(cb, N - 16) + (lane & 15)) * K +
-                           static_cast<int64_t>(st0) * 64 + 16 * (lane >> 4);
+        const int64_t pitch = W4 ? K / 2 : K;                      // bytes per Wq row
+        const int8_t* bp = B + (min(cb, N - 16) + (lane & 15)) * pitch +
+                           static_cast<int64_t>(st0) * kStepB + (kStepB / 4) * (lane >> 4);
         asm volatile("" ::: "memory");
 #pragma unroll
         for (int j = 0; j < kDecSteps; ++j)
-            fb[j] = *reinterpret_cast<const v4i*>(bp + 64 * min(j, S - 1));
+            fb[j] = *reinterpret_cast<const BRaw*>(bp + kStepB * min(j, S - 1));
         asm volatile("" ::: "memory");
     }
     // this wave's q loads are the ones older than its kDecSteps Wq loads;
@@ -2276,7 +2350,14 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
             // steps past S multiply zeros (MFMA does not branch on lanes)
             v4i fa = *reinterpret_cast<const v4i*>(rd + min(j, S - 1) * 1024);
             fa = j < S ? fa : zero;
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa, fb[j], acc, 0, 0, 0);
+            if constexpr (W4)
+                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa, w4_operand(fb[j]), acc, 0, 0, 0);
+            else
+                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa, fb[j], acc, 0, 0, 0);
+        }
+        if constexpr (W4) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[e] >>= 4;               // exact: 16 x the sum
         }
     }
     // Hand-over of the partials without cache maintenance: they are written
@@ -2548,7 +2629,7 @@ hipError_t launch_stage1_small(const void* x, DT x_dt, const int32_t* mod, const
     return hipGetLastError();
 }
 
-template <typename YT, typename LT>
+template <typename YT, typename LT, bool W4>
 static void launch_gemm_decode_t(const int8_t* q, const float* x_scale, const int8_t* wq,
                                  const float* w_scale, int64_t T, int64_t K, int64_t N,
                                  const int32_t* mod, const float* u, const float* u_part,
@@ -2556,25 +2637,25 @@ static void launch_gemm_decode_t(const int8_t* q, const float* x_scale, const in
                                  int32_t* part, int* tickets, void* y, hipStream_t s) {
     int ns, sp, ngroups;
     plan_decode(K, N, ns, sp, ngroups);
-    hipLaunchKernelGGL((k_gemm_decode<YT, LT>), dim3(static_cast<unsigned>(ngroups * ns)), dim3(256),
+    hipLaunchKernelGGL((k_gemm_decode<YT, LT, W4>), dim3(static_cast<unsigned>(ngroups * ns)), dim3(256),
                        0, s, q, wq, x_scale, w_scale, static_cast<int>(T), static_cast<int>(K),
                        static_cast<int>(N), ns, sp, mod, u, u_part, n_kslices, rank, n_mod,
                        static_cast<const LT*>(r_up), part, tickets, static_cast<YT*>(y));
 }
 
-template <typename YT, typename LT>
+template <typename YT, typename LT, bool W4>
 static void launch_gemm_small_t(const int8_t* q, const float* x_scale, const int8_t* wq,
                                 const float* w_scale, int64_t T, int64_t K, int64_t N,
                                 const int32_t* mod, const float* u, const float* u_part,
                                 int n_kslices, int rank, int n_mod, const void* r_up, int32_t* acc,
                                 void* y, hipStream_t s) {
-    hipLaunchKernelGGL((k_gemm_small<YT, LT>), dim3(static_cast<unsigned>(N / 16)), dim3(256), 0, s,
+    hipLaunchKernelGGL((k_gemm_small<YT, LT, W4>), dim3(static_cast<unsigned>(N / 16)), dim3(256), 0, s,
                        q, wq, x_scale, w_scale, static_cast<int>(T), static_cast<int>(K),
                        static_cast<int>(N), mod, u, u_part, n_kslices, rank, n_mod,
                        static_cast<const LT*>(r_up), acc, static_cast<YT*>(y));
 }
 
-template <typename YT, typename LT, bool CMC, bool ACC>
+template <typename YT, typename LT, bool CMC, bool ACC, bool W4>
 static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* wq,
                           const float* w_scale, int64_t T, int64_t K, int64_t N,
                           const int32_t* mod, const float* u, const uint8_t* u_hl, int rank,
@@ -2588,18 +2669,18 @@ static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* w
         if (part == nullptr || tickets == nullptr) S = 1;
         const dim3 gridk(8 * ((nt * S + 7) / 8));
         if (S > 1)
-            hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN, true>), gridk,
+            hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN, true, W4>), gridk,
                                dim3(128 * kGemmWavesN), 0, s, q, wq, x_scale, w_scale, T,
                                static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
                                u_hl, rank, n_mod, static_cast<const LT*>(r_up), acc,
                                static_cast<YT*>(y), S, part, tickets);
         else
-            hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN, false>), gridk,
+            hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN, false, W4>), gridk,
                                dim3(128 * kGemmWavesN), 0, s, q, wq, x_scale, w_scale, T,
                                static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
                                u_hl, rank, n_mod, static_cast<const LT*>(r_up), acc,
                                static_cast<YT*>(y), 1, nullptr, nullptr);
-    } else
+    } else if constexpr (!W4)
         hipLaunchKernelGGL((k_gemm<YT, LT, CMC, ACC>), grid, block, 0, s, q, wq, x_scale, w_scale, T,
                            static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
                            rank, n_mod, static_cast<const LT*>(r_up), acc, static_cast<YT*>(y));
@@ -2611,13 +2692,16 @@ hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        int32_t* dec_part, int* dec_tickets, int gk_splits, int32_t* gk_part,
                        int* gk_tickets, const float* u_part, int n_kslices,
                        int rank, int n_mod, const void* r_up, DT lr_dt, bool cmc, int32_t* acc,
-                       void* y, DT y_dt, hipStream_t s) {
+                       void* y, DT y_dt, hipStream_t s, bool w4) {
+    // packed 4-bit Wq: K % 64 == 0 (checked by the caller), so every batch
+    // takes the decode, small-batch or direct-to-LDS kernel
+    if (w4 && K % 64 != 0) return hipErrorInvalidValue;
     int dns = 0, dsp = 0, dng = 0;
     if (small_path(T, K)) plan_decode(K, N, dns, dsp, dng);
     if (small_path(T, K) && dec_part != nullptr && dec_tickets != nullptr && acc == nullptr &&
         dns <= kDecMaxSlices) {
         const float* uu = cmc ? u : nullptr;
-#define MASQ_DEC(YT, LT) launch_gemm_decode_t<YT, LT>(q, x_scale, wq, w_scale, T, K, N, mod, uu, u_part, n_kslices, rank, n_mod, r_up, dec_part, dec_tickets, y, s)
+#define MASQ_DEC(YT, LT) (w4 ? launch_gemm_decode_t<YT, LT, true> : launch_gemm_decode_t<YT, LT, false>)(q, x_scale, wq, w_scale, T, K, N, mod, uu, u_part, n_kslices, rank, n_mod, r_up, dec_part, dec_tickets, y, s)
         if (y_dt == DT::BF16) {
             if (lr_dt == DT::BF16) MASQ_DEC(bf16_t, bf16_t);
             else MASQ_DEC(bf16_t, float);
@@ -2630,7 +2714,7 @@ hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
     }
     if (small_path(T, K)) {
         const float* uu = cmc ? u : nullptr;
-#define MASQ_SMALL(YT, LT) launch_gemm_small_t<YT, LT>(q, x_scale, wq, w_scale, T, K, N, mod, uu, u_part, n_kslices, rank, n_mod, r_up, acc, y, s)
+#define MASQ_SMALL(YT, LT) (w4 ? launch_gemm_small_t<YT, LT, true> : launch_gemm_small_t<YT, LT, false>)(q, x_scale, wq, w_scale, T, K, N, mod, uu, u_part, n_kslices, rank, n_mod, r_up, acc, y, s)
         if (y_dt == DT::BF16) {
             if (lr_dt == DT::BF16) MASQ_SMALL(bf16_t, bf16_t);
             else MASQ_SMALL(bf16_t, float);
@@ -2641,7 +2725,7 @@ hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
 #undef MASQ_SMALL
         return hipGetLastError();
     }
-#define MASQ_GEMM(YT, LT, C, A) launch_gemm_t<YT, LT, C, A>(q, x_scale, wq, w_scale, T, K, N, mod, u, u_hl, rank, n_mod, r_up, acc, y, gk_splits, gk_part, gk_tickets, s)
+#define MASQ_GEMM(YT, LT, C, A) (w4 ? launch_gemm_t<YT, LT, C, A, true> : launch_gemm_t<YT, LT, C, A, false>)(q, x_scale, wq, w_scale, T, K, N, mod, u, u_hl, rank, n_mod, r_up, acc, y, gk_splits, gk_part, gk_tickets, s)
     // the int32 accumulator output exists only for the plain product (no
     // compensation); it is a separate instantiation because storing the
     // accumulators as well raises the epilogue's register pressure

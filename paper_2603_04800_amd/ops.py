@@ -41,6 +41,10 @@ _SIGS = {
     "masq_linear_stage1": (_FUSED_ARGS, ctypes.c_int),
     "masq_linear_stage2": (_FUSED_ARGS, ctypes.c_int),
     "masq_linear_fused_workspace_bytes": ([_i64, _i64, _i64, _i32, _i32], ctypes.c_size_t),
+    "masq_w4a8_gemm": ([_p, _p, _p, _p, _i64, _i64, _i64, _p, _p, _i32, _p], ctypes.c_int),
+    "masq_linear_fused_w4a8": (_FUSED_ARGS, ctypes.c_int),
+    "masq_linear_stage1_w4a8": (_FUSED_ARGS, ctypes.c_int),
+    "masq_linear_stage2_w4a8": (_FUSED_ARGS, ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -126,6 +130,22 @@ def w8a8_gemm(q, x_scale, wq, w_scale, want_acc=True, out_dtype=torch.float32, s
     return acc, y
 
 
+def w4a8_gemm(q, x_scale, wq4, w_scale, want_acc=True, out_dtype=torch.float32, stream=None):
+    """The same product with the 4-bit shared weight packed two codes per byte
+    (uint8 [N][K / 2], layout of :mod:`paper_2603_04800_amd.int4`)."""
+    T, K = q.shape
+    N = wq4.shape[0]
+    _need(wq4, torch.uint8, "wq4")
+    if wq4.shape[1] * 2 != K:
+        raise ValueError(f"wq4 holds {2 * wq4.shape[1]} codes a row, q has {K} columns")
+    acc = torch.empty((T, N), dtype=torch.int32, device=q.device) if want_acc else None
+    y = torch.empty((T, N), dtype=out_dtype, device=q.device) if out_dtype is not None else None
+    _check("masq_w4a8_gemm", _lib.masq_w4a8_gemm(
+        _ptr(q), _ptr(x_scale), _ptr(wq4), _ptr(w_scale), T, K, N, _ptr(acc), _ptr(y),
+        _dt(y) if y is not None else F32, _stream(stream)))
+    return acc, y
+
+
 def lowrank_comp(x, modality, inv_smooth, l_down, r_up, y, stream=None):
     """In place: y[t] += (x_t S_m^-1 L1^m) L2^m on non-text rows; returns y."""
     T, K = x.shape
@@ -146,14 +166,18 @@ def workspace_bytes(T, K, N, rank, n_mod) -> int:
 class Linear:
     """One modality-aware quantized linear with device-resident artifacts.
 
-    Holds inv_smooth [M][K] f32, wq [N][K] int8, w_scale [N] f32 and the
-    low-rank factors l_down [M-1][r][K], r_up [M-1][N][r] (f32 or bf16)."""
+    Holds inv_smooth [M][K] f32, wq [N][K] int8 (or, for the 4-bit shared
+    weight, uint8 [N][K / 2] packed codes), w_scale [N] f32 and the low-rank
+    factors l_down [M-1][r][K], r_up [M-1][N][r] (f32 or bf16)."""
 
     def __init__(self, inv_smooth, wq, w_scale, l_down=None, r_up=None):
         self.inv_smooth, self.wq, self.w_scale = inv_smooth, wq, w_scale
         self.l_down, self.r_up = l_down, r_up
         self.n_mod = inv_smooth.shape[0]
-        self.c_out, self.c_in = wq.shape
+        self.w4 = wq.dtype == torch.uint8
+        self.c_out, self.c_in = wq.shape[0], inv_smooth.shape[1]
+        if wq.shape[1] * (2 if self.w4 else 1) != self.c_in:
+            raise ValueError("wq does not match inv_smooth's width")
         self.rank = l_down.shape[1] if l_down is not None and l_down.dim() == 3 else 0
         self._ws = None
 
@@ -165,7 +189,12 @@ class Linear:
         def dev(a, dtype):
             return torch.as_tensor(a).to(device=device, dtype=dtype).contiguous()
 
-        return cls(dev(art["inv_smooth"], torch.float32), dev(art["wq"], torch.int8),
+        if int(art.get("weight_bits", 8)) == 4:
+            from . import int4
+            wq = dev(int4.pack(art["wq"]), torch.uint8)
+        else:
+            wq = dev(art["wq"], torch.int8)
+        return cls(dev(art["inv_smooth"], torch.float32), wq,
                    dev(art["w_scale"], torch.float32), dev(art["l_down"], lr),
                    dev(art["r_up"], lr))
 
@@ -179,6 +208,8 @@ class Linear:
         T = x.shape[0]
         ws = workspace if workspace is not None else self.workspace(T, x.device)
         lr_dt = _dt(self.l_down) if self.l_down is not None else F32
+        if self.w4:
+            fn += "_w4a8"
         _check(fn, getattr(_lib, fn)(
             _ptr(x), _dt(x), _ptr(modality), _ptr(self.inv_smooth), _ptr(self.wq),
             _ptr(self.w_scale), _ptr(self.l_down), _ptr(self.r_up), lr_dt, T, self.c_in,

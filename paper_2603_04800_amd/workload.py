@@ -18,22 +18,25 @@ from . import calibrate
 _KEYS = ("x", "modality", "inv_smooth", "wq", "w_scale", "l_down", "r_up")
 
 
-def _cache_path(cfg, proj, seed_extra):
+def _cache_path(cfg, proj, seed_extra, weight_bits):
     d = os.environ.get("MASQ_CACHE_DIR")
     if not d:
         return None
     os.makedirs(d, exist_ok=True)
-    return os.path.join(d, f"{cfg.name}__{proj.name}__{seed_extra}.npz")
+    tag = "" if weight_bits == 8 else f"__w{weight_bits}"
+    return os.path.join(d, f"{cfg.name}__{proj.name}__{seed_extra}{tag}.npz")
 
 
-def layer(cfg, proj_name: str | None = None, seed_extra: int = 0) -> dict:
+def layer(cfg, proj_name: str | None = None, seed_extra: int = 0, weight_bits: int = 8) -> dict:
     """Inputs and artifacts of one projection: x [T][K] f32 (bf16-exact for
-    bf16 workloads), modality [T] int32, and the calibration arrays."""
+    bf16 workloads), modality [T] int32, and the calibration arrays; with
+    weight_bits=4 the shared weight is quantised to 4-bit codes (kept as
+    int8 codes here; the device copy is packed)."""
     if isinstance(cfg, (int, str)):
         cfg = synth.config_by_name(str(cfg))
     proj = cfg.projections[0] if proj_name is None else \
         next(p for p in cfg.projections if p.name == proj_name)
-    path = _cache_path(cfg, proj, seed_extra)
+    path = _cache_path(cfg, proj, seed_extra, weight_bits)
     if path and os.path.exists(path):
         with np.load(path, allow_pickle=False) as f:
             out = {k: f[k] for k in _KEYS}
@@ -41,14 +44,14 @@ def layer(cfg, proj_name: str | None = None, seed_extra: int = 0) -> dict:
         li = synth.make_layer_inputs(cfg, seed_extra, projections=[proj.name])
         x = li.x[proj.input_key]
         art = calibrate.calibrate_layer(x, li.modality, li.w[proj.name], cfg.n_mod, cfg.rank,
-                                        cfg.lr_dtype)
+                                        cfg.lr_dtype, weight_bits=weight_bits)
         out = dict(x=x, modality=li.modality, **{k: art[k] for k in _KEYS[2:]})
         if path:
             tmp = path + ".tmp.npz"
             np.savez(tmp, **out)
             os.replace(tmp, path)
     out.update(cfg=cfg, proj=proj, n_mod=cfg.n_mod, rank=cfg.rank,
-               act_dtype=cfg.act_dtype, lr_dtype=cfg.lr_dtype)
+               act_dtype=cfg.act_dtype, lr_dtype=cfg.lr_dtype, weight_bits=weight_bits)
     return out
 
 

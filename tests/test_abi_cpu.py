@@ -124,3 +124,42 @@ def test_binding_refuses_host_tensors():
     x = torch.zeros(4, 64)
     with pytest.raises(ValueError):
         ops.smooth_quant(x, torch.zeros(4, dtype=torch.int32), torch.ones(1, 64))
+
+
+def _fused_w4(lib, fn="masq_linear_fused_w4a8", **kw):
+    a = dict(x=P, x_dt=1, mod=P, inv=P, wq=P, ws=P, ld=P, ru=P, lr_dt=1, T=16, K=128, N=64,
+             rank=16, n_mod=2, y=P, y_dt=1, work=P, work_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return getattr(lib, fn)(a["x"], a["x_dt"], a["mod"], a["inv"], a["wq"], a["ws"],
+                            a["ld"], a["ru"], a["lr_dt"], a["T"], a["K"], a["N"], a["rank"],
+                            a["n_mod"], a["y"], a["y_dt"], a["work"], a["work_bytes"],
+                            a["stream"])
+
+
+@pytest.mark.parametrize("fn", ["masq_linear_fused_w4a8", "masq_linear_stage1_w4a8",
+                                "masq_linear_stage2_w4a8"])
+@pytest.mark.parametrize("kw,code", [
+    # the packed weight needs c_in % 64 == 0 (16-column multiples are not enough)
+    (dict(K=48), 2), (dict(K=96), 2), (dict(K=200), 2),
+    (dict(wq=None), 1), (dict(wq=P + 8), 4), (dict(work_bytes=100), 5),
+    (dict(T=0, work=None, work_bytes=0), 0), (dict(K=64, T=0), 0),
+])
+def test_w4a8_fused_validates(lib, fn, kw, code):
+    assert _fused_w4(lib, fn, **kw) == code
+
+
+def test_w4a8_gemm_validates(lib):
+    f = lib.masq_w4a8_gemm
+    assert f(P, P, P, P, 8, 96, 64, P, None, 0, None) == 2         # c_in % 64 != 0
+    assert f(P, P, P, P, 8, 64, 40, P, None, 0, None) == 2         # c_out % 16 != 0
+    assert f(P, P, P, P, 8, 64, 64, None, None, 0, None) == 1      # no output
+    assert f(P, P, P + 4, P, 8, 64, 64, P, None, 0, None) == 4     # misaligned wq4
+    assert f(P, P, P, P, 8, 64, 64, None, P, 9, None) == 3
+    assert f(P, P, P, P, 0, 64, 64, P, None, 0, None) == 0         # empty batch
+
+
+def test_w4_linear_refuses_mismatched_packed_width():
+    import torch
+    from paper_2603_04800_amd import ops
+    with pytest.raises(ValueError):
+        ops.Linear(torch.ones(2, 128), torch.zeros(16, 128, dtype=torch.uint8), torch.ones(16))

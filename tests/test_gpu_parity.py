@@ -6,6 +6,9 @@ max relative error 1e-3 (fp32 workloads) or 1e-2 (bf16 workloads) under the
 row-rms-guarded metric ``oracle.inference.relerr``; text rows, which take no
 compensation, bit-exact.  Full-size workloads compare every code and scale and
 a sample of rows through the oracle's GEMM; the small cases compare all.
+The 4-bit shared weight (W4A8) is held to the same bar: the device gets the
+oracle's 4-bit codes packed two per byte, the oracle uses the codes as they
+are.
 """
 import numpy as np
 import pytest
@@ -56,8 +59,10 @@ def _check_layer(ops, L, rows=None, name=""):
     out_dtype = torch.bfloat16 if act == "bf16" else torch.float32
     T = xs_np.shape[0]
     rows = np.arange(T) if rows is None else rows
+    w4 = int(L.get("weight_bits", 8)) == 4
+    assert w4 == lin.w4
     print(f"[parity] {name} T={T} K={xs_np.shape[1]} N={L['wq'].shape[0]} r={L['rank']} "
-          f"M={L['n_mod']} rows={len(rows)}", flush=True)
+          f"M={L['n_mod']} rows={len(rows)} wbits={8 - 4 * w4}", flush=True)
 
     # smoothing + quantisation: every code and scale
     q, dx = ops.smooth_quant(x, mod, lin.inv_smooth)
@@ -67,7 +72,8 @@ def _check_layer(ops, L, rows=None, name=""):
     assert np.array_equal(dx.cpu().numpy().view(np.uint32), dx_ref.view(np.uint32)), "scales differ"
 
     # shared-weight GEMM: int32 accumulators and the dequantised product
-    acc, y0 = ops.w8a8_gemm(q, dx, lin.wq, lin.w_scale, want_acc=True, out_dtype=torch.float32)
+    gemm = ops.w4a8_gemm if w4 else ops.w8a8_gemm
+    acc, y0 = gemm(q, dx, lin.wq, lin.w_scale, want_acc=True, out_dtype=torch.float32)
     acc_ref, y0_ref = oinf.w8a8_gemm(q_ref[rows], dx_ref[rows], L["wq"], L["w_scale"])
     rows_t = torch.from_numpy(rows).to(acc.device)
     acc_np = acc.index_select(0, rows_t).cpu().numpy()
@@ -123,7 +129,7 @@ def test_workload_parity(ops, cfg_index, proj):
 
 # ------------------------------------------------------------------ edge cases
 def _random_layer(T, K, N, r, M, act, lr, layout="alternating", zero_rows=(), seed=0,
-                  counts=None):
+                  counts=None, weight_bits=8):
     rng = np.random.default_rng(seed)
     if counts is None:
         counts = [T // M + (1 if m < T % M else 0) for m in range(M)]
@@ -138,14 +144,15 @@ def _random_layer(T, K, N, r, M, act, lr, layout="alternating", zero_rows=(), se
     if act == "bf16":
         x = bf16_round(x)
     inv = rng.uniform(0.05, 3.0, (M, K)).astype(np.float32)
-    wq = rng.integers(-127, 128, (N, K)).astype(np.int8)
+    qmax = (1 << (weight_bits - 1)) - 1
+    wq = rng.integers(-qmax, qmax + 1, (N, K)).astype(np.int8)
     ws = rng.uniform(1e-4, 1e-2, N).astype(np.float32)
     ld = (rng.standard_normal((max(M - 1, 0), r, K)) / np.sqrt(K)).astype(np.float32)
     ru = (rng.standard_normal((max(M - 1, 0), N, r)) * 0.05).astype(np.float32)
     if lr == "bf16":
         ld, ru = bf16_round(ld), bf16_round(ru)
     return dict(x=x, modality=mod, inv_smooth=inv, wq=wq, w_scale=ws, l_down=ld, r_up=ru,
-                n_mod=M, rank=r, act_dtype=act, lr_dtype=lr)
+                n_mod=M, rank=r, act_dtype=act, lr_dtype=lr, weight_bits=weight_bits)
 
 
 _EDGE = {
@@ -242,3 +249,71 @@ def test_invalid_modality_ids_read_as_text(ops, K, r):
     y_np = _np(y)
     assert oinf.relerr(y_np, y_ref) <= 1e-2
     assert np.array_equal(y_np[bad], y_ref[bad])
+
+
+# ------------------------------------------------------------------ 4-bit shared weight
+# Full-size prefill (every tile of the direct-to-LDS GEMM) and decode (the
+# k-sliced Wq-streaming GEMM) with the weight calibrated to 4 bits.
+_FULL_W4 = [(1, None), (2, None)]
+
+
+@pytest.mark.parametrize("cfg_index,proj", _FULL_W4, ids=[f"cfg{c}" for c, _ in _FULL_W4])
+def test_w4a8_workload_parity(ops, cfg_index, proj):
+    from paper_2603_04800_amd import workload
+    L = workload.layer(cfg_index, proj, weight_bits=4)
+    assert np.abs(L["wq"]).max() <= 7
+    rows = None if L["x"].shape[0] * L["wq"].shape[0] <= 256 * 4096 else _sample_rows(L["modality"])
+    _check_layer(ops, L, rows, name=f"w4/cfg{cfg_index}")
+
+
+_EDGE_W4 = {
+    # decode GEMM (fused) and small-batch GEMM (int32 accumulators requested)
+    "w4_T1_k64": dict(T=1, K=64, N=32, r=16, M=2, act="bf16", lr="bf16"),
+    "w4_decode_t16_k4096": dict(T=16, K=4096, N=512, r=64, M=2, act="bf16", lr="bf16"),
+    "w4_decode_t7_k2624_n208": dict(T=7, K=2624, N=208, r=32, M=3, act="bf16", lr="bf16"),
+    "w4_decode_fp32_t9_k5184": dict(T=9, K=5184, N=96, r=16, M=2, act="f32", lr="f32"),
+    # rows too long for the k-sliced decode GEMM: the single-pass small-batch GEMM
+    "w4_small_t3_k20544": dict(T=3, K=20544, N=48, r=16, M=2, act="bf16", lr="bf16"),
+    # direct-to-LDS GEMM: split K over few tiles, one K stage ring tail,
+    # ragged T and N, fp32 activations and factors, four modalities, no split
+    "w4_splitk_runs_t700_k1024": dict(T=700, K=1024, N=528, r=64, M=3, act="bf16", lr="bf16",
+                                      layout="runs"),
+    "w4_ring_tail_k256": dict(T=520, K=256, N=272, r=16, M=2, act="bf16", lr="bf16",
+                              layout="runs"),
+    "w4_fp32_ragged_t300_k192": dict(T=300, K=192, N=80, r=16, M=2, act="f32", lr="f32",
+                                     layout="contiguous"),
+    "w4_bf16_act_fp32_factors": dict(T=130, K=192, N=64, r=16, M=2, act="bf16", lr="f32"),
+    "w4_four_modalities": dict(T=260, K=128, N=96, r=16, M=4, act="bf16", lr="bf16"),
+    "w4_rank0": dict(T=70, K=64, N=64, r=0, M=2, act="f32", lr="f32"),
+    "w4_no_split_t4096_n2048": dict(T=4096, K=128, N=2048, r=32, M=2, act="bf16", lr="bf16",
+                                    layout="runs"),
+}
+
+
+@pytest.mark.parametrize("name", list(_EDGE_W4))
+def test_w4a8_edge_case_parity(ops, name):
+    kw = dict(_EDGE_W4[name])
+    L = _random_layer(kw.pop("T"), kw.pop("K"), kw.pop("N"), kw.pop("r"), kw.pop("M"),
+                      kw.pop("act"), kw.pop("lr"), weight_bits=4, **kw)
+    if L["rank"] == 0:
+        L["l_down"] = L["l_down"][:, :0]
+        L["r_up"] = L["r_up"][:, :, :0]
+    rows = None if L["x"].shape[0] * L["wq"].shape[0] <= 1024 * 1024 else _sample_rows(L["modality"])
+    _check_layer(ops, L, rows, name=name)
+
+
+def test_w4a8_equals_w8a8_on_the_same_codes(ops):
+    """The packed path and the int8 path given the same (4-bit) codes agree
+    bit for bit, on the decode and on the prefill GEMM."""
+    from paper_2603_04800_amd import int4, workload
+    for T in (12, 600):
+        L = _random_layer(T, 1024, 256, 32, 3, "bf16", "bf16", weight_bits=4, seed=3)
+        x, mod, lin4 = workload.to_device(L)
+        L8 = dict(L, weight_bits=8)
+        _, _, lin8 = workload.to_device(L8)
+        assert lin4.w4 and not lin8.w4
+        assert torch.equal(lin4.wq.cpu(), torch.from_numpy(int4.pack(L["wq"])))
+        y4 = lin4(x, mod)
+        y8 = lin8(x, mod)
+        torch.cuda.synchronize()
+        assert torch.equal(y4.view(torch.int16), y8.view(torch.int16)), f"T={T}"
