@@ -48,7 +48,7 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
     w.dec_ns = w.dec_sp = w.dec_groups = 0;
     if (small_path(T, K) && T > 0 && N > 0) {
         plan_decode(K, N, w.dec_ns, w.dec_sp, w.dec_groups);
-        w.dec_part = reinterpret_cast<int32_t*>(carve(static_cast<size_t>(w.dec_ns) * kSmallMaxT *
+        w.dec_part = reinterpret_cast<int32_t*>(carve(static_cast<size_t>(w.dec_ns + 1) * kSmallMaxT *
                                                       static_cast<size_t>(N) * sizeof(int32_t)));
         w.dec_tickets = reinterpret_cast<int*>(carve(static_cast<size_t>(w.dec_groups) * sizeof(int)));
     }

@@ -65,6 +65,7 @@ inline int plan_gemm_splits(int64_t T, int64_t K, int64_t N) {
 constexpr int kDecSteps = 40;
 constexpr int kDecCh = 64;
 constexpr int kDecMaxSlices = 8;    // longer rows (K > 8 * 40 * 64) take the single-pass GEMM
+constexpr int kDecCmcBytes = 32768;  // LDS for the compensation operands of a k-slice workgroup
 inline void plan_decode(int64_t K, int64_t N, int& ns, int& sp, int& ngroups) {
     const int64_t nsteps = K / 64;
     const int64_t ns0 = (nsteps + kDecSteps - 1) / kDecSteps;
@@ -100,7 +101,8 @@ struct Workspace {
     uint8_t* u_hl;     // [T][256 B] u as bf16 hi | lo rows (rank <= 64, large batches)
     float* u_part;     // [n_kslices][T][rank] fp32 partial sums over k slices (n_kslices > 1)
     int* tickets;      // [ceil(T / kDownRows)] arrival counters of the slice workgroups
-    int32_t* dec_part; // small-batch path: [ns][kSmallMaxT][N] int32 partial sums per k slice
+    int32_t* dec_part; // small-batch path: [ns][kSmallMaxT][N] int32 partial sums per k slice,
+                       // then [kSmallMaxT][N] fp32 compensation terms
     int* dec_tickets;  // small-batch path: [ngroups] arrival counters (zeroed by stage 1)
     int dec_ns, dec_sp, dec_groups;   // plan_decode of the small-batch path
     int gk_splits;     // plan_gemm_splits

@@ -2290,6 +2290,14 @@ __global__ __launch_bounds__(256) void k_gemm_small(
 // sums of each slice go to the workspace; the last workgroup of a channel
 // group to arrive adds the slices in slice order and finishes the outputs
 // like the single-pass kernel (dequantisation, compensation, store).
+// The compensation term of the group's outputs is computed off that tail
+// when its operands fit in LDS: workgroup (g, s) takes the tokens t with
+// t % ns == s.  The u partials of those tokens and the L2 rows of the
+// group's channels are queued by DMA with the q slice, ahead of the Wq
+// loads, so they have landed long before Wq has; the workgroup adds the
+// partials (slice order), forms (x S^-1 L1) L2 for its tokens while its Wq
+// loads are still in flight, and hands the fp32 terms over beside the int32
+// partials.  The last workgroup then only adds.
 // W4: Wq holds packed 4-bit codes (K / 2 bytes a row, 8 bytes a lane a step,
 // unpacked into the MFMA operand in registers).
 template <typename YT, typename LT, bool W4>
@@ -2301,7 +2309,11 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
     const LT* __restrict__ r_up, int32_t* __restrict__ part, int* __restrict__ tickets,
     YT* __restrict__ y) {
     __shared__ __attribute__((aligned(16))) uint8_t sq[kDecSteps * 1024];
-    __shared__ float su[kSmallMaxT][kMaxRank];
+    // compensation operands (u partials of the token share, then L2 rows of
+    // the group's channels) or, when they do not fit, the u rows of the batch
+    __shared__ __attribute__((aligned(16))) uint8_t scm[kDecCmcBytes];
+    static_assert(sizeof(float) * kSmallMaxT * kMaxRank <= kDecCmcBytes, "u rows fit scm");
+    auto& su = *reinterpret_cast<float (*)[kSmallMaxT][kMaxRank]>(scm);
     __shared__ int s_last;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -2319,6 +2331,42 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
         const int8_t* qa = A + static_cast<int64_t>(min(t, T - 1)) * K +
                            static_cast<int64_t>(st0) * 64 + 16 * p;
         for (int j = wave; j < S; j += 4) lds_dma16(qa + 64 * j, sq0 + j * 1024);
+    }
+    // compensation operands of the token share, when they fit: the u slice
+    // partials as rows [slice][share token][r] fp32, then the L2 rows
+    // [modality - 1][channel of the group][r]; both padded to whole 1 KB
+    // DMA blocks (a block's pieces past the end repeat the last piece)
+    const bool cmc = u != nullptr;
+    const int uslices = (u_part != nullptr && n_kslices > 1) ? n_kslices : 1;
+    const float* usrc = uslices > 1 ? u_part : u;
+    const int nts = (T + ns - 1) / ns;                              // share tokens, at most
+    const int own = sl < T ? (T - sl + ns - 1) / ns : 0;            // this workgroup's
+    const int up_pieces = uslices * nts * (r >> 2);                 // 16-byte pieces
+    const int up_bytes = ((up_pieces * 16 + 1023) >> 10) << 10;
+    const int rrow = r * static_cast<int>(sizeof(LT));              // bytes of one L2 row
+    const int rp_pieces = cmc ? (n_mod - 1) * kDecCh * (rrow >> 4) : 0;
+    const bool early = cmc && nts <= 4 && up_bytes + rp_pieces * 16 <= kDecCmcBytes;
+    const uint32_t scm0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(scm));
+    int tmod = 0;                                   // modality of the thread's share output
+    if (early) {
+        const int ti = tid >> 6;
+        if (ti < own) tmod = sane_mod(mod[sl + ti * ns], n_mod);
+        const int upr = r >> 2;                                     // pieces per u row
+        for (int i = wave; i * 64 < up_pieces; i += 4) {
+            const int pc = min(i * 64 + lane, up_pieces - 1);
+            const int row = pc / upr, c = pc - row * upr;
+            const int s = row / nts, tt = min(sl + (row - s * nts) * ns, T - 1);
+            lds_dma16(usrc + (static_cast<int64_t>(s) * T + tt) * r + 4 * c, scm0 + i * 1024);
+        }
+        const int rpr = rrow >> 4;                                  // pieces per L2 row
+        for (int i = wave; i * 64 < rp_pieces; i += 4) {
+            const int pc = i * 64 + lane;                           // rp_pieces % 64 == 0
+            const int row = pc / rpr, c = pc - row * rpr;
+            const int mm = row / kDecCh, ch = min(g * kDecCh + (row - mm * kDecCh), N - 1);
+            lds_dma16(reinterpret_cast<const uint8_t*>(r_up + (static_cast<int64_t>(mm) * N + ch) * r) +
+                          16 * c,
+                      scm0 + up_bytes + i * 1024);
+        }
     }
     // every Wq step of the slice (steps past S repeat step S - 1 and are not
     // used; a wave past N reads the last channel block and stores nothing)
@@ -2340,6 +2388,32 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
     MASQ_WAIT_VMCNT_LGKM0(kDecSteps);
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
+    // while Wq streams in: u rows of the share (slice partials added in
+    // slice order, into slice 0's rows), then one compensation term per
+    // thread (share token tid / 64, channel tid % 64), k in order
+    float cterm = 0.f;
+    if (early) {
+        float* up = reinterpret_cast<float*>(scm);
+        const int stride = nts * r;                                 // floats per slice
+        for (int idx = 4 * tid; idx < stride; idx += 4 * 256) {
+            v4f v = *reinterpret_cast<const v4f*>(up + idx);
+            for (int s = 1; s < uslices; ++s) v = v + *reinterpret_cast<const v4f*>(up + s * stride + idx);
+            *reinterpret_cast<v4f*>(up + idx) = v;
+        }
+        __syncthreads();
+        if (tmod > 0) {
+            const float* ur = up + (tid >> 6) * r;
+            const LT* rr = reinterpret_cast<const LT*>(scm + up_bytes +
+                                                       ((tmod - 1) * kDecCh + (tid & 63)) * rrow);
+            for (int k0 = 0; k0 < r; k0 += 8) {
+                float rv[8];
+                Elem<LT>::load8(rr + k0, rv);
+#pragma unroll
+                for (int k = 0; k < 8; ++k) cterm = fmaf(ur[k0 + k], rv[k], cterm);
+            }
+        }
+    }
+    MASQ_SCHED_FENCE();
     v4i acc = {0, 0, 0, 0};
     {
         const int rt = lane & 15;
@@ -2376,6 +2450,11 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
                                    __HIP_MEMORY_SCOPE_AGENT);
         }
     }
+    // the share's compensation terms: fp32 bits in slot ns of the partials
+    if (tmod > 0 && g * kDecCh + (tid & 63) < N)
+        __hip_atomic_store(part + static_cast<int64_t>(ns) * kSmallMaxT * N +
+                               static_cast<int64_t>(sl + (tid >> 6) * ns) * N + g * kDecCh + (tid & 63),
+                           __float_as_int(cterm), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     MASQ_WAIT_VMCNT_LGKM0(0);
     __syncthreads();
     if (tid == 0)
@@ -2391,13 +2470,13 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
     // ns - 1 and are not added), their scales and modality ids, the L2 rows
     // of the group's channels for every non-text modality (into the q
     // buffer, free now, slot (m - 1) kDecCh + o, when they fit in
-    // kRStage bytes) and the u rows of the batch.
+    // kRStage bytes) and the u rows of the batch; or, when the slices have
+    // formed the compensation terms, those terms.
     constexpr int kOut = kSmallMaxT * kDecCh / 256;
     constexpr int kRStage = 16384;
     constexpr int kRPieces = kRStage / 16 / 256;                       // per thread
-    const bool cmc = u != nullptr;
     int pv[kOut][kDecMaxSlices], mv[kOut];
-    float dxv[kOut], dwv[kOut];
+    float dxv[kOut], dwv[kOut], cv[kOut];
 #pragma unroll
     for (int i = 0; i < kOut; ++i) {
         const int idx = tid + 256 * i;
@@ -2407,12 +2486,15 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
         for (int q = 0; q < kDecMaxSlices; ++q)
             pv[i][q] = __hip_atomic_load(pa + static_cast<int64_t>(min(q, ns - 1)) * kSmallMaxT * N,
                                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        cv[i] = early ? __int_as_float(__hip_atomic_load(pa + static_cast<int64_t>(ns) * kSmallMaxT * N,
+                                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+                      : 0.f;
         dxv[i] = x_scale[t];
         dwv[i] = w_scale[ch];
         mv[i] = cmc ? sane_mod(mod[t], n_mod) : 0;
     }
     const int row_bytes = r * static_cast<int>(sizeof(LT));
-    const bool staged = cmc && (n_mod - 1) * kDecCh * row_bytes <= kRStage;
+    const bool staged = cmc && !early && (n_mod - 1) * kDecCh * row_bytes <= kRStage;
     const int per_row = row_bytes >> 4;                                // 16-byte pieces per row
     const int pieces = staged ? (n_mod - 1) * kDecCh * per_row : 0;
     v4i rpc[kRPieces];
@@ -2430,9 +2512,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
     // u rows: one v4f of T x r per thread, the k slices in batches of kUB
     // (the first issued with the loads above), when the batch is small
     // enough; else the general loop
-    const bool u_fast = cmc && T * r <= 4 * 256;
-    const int uslices = (u_part != nullptr && n_kslices > 1) ? n_kslices : 1;
-    const float* usrc = uslices > 1 ? u_part : u;
+    const bool u_fast = cmc && !early && T * r <= 4 * 256;
     constexpr int kUB = kUBatch;
     v4f up[kUB];
     if (u_fast && 4 * tid < T * r) {
@@ -2468,7 +2548,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
             const int tt = (4 * tid) / r, c = 4 * tid - tt * r;
             *reinterpret_cast<v4f*>(&su[tt][c]) = v;
         }
-    } else if (cmc) {
+    } else if (cmc && !early) {
         small_u_rows(su, u, u_part, n_kslices, T, r, tid);
     }
     __syncthreads();
@@ -2482,7 +2562,9 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
         for (int q = 1; q < kDecMaxSlices; ++q) a += q < ns ? pv[i][q] : 0;
         float v = (static_cast<float>(a) * dxv[i]) * dwv[i];
         const int m = mv[i];
-        if (m > 0) {
+        if (m > 0 && early) {
+            v += cv[i];
+        } else if (m > 0) {
             float c = 0.f;
             if (staged) {
                 const LT* rr = reinterpret_cast<const LT*>(sq + ((m - 1) * kDecCh + o) * row_bytes);
