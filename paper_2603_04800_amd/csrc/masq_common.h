@@ -17,7 +17,7 @@ constexpr int kDownRows = kRowsDown;
 constexpr int kDownStep = 512;    // k granularity of a down-projection slice (128 per wave)
 constexpr int kMaxRank = 256;
 constexpr int kSmallMaxT = 16;    // batches this small use the Wq-streaming GEMM
-constexpr int kSmallSlices = 32;  // down-projection k slices (at most; >= 512 columns each) summed by that GEMM
+constexpr int kSmallSlices = 64;  // down-projection k slices (at most; >= 512 columns each) summed by that GEMM
 constexpr int kUBatch = 16;        // slice partials of u a thread keeps in flight when adding them
 
 // The small-batch path: the Wq-streaming GEMM, which also adds the

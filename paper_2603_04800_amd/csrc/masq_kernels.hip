@@ -520,16 +520,14 @@ __device__ __forceinline__ unsigned tile_presence(const int* smod) {
 // without non-text rows are skipped (their u rows are never read).
 constexpr int kDownWaves = 8;
 
-template <typename XT, typename LT>
-__device__ __forceinline__ void down_tile(const XT* __restrict__ x, const int32_t* __restrict__ mod,
-                                          const float* __restrict__ inv_s,
-                                          const LT* __restrict__ l_down, int64_t T, int K, int r,
-                                          int n_mod, int kslice, int n_kslices,
-                                          float* __restrict__ u, float* __restrict__ u_part,
-                                          int* __restrict__ tickets, int tile, int s) {
-    __shared__ int smod[kRowsDown];
-    __shared__ float red[kDownWaves][kRowsDown][64];
-    __shared__ int last;
+template <int NW, typename XT, typename LT>
+__device__ __forceinline__ void down_tile_in(const XT* __restrict__ x, const int32_t* __restrict__ mod,
+                                             const float* __restrict__ inv_s,
+                                             const LT* __restrict__ l_down, int64_t T, int K, int r,
+                                             int n_mod, int kslice, int n_kslices,
+                                             float* __restrict__ u, float* __restrict__ u_part,
+                                             int* __restrict__ tickets, int tile, int s, int* smod,
+                                             float (*red)[kRowsDown][64], int* last_flag) {
     const int tid = threadIdx.x;
     const int64_t row0 = static_cast<int64_t>(tile) * kRowsDown;
     const int kb = s * kslice;
@@ -543,24 +541,24 @@ __device__ __forceinline__ void down_tile(const XT* __restrict__ x, const int32_
     if (!present) return;                                            // uniform per tile
     float* out = n_kslices > 1 ? u_part + static_cast<int64_t>(s) * T * r : u;
     for (int c0 = 0; c0 < r; c0 += 64)
-        down_group<kDownWaves, XT, LT>(x, inv_s, l_down, row0, T, K, r, n_mod, kb, ke, c0, smod,
-                                       present, red, [&](int row, int col, float v) {
-                                           const int64_t t = row0 + row;
-                                           if (t < T) out[t * r + col] = v;
-                                       });
+        down_group<NW, XT, LT>(x, inv_s, l_down, row0, T, K, r, n_mod, kb, ke, c0, smod, present,
+                               red, [&](int row, int col, float v) {
+                                   const int64_t t = row0 + row;
+                                   if (t < T) out[t * r + col] = v;
+                               });
     if (n_kslices == 1 || tickets == nullptr) return;   // the consumer adds the partials
 
     __threadfence();                 // this slice's partials are visible device-wide ...
     __syncthreads();
-    if (tid == 0) last = atomicAdd(&tickets[tile], 1) == n_kslices - 1;
+    if (tid == 0) *last_flag = atomicAdd(&tickets[tile], 1) == n_kslices - 1;
     __syncthreads();
-    if (!last) return;
+    if (!*last_flag) return;
     __threadfence();                 // ... before the last arrival reads them all
     // 4 consecutive values per thread (r % 16 == 0); the partials of 8 slices
     // are loaded together and added in slice order
     const int rows = static_cast<int>(min<int64_t>(kDownRows, T - row0));
     const int64_t slice = T * r;
-    for (int idx = 4 * tid; idx < rows * r; idx += 4 * 64 * kDownWaves) {
+    for (int idx = 4 * tid; idx < rows * r; idx += 4 * 64 * NW) {
         const int64_t e = row0 * r + idx;
         v4f v = *reinterpret_cast<const v4f*>(u_part + e);
         for (int q0 = 1; q0 < n_kslices; q0 += 8) {
@@ -576,6 +574,20 @@ __device__ __forceinline__ void down_tile(const XT* __restrict__ x, const int32_
         }
         *reinterpret_cast<v4f*>(u + e) = v;
     }
+}
+
+template <typename XT, typename LT>
+__device__ __forceinline__ void down_tile(const XT* __restrict__ x, const int32_t* __restrict__ mod,
+                                          const float* __restrict__ inv_s,
+                                          const LT* __restrict__ l_down, int64_t T, int K, int r,
+                                          int n_mod, int kslice, int n_kslices,
+                                          float* __restrict__ u, float* __restrict__ u_part,
+                                          int* __restrict__ tickets, int tile, int s) {
+    __shared__ int smod[kRowsDown];
+    __shared__ float red[kDownWaves][kRowsDown][64];
+    __shared__ int last;
+    down_tile_in<kDownWaves, XT, LT>(x, mod, inv_s, l_down, T, K, r, n_mod, kslice, n_kslices, u,
+                                     u_part, tickets, tile, s, smod, red, &last);
 }
 
 template <typename XT, typename LT>
@@ -734,21 +746,25 @@ __global__ __launch_bounds__(256, 2) void k_down_wide(const XT* __restrict__ x,
 
 // Stage 1 of the small-batch path in one launch: workgroups [0, T) quantise
 // one row each, workgroups [T, T + n_kslices) compute one k slice of the
-// down-projection (partials left for the GEMM to add).  Workgroup 0 also
-// clears zero_ints (the decode GEMM's arrival counters).
+// down-projection (partials left for the GEMM to add).  256 threads: four
+// waves per slice of 512 columns, so the many small slices start at once.
+// Workgroup 0 also clears zero_ints (the decode GEMM's arrival counters).
 template <typename XT, typename LT>
-__global__ __launch_bounds__(64 * kDownWaves) void k_stage1_small(
+__global__ __launch_bounds__(256) void k_stage1_small(
     const XT* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
     const LT* __restrict__ l_down, int T, int K, int r, int n_mod, int kslice, int n_kslices,
     int8_t* __restrict__ q, float* __restrict__ x_scale, float* __restrict__ u,
     float* __restrict__ u_part, int* __restrict__ zero_ints, int n_zero) {
+    __shared__ int smod[kRowsDown];
+    __shared__ float red[4][kRowsDown][64];
+    __shared__ int last;
     if (blockIdx.x == 0)
         for (int i = threadIdx.x; i < n_zero; i += blockDim.x) zero_ints[i] = 0;
     if (static_cast<int>(blockIdx.x) < T) {
-        sq_row<XT, 64 * kDownWaves, kSqChunks / 2>(x, mod, inv_s, K, n_mod, q, x_scale, blockIdx.x);
+        sq_row<XT, 256, kSqChunks / 2>(x, mod, inv_s, K, n_mod, q, x_scale, blockIdx.x);
     } else if (l_down != nullptr) {
-        down_tile<XT, LT>(x, mod, inv_s, l_down, T, K, r, n_mod, kslice, n_kslices, u, u_part,
-                          nullptr, 0, blockIdx.x - T);
+        down_tile_in<4, XT, LT>(x, mod, inv_s, l_down, T, K, r, n_mod, kslice, n_kslices, u,
+                                u_part, nullptr, 0, blockIdx.x - T, smod, red, &last);
     }
 }
 
@@ -2691,7 +2707,7 @@ static void launch_stage1_small_t(const void* x, const int32_t* mod, const float
                                   const void* ld, int64_t T, int64_t K, int rank, int n_mod,
                                   bool cmc, const Workspace& w, hipStream_t s) {
     const unsigned blocks = static_cast<unsigned>(T + (cmc ? w.n_kslices : 0));
-    hipLaunchKernelGGL((k_stage1_small<XT, LT>), dim3(blocks), dim3(64 * kDownWaves), 0, s,
+    hipLaunchKernelGGL((k_stage1_small<XT, LT>), dim3(blocks), dim3(256), 0, s,
                        static_cast<const XT*>(x), mod, inv_s, cmc ? static_cast<const LT*>(ld) : nullptr,
                        static_cast<int>(T), static_cast<int>(K), rank, n_mod, w.kslice, w.n_kslices,
                        w.q, w.x_scale, w.u, w.u_part, w.dec_tickets,
