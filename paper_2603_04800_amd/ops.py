@@ -229,6 +229,48 @@ class Linear:
     def stage2(self, x, modality, out, workspace=None, stream=None):
         return self._call("masq_linear_stage2", x, modality, out, workspace, stream)
 
+    def bind(self, x, modality, out, workspace=None, stream=None):
+        """The layer's calls on fixed buffers with their arguments checked and
+        converted once, for tight loops: returns an object whose stage1(),
+        stage2() and __call__() each make one C call."""
+        return BoundLinear(self, x, modality, out, workspace, stream)
+
+
+class BoundLinear:
+    """Pre-marshalled masq_linear_fused / _stage1 / _stage2 calls (see
+    :meth:`Linear.bind`); keeps its tensors alive."""
+
+    def __init__(self, lin, x, modality, out, workspace=None, stream=None):
+        T = x.shape[0]
+        ws = workspace if workspace is not None else lin.workspace(T, x.device)
+        if ws.numel() < workspace_bytes(T, lin.c_in, lin.c_out, lin.rank, lin.n_mod):
+            raise ValueError("workspace too small")
+        lr_dt = _dt(lin.l_down) if lin.l_down is not None else F32
+        self._args = (_ptr(x), _dt(x), _ptr(modality), _ptr(lin.inv_smooth), _ptr(lin.wq),
+                      _ptr(lin.w_scale), _ptr(lin.l_down), _ptr(lin.r_up), lr_dt, T, lin.c_in,
+                      lin.c_out, lin.rank, lin.n_mod, _ptr(out), _dt(out), _ptr(ws), ws.numel(),
+                      _stream(stream))
+        sfx = "_w4a8" if lin.w4 else ""
+        self._names = tuple(n + sfx for n in ("masq_linear_fused", "masq_linear_stage1",
+                                              "masq_linear_stage2"))
+        self._fns = tuple(getattr(_lib, n) for n in self._names)
+        self._keep = (lin, x, modality, out, ws)
+
+    def __call__(self):
+        code = self._fns[0](*self._args)
+        if code:
+            raise MasqError(self._names[0], code)
+
+    def stage1(self):
+        code = self._fns[1](*self._args)
+        if code:
+            raise MasqError(self._names[1], code)
+
+    def stage2(self):
+        code = self._fns[2](*self._args)
+        if code:
+            raise MasqError(self._names[2], code)
+
 
 def linear_fused(x, modality, inv_smooth, wq, w_scale, l_down=None, r_up=None,
                  out_dtype=None, stream=None):

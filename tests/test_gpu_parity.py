@@ -232,6 +232,24 @@ def test_empty_batch_is_a_noop(ops):
     assert y.shape == (0, 32)
 
 
+@pytest.mark.parametrize("T,K", [(16, 2048), (300, 512)])
+def test_bound_calls_equal_the_layer(ops, T, K):
+    """Linear.bind: the pre-marshalled fused call and its two stages give the
+    layer's output bit for bit (small-batch and tiled paths)."""
+    from paper_2603_04800_amd import workload
+    L = _random_layer(T, K, 128, 32, 3, "bf16", "bf16")
+    x, mod, lin = workload.to_device(L)
+    y_ref = lin(x, mod)
+    y1, y2 = torch.empty_like(y_ref), torch.empty_like(y_ref)
+    b1, b2 = lin.bind(x, mod, y1), lin.bind(x, mod, y2)
+    b1()
+    b2.stage1()
+    b2.stage2()
+    torch.cuda.synchronize()
+    assert torch.equal(y1.view(torch.int16), y_ref.view(torch.int16))
+    assert torch.equal(y2.view(torch.int16), y_ref.view(torch.int16))
+
+
 @pytest.mark.parametrize("K,r", [(128, 16), (512, 64)])
 def test_invalid_modality_ids_read_as_text(ops, K, r):
     """Ids outside [0, n_mod) are documented to be read as text: the layer then
