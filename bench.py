@@ -1,6 +1,7 @@
 """Benchmark of the modality-aware W8A8 + low-rank linear on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload I] [--no-cpu]
+                    [--method masquant|smoothquant]
 
 A step is one pass of the hot path over every projection of the workload:
 per projection, smoothing + per-token int8 quantisation + the rank-r
@@ -47,6 +48,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=1)
+    ap.add_argument("--method", default="masquant", choices=("masquant", "smoothquant"),
+                    help="smoothquant: the comparator on the same kernels (unified smoothing "
+                         "factor, no compensation), to measure what the compensation costs")
     ap.add_argument("--copies", type=int, default=2,
                     help="rotating input/output sets so no step reuses the last one's cache")
     ap.add_argument("--no-cpu", action="store_true")
@@ -303,7 +307,7 @@ def main():
 
     t0 = time.time()
     cfg = CONFIGS[args.workload]
-    layers = [workload.layer(cfg, p.name) for p in cfg.projections]
+    layers = [workload.layer(cfg, p.name, method=args.method) for p in cfg.projections]
     log(f"[bench] workload {cfg.name}: {len(layers)} projection(s), inputs + calibration "
         f"{time.time() - t0:.1f}s")
     out_dtype = torch.bfloat16 if cfg.act_dtype == "bf16" else torch.float32
@@ -407,7 +411,8 @@ def main():
         "config": {
             "workload": cfg.name, "tokens": int(T),
             "projections": [[p.name, int(p.c_in), int(p.c_out)] for p in cfg.projections],
-            "rank": int(cfg.rank), "modality_counts": list(map(int, cfg.counts)),
+            "method": args.method, "rank": int(layers[0]["rank"]),
+            "modality_counts": list(map(int, cfg.counts)),
             "io_dtype": cfg.act_dtype, "weight_dtype": "int8", "factor_dtype": cfg.lr_dtype,
             "rotating_copies": copies,
         },

@@ -184,3 +184,22 @@ def calibrate_layer(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: i
     return dict(inv_smooth=inv, s32=s32, wq=wq, w_scale=w_scale,
                 l_down=np.ascontiguousarray(l_down), r_up=np.ascontiguousarray(r_up),
                 rank=rank, n_mod=n_mod, lr_dtype=lr_dtype, weight_bits=weight_bits)
+
+
+def calibrate_smoothquant(x: np.ndarray, w: np.ndarray, n_mod: int, lr_dtype: str = "bf16",
+                          weight_bits: int = 8) -> dict:
+    """The SmoothQuant comparator on the same kernels: one unified factor for
+    every token, s^uni_i = sqrt(max_t |x_ti| / max_j |w_ji|) over the rows of
+    all modalities (Sec. 4.1), the shared weight Q(S^uni W), no compensation
+    (rank 0).  inv_smooth repeats the unified factor for each modality id."""
+    x = np.asarray(x, np.float32)
+    w = np.asarray(w, np.float32)
+    s32, _ = smoothing_factors(x, np.zeros(x.shape[0], np.int32), w, 1)
+    wq, w_scale = quantize_shared_weight(w, s32[0], weight_bits)
+    k, n = w.shape
+    inv = (np.float32(1.0) / s32).astype(np.float32)
+    return dict(inv_smooth=np.ascontiguousarray(np.repeat(inv, n_mod, axis=0)),
+                s32=np.repeat(s32, n_mod, axis=0), wq=wq, w_scale=w_scale,
+                l_down=np.zeros((max(n_mod - 1, 0), 0, k), np.float32),
+                r_up=np.zeros((max(n_mod - 1, 0), n, 0), np.float32),
+                rank=0, n_mod=n_mod, lr_dtype=lr_dtype, weight_bits=weight_bits)

@@ -18,39 +18,53 @@ from . import calibrate
 _KEYS = ("x", "modality", "inv_smooth", "wq", "w_scale", "l_down", "r_up")
 
 
-def _cache_path(cfg, proj, seed_extra, weight_bits):
+METHODS = ("masquant", "smoothquant")
+
+
+def _cache_path(cfg, proj, seed_extra, weight_bits, method):
     d = os.environ.get("MASQ_CACHE_DIR")
     if not d:
         return None
     os.makedirs(d, exist_ok=True)
-    tag = "" if weight_bits == 8 else f"__w{weight_bits}"
+    tag = ("" if weight_bits == 8 else f"__w{weight_bits}") + \
+          ("" if method == "masquant" else f"__{method}")
     return os.path.join(d, f"{cfg.name}__{proj.name}__{seed_extra}{tag}.npz")
 
 
-def layer(cfg, proj_name: str | None = None, seed_extra: int = 0, weight_bits: int = 8) -> dict:
+def layer(cfg, proj_name: str | None = None, seed_extra: int = 0, weight_bits: int = 8,
+          method: str = "masquant") -> dict:
     """Inputs and artifacts of one projection: x [T][K] f32 (bf16-exact for
     bf16 workloads), modality [T] int32, and the calibration arrays; with
     weight_bits=4 the shared weight is quantised to 4-bit codes (kept as
-    int8 codes here; the device copy is packed)."""
+    int8 codes here; the device copy is packed).  method="smoothquant" gives
+    the comparator instead: the unified smoothing factor for every token and
+    no compensation (rank 0)."""
+    if method not in METHODS:
+        raise ValueError(f"method must be one of {METHODS}")
     if isinstance(cfg, (int, str)):
         cfg = synth.config_by_name(str(cfg))
     proj = cfg.projections[0] if proj_name is None else \
         next(p for p in cfg.projections if p.name == proj_name)
-    path = _cache_path(cfg, proj, seed_extra, weight_bits)
+    path = _cache_path(cfg, proj, seed_extra, weight_bits, method)
     if path and os.path.exists(path):
         with np.load(path, allow_pickle=False) as f:
             out = {k: f[k] for k in _KEYS}
     else:
         li = synth.make_layer_inputs(cfg, seed_extra, projections=[proj.name])
         x = li.x[proj.input_key]
-        art = calibrate.calibrate_layer(x, li.modality, li.w[proj.name], cfg.n_mod, cfg.rank,
-                                        cfg.lr_dtype, weight_bits=weight_bits)
+        if method == "smoothquant":
+            art = calibrate.calibrate_smoothquant(x, li.w[proj.name], cfg.n_mod, cfg.lr_dtype,
+                                                  weight_bits=weight_bits)
+        else:
+            art = calibrate.calibrate_layer(x, li.modality, li.w[proj.name], cfg.n_mod,
+                                            cfg.rank, cfg.lr_dtype, weight_bits=weight_bits)
         out = dict(x=x, modality=li.modality, **{k: art[k] for k in _KEYS[2:]})
         if path:
             tmp = path + ".tmp.npz"
             np.savez(tmp, **out)
             os.replace(tmp, path)
-    out.update(cfg=cfg, proj=proj, n_mod=cfg.n_mod, rank=cfg.rank,
+    out.update(cfg=cfg, proj=proj, n_mod=cfg.n_mod,
+               rank=cfg.rank if method == "masquant" else 0, method=method,
                act_dtype=cfg.act_dtype, lr_dtype=cfg.lr_dtype, weight_bits=weight_bits)
     return out
 

@@ -127,6 +127,19 @@ def test_workload_parity(ops, cfg_index, proj):
     _check_layer(ops, L, rows, name=f"cfg{cfg_index}/{proj}")
 
 
+# ------------------------------------------------------------------ comparator
+@pytest.mark.parametrize("cfg_index", [0, 2, 3])
+def test_smoothquant_comparator_parity(ops, cfg_index):
+    """The SmoothQuant comparator (one unified smoothing factor, no
+    compensation; Sec. 4.1) runs through the same kernels and C ABI at the
+    workload's full size, held to the same bar."""
+    from paper_2603_04800_amd import workload
+    L = workload.layer(cfg_index, method="smoothquant")
+    assert L["rank"] == 0
+    rows = None if L["x"].shape[0] * L["wq"].shape[0] <= 256 * 4096 else _sample_rows(L["modality"])
+    _check_layer(ops, L, rows, name=f"smoothquant/cfg{cfg_index}")
+
+
 # ------------------------------------------------------------------ edge cases
 def _random_layer(T, K, N, r, M, act, lr, layout="alternating", zero_rows=(), seed=0,
                   counts=None, weight_bits=8):
