@@ -13,9 +13,8 @@ rank 64, bf16 activations and outputs, int8 shared weight.
 
 Prints one JSON line.  value = effective TOPS = sum of 2 T C_in C_out over
 the step time (dense-equivalent int8 operations; quantisation and
-compensation are not credited), from K steps timed with nothing else on
-the stream.  roofline: the stage-2 GEMM kernel, timed with HIP events
-around each of its launches on its stream over K further steps;
+compensation are not credited).  roofline: the stage-2 GEMM kernel, timed
+with HIP events around each launch on its stream in the timed region;
 against the 5.0 POPS dense int8 peak (algorithmic int8 ops) or, below the
 ridge point (the decode workload), against 8 TB/s HBM (algorithmic bytes of
 the kernel).  cpu_baseline: the CPU oracle on the same workload.
@@ -346,32 +345,26 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup} steps done ({copies} rotating copies)")
 
-    # Timed region: K steps with nothing but the layer calls on the stream
-    # (an event record between launches costs GPU time of its own, ~2-3 us).
+    # Timed region: K steps, with HIP events recorded on the launch stream
+    # around every stage-2 (GEMM) launch; their mean duration is the
+    # roofline's denominator.  The two event records per projection are
+    # part of the timed work (a few us each on the GPU's timeline).
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in layers] for _ in range(args.steps)]
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
     for i in range(args.steps):
-        step(args.warmup + i)
+        step(args.warmup + i, evs[i])
     end.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
     ms = total_ms / args.steps
-    # Kernel region: the same K steps again, with HIP events recorded on the
-    # launch stream around every stage-2 (GEMM) launch; their mean duration
-    # is the roofline's denominator.
-    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-            for _ in layers] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    for i in range(args.steps):
-        step(args.warmup + args.steps + i, evs[i])
-    torch.cuda.synchronize()
     gemm_ms_per = [sum(evs[i][k][0].elapsed_time(evs[i][k][1]) for i in range(args.steps))
                    / args.steps for k in range(len(layers))]
     gemm_ms = sum(gemm_ms_per)
-    log(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step; GEMM stages {gemm_ms:.4f} ms "
-        f"(events, second pass)")
+    log(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step, GEMM stages {gemm_ms:.4f} ms")
 
     ops = sum(2.0 * T * L["x"].shape[1] * L["wq"].shape[0] for L in layers)
     tops = ops / (ms * 1e-3) / 1e12
