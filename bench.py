@@ -1,7 +1,7 @@
 """Benchmark of the modality-aware W8A8 + low-rank linear on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload I] [--no-cpu]
-                    [--method masquant|smoothquant]
+                    [--method masquant|smoothquant] [--weight-bits 8|4]
 
 A step is one pass of the hot path over every projection of the workload:
 per projection, smoothing + per-token int8 quantisation + the rank-r
@@ -47,6 +47,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=1)
+    ap.add_argument("--weight-bits", type=int, default=8, choices=(8, 4),
+                    help="4: the W4A8 setting (shared weight as packed 4-bit codes)")
     ap.add_argument("--method", default="masquant", choices=("masquant", "smoothquant"),
                     help="smoothquant: the comparator on the same kernels (unified smoothing "
                          "factor, no compensation), to measure what the compensation costs")
@@ -92,7 +94,8 @@ def algorithmic_bytes(L) -> int:
     act = 2 if L["act_dtype"] == "bf16" else 4
     lr = 2 if L["lr_dtype"] == "bf16" else 4
     present = len(set(L["modality"].tolist()) - {0})
-    return (T * K * act + T * N * act + N * K + N * 4 + L["n_mod"] * K * 4
+    wbytes = N * K * int(L.get("weight_bits", 8)) // 8
+    return (T * K * act + T * N * act + wbytes + N * 4 + L["n_mod"] * K * 4
             + present * L["rank"] * (K + N) * lr + T * 4)
 
 
@@ -278,7 +281,8 @@ def gemm_bytes(L) -> int:
     out = 2 if L["act_dtype"] == "bf16" else 4
     lr = 2 if L["lr_dtype"] == "bf16" else 4
     present = len(set(L["modality"].tolist()) - {0})
-    return (T * K + N * K + T * N * out + N * 4 + T * 4 + T * 4
+    wbytes = N * K * int(L.get("weight_bits", 8)) // 8
+    return (T * K + wbytes + T * N * out + N * 4 + T * 4 + T * 4
             + (T * L["rank"] * 4 + present * L["rank"] * N * lr if present else 0))
 
 
@@ -306,7 +310,8 @@ def main():
 
     t0 = time.time()
     cfg = CONFIGS[args.workload]
-    layers = [workload.layer(cfg, p.name, method=args.method) for p in cfg.projections]
+    layers = [workload.layer(cfg, p.name, method=args.method, weight_bits=args.weight_bits)
+              for p in cfg.projections]
     log(f"[bench] workload {cfg.name}: {len(layers)} projection(s), inputs + calibration "
         f"{time.time() - t0:.1f}s")
     out_dtype = torch.bfloat16 if cfg.act_dtype == "bf16" else torch.float32
@@ -380,7 +385,8 @@ def main():
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": INT8_PEAK_TOPS,
                 "unit": "TOPS", "frac": round(achieved / INT8_PEAK_TOPS, 4)}
     src_hash = kernel_source_hash()
-    traffic = traffic_from_profiles(cfg.name, src_hash)
+    traffic = (traffic_from_profiles(cfg.name, src_hash)
+               if args.weight_bits == 8 and args.method == "masquant" else None)
     roof.update({
         "kernel": gemm_kernel_label(layers),
         "traffic": traffic,
@@ -406,7 +412,9 @@ def main():
             "projections": [[p.name, int(p.c_in), int(p.c_out)] for p in cfg.projections],
             "method": args.method, "rank": int(layers[0]["rank"]),
             "modality_counts": list(map(int, cfg.counts)),
-            "io_dtype": cfg.act_dtype, "weight_dtype": "int8", "factor_dtype": cfg.lr_dtype,
+            "io_dtype": cfg.act_dtype,
+            "weight_dtype": "int8" if args.weight_bits == 8 else "int4 (packed, W4A8)",
+            "factor_dtype": cfg.lr_dtype,
             "rotating_copies": copies,
         },
         "effective_GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
