@@ -137,6 +137,28 @@ __device__ __forceinline__ v4i w4_operand(v2i p) {
     return v4i{(p.x << 4) & kHi, p.x & kHi, (p.y << 4) & kHi, p.y & kHi};
 }
 
+// ================================================================ LDS DMA
+// One 16-byte lane of an LDS-DMA load: the wave writes 64 x 16 contiguous
+// bytes at LDS address m0 (wave-uniform), lane i at m0 + 16 i.
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :: "v"(src), "s"(lds_addr) : "memory", "m0");
+}
+
+// Scheduling fence: the compiler may move no instruction across it, so the
+// software pipeline below keeps the order it is written in.
+#define MASQ_SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
+
+// s_waitcnt vmcnt(n) lgkmcnt(0) (expcnt unconstrained).
+#define MASQ_WAIT_VMCNT_LGKM0(n) \
+    __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (0 << 8))
+
+// One 4-byte lane of an LDS-DMA load: lane i writes LDS address m0 + 4 i.
+__device__ __forceinline__ void lds_dma4(const void* src, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+                 :: "v"(src), "s"(lds_addr) : "memory", "m0");
+}
+
 // ================================================================ smoothing + quant
 // One workgroup per token row (small batches, where a row's latency
 // matters): the first 256 x 8 x kSqChunks elements of the row are loaded
@@ -777,10 +799,14 @@ __global__ __launch_bounds__(256) void k_stage1_small(
 // non-text modality present).  Absmax and u are combined across waves in
 // LDS in a fixed order.  Pass 2 re-reads the wave's part (from cache) and
 // writes the int8 codes with the row's reciprocal scale.
+// SL (32 rows): the smoothing factors of every modality ([n_mod][K] fp32,
+// at most kFuseInvBytes) are copied to LDS by DMA at the start and read from
+// there instead of being loaded with every step of every row group.
 constexpr int kFuseWaves = 8;
 constexpr int kFuseWideMinT = 8192;    // batches from this size take 32 rows per workgroup
+constexpr int kFuseInvBytes = 65536;
 
-template <typename XT, int RG>
+template <typename XT, int RG, bool SL = false>
 __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
     const XT* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
     const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod,
@@ -793,13 +819,23 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
     __shared__ float samax[kFuseWaves][kRows];
     __shared__ float red[kFuseWaves][kRows][64];
     __shared__ float srq[kRows];
+    __shared__ __attribute__((aligned(16))) float s_inv[SL ? kFuseInvBytes / 4 : 4];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kRows;
+    if constexpr (SL) {
+        // n_mod K / 4 pieces of 16 bytes in 1 KB blocks (the last block's
+        // pieces past the end repeat the last piece; the host checks the fit)
+        const int pieces = n_mod * K / 4;
+        const uint32_t b0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(s_inv));
+        for (int i = wave; i * 64 < pieces; i += kFuseWaves)
+            lds_dma16(inv_s + 4 * min(i * 64 + lane, pieces - 1), b0 + i * 1024);
+    }
     if (tid < kRows) {
         const int64_t t = row0 + tid;
         smod[tid] = t < T ? sane_mod(mod[t], n_mod) : 0;
     }
+    if constexpr (SL) MASQ_WAIT_VMCNT_LGKM0(0);      // this wave's share of the factors
     __syncthreads();
     // non-text modalities present in the tile, as a list (scalar registers:
     // the MFMA loop below must branch on it, MFMA ignores EXEC)
@@ -858,7 +894,7 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
 #pragma unroll
             for (int g = 0; g < RG; ++g) {
                 S.xr[g][uu].load(xrow[g] + kc);
-                S.sr[g][uu].load(srow[g] + kc);
+                if constexpr (!SL) S.sr[g][uu].load(srow[g] + kc);
             }
             if (np > 0) {
 #pragma unroll
@@ -879,7 +915,14 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
             for (int uu = 0; uu < kU; ++uu) {
                 float xv[8], sv[8], xs[8];
                 S.xr[g][uu].to_f32(xv);
-                S.sr[g][uu].to_f32(sv);
+                if constexpr (SL) {
+                    const int k = k0 + kStep * uu + 8 * kg;
+                    const float* sp = s_inv + mrow[g] * K + (k < ke ? k : ke - 8);
+                    *reinterpret_cast<v4f*>(sv) = *reinterpret_cast<const v4f*>(sp);
+                    *reinterpret_cast<v4f*>(sv + 4) = *reinterpret_cast<const v4f*>(sp + 4);
+                } else {
+                    S.sr[g][uu].to_f32(sv);
+                }
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     xs[e] = xv[e] * sv[e];
@@ -1022,7 +1065,7 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
             const int64_t tl = live[g] ? tq : row0;
             const int kl = live[g] ? k : kb;
             const XT* xr2 = x + tl * static_cast<int64_t>(K);
-            const float* sr2 = inv_s + static_cast<int64_t>(smod[qr]) * K;
+            const float* sr2 = (SL ? s_inv : inv_s) + static_cast<int64_t>(smod[qr]) * K;
             Elem<XT>::load8(xr2 + kl, *reinterpret_cast<float(*)[8]>(xv[g]));
             Elem<XT>::load8(xr2 + kl + 8, *reinterpret_cast<float(*)[8]>(xv[g] + 8));
             load8_f32(sr2 + kl, *reinterpret_cast<float(*)[8]>(sv[g]));
@@ -1819,26 +1862,6 @@ constexpr int kDmaStageBytes = 2 * kTileM * kDmaStageK;     // A + B
 // 16-byte slots (r % 4) * 4 + (chunk ^ (r / 4 % 4)).)
 __device__ __forceinline__ int swz4(int row) { return (row >> 2) & 3; }
 
-// One 16-byte lane of an LDS-DMA load: the wave writes 64 x 16 contiguous
-// bytes at LDS address m0 (wave-uniform), lane i at m0 + 16 i.
-__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-                 :: "v"(src), "s"(lds_addr) : "memory", "m0");
-}
-
-// Scheduling fence: the compiler may move no instruction across it, so the
-// software pipeline below keeps the order it is written in.
-#define MASQ_SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
-
-// s_waitcnt vmcnt(n) lgkmcnt(0) (expcnt unconstrained).
-#define MASQ_WAIT_VMCNT_LGKM0(n) \
-    __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (0 << 8))
-
-// One 4-byte lane of an LDS-DMA load: lane i writes LDS address m0 + 4 i.
-__device__ __forceinline__ void lds_dma4(const void* src, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
-                 :: "v"(src), "s"(lds_addr) : "memory", "m0");
-}
 
 // NWN waves along the channels: 2 (four waves of 128 x 128, one per SIMD)
 // or 4 (eight waves of 128 x 64, two per SIMD).
@@ -2690,13 +2713,20 @@ hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const
     const bool wide = T >= kFuseWideMinT;
     const int rows = wide ? 32 : 16;
     const dim3 grid(static_cast<unsigned>((T + rows - 1) / rows)), block(64 * kFuseWaves);
-#define MASQ_F1(XT, RG) hipLaunchKernelGGL((k_stage1_fused<XT, RG>), grid, block, 0, s, \
+#define MASQ_F1(XT, RG, SL) hipLaunchKernelGGL((k_stage1_fused<XT, RG, SL>), grid, block, 0, s, \
         static_cast<const XT*>(x), mod, inv_s, static_cast<const bf16_t*>(l_down), T, \
         static_cast<int>(K), rank, n_mod, q, x_scale, u, u_hl, zero_ints, n_zero)
+    // 32 rows: smoothing factors from LDS when all modalities' fit (bf16
+    // activations); 16 rows keep them in registers (their pass 1 was no
+    // faster with them in LDS and a deeper load pipeline)
+    const bool sl = wide &&
+                    ((static_cast<int64_t>(n_mod) * K * 4 + 1023) / 1024) * 1024 <= kFuseInvBytes;
     if (x_dt == DT::BF16) {
-        if (wide) MASQ_F1(bf16_t, 2); else MASQ_F1(bf16_t, 1);
+        if (sl) MASQ_F1(bf16_t, 2, true);
+        else if (wide) MASQ_F1(bf16_t, 2, false);
+        else MASQ_F1(bf16_t, 1, false);
     } else {
-        if (wide) MASQ_F1(float, 2); else MASQ_F1(float, 1);
+        if (wide) MASQ_F1(float, 2, false); else MASQ_F1(float, 1, false);
     }
 #undef MASQ_F1
     return hipGetLastError();
