@@ -783,7 +783,7 @@ __global__ __launch_bounds__(256) void k_stage1_small(
     if (blockIdx.x == 0)
         for (int i = threadIdx.x; i < n_zero; i += blockDim.x) zero_ints[i] = 0;
     if (static_cast<int>(blockIdx.x) < T) {
-        sq_row<XT, 256, kSqChunks / 2>(x, mod, inv_s, K, n_mod, q, x_scale, blockIdx.x);
+        sq_row<XT, 256, kSqChunks>(x, mod, inv_s, K, n_mod, q, x_scale, blockIdx.x);
     } else if (l_down != nullptr) {
         down_tile_in<4, XT, LT>(x, mod, inv_s, l_down, T, K, r, n_mod, kslice, n_kslices, u,
                                 u_part, nullptr, 0, blockIdx.x - T, smod, red, &last);
