@@ -127,6 +127,50 @@ def test_workload_parity(ops, cfg_index, proj):
     _check_layer(ops, L, rows, name=f"cfg{cfg_index}/{proj}")
 
 
+# ------------------------------------------------------------------ random sweep
+def _sweep_cases(n=24, seed=2024):
+    """Seeded random valid shapes across the dispatch boundaries: batches of
+    1-16 tokens (small-batch and decode GEMMs), 17-300 and 300-1300 tokens
+    (tiled GEMM, split K on small grids); K a multiple of 64 (direct-to-LDS,
+    decode, W4A8) or, every fifth case, a ragged multiple of 16 (general-K
+    GEMM); N a multiple of 16; rank 0-64; one to four modalities; fp32 or
+    bf16 activations and factors; contiguous, alternating or run layouts."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        lo, hi = [(1, 17), (17, 301), (301, 1301), (1, 1301)][i % 4]
+        T = int(rng.integers(lo, hi))
+        ragged = i % 5 == 0
+        K = 16 * (4 * int(rng.integers(1, 40)) + int(rng.integers(1, 4))) if ragged \
+            else 64 * int(rng.integers(1, 40))
+        w4 = not ragged and i % 3 == 1
+        N = 16 * int(rng.integers(1, 48))
+        M = int(rng.integers(1, 5))
+        r = 0 if M == 1 else 16 * int(rng.integers(0, 5))
+        act = str(rng.choice(["f32", "bf16"]))
+        lr = str(rng.choice(["f32", "bf16"]))
+        layout = str(rng.choice(["contiguous", "alternating", "runs"]))
+        cases.append(dict(T=T, K=K, N=N, r=r, M=M, act=act, lr=lr, layout=layout,
+                          weight_bits=4 if w4 else 8, seed=int(seed + i)))
+    return cases
+
+
+_SWEEP = _sweep_cases()
+
+
+@pytest.mark.parametrize("case", _SWEEP, ids=[
+    f"T{c['T']}_K{c['K']}_N{c['N']}_r{c['r']}_M{c['M']}_{c['act']}_{c['lr']}_{c['layout']}_w{c['weight_bits']}"
+    for c in _SWEEP])
+def test_random_shape_parity(ops, case):
+    kw = dict(case)
+    L = _random_layer(kw.pop("T"), kw.pop("K"), kw.pop("N"), kw.pop("r"), kw.pop("M"),
+                      kw.pop("act"), kw.pop("lr"), **kw)
+    if L["rank"] == 0:
+        L["l_down"] = L["l_down"][:, :0]
+        L["r_up"] = L["r_up"][:, :, :0]
+    _check_layer(ops, L, name="sweep")
+
+
 # ------------------------------------------------------------------ comparator
 @pytest.mark.parametrize("cfg_index", [0, 2, 3])
 def test_smoothquant_comparator_parity(ops, cfg_index):
