@@ -1,7 +1,7 @@
 """Benchmark of the modality-aware W8A8 + low-rank linear on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload I] [--no-cpu]
-                    [--method masquant|smoothquant] [--weight-bits 8|4]
+                    [--method masquant|smoothquant|mas] [--weight-bits 8|4]
 
 A step is one pass of the hot path over every projection of the workload:
 per projection, smoothing + per-token int8 quantisation + the rank-r
@@ -49,9 +49,10 @@ def parse():
     ap.add_argument("--workload", type=int, default=1)
     ap.add_argument("--weight-bits", type=int, default=8, choices=(8, 4),
                     help="4: the W4A8 setting (shared weight as packed 4-bit codes)")
-    ap.add_argument("--method", default="masquant", choices=("masquant", "smoothquant"),
-                    help="smoothquant: the comparator on the same kernels (unified smoothing "
-                         "factor, no compensation), to measure what the compensation costs")
+    ap.add_argument("--method", default="masquant", choices=("masquant", "smoothquant", "mas"),
+                    help="comparators on the same kernels: smoothquant (one unified smoothing "
+                         "factor, no compensation) or mas (MAS-only: a weight per modality, no "
+                         "compensation; layouts whose runs start at multiples of 4 tokens)")
     ap.add_argument("--copies", type=int, default=2,
                     help="rotating input/output sets so no step reuses the last one's cache")
     ap.add_argument("--no-cpu", action="store_true")
@@ -86,15 +87,24 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def _weight_bytes(L) -> int:
+    """Bytes of the weight(s) a step reads: the shared weight at its bit width,
+    or, for the MAS-only comparator, the weight of every modality present."""
+    wq = L["wq"]
+    if wq.ndim == 3:
+        return len(set(L["modality"].tolist())) * wq.shape[1] * wq.shape[2]
+    return wq.shape[0] * wq.shape[1] * int(L.get("weight_bits", 8)) // 8
+
+
 def algorithmic_bytes(L) -> int:
     """Bytes the layer itself must move: X, Y, Wq, scales, smoothing vectors,
     factors of the non-text modalities present, modality ids."""
     T, K = L["x"].shape
-    N = L["wq"].shape[0]
+    N = L["wq"].shape[-2]
     act = 2 if L["act_dtype"] == "bf16" else 4
     lr = 2 if L["lr_dtype"] == "bf16" else 4
     present = len(set(L["modality"].tolist()) - {0})
-    wbytes = N * K * int(L.get("weight_bits", 8)) // 8
+    wbytes = _weight_bytes(L)
     return (T * K * act + T * N * act + wbytes + N * 4 + L["n_mod"] * K * 4
             + present * L["rank"] * (K + N) * lr + T * 4)
 
@@ -247,7 +257,7 @@ def cpu_baseline(layers, min_seconds=10.0, max_runs=64):
                         L["l_down"], L["r_up"])
         dt += time.perf_counter() - t0
         runs += 1
-    ops = sum(2.0 * L["x"].shape[0] * L["x"].shape[1] * L["wq"].shape[0] for L in layers)
+    ops = sum(2.0 * L["x"].shape[0] * L["x"].shape[1] * L["wq"].shape[-2] for L in layers)
     T = layers[0]["x"].shape[0]
     n_text = int((np.asarray(layers[0]["modality"]) == 0).sum())
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
@@ -277,11 +287,11 @@ def gemm_bytes(L) -> int:
     rank-r rows u, the factors of the non-text modalities present, modality
     ids and the output."""
     T, K = L["x"].shape
-    N = L["wq"].shape[0]
+    N = L["wq"].shape[-2]
     out = 2 if L["act_dtype"] == "bf16" else 4
     lr = 2 if L["lr_dtype"] == "bf16" else 4
     present = len(set(L["modality"].tolist()) - {0})
-    wbytes = N * K * int(L.get("weight_bits", 8)) // 8
+    wbytes = _weight_bytes(L)
     return (T * K + wbytes + T * N * out + N * 4 + T * 4 + T * 4
             + (T * L["rank"] * 4 + present * L["rank"] * N * lr if present else 0))
 
@@ -371,7 +381,7 @@ def main():
     gemm_ms = sum(gemm_ms_per)
     log(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step, GEMM stages {gemm_ms:.4f} ms")
 
-    ops = sum(2.0 * T * L["x"].shape[1] * L["wq"].shape[0] for L in layers)
+    ops = sum(2.0 * T * L["x"].shape[1] * L["wq"].shape[-2] for L in layers)
     tops = ops / (ms * 1e-3) / 1e12
     nbytes = sum(algorithmic_bytes(L) for L in layers)
     gbytes = sum(gemm_bytes(L) for L in layers)
@@ -388,7 +398,8 @@ def main():
     traffic = (traffic_from_profiles(cfg.name, src_hash)
                if args.weight_bits == 8 and args.method == "masquant" else None)
     roof.update({
-        "kernel": gemm_kernel_label(layers),
+        "kernel": (gemm_kernel_label(layers) if args.method != "mas" else
+                   "masq_w8a8_gemm per run of one modality (stage 2: int8 GEMM + dequant)"),
         "traffic": traffic,
         "gemm_ms": round(gemm_ms, 5),
         "ops_per_step": int(ops), "algorithmic_bytes_per_step": int(gbytes),
@@ -423,7 +434,7 @@ def main():
         "roofline": roof,
         "kernel_source_sha256_16": src_hash,
     }
-    if not args.no_cpu:
+    if not args.no_cpu and args.method == "masquant":
         try:
             record["cpu_baseline"] = cpu_baseline(layers)
         except Exception as e:          # the baseline is a report, never the measurement

@@ -203,3 +203,21 @@ def calibrate_smoothquant(x: np.ndarray, w: np.ndarray, n_mod: int, lr_dtype: st
                 l_down=np.zeros((max(n_mod - 1, 0), 0, k), np.float32),
                 r_up=np.zeros((max(n_mod - 1, 0), n, 0), np.float32),
                 rank=0, n_mod=n_mod, lr_dtype=lr_dtype, weight_bits=weight_bits)
+
+
+def calibrate_mas_only(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: int,
+                       lr_dtype: str = "bf16") -> dict:
+    """The MAS-only comparator (Sec. 4.2, without the shared weight): the
+    per-modality MAS factors as for MASQuant, and one int8 weight per
+    modality, Q(S_m W) per output channel; no compensation.  wq [M][N][K],
+    w_scale [M][N]."""
+    x = np.asarray(x, np.float32)
+    w = np.asarray(w, np.float32)
+    s32, inv = smoothing_factors(x, np.asarray(modality, np.int32), w, n_mod)
+    qs = [quantize_shared_weight(w, s32[m], 8) for m in range(n_mod)]
+    k, n = w.shape
+    return dict(inv_smooth=inv, s32=s32, wq=np.stack([q for q, _ in qs]),
+                w_scale=np.stack([sc for _, sc in qs]),
+                l_down=np.zeros((max(n_mod - 1, 0), 0, k), np.float32),
+                r_up=np.zeros((max(n_mod - 1, 0), n, 0), np.float32),
+                rank=0, n_mod=n_mod, lr_dtype=lr_dtype, weight_bits=8)

@@ -272,6 +272,103 @@ class BoundLinear:
             raise MasqError(self._names[2], code)
 
 
+def modality_runs(modality) -> list:
+    """Maximal runs (start, length, modality id) of equal ids, from a host copy
+    of the per-token ids (a layout plan, made once per batch layout)."""
+    import numpy as np
+    m = np.asarray(modality.cpu() if hasattr(modality, "cpu") else modality)
+    if m.size == 0:
+        return []
+    cut = np.flatnonzero(np.diff(m)) + 1
+    starts = np.concatenate([[0], cut])
+    ends = np.concatenate([cut, [m.size]])
+    return [(int(a), int(b - a), int(m[a])) for a, b in zip(starts, ends)]
+
+
+class MasOnlyLinear:
+    """The MAS-only comparator (Sec. 4.2 without the shared weight): every
+    modality has its own int8 weight Q(S_m W), no compensation.  It runs on
+    the library's own entry points: masq_smooth_quant over all rows (each
+    with its modality's factors), then masq_w8a8_gemm on each run of equal
+    modality ids with that modality's weight, reading and writing the run's
+    rows in place.  Runs must start at multiples of 4 tokens (16-byte
+    alignment of the per-token scales), as in contiguous layouts.
+
+    Holds inv_smooth [M][K] f32, wq [M][N][K] int8, w_scale [M][N] f32."""
+
+    def __init__(self, inv_smooth, wq, w_scale):
+        if wq.dim() != 3 or wq.dtype != torch.int8:
+            raise ValueError("wq must be int8 [M][N][K]")
+        self.inv_smooth, self.wq, self.w_scale = inv_smooth, wq, w_scale
+        self.n_mod, self.c_out, self.c_in = wq.shape
+        self.rank = 0
+
+    @classmethod
+    def from_arrays(cls, art: dict, device="cuda"):
+        def dev(a, dtype):
+            return torch.as_tensor(a).to(device=device, dtype=dtype).contiguous()
+        return cls(dev(art["inv_smooth"], torch.float32), dev(art["wq"], torch.int8),
+                   dev(art["w_scale"], torch.float32))
+
+    def workspace(self, T, device):
+        """Codes [T][K] int8 then scales [T] f32 (256-byte aligned)."""
+        q_bytes = (T * self.c_in + 255) // 256 * 256
+        return torch.empty(max(q_bytes + 4 * T, 256), dtype=torch.uint8, device=device)
+
+    def bind(self, x, modality, out, workspace=None, stream=None):
+        return BoundMasOnly(self, x, modality, out, workspace, stream)
+
+    def __call__(self, x, modality, out=None, out_dtype=None, stream=None):
+        if out is None:
+            out = torch.empty((x.shape[0], self.c_out), device=x.device,
+                              dtype=out_dtype or x.dtype)
+        if x.shape[0]:
+            self.bind(x, modality, out, stream=stream)()
+        return out
+
+
+class BoundMasOnly:
+    """Pre-marshalled calls of :class:`MasOnlyLinear` on fixed buffers:
+    stage1() quantises every row, stage2() runs the per-run GEMMs."""
+
+    def __init__(self, lin, x, modality, out, workspace=None, stream=None):
+        T, K = x.shape
+        N = lin.c_out
+        ws = workspace if workspace is not None else lin.workspace(T, x.device)
+        q_bytes = (T * K + 255) // 256 * 256
+        if ws.numel() < q_bytes + 4 * T:
+            raise ValueError("workspace too small")
+        q = ws[: T * K].view(torch.int8).view(T, K)
+        dx = ws[q_bytes: q_bytes + 4 * T].view(torch.float32)
+        runs = modality_runs(modality)
+        if any(a % 4 for a, _, _ in runs):
+            raise ValueError("the MAS-only comparator needs runs starting at multiples of 4 tokens")
+        st = _stream(stream)
+        self._sq = (_ptr(x), _dt(x), _ptr(modality), _ptr(lin.inv_smooth), T, K, lin.n_mod,
+                    _ptr(q), _ptr(dx), st)
+        ydt, esz = _dt(out), out.element_size()
+        self._gemms = []
+        for a, n, m in runs:
+            mm = m if 0 <= m < lin.n_mod else 0          # out-of-range ids read as text
+            self._gemms.append((ctypes.c_void_p(q.data_ptr() + a * K),
+                                ctypes.c_void_p(dx.data_ptr() + 4 * a),
+                                ctypes.c_void_p(lin.wq[mm].data_ptr()),
+                                ctypes.c_void_p(lin.w_scale[mm].data_ptr()), n, K, N, None,
+                                ctypes.c_void_p(out.data_ptr() + a * N * esz), ydt, st))
+        self._keep = (lin, x, modality, out, ws)
+
+    def stage1(self):
+        _check("masq_smooth_quant", _lib.masq_smooth_quant(*self._sq))
+
+    def stage2(self):
+        for g in self._gemms:
+            _check("masq_w8a8_gemm", _lib.masq_w8a8_gemm(*g))
+
+    def __call__(self):
+        self.stage1()
+        self.stage2()
+
+
 def linear_fused(x, modality, inv_smooth, wq, w_scale, l_down=None, r_up=None,
                  out_dtype=None, stream=None):
     """Functional form of :class:`Linear` (allocates its workspace per call)."""

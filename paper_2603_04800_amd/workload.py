@@ -18,7 +18,7 @@ from . import calibrate
 _KEYS = ("x", "modality", "inv_smooth", "wq", "w_scale", "l_down", "r_up")
 
 
-METHODS = ("masquant", "smoothquant")
+METHODS = ("masquant", "smoothquant", "mas")
 
 
 def _cache_path(cfg, proj, seed_extra, weight_bits, method):
@@ -37,8 +37,9 @@ def layer(cfg, proj_name: str | None = None, seed_extra: int = 0, weight_bits: i
     bf16 workloads), modality [T] int32, and the calibration arrays; with
     weight_bits=4 the shared weight is quantised to 4-bit codes (kept as
     int8 codes here; the device copy is packed).  method="smoothquant" gives
-    the comparator instead: the unified smoothing factor for every token and
-    no compensation (rank 0)."""
+    the comparator with the unified smoothing factor for every token and no
+    compensation (rank 0); method="mas" the MAS-only comparator, one weight
+    per modality (wq [M][N][K], w_scale [M][N]) and no compensation."""
     if method not in METHODS:
         raise ValueError(f"method must be one of {METHODS}")
     if isinstance(cfg, (int, str)):
@@ -55,6 +56,11 @@ def layer(cfg, proj_name: str | None = None, seed_extra: int = 0, weight_bits: i
         if method == "smoothquant":
             art = calibrate.calibrate_smoothquant(x, li.w[proj.name], cfg.n_mod, cfg.lr_dtype,
                                                   weight_bits=weight_bits)
+        elif method == "mas":
+            if weight_bits != 8:
+                raise ValueError("the MAS-only comparator is built for 8-bit weights")
+            art = calibrate.calibrate_mas_only(x, li.modality, li.w[proj.name], cfg.n_mod,
+                                               cfg.lr_dtype)
         else:
             art = calibrate.calibrate_layer(x, li.modality, li.w[proj.name], cfg.n_mod,
                                             cfg.rank, cfg.lr_dtype, weight_bits=weight_bits)
@@ -77,5 +83,8 @@ def to_device(layer_arrays: dict, device="cuda"):
     act = torch.bfloat16 if layer_arrays["act_dtype"] == "bf16" else torch.float32
     x = torch.from_numpy(layer_arrays["x"]).to(device=device, dtype=act).contiguous()
     mod = torch.from_numpy(layer_arrays["modality"]).to(device=device).contiguous()
-    lin = ops.Linear.from_arrays(layer_arrays, device)
+    if layer_arrays.get("method") == "mas":
+        lin = ops.MasOnlyLinear.from_arrays(layer_arrays, device)
+    else:
+        lin = ops.Linear.from_arrays(layer_arrays, device)
     return x, mod, lin

@@ -109,3 +109,24 @@ def test_product_smoothquant_calibration_matches_oracle(n_mod):
     assert np.array_equal(got["wq"], ref["wq"])
     assert np.array_equal(got["w_scale"], ref["w_scale"])
     assert got["l_down"].shape == ref["l_down"].shape and got["r_up"].shape == ref["r_up"].shape
+
+
+def test_product_mas_only_calibration_matches_oracle():
+    """The MAS-only comparator's artifacts for the GPU: per-modality factors
+    and one weight Q(S_m W) per modality, equal to the oracle's bit for bit."""
+    x, mod, w = _layer(8)
+    got = pcal.calibrate_mas_only(x, mod, w, 3, lr_dtype="f32")
+    wmax = cal.weight_range(w)
+    for m in range(3):
+        s32, inv = cal.smoothing_factor(cal.channel_range(x, mod, m), wmax)
+        wq, w_scale, _ = cal.quantize_weight(w, s32)
+        assert np.array_equal(got["inv_smooth"][m], inv)
+        assert np.array_equal(got["wq"][m], wq)
+        assert np.array_equal(got["w_scale"][m], w_scale)
+    # and the per-modality composition is the oracle's MAS-only layer
+    y = np.zeros((x.shape[0], w.shape[1]), np.float32)
+    for m in range(3):
+        rows = mod == m
+        y[rows] = inf.linear(x[rows], np.zeros(rows.sum(), np.int32), got["inv_smooth"][m][None],
+                             got["wq"][m], got["w_scale"][m])
+    assert np.array_equal(y, cmp.mas_only_linear(x, mod, w, 3))

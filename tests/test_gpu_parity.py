@@ -184,6 +184,31 @@ def test_smoothquant_comparator_parity(ops, cfg_index):
     _check_layer(ops, L, rows, name=f"smoothquant/cfg{cfg_index}")
 
 
+@pytest.mark.parametrize("cfg_index", [0, 1, 2])
+def test_mas_only_comparator_parity(ops, cfg_index):
+    """The MAS-only comparator (a weight per modality, no compensation;
+    Sec. 4.2) through masq_smooth_quant and per-run masq_w8a8_gemm calls:
+    outputs bit-exact against the oracle's layer, modality by modality
+    (sampled rows at full size)."""
+    from paper_2603_04800_amd import workload
+    L = workload.layer(cfg_index, method="mas")
+    x, mod, lin = workload.to_device(L)
+    act = L["act_dtype"]
+    y = lin(x, mod, out_dtype=torch.bfloat16 if act == "bf16" else torch.float32)
+    torch.cuda.synchronize()
+    mod_np = L["modality"]
+    rows = np.arange(mod_np.shape[0]) if L["x"].shape[0] * L["wq"].shape[1] <= 256 * 4096 \
+        else _sample_rows(mod_np)
+    y_np = _np(y)
+    for m in range(L["n_mod"]):
+        rm = rows[mod_np[rows] == m]
+        if rm.size == 0:
+            continue
+        ref = oinf.linear(L["x"][rm], np.zeros(rm.size, np.int32), L["inv_smooth"][m][None],
+                          L["wq"][m], L["w_scale"][m])
+        assert np.array_equal(y_np[rm], oinf.to_output(ref, act)), f"modality {m} differs"
+
+
 # ------------------------------------------------------------------ edge cases
 def _random_layer(T, K, N, r, M, act, lr, layout="alternating", zero_rows=(), seed=0,
                   counts=None, weight_bits=8):
