@@ -58,7 +58,8 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--summarize-profiles", metavar="DIR", default=None,
                     help="write the profiles/ summaries of the rocprofv3 runs under DIR "
-                         "(trace/, fetch/, write/, copy_fetch/, copy_write/ and their .log)")
+                         "(trace/, fetch/, write/, copy_fetch/, copy_write/ and their .log; "
+                         "mfma/ and lds/ for the counter summary)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (5 times): the "
                          "reference for scaling HBM traffic counters")
@@ -124,6 +125,12 @@ PROFILE_COMMANDS = {
     "write": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc WRITE_SIZE --output-format csv "
              "-d <out>/write -o run -- python3 <repo>/bench.py --workload {w} --steps 3 "
              "--warmup 1 --no-cpu",
+    "mfma": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_I8 "
+            "GRBM_GUI_ACTIVE --kernel-trace --output-format csv -d <out>/mfma -o run -- python3 "
+            "<repo>/bench.py --workload {w} --steps 3 --warmup 1 --no-cpu",
+    "lds": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE "
+           "SQ_INSTS_LDS SQ_WAVES --kernel-trace --output-format csv -d <out>/lds -o run -- "
+           "python3 <repo>/bench.py --workload {w} --steps 3 --warmup 1 --no-cpu",
     "copy_fetch": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc FETCH_SIZE --output-format csv "
                   "-d <out>/copy_fetch -o run -- python3 <repo>/bench.py --copy-probe 512",
     "copy_write": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc WRITE_SIZE --output-format csv "
@@ -176,6 +183,59 @@ def _per_dispatch(directory: str, counter: str, name_part: str):
     return vals
 
 
+def _per_dispatch_all(directory: str, name_part: str):
+    """{dispatch id: {counter: value summed over instances, "us": duration}}
+    of the dispatches whose kernel name contains name_part."""
+    out = {}
+    for r in _csv_rows(directory, "counter_collection.csv"):
+        if name_part not in r["Kernel_Name"]:
+            continue
+        d = out.setdefault(r["Dispatch_Id"], {
+            "us": (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3})
+        d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return out
+
+
+def summarize_counters(out: str, workload: int, cfg, src_hash: str, cmds: dict):
+    """profiles/k_gemm_counters_<workload>.txt from the mfma/ and lds/ runs:
+    MFMA utilisation of the GEMM and of stage 1 (rocprofv3's MfmaUtil: MFMA
+    busy cycles over the kernel's GPU-active cycles times the SIMD count),
+    the int8 MFMA operations counted (SQ_INSTS_VALU_MFMA_MOPS_I8 x 512), the
+    clock implied by GRBM_GUI_ACTIVE (summed over the 8 XCDs) and the
+    kernel time, and the LDS bank-conflict share."""
+    for kind in ("mfma", "lds"):
+        h = _bench_hash_in_log(os.path.join(out, f"{kind}.log"))
+        if h != src_hash:
+            raise SystemExit(f"{kind} run was taken on kernel source {h}, tree is {src_hash}")
+    lines = [f"# rocprofv3 counters of the GEMM (k_gemm*) and stage-1 kernels, workload {cfg.name}",
+             f"# command (mfma): {cmds['mfma']}", f"# command (lds): {cmds['lds']}",
+             "# per-dispatch means; gemm_clock_ghz = GRBM_GUI_ACTIVE / 8 XCDs / kernel time; "
+             "lds_conflict_share = SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE",
+             f"kernel_source_sha256_16: {src_hash}"]
+    for label, part in (("gemm", GEMM_KERNEL), ("stage1", "stage1")):
+        m = list(_per_dispatch_all(os.path.join(out, "mfma"), part).values())
+        l = list(_per_dispatch_all(os.path.join(out, "lds"), part).values())
+        if not m or not l:
+            continue
+        mean = lambda rows, k: sum(r.get(k, 0.0) for r in rows) / len(rows)
+        us = mean(m, "us")
+        if label == "gemm":      # GRBM_GUI_ACTIVE also counts time around a dispatch:
+            lines.append(f"gemm_clock_ghz: "   # only meaningful for the long GEMM
+                         f"{mean(m, 'GRBM_GUI_ACTIVE') / 8 / (mean(m, 'us') * 1e3):.3f}")
+        lines += [f"{label}_dispatches: {len(m)}",
+                  f"{label}_kernel_us: {us:.2f}",
+                  f"{label}_mfma_util_percent: {mean(m, 'MfmaUtil'):.2f}",
+                  f"{label}_int8_mfma_ops: {mean(m, 'SQ_INSTS_VALU_MFMA_MOPS_I8') * 512:.6e}",
+                  f"{label}_lds_instructions: {mean(l, 'SQ_INSTS_LDS'):.0f}",
+                  f"{label}_lds_conflict_share: "
+                  f"{mean(l, 'SQ_LDS_BANK_CONFLICT') / max(mean(l, 'SQ_LDS_IDX_ACTIVE'), 1):.4f}",
+                  f"{label}_waves: {mean(l, 'SQ_WAVES'):.0f}"]
+    path = os.path.join(ROOT, "profiles", f"k_gemm_counters_{cfg.name}.txt")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(open(path).read())
+
+
 def _bench_hash_in_log(path: str):
     with open(path) as f:
         for line in f:
@@ -190,12 +250,16 @@ def summarize_profiles(out: str, workload: int):
     from synth.workloads import CONFIGS
     cfg = CONFIGS[workload]
     src_hash = kernel_source_hash()
+    cmds = {k: v.format(w=workload) for k, v in PROFILE_COMMANDS.items()}
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    if os.path.isdir(os.path.join(out, "mfma")) and os.path.isdir(os.path.join(out, "lds")):
+        summarize_counters(out, workload, cfg, src_hash, cmds)
+    if not os.path.isdir(os.path.join(out, "trace")):
+        return
     for kind in ("trace", "fetch", "write"):
         h = _bench_hash_in_log(os.path.join(out, f"{kind}.log"))
         if h != src_hash:
             raise SystemExit(f"{kind} run was taken on kernel source {h}, tree is {src_hash}")
-    cmds = {k: v.format(w=workload) for k, v in PROFILE_COMMANDS.items()}
-    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
 
     stats = _csv_rows(os.path.join(out, "trace"), "kernel_stats.csv")
     with open(_profile_path("trace", cfg.name), "w") as f:
