@@ -60,6 +60,10 @@ def parse():
                     help="write the profiles/ summaries of the rocprofv3 runs under DIR "
                          "(trace/, fetch/, write/, copy_fetch/, copy_write/ and their .log; "
                          "mfma/ and lds/ for the counter summary)")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="only time the calibration's exact steps (channel ranges, MAS factors, "
+                         "Q(S_t W)) on the GPU against the host implementation, on the "
+                         "workload's first projection")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (5 times): the "
                          "reference for scaling HBM traffic counters")
@@ -78,6 +82,49 @@ def copy_probe(mib: int):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "launches": 5}))
+
+
+def calibration_timing(workload: int, reps: int = 20):
+    """GPU (masq_channel_range, masq_smoothing_factors, masq_quantize_weight)
+    against the host calibration (calibrate.smoothing_factors and
+    quantize_shared_weight) on one projection's X and float weight."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2603_04800_amd import calibrate, ops
+    cfg = synth.CONFIGS[workload]
+    p = cfg.projections[0]
+    li = synth.make_layer_inputs(cfg, 0, projections=[p.name])
+    x, w = np.asarray(li.x[p.input_key], np.float32), np.asarray(li.w[p.name], np.float32)
+    dev = torch.device("cuda:0")
+    xt = torch.from_numpy(x).to(dev, torch.bfloat16 if cfg.act_dtype == "bf16" else torch.float32)
+    mt = torch.from_numpy(np.asarray(li.modality, np.int32)).to(dev)
+    wt = torch.from_numpy(np.ascontiguousarray(w)).to(dev)
+
+    def gpu():
+        r = ops.channel_range(xt, mt, cfg.n_mod)
+        s, _ = ops.smoothing_factors(r, wt)
+        return ops.quantize_weight(wt, s[0].contiguous())
+
+    for _ in range(3):
+        gpu()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        gpu()
+    e1.record()
+    torch.cuda.synchronize()
+    gpu_ms = e0.elapsed_time(e1) / reps
+    t0 = time.perf_counter()
+    s32, _ = calibrate.smoothing_factors(x, li.modality, w, cfg.n_mod)
+    calibrate.quantize_shared_weight(w, s32[0])
+    host_ms = (time.perf_counter() - t0) * 1e3
+    print(json.dumps({"metric": "calibration: channel ranges, MAS factors, Q(S_t W)",
+                      "workload": cfg.name, "c_in": int(w.shape[0]), "c_out": int(w.shape[1]),
+                      "tokens": int(x.shape[0]), "gpu_ms": round(gpu_ms, 4),
+                      "host_ms": round(host_ms, 1), "host_threads": torch.get_num_threads()}))
 
 
 def kernel_source_hash() -> str:
@@ -364,6 +411,9 @@ def main():
     args = parse()
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.calibrate:
+        calibration_timing(args.workload)
         return
     if args.summarize_profiles:
         summarize_profiles(args.summarize_profiles, args.workload)

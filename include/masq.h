@@ -186,6 +186,47 @@ masq_status masq_linear_stage2_w4a8(const void* x, masq_dtype x_dt, const int32_
                                     int32_t rank, int32_t n_mod, void* y, masq_dtype y_dt,
                                     void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Calibration on the GPU: the exact part of the offline calibration that
+ * gives the smoothing factors and the shared weight (the compensation
+ * factors L1, L2 need a whitening and a truncated SVD and are not here).
+ * Each result is bit-exact against its definition: maxima are exact, the
+ * factor and the weight step are computed in fp64 and rounded once to fp32.
+ *
+ * masq_channel_range: range[m][i] = max |x_ti| over the tokens t of modality
+ * m (Sec. 4.1, R^m); 0 where a modality has no tokens.  x [T][c_in] f32 or
+ * bf16; modality [T]; tokens whose id is outside [0, n_mod) belong to no
+ * modality.  range: [n_mod][c_in] f32, fully overwritten.  T == 0 gives
+ * zeros.
+ *
+ * masq_smoothing_factors: the MAS initial factors (Sec. 4.2, alpha = 1/2),
+ * smooth[m][i] = fl32(sqrt(max(range[m][i], 1e-5) / max(w_i, 1e-5))) with
+ * w_i = max_j |w[i][j]| in fp64, and inv_smooth[m][i] = fl32(1 / smooth[m][i])
+ * (correctly rounded).  w is the float weight in the paper's layout
+ * [c_in][c_out] f32; smooth, inv_smooth: [n_mod][c_in] f32.
+ *
+ * masq_quantize_weight: the shared weight Q(S_t W) (Sec. 4.3; eq. PTQ per
+ * output channel, symmetric, z = 0): with v_io = smooth_text[i] * w[i][o]
+ * (exact in fp64), w_scale[o] = fl32(d_o), d_o = max_i |v_io| / qmax, and
+ * wq[o][i] = clamp(rint(v_io / d_o), -qmax, qmax) (fp64, round half to
+ * even; 0 when d_o = 0).  bits = 8 (qmax 127) or 4 (qmax 7, the W4A8
+ * setting; codes are returned one per byte, unpacked).  wq: [c_out][c_in]
+ * int8; w_scale: [c_out] f32.
+ *
+ * Preconditions as for the layer calls (c_in, c_out multiples of 16,
+ * 1 <= n_mod <= 4, 16-byte aligned pointers); violations return an error
+ * before anything is enqueued.
+ */
+masq_status masq_channel_range(const void* x, masq_dtype x_dt, const int32_t* modality,
+                               int64_t T, int64_t c_in, int32_t n_mod, float* range,
+                               void* stream);
+masq_status masq_smoothing_factors(const float* range, const float* w, int64_t c_in,
+                                   int64_t c_out, int32_t n_mod, float* smooth,
+                                   float* inv_smooth, void* stream);
+masq_status masq_quantize_weight(const float* w, const float* smooth_text, int64_t c_in,
+                                 int64_t c_out, int32_t bits, int8_t* wq, float* w_scale,
+                                 void* stream);
+
 #ifdef __cplusplus
 }
 #endif

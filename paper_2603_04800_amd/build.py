@@ -20,7 +20,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "libmasq.so")
-SOURCES = ("masq_kernels.hip", "masq_api.hip")
+SOURCES = ("masq_kernels.hip", "masq_api.hip", "masq_calib.hip")
 
 
 def hipcc() -> str:

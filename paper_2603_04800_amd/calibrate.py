@@ -167,6 +167,40 @@ def calibrate_layer(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: i
     w = np.asarray(w, np.float32)
     s32, inv = smoothing_factors(x, modality, w, n_mod)
     wq, w_scale = quantize_shared_weight(w, s32[0], weight_bits)
+    return _with_cmc_factors(x, modality, w, s32, inv, wq, w_scale, n_mod, rank, lr_dtype,
+                             ridge, seed, weight_bits)
+
+
+def calibrate_layer_gpu(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: int,
+                        rank: int, lr_dtype: str = "bf16", ridge: float = 1e-6,
+                        seed: int = 0, weight_bits: int = 8, device: str = "cuda:0") -> dict:
+    """calibrate_layer with its exact steps on the GPU: the channel ranges,
+    the MAS factors and Q(S_t W) (masq_channel_range, masq_smoothing_factors,
+    masq_quantize_weight).  The compensation factors (whitening and the
+    truncated SVD) are then formed on the host as in calibrate_layer, so the
+    result is the same, array for array."""
+    import torch
+
+    from . import ops
+    x = np.asarray(x, np.float32)
+    modality = np.asarray(modality, np.int32)
+    w = np.asarray(w, np.float32)
+    xt = torch.from_numpy(x).to(device)
+    mt = torch.from_numpy(modality).to(device)
+    wt = torch.from_numpy(np.ascontiguousarray(w)).to(device)
+    rng = ops.channel_range(xt, mt, n_mod)
+    s_t, inv_t = ops.smoothing_factors(rng, wt)
+    wq_t, ws_t = ops.quantize_weight(wt, s_t[0].contiguous(), bits=weight_bits)
+    s32, inv = s_t.cpu().numpy(), inv_t.cpu().numpy()
+    wq, w_scale = wq_t.cpu().numpy(), ws_t.cpu().numpy()
+    return _with_cmc_factors(x, modality, w, s32, inv, wq, w_scale, n_mod, rank, lr_dtype,
+                             ridge, seed, weight_bits)
+
+
+def _with_cmc_factors(x, modality, w, s32, inv, wq, w_scale, n_mod, rank, lr_dtype, ridge,
+                      seed, weight_bits) -> dict:
+    """The compensation factors of every non-text modality against the shared
+    weight (wq, w_scale), and the artifact dict."""
     k, n = w.shape
     l_down = np.zeros((max(n_mod - 1, 0), rank, k), np.float32)
     r_up = np.zeros((max(n_mod - 1, 0), n, rank), np.float32)

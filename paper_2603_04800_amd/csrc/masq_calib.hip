@@ -1,0 +1,215 @@
+// Calibration on the GPU: the exact, non-iterative part of the offline
+// calibration that produces the layer's smoothing factors and shared weight.
+//
+//   R^m_i   = max over the tokens of modality m of |x_ti|         (Sec. 4.1)
+//   s^m_i   = sqrt(max(R^m_i, 1e-5) / max(w_i, 1e-5)),            (Sec. 4.2,
+//             w_i = max_j |w_ij| over the output channels           alpha = 1/2)
+//   Q(S_t W): per output channel o, step d_o = max_i |s^t_i w_io| / qmax and
+//             codes rint((s^t_i w_io) / d_o) clamped to [-qmax, qmax]  (eq. PTQ)
+//
+// Every quantity that decides a value is computed in the same precision as
+// the definition's host implementation (fp64 for the factor and the weight
+// step, one rounding to fp32 at the end), so the results are bit-exact.
+// The C ABI of these calls is declared in masq.h.
+
+#include <hip/hip_runtime.h>
+
+#include "masq.h"
+
+namespace {
+
+using bf16_t = unsigned short;
+
+__device__ __forceinline__ float load_abs(const float* p) { return fabsf(*p); }
+__device__ __forceinline__ float load_abs(const bf16_t* p) {
+    return fabsf(__uint_as_float(static_cast<uint32_t>(*p) << 16));
+}
+
+// range [n_mod][K] := 0 (the maxima below are taken with integer atomics on
+// the bits of non-negative floats, which order like the values).
+__global__ __launch_bounds__(256) void k_zero_f32(float* __restrict__ p, int64_t n) {
+    for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n; i += gridDim.x * 256ll) p[i] = 0.f;
+}
+
+// grid (ceil(K / 256), row chunks): thread = column i, rows of its chunk;
+// per-modality maxima in registers, then one atomic max per modality.
+// Tokens whose id is outside [0, n_mod) belong to no modality.
+template <typename XT>
+__global__ __launch_bounds__(256) void k_channel_range(const XT* __restrict__ x,
+                                                       const int32_t* __restrict__ mod,
+                                                       int64_t T, int K, int n_mod,
+                                                       int rows_per_chunk,
+                                                       float* __restrict__ range) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= K) return;
+    const int64_t t0 = static_cast<int64_t>(blockIdx.y) * rows_per_chunk;
+    const int64_t t1 = t0 + rows_per_chunk < T ? t0 + rows_per_chunk : T;
+    float m[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int64_t t = t0; t < t1; ++t) {
+        const int mm = mod[t];                                 // uniform across the block
+        const float a = load_abs(x + t * K + i);
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (mm == k) m[k] = fmaxf(m[k], a);
+    }
+    for (int k = 0; k < n_mod; ++k)
+        if (m[k] > 0.f)
+            atomicMax(reinterpret_cast<int*>(range + static_cast<int64_t>(k) * K + i),
+                      __float_as_int(m[k]));
+}
+
+// One wave per input channel i: w_i = max_j |w_ij| over its row of W
+// [K][N], then s^m_i = fl32(sqrt(max(R, 1e-5) / max(w_i, 1e-5))) in fp64 for
+// every modality and inv = fl32(1 / s) (correctly rounded).
+__global__ __launch_bounds__(256) void k_smoothing_factors(const float* __restrict__ range,
+                                                           const float* __restrict__ w, int K,
+                                                           int N, int n_mod,
+                                                           float* __restrict__ s,
+                                                           float* __restrict__ inv_s) {
+    const int lane = threadIdx.x & 63;
+    const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (i >= K) return;
+    const float* row = w + static_cast<int64_t>(i) * N;
+    float a = 0.f;
+    for (int j = lane; j < N; j += 64) a = fmaxf(a, fabsf(row[j]));
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) a = fmaxf(a, __shfl_xor(a, o));
+    if (lane < n_mod) {
+        const double r = static_cast<double>(range[static_cast<int64_t>(lane) * K + i]);
+        const double v = sqrt(fmax(r, 1e-5) / fmax(static_cast<double>(a), 1e-5));
+        const float s32 = static_cast<float>(v);
+        s[static_cast<int64_t>(lane) * K + i] = s32;
+        inv_s[static_cast<int64_t>(lane) * K + i] = 1.0f / s32;
+    }
+}
+
+// Q(S_t W) for 64 output channels per workgroup (W [K][N] fp32, paper layout;
+// codes written as wq [N][K]).  Pass 1: step d_o = max_i |s_i w_io| / qmax in
+// fp64 (s_i w_io is exact in fp64).  Pass 2: 64 x 64 blocks of codes
+// rint(s_i w_io / d_o) (fp64 division, round half to even), transposed
+// through LDS so both the reads (along o) and the writes (along i) are
+// contiguous.
+__global__ __launch_bounds__(256) void k_quantize_weight(const float* __restrict__ w,
+                                                         const float* __restrict__ s_text,
+                                                         int K, int N, int qmax,
+                                                         int8_t* __restrict__ wq,
+                                                         float* __restrict__ w_scale) {
+    __shared__ double smax[4][64];
+    __shared__ double sdelta[64];
+    __shared__ int8_t tile[64][65];
+    const int tid = threadIdx.x, ol = tid & 63, part = tid >> 6;
+    const int o0 = blockIdx.x * 64;
+    const int o = o0 + ol;
+    double a = 0.0;
+    if (o < N)
+        for (int i = part; i < K; i += 4)
+            a = fmax(a, fabs(static_cast<double>(s_text[i]) * static_cast<double>(w[static_cast<int64_t>(i) * N + o])));
+    smax[part][ol] = a;
+    __syncthreads();
+    if (tid < 64) {
+        const double m = fmax(fmax(smax[0][tid], smax[1][tid]), fmax(smax[2][tid], smax[3][tid]));
+        const double d = m / qmax;
+        sdelta[tid] = d;
+        if (o0 + tid < N) w_scale[o0 + tid] = static_cast<float>(d);
+    }
+    __syncthreads();
+    const double d = sdelta[ol];
+    for (int i0 = 0; i0 < K; i0 += 64) {
+        // read: thread (ol, part) takes rows i0 + part + 4 k of channel o
+        for (int k = 0; k < 16; ++k) {
+            const int il = part + 4 * k, i = i0 + il;
+            int c = 0;
+            if (o < N && i < K && d > 0.0) {
+                const double v = static_cast<double>(s_text[i]) * static_cast<double>(w[static_cast<int64_t>(i) * N + o]);
+                const double r = rint(v / d);
+                c = static_cast<int>(fmin(fmax(r, static_cast<double>(-qmax)), static_cast<double>(qmax)));
+            }
+            tile[ol][il] = static_cast<int8_t>(c);
+        }
+        __syncthreads();
+        // write: thread (ol', part) writes 16 consecutive codes of channel o0 + ol' ... as
+        // row (tid / 4) of the block, 16 bytes at 16 (tid % 4)
+        {
+            const int orow = tid >> 2, seg = (tid & 3) * 16;
+            const int oo = o0 + orow;
+            if (oo < N) {
+                int8_t* dst = wq + static_cast<int64_t>(oo) * K + i0 + seg;
+                for (int e = 0; e < 16; ++e)
+                    if (i0 + seg + e < K) dst[e] = tile[orow][seg + e];
+            }
+        }
+        __syncthreads();
+    }
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+masq_status masq_channel_range(const void* x, masq_dtype x_dt, const int32_t* modality,
+                               int64_t T, int64_t c_in, int32_t n_mod, float* range,
+                               void* stream) {
+    if (x_dt != MASQ_F32 && x_dt != MASQ_BF16) return MASQ_ERR_DTYPE;
+    if (T < 0 || c_in <= 0 || c_in % 16 != 0 || c_in > (1LL << 30) || n_mod < 1 || n_mod > 4)
+        return MASQ_ERR_SHAPE;
+    if (!range || (T > 0 && (!x || !modality))) return MASQ_ERR_NULL;
+    if (!aligned16(range) || (T > 0 && (!aligned16(x) || !aligned16(modality))))
+        return MASQ_ERR_ALIGN;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    const int64_t n = static_cast<int64_t>(n_mod) * c_in;
+    hipLaunchKernelGGL(k_zero_f32, dim3(static_cast<unsigned>((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024)),
+                       dim3(256), 0, s, range, n);
+    if (T > 0) {
+        const int K = static_cast<int>(c_in);
+        const int64_t col_blocks = (K + 255) / 256;
+        int64_t chunks = (2048 + col_blocks - 1) / col_blocks;          // about 2048 workgroups
+        if (chunks > T) chunks = T;
+        const int rows = static_cast<int>((T + chunks - 1) / chunks);
+        chunks = (T + rows - 1) / rows;
+        const dim3 grid(static_cast<unsigned>(col_blocks), static_cast<unsigned>(chunks));
+        if (x_dt == MASQ_BF16)
+            hipLaunchKernelGGL(k_channel_range<bf16_t>, grid, dim3(256), 0, s,
+                               static_cast<const bf16_t*>(x), modality, T, K, n_mod, rows, range);
+        else
+            hipLaunchKernelGGL(k_channel_range<float>, grid, dim3(256), 0, s,
+                               static_cast<const float*>(x), modality, T, K, n_mod, rows, range);
+    }
+    return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
+}
+
+masq_status masq_smoothing_factors(const float* range, const float* w, int64_t c_in,
+                                   int64_t c_out, int32_t n_mod, float* smooth,
+                                   float* inv_smooth, void* stream) {
+    if (c_in <= 0 || c_in % 16 != 0 || c_out <= 0 || c_out % 16 != 0 || c_in > (1LL << 30) ||
+        c_out > (1LL << 30) || n_mod < 1 || n_mod > 4)
+        return MASQ_ERR_SHAPE;
+    if (!range || !w || !smooth || !inv_smooth) return MASQ_ERR_NULL;
+    if (!aligned16(range) || !aligned16(w) || !aligned16(smooth) || !aligned16(inv_smooth))
+        return MASQ_ERR_ALIGN;
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(k_smoothing_factors, dim3(static_cast<unsigned>((c_in + 3) / 4)), dim3(256),
+                       0, static_cast<hipStream_t>(stream), range, w, static_cast<int>(c_in),
+                       static_cast<int>(c_out), n_mod, smooth, inv_smooth);
+    return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
+}
+
+masq_status masq_quantize_weight(const float* w, const float* smooth_text, int64_t c_in,
+                                 int64_t c_out, int32_t bits, int8_t* wq, float* w_scale,
+                                 void* stream) {
+    if (c_in <= 0 || c_in % 16 != 0 || c_out <= 0 || c_out % 16 != 0 || c_in > (1LL << 30) ||
+        c_out > (1LL << 30) || (bits != 8 && bits != 4))
+        return MASQ_ERR_SHAPE;
+    if (!w || !smooth_text || !wq || !w_scale) return MASQ_ERR_NULL;
+    if (!aligned16(w) || !aligned16(smooth_text) || !aligned16(wq) || !aligned16(w_scale))
+        return MASQ_ERR_ALIGN;
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(k_quantize_weight, dim3(static_cast<unsigned>((c_out + 63) / 64)), dim3(256),
+                       0, static_cast<hipStream_t>(stream), w, smooth_text, static_cast<int>(c_in),
+                       static_cast<int>(c_out), (1 << (bits - 1)) - 1, wq, w_scale);
+    return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
+}
+
+}  // extern "C"

@@ -45,6 +45,9 @@ _SIGS = {
     "masq_linear_fused_w4a8": (_FUSED_ARGS, ctypes.c_int),
     "masq_linear_stage1_w4a8": (_FUSED_ARGS, ctypes.c_int),
     "masq_linear_stage2_w4a8": (_FUSED_ARGS, ctypes.c_int),
+    "masq_channel_range": ([_p, _i32, _p, _i64, _i64, _i32, _p, _p], ctypes.c_int),
+    "masq_smoothing_factors": ([_p, _p, _i64, _i64, _i32, _p, _p, _p], ctypes.c_int),
+    "masq_quantize_weight": ([_p, _p, _i64, _i64, _i32, _p, _p, _p], ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -157,6 +160,41 @@ def lowrank_comp(x, modality, inv_smooth, l_down, r_up, y, stream=None):
         _ptr(x), _dt(x), _ptr(modality), _ptr(inv_smooth), _ptr(l_down), _ptr(r_up), lr_dt,
         T, K, N, rank, n_mod, _ptr(y), _dt(y), _stream(stream)))
     return y
+
+
+def channel_range(x, modality, n_mod, stream=None):
+    """Per-modality channel ranges R^m [n_mod][K] f32 (calibration, Sec. 4.1)."""
+    T, K = x.shape
+    _need(modality, torch.int32, "modality")
+    out = torch.empty((n_mod, K), dtype=torch.float32, device=x.device)
+    _check("masq_channel_range", _lib.masq_channel_range(
+        _ptr(x), _dt(x), _ptr(modality), T, K, n_mod, _ptr(out), _stream(stream)))
+    return out
+
+
+def smoothing_factors(range_, w, stream=None):
+    """MAS factors from the ranges and the float weight W [K][N] (paper layout):
+    (s [n_mod][K], inv_s [n_mod][K]) f32 (Sec. 4.2)."""
+    n_mod, K = range_.shape
+    _need(range_, torch.float32, "range")
+    _need(w, torch.float32, "w")
+    s = torch.empty_like(range_)
+    inv = torch.empty_like(range_)
+    _check("masq_smoothing_factors", _lib.masq_smoothing_factors(
+        _ptr(range_), _ptr(w), K, w.shape[1], n_mod, _ptr(s), _ptr(inv), _stream(stream)))
+    return s, inv
+
+
+def quantize_weight(w, smooth_text, bits=8, stream=None):
+    """Q(S_t W) per output channel: (codes int8 [N][K], steps f32 [N]) (Sec. 4.3)."""
+    K, N = w.shape
+    _need(w, torch.float32, "w")
+    _need(smooth_text, torch.float32, "smooth_text")
+    wq = torch.empty((N, K), dtype=torch.int8, device=w.device)
+    scale = torch.empty((N,), dtype=torch.float32, device=w.device)
+    _check("masq_quantize_weight", _lib.masq_quantize_weight(
+        _ptr(w), _ptr(smooth_text), K, N, bits, _ptr(wq), _ptr(scale), _stream(stream)))
+    return wq, scale
 
 
 def workspace_bytes(T, K, N, rank, n_mod) -> int:

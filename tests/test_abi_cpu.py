@@ -163,3 +163,22 @@ def test_w4_linear_refuses_mismatched_packed_width():
     from paper_2603_04800_amd import ops
     with pytest.raises(ValueError):
         ops.Linear(torch.ones(2, 128), torch.zeros(16, 128, dtype=torch.uint8), torch.ones(16))
+
+
+def test_calibration_calls_validate(lib):
+    """The GPU calibration entry points check sizes, dtypes, pointers and
+    alignment before enqueueing anything."""
+    P = 1 << 20
+    cr, sf, qw = lib.masq_channel_range, lib.masq_smoothing_factors, lib.masq_quantize_weight
+    assert cr(P, 2, P, 8, 64, 2, P, None) == 3              # unknown activation dtype
+    assert cr(P, 1, P, 8, 40, 2, P, None) == 2              # c_in % 16 != 0
+    assert cr(P, 1, P, 8, 64, 5, P, None) == 2              # n_mod > 4
+    assert cr(P, 1, P, -1, 64, 2, P, None) == 2             # T < 0
+    assert cr(P, 1, None, 8, 64, 2, P, None) == 1           # no modality ids
+    assert cr(P, 1, P, 8, 64, 2, P + 8, None) == 4          # misaligned output
+    assert sf(P, P, 64, 40, 2, P, P, None) == 2             # c_out % 16 != 0
+    assert sf(P, None, 64, 64, 2, P, P, None) == 1          # no weight
+    assert sf(P, P, 64, 64, 0, P, P, None) == 2             # n_mod < 1
+    assert qw(P, P, 64, 64, 6, P, P, None) == 2             # bits must be 8 or 4
+    assert qw(P, P, 48, 64, 8, P + 4, P, None) == 4         # misaligned codes
+    assert qw(P, P, 64, 64, 8, P, None, None) == 1          # no step output
