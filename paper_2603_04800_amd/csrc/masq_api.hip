@@ -82,8 +82,7 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
     }
     w.dw_slices = w.dw_kslice = 0;
     w.dw_part = nullptr;
-    if (rank > 0 && rank <= 64 && n_mod > 1 && !small_path(T, K) && T >= kDownWideMinT &&
-        K >= kDownWideMinK) {
+    if (rank > 0 && rank <= 64 && n_mod > 1 && !small_path(T, K) && down_wide(T, K)) {
         plan_down_wide(T, K, w.dw_slices, w.dw_kslice);
         w.dw_part = reinterpret_cast<float*>(carve(static_cast<size_t>(w.dw_slices) * T *
                                                    static_cast<size_t>(rank) * sizeof(float)));

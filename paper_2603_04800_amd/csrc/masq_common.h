@@ -24,14 +24,22 @@ constexpr int kUBatch = 16;        // slice partials of u a thread keeps in flig
 // down-projection's k-slice partials itself.
 inline bool small_path(int64_t T, int64_t K) { return T <= kSmallMaxT && K % 64 == 0; }
 
-// Stage 1 of large batches with long rows, bf16 factors, rank <= 64
-// (fused_stage1_ok): the down-projection runs over 128-row tiles and S k
+// Stage 1 of large batches with bf16 factors, rank <= 64 (fused_stage1_ok),
+// in its wide form: the down-projection runs over 128-row tiles and S k
 // slices of kslice columns (about 512 workgroups, slices of at least 256
 // columns); the quantisation kernel then adds the slices' partials into u.
-// (Shorter rows keep the fused stage 1, which reads each row once.)
-constexpr int64_t kDownWideMinT = 1024;
-constexpr int64_t kDownWideMinK = 8192;
+// The fused stage 1 walks each 16-row tile along its whole row, so its time
+// grows with K and hardly with T until its T / 16 workgroups reach one per
+// compute unit (4096 tokens); it keeps rows shorter than 2048 columns (too
+// few k slices for the wide form) and, from 4096 tokens on, rows shorter
+// than 8192 columns (where reading each row once, not twice, wins).
+constexpr int64_t kDownWideMinK = 2048;
+constexpr int64_t kFusedFullT = 4096;
+constexpr int64_t kDownWideLongK = 8192;
 constexpr int kDownWideRows = 128;
+inline bool down_wide(int64_t T, int64_t K) {
+    return K >= kDownWideMinK && (T < kFusedFullT || K >= kDownWideLongK);
+}
 inline void plan_down_wide(int64_t T, int64_t K, int& S, int& kslice) {
     const int64_t tiles = (T + kDownWideRows - 1) / kDownWideRows;
     int64_t want = (512 + tiles - 1) / tiles;

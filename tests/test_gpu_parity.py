@@ -270,8 +270,18 @@ _EDGE = {
     "splitk_fp32_ragged": dict(T=260, K=1600, N=272, r=16, M=2, act="f32", lr="f32"),
     # the compensation operands loaded as extra stages of the K ring: the
     # shortest ring (four 64-byte stages), ranks below 64, mixed tiles
-    # wide down-projection (at least 1024 tokens, rows of 8192 and more):
-    # ragged last k slice, ranks below 64, fp32 activations
+    # wide down-projection (rows of 2048 columns and more below 4096 tokens,
+    # of 8192 and more at any batch): ragged last k slice, ranks below 64,
+    # fp32 activations, the smallest batch above the decode path, and the
+    # batches either side of the 4096-token switch to the fused stage 1
+    "down_wide_t17_k2048": dict(T=17, K=2048, N=32, r=64, M=3, act="bf16", lr="bf16",
+                                layout="alternating"),
+    "down_wide_t600_k2112_f32": dict(T=600, K=2112, N=48, r=16, M=2, act="f32", lr="bf16"),
+    "down_wide_t4095_k2048": dict(T=4095, K=2048, N=16, r=64, M=3, act="bf16", lr="bf16",
+                                  layout="runs"),
+    "stage1_fused_t4096_k2048": dict(T=4096, K=2048, N=16, r=64, M=3, act="bf16", lr="bf16",
+                                     layout="runs"),
+    "stage1_fused_t300_k1984": dict(T=300, K=1984, N=48, r=32, M=2, act="bf16", lr="bf16"),
     "down_wide_t1100_k8208_r32": dict(T=1100, K=8208, N=32, r=32, M=3, act="bf16", lr="bf16",
                                       layout="runs"),
     "down_wide_f32_t1030_k8192_r48": dict(T=1030, K=8192, N=16, r=48, M=2, act="f32",
