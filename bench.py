@@ -124,7 +124,54 @@ def calibration_timing(workload: int, reps: int = 20):
     print(json.dumps({"metric": "calibration: channel ranges, MAS factors, Q(S_t W)",
                       "workload": cfg.name, "c_in": int(w.shape[0]), "c_out": int(w.shape[1]),
                       "tokens": int(x.shape[0]), "gpu_ms": round(gpu_ms, 4),
-                      "host_ms": round(host_ms, 1), "host_threads": torch.get_num_threads()}))
+                      "host_ms": round(host_ms, 1), "host_threads": torch.get_num_threads()}),
+          flush=True)
+    if cfg.n_mod < 2 or cfg.rank == 0:
+        return
+    # the compensation factors of the first non-text modality (Sec. 4.3):
+    # the GPU path (smoothed rows, dW and every large product on the GPU,
+    # the small decompositions on the host) against the host calibration
+    m = 1
+    wq_h, ws_h = calibrate.quantize_shared_weight(w, s32[0])
+    r = ops.channel_range(xt, mt, cfg.n_mod)
+    s_t, _ = ops.smoothing_factors(r, wt)
+    wq_t, ws_t = ops.quantize_weight(wt, s_t[0].contiguous())
+    sm = s_t[m].contiguous()
+    rows = torch.from_numpy(np.flatnonzero(li.modality == m).astype(np.int32)).to(dev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    z = ops.gather_smoothed(xt, rows, sm)
+    dw = ops.weight_difference(wt, sm, wq_t, ws_t)
+    l1, l2 = calibrate.cmc_factors_gpu(z, dw, cfg.rank, seed=m)
+    gpu_cmc_s = time.perf_counter() - t0
+    # the Gram product alone (the whitening's largest GEMM), timed with events
+    thin = z.shape[0] < z.shape[1]
+    gram = (lambda: ops.dgemm(z, z.T)) if thin else (lambda: ops.dgemm(z.T, z))
+    gram()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(5):
+        gram()
+    e1.record()
+    torch.cuda.synchronize()
+    gram_ms = e0.elapsed_time(e1) / 5
+    n_r, k_c = z.shape
+    gram_flops = 2.0 * (n_r * n_r * k_c if thin else k_c * k_c * n_r)
+    del z, dw
+    t0 = time.perf_counter()
+    zh = x[li.modality == m].astype(np.float64) / s32[m].astype(np.float64)[None, :]
+    dwh = calibrate._weight_difference(w, s32[m], wq_h, ws_h)
+    h1, h2 = calibrate.cmc_factors(zh, dwh, cfg.rank, seed=m)
+    host_cmc_s = time.perf_counter() - t0
+    rel = float(np.linalg.norm(l1 @ l2 - h1 @ h2) / max(np.linalg.norm(h1 @ h2), 1e-300))
+    print(json.dumps({"metric": "calibration: compensation factors of one modality",
+                      "workload": cfg.name, "modality": m, "rows": int(n_r),
+                      "c_in": int(w.shape[0]), "c_out": int(w.shape[1]), "rank": cfg.rank,
+                      "gram": "Z Z^T" if thin else "Z^T Z", "gram_ms": round(gram_ms, 3),
+                      "gram_tflops": round(gram_flops / gram_ms / 1e9, 2),
+                      "gram_frac_fp64_peak": round(gram_flops / gram_ms / 1e9 / 78.6, 4),
+                      "gpu_s": round(gpu_cmc_s, 2), "host_s": round(host_cmc_s, 2),
+                      "l1l2_relative_difference": rel}), flush=True)
 
 
 def kernel_source_hash() -> str:

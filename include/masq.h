@@ -227,6 +227,46 @@ masq_status masq_quantize_weight(const float* w, const float* smooth_text, int64
                                  int64_t c_out, int32_t bits, int8_t* wq, float* w_scale,
                                  void* stream);
 
+/* Inputs and products of the compensation factors' calibration (Sec. 3.2
+ * and 4.3; eq. l1l2): L1^m, L2^m minimise ||Z_m (dW_m - L1 L2)||_F over the
+ * smoothed calibration rows Z_m = X_m S_m^-1 of modality m, with the weight
+ * difference dW_m = S_m W - Q(S_t W).  The whitening of Z_m (from its Gram
+ * matrix) and the truncated SVD are built from these calls; their small
+ * eigen-, QR and SVD decompositions stay with the caller.
+ *
+ * masq_gather_smoothed: z[i][c] = x[rows[i]][c] / smooth[c] in fp64 (the
+ * operands are exact, the division correctly rounded), for i < n_rows; a
+ * row index outside [0, T) gives a zero row.  x: [T][c_in] f32 or bf16;
+ * rows: [n_rows] int32; smooth: [c_in] f32 (S_m's diagonal); z: [n_rows]
+ * [c_in] f64, caller-allocated.  n_rows = 0 is a no-op.
+ *
+ * masq_weight_difference: dw[i][o] = smooth[i] * w[i][o] - wq[o][i] *
+ * w_scale[o] in fp64 (both products are exact, so the subtraction is the
+ * only rounding).  w: [c_in][c_out] f32 (paper layout); smooth: [c_in] f32
+ * (S_m); wq: [c_out][c_in] int8 codes of Q(S_t W) (8- or 4-bit, one code a
+ * byte) with steps w_scale [c_out] f32; dw: [c_in][c_out] f64.
+ *
+ * masq_dgemm: c[i * ldc + j] = sum_k A(i, k) B(k, j) (+ beta * c[i * ldc +
+ * j] when beta != 0) for i < m, j < n, in fp64, with A(i, k) = a[i *
+ * a_row_stride + k * a_col_stride] and B(k, j) = b[k * b_row_stride + j *
+ * b_col_stride] (element strides, so a transposed operand is a stride swap).
+ * Each sum runs in increasing k with fused multiply-adds; beta * c is added
+ * after it.  c must not overlap a or b.  k = 0 gives beta * c (or zeros);
+ * m = 0 or n = 0 is a no-op.  Pointers 8-byte aligned; m <= 65535 * 128.
+ *
+ * Preconditions as for the calls above; violations return an error before
+ * anything is enqueued.
+ */
+masq_status masq_gather_smoothed(const void* x, masq_dtype x_dt, int64_t T, int64_t c_in,
+                                 const int32_t* rows, int64_t n_rows, const float* smooth,
+                                 double* z, void* stream);
+masq_status masq_weight_difference(const float* w, const float* smooth, const int8_t* wq,
+                                   const float* w_scale, int64_t c_in, int64_t c_out,
+                                   double* dw, void* stream);
+masq_status masq_dgemm(int64_t m, int64_t n, int64_t k, const double* a, int64_t a_row_stride,
+                       int64_t a_col_stride, const double* b, int64_t b_row_stride,
+                       int64_t b_col_stride, double beta, double* c, int64_t ldc, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

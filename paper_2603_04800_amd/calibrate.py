@@ -155,6 +155,108 @@ def cmc_factors(z: np.ndarray, dw: np.ndarray, rank: int, ridge: float = 1e-6, s
     return l1, l2
 
 
+class _WhiteningGPU:
+    """_Whitening with its large products on the GPU (masq_dgemm): the Gram
+    matrix of Z (Z^T Z, or Z Z^T when Z has fewer rows than columns), the
+    thin basis P = Z^T U_z Sigma^-1, and every application of T or T^-1.
+    The eigen-decomposition of the Gram matrix and the diagonal scaling of
+    the small intermediate P^T A stay on the host, in the same order of
+    operations as _Whitening."""
+
+    def __init__(self, z, ridge: float):
+        import torch
+
+        from . import ops
+        self.ops, self.torch, self.dev = ops, torch, z.device
+        n, k = z.shape
+        if n >= k:
+            c = ops.dgemm(z.T, z).cpu().numpy()
+            eps = ridge * np.trace(c) / k
+            lam, p = np.linalg.eigh(c + eps * np.eye(k))
+            lam = np.maximum(lam, 0.0)
+            self.p = torch.from_numpy(np.ascontiguousarray(p)).to(self.dev)
+            self.sq = np.sqrt(lam)
+            self.isq = np.where(lam > 0, 1.0 / np.sqrt(np.where(lam > 0, lam, 1.0)), 0.0)
+            self.add = self.add_inv = 0.0
+        else:
+            mu, uz = np.linalg.eigh(ops.dgemm(z, z.T).cpu().numpy())
+            keep = mu > mu.max() * 1e-13 if mu.size and mu.max() > 0 else np.zeros(mu.shape, bool)
+            mu, uz = mu[keep], uz[:, keep]
+            sig = np.sqrt(mu)
+            eps = ridge * np.sum(mu) / k
+            self.p = ops.dgemm(z.T, torch.from_numpy(np.ascontiguousarray(uz / sig[None, :]))
+                               .to(self.dev))                 # [K][n] orthonormal columns
+            self.add = np.sqrt(eps)
+            self.sq = np.sqrt(sig ** 2 + eps) - self.add
+            with np.errstate(divide="ignore"):
+                base = 1.0 / self.add if eps > 0 else 0.0
+                self.isq = np.where(sig ** 2 + eps > 0, 1.0 / np.sqrt(sig ** 2 + eps), 0.0) - base
+            self.add_inv = base
+
+    def _apply(self, a, d: np.ndarray, add: float):
+        t = self.ops.dgemm(self.p.T, a).cpu().numpy()
+        t = self.torch.from_numpy(np.ascontiguousarray(d[:, None] * t)).to(self.dev)
+        if add == 0.0:
+            return self.ops.dgemm(self.p, t)
+        return self.ops.dgemm(self.p, t, c=a.contiguous().clone(), beta=add)
+
+    def apply(self, a):                                    # T @ a, a [K][c] on the device
+        return self._apply(a, self.sq, self.add)
+
+    def apply_inv(self, a):                                # T^-1 @ a
+        return self._apply(a, self.isq, self.add_inv)
+
+
+def _qr_q(a):
+    """Q of the reduced QR factorisation of a device matrix (on the host)."""
+    import torch
+    q, _ = np.linalg.qr(a.cpu().numpy())
+    return torch.from_numpy(np.ascontiguousarray(q)).to(a.device)
+
+
+def _truncated_svd_gpu(wh: _WhiteningGPU, dw, r: int, seed: int):
+    """_truncated_svd with the products on the GPU: the same seeded range
+    finder and power iterations; the QR factorisations of the K x ell and
+    N x ell blocks and the final SVDs on the host.  Returns host arrays."""
+    import torch
+
+    from . import ops
+    k, n = dw.shape
+    if min(k, n) <= EXACT_SVD_MAX or r >= min(k, n) // 2:
+        u, s, vt = np.linalg.svd(wh.apply(dw).cpu().numpy(), full_matrices=False)
+        return u[:, :r], s[:r], vt[:r]
+    rng = np.random.default_rng(seed)
+    ell = min(r + 10, k, n)
+    omega = torch.from_numpy(rng.standard_normal((n, ell))).to(dw.device)
+    q = _qr_q(wh.apply(ops.dgemm(dw, omega)))
+    for _ in range(2):
+        q = _qr_q(ops.dgemm(dw.T, wh.apply(q)))
+        q = _qr_q(wh.apply(ops.dgemm(dw, q)))
+    b = ops.dgemm(dw.T, wh.apply(q)).cpu().numpy().T     # q^T T dW, ell x n
+    ub, s, vt = np.linalg.svd(b, full_matrices=False)
+    return (q.cpu().numpy() @ ub)[:, :r], s[:r], vt[:r]
+
+
+def cmc_factors_gpu(z, dw, rank: int, ridge: float = 1e-6, seed: int = 0):
+    """cmc_factors from device inputs: z [n][K] and dw [K][N] fp64 tensors
+    (masq_gather_smoothed, masq_weight_difference).  Returns host L1 [K][r],
+    L2 [r][N]."""
+    import torch
+    k, n = dw.shape
+    l1 = np.zeros((k, rank))
+    l2 = np.zeros((rank, n))
+    if rank == 0 or z.shape[0] == 0:
+        return l1, l2
+    wh = _WhiteningGPU(z, ridge)
+    if not np.any(wh.sq):                 # Z = 0: no whitening, no compensation
+        return l1, l2
+    u, s, vt = _truncated_svd_gpu(wh, dw, min(rank, k, n), seed)
+    rr = s.shape[0]
+    l1[:, :rr] = wh.apply_inv(torch.from_numpy(np.ascontiguousarray(u)).to(dw.device)).cpu().numpy()
+    l2[:rr] = s[:, None] * vt
+    return l1, l2
+
+
 def calibrate_layer(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: int,
                     rank: int, lr_dtype: str = "bf16", ridge: float = 1e-6,
                     seed: int = 0, weight_bits: int = 8) -> dict:
@@ -173,12 +275,17 @@ def calibrate_layer(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: i
 
 def calibrate_layer_gpu(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: int,
                         rank: int, lr_dtype: str = "bf16", ridge: float = 1e-6,
-                        seed: int = 0, weight_bits: int = 8, device: str = "cuda:0") -> dict:
+                        seed: int = 0, weight_bits: int = 8, device: str = "cuda:0",
+                        cmc_on_gpu: bool = False) -> dict:
     """calibrate_layer with its exact steps on the GPU: the channel ranges,
     the MAS factors and Q(S_t W) (masq_channel_range, masq_smoothing_factors,
-    masq_quantize_weight).  The compensation factors (whitening and the
-    truncated SVD) are then formed on the host as in calibrate_layer, so the
-    result is the same, array for array."""
+    masq_quantize_weight).  By default the compensation factors (whitening
+    and the truncated SVD) are then formed on the host as in calibrate_layer,
+    so the result is the same, array for array.  With cmc_on_gpu the
+    smoothed rows, dW and every large product of the whitening and the
+    truncated SVD run on the GPU too (masq_gather_smoothed,
+    masq_weight_difference, masq_dgemm); the factors then equal the host's up
+    to rounding."""
     import torch
 
     from . import ops
@@ -193,8 +300,28 @@ def calibrate_layer_gpu(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mo
     wq_t, ws_t = ops.quantize_weight(wt, s_t[0].contiguous(), bits=weight_bits)
     s32, inv = s_t.cpu().numpy(), inv_t.cpu().numpy()
     wq, w_scale = wq_t.cpu().numpy(), ws_t.cpu().numpy()
-    return _with_cmc_factors(x, modality, w, s32, inv, wq, w_scale, n_mod, rank, lr_dtype,
-                             ridge, seed, weight_bits)
+    if not cmc_on_gpu:
+        return _with_cmc_factors(x, modality, w, s32, inv, wq, w_scale, n_mod, rank, lr_dtype,
+                                 ridge, seed, weight_bits)
+    k, n = w.shape
+    l_down = np.zeros((max(n_mod - 1, 0), rank, k), np.float32)
+    r_up = np.zeros((max(n_mod - 1, 0), n, rank), np.float32)
+    if rank > 0 and n_mod > 1:
+        for m in range(1, n_mod):
+            rows = torch.from_numpy(np.flatnonzero(modality == m).astype(np.int32)).to(device)
+            sm = s_t[m].contiguous()
+            z = ops.gather_smoothed(xt, rows, sm)
+            dw = ops.weight_difference(wt, sm, wq_t, ws_t)
+            l1, l2 = cmc_factors_gpu(z, dw, rank, ridge, seed + m)
+            l_down[m - 1] = l1.T
+            r_up[m - 1] = l2.T
+            del z, dw
+    if lr_dtype == "bf16":
+        l_down = _to_bf16_values(l_down)
+        r_up = _to_bf16_values(r_up)
+    return dict(inv_smooth=inv, s32=s32, wq=wq, w_scale=w_scale,
+                l_down=np.ascontiguousarray(l_down), r_up=np.ascontiguousarray(r_up),
+                rank=rank, n_mod=n_mod, lr_dtype=lr_dtype, weight_bits=weight_bits)
 
 
 def _with_cmc_factors(x, modality, w, s32, inv, wq, w_scale, n_mod, rank, lr_dtype, ridge,

@@ -7,6 +7,11 @@
 //   Q(S_t W): per output channel o, step d_o = max_i |s^t_i w_io| / qmax and
 //             codes rint((s^t_i w_io) / d_o) clamped to [-qmax, qmax]  (eq. PTQ)
 //
+// and the inputs and products of the compensation factors' calibration:
+// the smoothed rows Z_m = X_m S_m^-1 of one modality, the weight difference
+// dW_m = S_m W - Q(S_t W), and an fp64 GEMM for the Gram matrix, the
+// whitening and the randomized truncated SVD (Sec. 3.2, 4.3).
+//
 // Every quantity that decides a value is computed in the same precision as
 // the definition's host implementation (fp64 for the factor and the weight
 // step, one rounding to fp32 at the end), so the results are bit-exact.
@@ -142,7 +147,159 @@ __global__ __launch_bounds__(256) void k_quantize_weight(const float* __restrict
     }
 }
 
+// ------------------------------------------------------------------ CMC inputs
+// The compensation factors (Sec. 3.2, 4.3; eq. l1l2) come from the smoothed
+// calibration rows Z_m = X_m S_m^-1 of one modality, their Gram matrix, and
+// the weight difference dW_m = S_m W - Q(S_t W); the products below are the
+// heavy part of that calibration at full layer sizes.
+
+__device__ __forceinline__ double load_f64(const float* p) { return static_cast<double>(*p); }
+__device__ __forceinline__ double load_f64(const bf16_t* p) {
+    return static_cast<double>(__uint_as_float(static_cast<uint32_t>(*p) << 16));
+}
+
+// z [n][K]: z_ic = x[rows[i]][c] / s_c in fp64 (exact operands, one
+// correctly rounded division); a row index outside [0, T) gives a zero row.
+// grid (ceil(K / 256), row chunks).
+template <typename XT>
+__global__ __launch_bounds__(256) void k_gather_smoothed(const XT* __restrict__ x, int64_t T, int K,
+                                                         const int32_t* __restrict__ rows,
+                                                         int64_t n, const float* __restrict__ s,
+                                                         double* __restrict__ z) {
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    if (c >= K) return;
+    const double sc = static_cast<double>(s[c]);
+    for (int64_t i = blockIdx.y; i < n; i += gridDim.y) {
+        const int64_t r = rows[i];
+        double v = 0.0;
+        if (r >= 0 && r < T) v = load_f64(x + r * K + c) / sc;
+        z[i * K + c] = v;
+    }
+}
+
+// dw [K][N] = s_i w_io - wq_oi d_o in fp64: both products are exact (24 x 24
+// and 8 x 24 significant bits), so the one subtraction is the only rounding.
+// 64 x 64 blocks: the codes wq [N][K] are read along i and transposed
+// through LDS, w and dw are read and written along o.
+__global__ __launch_bounds__(256) void k_weight_difference(const float* __restrict__ w,
+                                                           const float* __restrict__ s,
+                                                           const int8_t* __restrict__ wq,
+                                                           const float* __restrict__ w_scale,
+                                                           int K, int N, double* __restrict__ dw) {
+    __shared__ int8_t tile[64][65];                         // [o][i]
+    const int tid = threadIdx.x;
+    const int o0 = blockIdx.x * 64, i0 = blockIdx.y * 64;
+    {
+        const int orow = tid >> 2, seg = (tid & 3) * 16, o = o0 + orow;
+        for (int e = 0; e < 16; ++e) {
+            const int i = i0 + seg + e;
+            tile[orow][seg + e] = (o < N && i < K) ? wq[static_cast<int64_t>(o) * K + i] : int8_t(0);
+        }
+    }
+    __syncthreads();
+    const int ol = tid & 63, o = o0 + ol;
+    if (o >= N) return;
+    const double d = static_cast<double>(w_scale[o]);
+    for (int il = tid >> 6; il < 64; il += 4) {
+        const int i = i0 + il;
+        if (i >= K) break;
+        const int64_t at = static_cast<int64_t>(i) * N + o;
+        const double a = static_cast<double>(s[i]) * static_cast<double>(w[at]);
+        const double b = static_cast<double>(tile[ol][il]) * d;
+        dw[at] = a - b;
+    }
+}
+
+// C [m][n] (row stride ldc) = A B (+ beta C), fp64, with A (i, k) at
+// a[i * ars + k * acs] and B (k, j) at b[k * brs + j * bcs], so transposed
+// operands are strides, not copies.  128 x 128 tiles, 256 threads of 8 x 8
+// outputs (rows ty + 16 u, columns tx + 16 v), k in steps of 16 staged
+// through LDS with the next step's loads in flight.  Every element is summed
+// in increasing k by fused multiply-adds; beta C is added after.
+constexpr int kDgTile = 128;
+constexpr int kDgStep = 16;
+__global__ __launch_bounds__(256) void k_dgemm(int64_t M, int64_t N, int64_t K,
+                                               const double* __restrict__ a, int64_t ars,
+                                               int64_t acs, const double* __restrict__ b,
+                                               int64_t brs, int64_t bcs, double beta,
+                                               double* __restrict__ c, int64_t ldc) {
+    __shared__ double as[kDgStep][kDgTile + 1];
+    __shared__ double bs[kDgStep][kDgTile + 1];
+    const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+    const int64_t i0 = static_cast<int64_t>(blockIdx.y) * kDgTile;
+    const int64_t j0 = static_cast<int64_t>(blockIdx.x) * kDgTile;
+    // staging: element e = tid + 256 q of each 128 x 16 operand block; the
+    // fastest-moving index follows the operand's unit-stride direction
+    const bool a_k_fast = acs == 1, b_k_fast = bcs != 1;
+    double ra[8], rb[8];
+    auto load = [&](int64_t k0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int e = tid + 256 * q;
+            const int kk = a_k_fast ? (e & 15) : (e >> 7);
+            const int ii = a_k_fast ? (e >> 4) : (e & 127);
+            const int64_t i = i0 + ii, k = k0 + kk;
+            ra[q] = (i < M && k < K) ? a[i * ars + k * acs] : 0.0;
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int e = tid + 256 * q;
+            const int kk = b_k_fast ? (e & 15) : (e >> 7);
+            const int jj = b_k_fast ? (e >> 4) : (e & 127);
+            const int64_t j = j0 + jj, k = k0 + kk;
+            rb[q] = (j < N && k < K) ? b[k * brs + j * bcs] : 0.0;
+        }
+    };
+    auto stash = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int e = tid + 256 * q;
+            as[a_k_fast ? (e & 15) : (e >> 7)][a_k_fast ? (e >> 4) : (e & 127)] = ra[q];
+            bs[b_k_fast ? (e & 15) : (e >> 7)][b_k_fast ? (e >> 4) : (e & 127)] = rb[q];
+        }
+    };
+    double acc[8][8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int v = 0; v < 8; ++v) acc[u][v] = 0.0;
+    if (K > 0) load(0);
+    for (int64_t k0 = 0; k0 < K; k0 += kDgStep) {
+        __syncthreads();
+        stash();
+        __syncthreads();
+        if (k0 + kDgStep < K) load(k0 + kDgStep);
+#pragma unroll 4
+        for (int kk = 0; kk < kDgStep; ++kk) {
+            double av[8], bv[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) av[u] = as[kk][ty + 16 * u];
+#pragma unroll
+            for (int v = 0; v < 8; ++v) bv[v] = bs[kk][tx + 16 * v];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+#pragma unroll
+                for (int v = 0; v < 8; ++v) acc[u][v] = fma(av[u], bv[v], acc[u][v]);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int64_t i = i0 + ty + 16 * u;
+        if (i >= M) break;
+#pragma unroll
+        for (int v = 0; v < 8; ++v) {
+            const int64_t j = j0 + tx + 16 * v;
+            if (j < N) {
+                double r = acc[u][v];
+                if (beta != 0.0) r = r + beta * c[i * ldc + j];
+                c[i * ldc + j] = r;
+            }
+        }
+    }
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
 
 }  // namespace
 
@@ -209,6 +366,68 @@ masq_status masq_quantize_weight(const float* w, const float* smooth_text, int64
     hipLaunchKernelGGL(k_quantize_weight, dim3(static_cast<unsigned>((c_out + 63) / 64)), dim3(256),
                        0, static_cast<hipStream_t>(stream), w, smooth_text, static_cast<int>(c_in),
                        static_cast<int>(c_out), (1 << (bits - 1)) - 1, wq, w_scale);
+    return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
+}
+
+masq_status masq_gather_smoothed(const void* x, masq_dtype x_dt, int64_t T, int64_t c_in,
+                                 const int32_t* rows, int64_t n_rows, const float* smooth,
+                                 double* z, void* stream) {
+    if (x_dt != MASQ_F32 && x_dt != MASQ_BF16) return MASQ_ERR_DTYPE;
+    if (T < 0 || n_rows < 0 || c_in <= 0 || c_in % 16 != 0 || c_in > (1LL << 30))
+        return MASQ_ERR_SHAPE;
+    if (n_rows == 0) return MASQ_OK;
+    if (!rows || !smooth || !z || (T > 0 && !x)) return MASQ_ERR_NULL;
+    if (!aligned16(rows) || !aligned16(smooth) || !aligned16(z) || (T > 0 && !aligned16(x)))
+        return MASQ_ERR_ALIGN;
+    (void)hipGetLastError();
+    const int K = static_cast<int>(c_in);
+    const int64_t col_blocks = (K + 255) / 256;
+    int64_t chunks = (2048 + col_blocks - 1) / col_blocks;
+    if (chunks > n_rows) chunks = n_rows;
+    if (chunks > 65535) chunks = 65535;
+    const dim3 grid(static_cast<unsigned>(col_blocks), static_cast<unsigned>(chunks));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (x_dt == MASQ_BF16)
+        hipLaunchKernelGGL(k_gather_smoothed<bf16_t>, grid, dim3(256), 0, s,
+                           static_cast<const bf16_t*>(x), T, K, rows, n_rows, smooth, z);
+    else
+        hipLaunchKernelGGL(k_gather_smoothed<float>, grid, dim3(256), 0, s,
+                           static_cast<const float*>(x), T, K, rows, n_rows, smooth, z);
+    return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
+}
+
+masq_status masq_weight_difference(const float* w, const float* smooth, const int8_t* wq,
+                                   const float* w_scale, int64_t c_in, int64_t c_out,
+                                   double* dw, void* stream) {
+    if (c_in <= 0 || c_in % 16 != 0 || c_out <= 0 || c_out % 16 != 0 || c_in > (1LL << 30) ||
+        c_out > (1LL << 30) || (c_in + 63) / 64 > 65535)
+        return MASQ_ERR_SHAPE;
+    if (!w || !smooth || !wq || !w_scale || !dw) return MASQ_ERR_NULL;
+    if (!aligned16(w) || !aligned16(smooth) || !aligned16(wq) || !aligned16(w_scale) ||
+        !aligned16(dw))
+        return MASQ_ERR_ALIGN;
+    (void)hipGetLastError();
+    const dim3 grid(static_cast<unsigned>((c_out + 63) / 64), static_cast<unsigned>((c_in + 63) / 64));
+    hipLaunchKernelGGL(k_weight_difference, grid, dim3(256), 0, static_cast<hipStream_t>(stream),
+                       w, smooth, wq, w_scale, static_cast<int>(c_in), static_cast<int>(c_out), dw);
+    return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
+}
+
+masq_status masq_dgemm(int64_t m, int64_t n, int64_t k, const double* a, int64_t a_row_stride,
+                       int64_t a_col_stride, const double* b, int64_t b_row_stride,
+                       int64_t b_col_stride, double beta, double* c, int64_t ldc, void* stream) {
+    if (m < 0 || n < 0 || k < 0 || a_row_stride < 0 || a_col_stride < 0 || b_row_stride < 0 ||
+        b_col_stride < 0 || (m + kDgTile - 1) / kDgTile > 65535 ||
+        (n + kDgTile - 1) / kDgTile > 0x7fffffffLL || (m > 0 && n > 0 && ldc < n))
+        return MASQ_ERR_SHAPE;
+    if (m == 0 || n == 0) return MASQ_OK;
+    if (!c || (k > 0 && (!a || !b))) return MASQ_ERR_NULL;
+    if (!aligned8(c) || (k > 0 && (!aligned8(a) || !aligned8(b)))) return MASQ_ERR_ALIGN;
+    (void)hipGetLastError();
+    const dim3 grid(static_cast<unsigned>((n + kDgTile - 1) / kDgTile),
+                    static_cast<unsigned>((m + kDgTile - 1) / kDgTile));
+    hipLaunchKernelGGL(k_dgemm, grid, dim3(256), 0, static_cast<hipStream_t>(stream), m, n, k, a,
+                       a_row_stride, a_col_stride, b, b_row_stride, b_col_stride, beta, c, ldc);
     return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
 }
 

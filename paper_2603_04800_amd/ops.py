@@ -48,6 +48,10 @@ _SIGS = {
     "masq_channel_range": ([_p, _i32, _p, _i64, _i64, _i32, _p, _p], ctypes.c_int),
     "masq_smoothing_factors": ([_p, _p, _i64, _i64, _i32, _p, _p, _p], ctypes.c_int),
     "masq_quantize_weight": ([_p, _p, _i64, _i64, _i32, _p, _p, _p], ctypes.c_int),
+    "masq_gather_smoothed": ([_p, _i32, _i64, _i64, _p, _i64, _p, _p, _p], ctypes.c_int),
+    "masq_weight_difference": ([_p, _p, _p, _p, _i64, _i64, _p, _p], ctypes.c_int),
+    "masq_dgemm": ([_i64, _i64, _i64, _p, _i64, _i64, _p, _i64, _i64, ctypes.c_double, _p, _i64,
+                    _p], ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -195,6 +199,62 @@ def quantize_weight(w, smooth_text, bits=8, stream=None):
     _check("masq_quantize_weight", _lib.masq_quantize_weight(
         _ptr(w), _ptr(smooth_text), K, N, bits, _ptr(wq), _ptr(scale), _stream(stream)))
     return wq, scale
+
+
+def gather_smoothed(x, rows, smooth, stream=None):
+    """Smoothed calibration rows of one modality, fp64 [n][K]:
+    x[rows[i]] / smooth (Sec. 4.3)."""
+    T, K = x.shape
+    _need(rows, torch.int32, "rows")
+    _need(smooth, torch.float32, "smooth")
+    z = torch.empty((rows.shape[0], K), dtype=torch.float64, device=x.device)
+    _check("masq_gather_smoothed", _lib.masq_gather_smoothed(
+        _ptr(x), _dt(x), T, K, _ptr(rows), rows.shape[0], _ptr(smooth), _ptr(z),
+        _stream(stream)))
+    return z
+
+
+def weight_difference(w, smooth, wq, w_scale, stream=None):
+    """dW = S_m W - Q(S_t W), fp64 [K][N] (Sec. 4.3), from the float weight
+    W [K][N], S_m's diagonal and the shared weight's codes [N][K] and steps."""
+    K, N = w.shape
+    _need(w, torch.float32, "w")
+    _need(smooth, torch.float32, "smooth")
+    _need(wq, torch.int8, "wq")
+    _need(w_scale, torch.float32, "w_scale")
+    dw = torch.empty((K, N), dtype=torch.float64, device=w.device)
+    _check("masq_weight_difference", _lib.masq_weight_difference(
+        _ptr(w), _ptr(smooth), _ptr(wq), _ptr(w_scale), K, N, _ptr(dw), _stream(stream)))
+    return dw
+
+
+def _view_ptr(t):
+    if not t.is_cuda:
+        raise ValueError("tensors must live on the GPU")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def dgemm(a, b, c=None, beta=0.0, stream=None):
+    """C = A B (+ beta C) in fp64.  a [m][k] and b [k][n] are 2-D fp64 device
+    tensors of any strides (a transpose view costs nothing); c, if given,
+    is a contiguous [m][n] fp64 tensor, updated in place."""
+    _need(a, torch.float64, "a")
+    _need(b, torch.float64, "b")
+    m, k = a.shape
+    k2, n = b.shape
+    if k != k2:
+        raise ValueError(f"inner sizes differ: {k} and {k2}")
+    if c is None:
+        if beta != 0.0:
+            raise ValueError("beta needs c")
+        c = torch.empty((m, n), dtype=torch.float64, device=a.device)
+    _need(c, torch.float64, "c")
+    if tuple(c.shape) != (m, n):
+        raise ValueError(f"c must be [{m}][{n}]")
+    _check("masq_dgemm", _lib.masq_dgemm(
+        m, n, k, _view_ptr(a), a.stride(0), a.stride(1), _view_ptr(b), b.stride(0), b.stride(1),
+        float(beta), _ptr(c), n, _stream(stream)))
+    return c
 
 
 def workspace_bytes(T, K, N, rank, n_mod) -> int:

@@ -182,3 +182,29 @@ def test_calibration_calls_validate(lib):
     assert qw(P, P, 64, 64, 6, P, P, None) == 2             # bits must be 8 or 4
     assert qw(P, P, 48, 64, 8, P + 4, P, None) == 4         # misaligned codes
     assert qw(P, P, 64, 64, 8, P, None, None) == 1          # no step output
+
+
+def test_cmc_calibration_calls_validate(lib):
+    """masq_gather_smoothed, masq_weight_difference and masq_dgemm check
+    sizes, dtypes, pointers and alignment before enqueueing anything."""
+    import ctypes
+    P = 1 << 20
+    gs, wd, dg = lib.masq_gather_smoothed, lib.masq_weight_difference, lib.masq_dgemm
+    assert gs(P, 2, 8, 64, P, 4, P, P, None) == 3            # unknown activation dtype
+    assert gs(P, 1, 8, 40, P, 4, P, P, None) == 2            # c_in % 16 != 0
+    assert gs(P, 1, 8, 64, P, -1, P, P, None) == 2           # n_rows < 0
+    assert gs(P, 1, 8, 64, None, 4, P, P, None) == 1         # no row list
+    assert gs(P, 1, 8, 64, P, 4, P, P + 8, None) == 4        # misaligned output
+    assert gs(None, 1, 0, 64, None, 0, None, None, None) == 0   # nothing to gather
+    assert wd(P, P, P, P, 64, 40, P, None) == 2              # c_out % 16 != 0
+    assert wd(P, P, None, P, 64, 64, P, None) == 1           # no codes
+    assert wd(P, P, P, P, 64, 64, P + 8, None) == 4          # misaligned output
+    one = ctypes.c_double(0.0)
+    assert dg(-1, 4, 4, P, 4, 1, P, 4, 1, one, P, 4, None) == 2       # m < 0
+    assert dg(4, 4, 4, P, -4, 1, P, 4, 1, one, P, 4, None) == 2       # negative stride
+    assert dg(4, 8, 4, P, 4, 1, P, 8, 1, one, P, 4, None) == 2        # ldc < n
+    assert dg(65535 * 128 + 1, 4, 4, P, 4, 1, P, 4, 1, one, P, 4, None) == 2
+    assert dg(4, 4, 4, None, 4, 1, P, 4, 1, one, P, 4, None) == 1     # no A
+    assert dg(4, 4, 0, None, 0, 0, None, 0, 0, one, None, 4, None) == 1   # k = 0 still writes c
+    assert dg(4, 4, 4, P + 4, 4, 1, P, 4, 1, one, P, 4, None) == 4    # misaligned A
+    assert dg(0, 4, 4, None, 4, 1, None, 4, 1, one, None, 4, None) == 0   # empty output

@@ -1,6 +1,9 @@
-"""GPU parity of the calibration kernels (masq_channel_range,
-masq_smoothing_factors, masq_quantize_weight) against the oracle's
-definitions (oracle/calibration.py): bit-exact, through the C ABI."""
+"""GPU parity of the calibration kernels through the C ABI, against the
+oracle's definitions (oracle/calibration.py): masq_channel_range,
+masq_smoothing_factors, masq_quantize_weight, masq_gather_smoothed and
+masq_weight_difference bit-exact; masq_dgemm within the fp64 rounding bound;
+the compensation factors built on them equal to the oracle's (and to the
+host calibration's) up to rounding."""
 import numpy as np
 import pytest
 import torch
@@ -86,3 +89,147 @@ def test_gpu_assisted_layer_calibration_equals_host(ops, cfg_index, bits):
                                         weight_bits=bits)
     for k in ("inv_smooth", "s32", "wq", "w_scale", "l_down", "r_up"):
         assert np.array_equal(np.asarray(gpu[k]), np.asarray(host[k])), k
+
+
+# ------------------------------------------------- compensation-factor inputs
+_U = 2.0 ** -53
+
+
+def _dgemm_bound(a, b):
+    """|fl(AB) - AB| <= k u |A| |B| (first order) for any summation order, so
+    two computed products differ by at most twice that."""
+    k = a.shape[1]
+    return 2.0 * (k + 2) * _U * (np.abs(a) @ np.abs(b)) + 1e-300
+
+
+@pytest.mark.parametrize("m,n,k", [(130, 77, 300), (1, 1, 1), (257, 129, 16), (5, 300, 17),
+                                   (128, 256, 1031)])
+@pytest.mark.parametrize("ta,tb", [(False, False), (True, False), (False, True), (True, True)])
+def test_dgemm_within_the_fp64_bound(ops, m, n, k, ta, tb):
+    """masq_dgemm with transposed operands passed as strides, ragged tiles,
+    and beta != 0, against NumPy's fp64 product within the rounding bound."""
+    rng = np.random.default_rng(m * 7 + n * 3 + k)
+    a = rng.standard_normal((m, k)) * rng.uniform(0.1, 10.0, k)[None, :]
+    b = rng.standard_normal((k, n))
+    c0 = rng.standard_normal((m, n))
+    dev = torch.device("cuda:0")
+    at = torch.from_numpy(np.ascontiguousarray(a.T)).to(dev).T if ta else torch.from_numpy(a).to(dev)
+    bt = torch.from_numpy(np.ascontiguousarray(b.T)).to(dev).T if tb else torch.from_numpy(b).to(dev)
+    c = ops.dgemm(at, bt).cpu().numpy()
+    assert np.all(np.abs(c - a @ b) <= _dgemm_bound(a, b))
+    cb = ops.dgemm(at, bt, c=torch.from_numpy(c0.copy()).to(dev), beta=-0.75).cpu().numpy()
+    ref = a @ b + (-0.75) * c0
+    assert np.all(np.abs(cb - ref) <= _dgemm_bound(a, b) + 2 * _U * np.abs(ref) + 1e-300)
+
+
+def test_dgemm_degenerate_sizes(ops):
+    dev = torch.device("cuda:0")
+    z = torch.zeros((3, 0), dtype=torch.float64, device=dev)
+    out = ops.dgemm(z, torch.zeros((0, 4), dtype=torch.float64, device=dev))
+    assert np.array_equal(out.cpu().numpy(), np.zeros((3, 4)))          # k = 0 gives zeros
+    c = torch.full((3, 4), 2.0, dtype=torch.float64, device=dev)
+    ops.dgemm(z, torch.zeros((0, 4), dtype=torch.float64, device=dev), c=c, beta=0.5)
+    assert np.array_equal(c.cpu().numpy(), np.ones((3, 4)))             # k = 0: beta c
+    e = ops.dgemm(torch.zeros((0, 5), dtype=torch.float64, device=dev),
+                  torch.ones((5, 2), dtype=torch.float64, device=dev))
+    assert e.shape == (0, 2)
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_gather_smoothed_is_exact(ops, act):
+    """Z_m = X_m S_m^-1 (Sec. 4.3) in fp64, bit for bit; indices outside
+    [0, T) give zero rows."""
+    rng = np.random.default_rng(11)
+    T, K = 200, 272
+    x = (rng.standard_normal((T, K)) * 20).astype(np.float32)
+    if act == "bf16":
+        x = bf16_round(x)
+    s = rng.uniform(0.01, 50.0, K).astype(np.float32)
+    rows = np.concatenate([rng.permutation(T)[:150], [-1, T, 10 ** 6]]).astype(np.int32)
+    dev = torch.device("cuda:0")
+    xt = torch.from_numpy(x).to(dev, torch.bfloat16 if act == "bf16" else torch.float32)
+    z = ops.gather_smoothed(xt, torch.from_numpy(rows).to(dev), torch.from_numpy(s).to(dev))
+    ref = np.zeros((rows.size, K))
+    ok = (rows >= 0) & (rows < T)
+    ref[ok] = x[rows[ok]].astype(np.float64) / s.astype(np.float64)[None, :]
+    assert np.array_equal(z.cpu().numpy().view(np.uint64), ref.view(np.uint64))
+
+
+@pytest.mark.parametrize("K,N,bits", [(80, 48, 8), (3584, 512, 8), (192, 272, 4)])
+def test_weight_difference_is_exact(ops, K, N, bits):
+    """dW_m = S_m W - Q(S_t W) (Sec. 4.3) bit for bit against the oracle's
+    definition, with the oracle's own factors and shared weight."""
+    rng = np.random.default_rng(K + N + bits)
+    w = (rng.standard_normal((K, N)) / np.sqrt(K)).astype(np.float32)
+    s_t = rng.uniform(0.05, 20.0, K).astype(np.float32)
+    s_m = rng.uniform(0.05, 20.0, K).astype(np.float32)
+    wq, ws, wdq = cal.quantize_weight(w, s_t, bits)
+    ref = cal.weight_difference(w, s_m, s_t, wdq)
+    dev = torch.device("cuda:0")
+    dw = ops.weight_difference(torch.from_numpy(w).to(dev), torch.from_numpy(s_m).to(dev),
+                               torch.from_numpy(wq).to(dev), torch.from_numpy(ws).to(dev))
+    assert np.array_equal(dw.cpu().numpy().view(np.uint64), ref.view(np.uint64))
+
+
+def _product_relerr(l1, l2, l1_ref, l2_ref):
+    a, b = np.asarray(l1) @ np.asarray(l2), np.asarray(l1_ref) @ np.asarray(l2_ref)
+    return np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300)
+
+
+@pytest.mark.parametrize("n_rows,K,N,rank", [(300, 96, 80, 16), (40, 128, 64, 16),
+                                             (0, 64, 48, 16), (500, 256, 192, 64)])
+def test_gpu_cmc_factors_match_the_oracle(ops, n_rows, K, N, rank):
+    """L1 L2 from the GPU whitening and truncated SVD (Sec. 3.2, 4.3; eq.
+    l1l2) equal the oracle's dense construction up to fp64 rounding: more
+    rows than channels (Gram Z^T Z), fewer (Gram Z Z^T), none."""
+    from paper_2603_04800_amd import calibrate
+    rng = np.random.default_rng(n_rows + K)
+    z = rng.standard_normal((n_rows, K)) * rng.uniform(0.1, 30.0, K)[None, :]
+    dw = rng.standard_normal((K, N)) * 1e-2
+    dev = torch.device("cuda:0")
+    l1, l2 = calibrate.cmc_factors_gpu(torch.from_numpy(z).to(dev),
+                                       torch.from_numpy(dw).to(dev), rank)
+    if n_rows == 0:
+        assert not np.any(l1) and not np.any(l2)
+        return
+    l1_ref, l2_ref = cal.cmc_factors(z, dw, rank)
+    lp, lo = l1 @ l2, l1_ref @ l2_ref                      # the host calibration's bar
+    assert np.abs(lp - lo).max() <= 1e-5 * max(np.abs(lo).max(), 1e-30)
+
+
+def test_gpu_randomized_svd_matches_the_host_one(ops):
+    """Layers above 1024 channels take the seeded randomized truncated SVD:
+    the GPU products give the host's factors up to rounding (same seed)."""
+    from paper_2603_04800_amd import calibrate
+    rng = np.random.default_rng(5)
+    K, N, n_rows, rank = 1152, 1088, 700, 32
+    z = rng.standard_normal((n_rows, K)) * rng.uniform(0.1, 30.0, K)[None, :]
+    dw = rng.standard_normal((K, N)) * 1e-2 + \
+        (rng.standard_normal((K, 40)) @ rng.standard_normal((40, N))) * 1e-2
+    dev = torch.device("cuda:0")
+    l1, l2 = calibrate.cmc_factors_gpu(torch.from_numpy(z).to(dev),
+                                       torch.from_numpy(dw).to(dev), rank, seed=9)
+    l1_ref, l2_ref = calibrate.cmc_factors(z, dw, rank, seed=9)
+    assert _product_relerr(l1, l2, l1_ref, l2_ref) < 1e-8
+
+
+@pytest.mark.parametrize("cfg_index", [0, 3])
+def test_layer_calibration_with_cmc_on_gpu(ops, cfg_index):
+    """calibrate_layer_gpu(cmc_on_gpu=True) against the host calibration: the
+    exact artifacts equal, the compensation's reconstruction L1 L2 of every
+    non-text modality within the factors' storage rounding (bf16: 2^-8)."""
+    from paper_2603_04800_amd import calibrate
+    cfg = synth.CONFIGS[cfg_index]
+    li = synth.make_layer_inputs(cfg, 0)
+    p = cfg.projections[0]
+    x, w = li.x[p.input_key], li.w[p.name]
+    host = calibrate.calibrate_layer(x, li.modality, w, cfg.n_mod, cfg.rank, cfg.lr_dtype)
+    gpu = calibrate.calibrate_layer_gpu(x, li.modality, w, cfg.n_mod, cfg.rank, cfg.lr_dtype,
+                                        cmc_on_gpu=True)
+    for k in ("inv_smooth", "s32", "wq", "w_scale"):
+        assert np.array_equal(np.asarray(gpu[k]), np.asarray(host[k])), k
+    tol = 2.0 ** -7 if cfg.lr_dtype == "bf16" else 1e-6
+    for m in range(cfg.n_mod - 1):
+        err = _product_relerr(gpu["l_down"][m].astype(np.float64).T, gpu["r_up"][m].astype(np.float64).T,
+                              host["l_down"][m].astype(np.float64).T, host["r_up"][m].astype(np.float64).T)
+        assert err < tol, (m, err)

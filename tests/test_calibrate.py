@@ -115,3 +115,37 @@ def test_synth_bf16_inputs_are_representable():
     x = li.x["x"]
     bits = x.view(np.uint32)
     assert not np.any(bits & 0xFFFF)
+
+
+def test_gpu_cmc_driver_logic_with_host_products(monkeypatch):
+    """The GPU compensation-factor driver (cmc_factors_gpu) with masq_dgemm
+    replaced by a CPU product: the same L1 L2 as the host calibration, for
+    the dense and thin whitening and the randomized truncation.  This checks
+    the driver's host logic; the kernels themselves are GPU tests."""
+    import torch
+
+    from paper_2603_04800_amd import ops
+
+    def dgemm(a, b, c=None, beta=0.0, stream=None):
+        out = a @ b
+        if c is not None:
+            c.copy_(out + beta * c)
+            return c
+        return out.contiguous()
+
+    monkeypatch.setattr(ops, "dgemm", dgemm)
+    monkeypatch.setattr(pcal, "EXACT_SVD_MAX", 16)
+    rng = np.random.default_rng(8)
+    for n_rows, K, N, r in ((120, 64, 48, 8), (30, 64, 48, 8), (120, 40, 24, 20)):
+        z = rng.standard_normal((n_rows, K)) * rng.uniform(0.2, 4, K)[None, :]
+        dw = rng.standard_normal((K, N))
+        l1, l2 = pcal.cmc_factors_gpu(torch.from_numpy(z), torch.from_numpy(dw), r, seed=3)
+        h1, h2 = pcal.cmc_factors(z, dw, r, seed=3)
+        lp, lo = l1 @ l2, h1 @ h2
+        assert np.abs(lp - lo).max() <= 1e-9 * np.abs(lo).max(), (n_rows, K, N, r)
+    l1, l2 = pcal.cmc_factors_gpu(torch.zeros((0, 64), dtype=torch.float64),
+                                  torch.from_numpy(rng.standard_normal((64, 48))), 8)
+    assert not np.any(l1) and not np.any(l2)
+    l1, l2 = pcal.cmc_factors_gpu(torch.zeros((10, 64), dtype=torch.float64),
+                                  torch.from_numpy(rng.standard_normal((64, 48))), 8)
+    assert not np.any(l1) and not np.any(l2)
