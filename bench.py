@@ -64,6 +64,11 @@ def parse():
                     help="only time the calibration's exact steps (channel ranges, MAS factors, "
                          "Q(S_t W)) on the GPU against the host implementation, on the "
                          "workload's first projection")
+    ap.add_argument("--cmc-study", action="store_true",
+                    help="only print the compensation study of the workload's first projection: "
+                         "effective rank of dW before and after whitening, and SQNR against "
+                         "the rank ratio, whitened and not, beside the comparators "
+                         "(weights at --weight-bits)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (5 times): the "
                          "reference for scaling HBM traffic counters")
@@ -461,6 +466,11 @@ def main():
         return
     if args.calibrate:
         calibration_timing(args.workload)
+        return
+    if args.cmc_study:
+        from paper_2603_04800_amd import study
+        for row in study.cmc_study(args.workload, weight_bits=args.weight_bits):
+            print(json.dumps(row), flush=True)
         return
     if args.summarize_profiles:
         summarize_profiles(args.summarize_profiles, args.workload)

@@ -207,6 +207,19 @@ class _WhiteningGPU:
         return self._apply(a, self.isq, self.add_inv)
 
 
+class _NoWhitening:
+    """T = I: the plain truncated SVD of dW, the non-whitened baseline that
+    the paper's SQNR-against-rank comparison sets beside CMC (Sec. 5)."""
+
+    sq = np.ones(1)
+
+    def apply(self, a):
+        return a
+
+    def apply_inv(self, a):
+        return a
+
+
 def _qr_q(a):
     """Q of the reduced QR factorisation of a device matrix (on the host)."""
     import torch
@@ -237,17 +250,19 @@ def _truncated_svd_gpu(wh: _WhiteningGPU, dw, r: int, seed: int):
     return (q.cpu().numpy() @ ub)[:, :r], s[:r], vt[:r]
 
 
-def cmc_factors_gpu(z, dw, rank: int, ridge: float = 1e-6, seed: int = 0):
+def cmc_factors_gpu(z, dw, rank: int, ridge: float = 1e-6, seed: int = 0,
+                    whiten: bool = True):
     """cmc_factors from device inputs: z [n][K] and dw [K][N] fp64 tensors
     (masq_gather_smoothed, masq_weight_difference).  Returns host L1 [K][r],
-    L2 [r][N]."""
+    L2 [r][N].  whiten=False drops the whitening (T = I): the best rank-r
+    approximation of dW itself."""
     import torch
     k, n = dw.shape
     l1 = np.zeros((k, rank))
     l2 = np.zeros((rank, n))
     if rank == 0 or z.shape[0] == 0:
         return l1, l2
-    wh = _WhiteningGPU(z, ridge)
+    wh = _WhiteningGPU(z, ridge) if whiten else _NoWhitening()
     if not np.any(wh.sq):                 # Z = 0: no whitening, no compensation
         return l1, l2
     u, s, vt = _truncated_svd_gpu(wh, dw, min(rank, k, n), seed)
@@ -276,7 +291,7 @@ def calibrate_layer(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: i
 def calibrate_layer_gpu(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mod: int,
                         rank: int, lr_dtype: str = "bf16", ridge: float = 1e-6,
                         seed: int = 0, weight_bits: int = 8, device: str = "cuda:0",
-                        cmc_on_gpu: bool = False) -> dict:
+                        cmc_on_gpu: bool = False, whiten: bool = True) -> dict:
     """calibrate_layer with its exact steps on the GPU: the channel ranges,
     the MAS factors and Q(S_t W) (masq_channel_range, masq_smoothing_factors,
     masq_quantize_weight).  By default the compensation factors (whitening
@@ -285,7 +300,8 @@ def calibrate_layer_gpu(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mo
     smoothed rows, dW and every large product of the whitening and the
     truncated SVD run on the GPU too (masq_gather_smoothed,
     masq_weight_difference, masq_dgemm); the factors then equal the host's up
-    to rounding."""
+    to rounding.  whiten=False (with cmc_on_gpu) gives the non-whitened
+    baseline's factors."""
     import torch
 
     from . import ops
@@ -312,7 +328,7 @@ def calibrate_layer_gpu(x: np.ndarray, modality: np.ndarray, w: np.ndarray, n_mo
             sm = s_t[m].contiguous()
             z = ops.gather_smoothed(xt, rows, sm)
             dw = ops.weight_difference(wt, sm, wq_t, ws_t)
-            l1, l2 = cmc_factors_gpu(z, dw, rank, ridge, seed + m)
+            l1, l2 = cmc_factors_gpu(z, dw, rank, ridge, seed + m, whiten=whiten)
             l_down[m - 1] = l1.T
             r_up[m - 1] = l2.T
             del z, dw

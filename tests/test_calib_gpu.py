@@ -233,3 +233,48 @@ def test_layer_calibration_with_cmc_on_gpu(ops, cfg_index):
         err = _product_relerr(gpu["l_down"][m].astype(np.float64).T, gpu["r_up"][m].astype(np.float64).T,
                               host["l_down"][m].astype(np.float64).T, host["r_up"][m].astype(np.float64).T)
         assert err < tol, (m, err)
+
+
+def test_unwhitened_factors_are_the_truncated_svd_of_dw(ops):
+    """whiten=False: L1 L2 is the best rank-r approximation of dW itself
+    (Eckart-Young; the library SVD serves as the definition)."""
+    from paper_2603_04800_amd import calibrate
+    rng = np.random.default_rng(21)
+    z = rng.standard_normal((90, 64)) * rng.uniform(0.1, 30.0, 64)[None, :]
+    dw = rng.standard_normal((64, 48))
+    dev = torch.device("cuda:0")
+    l1, l2 = calibrate.cmc_factors_gpu(torch.from_numpy(z).to(dev), torch.from_numpy(dw).to(dev),
+                                       16, whiten=False)
+    u, s, vt = np.linalg.svd(dw, full_matrices=False)
+    best = (u[:, :16] * s[:16]) @ vt[:16]
+    assert np.abs(l1 @ l2 - best).max() <= 1e-10 * np.abs(best).max()
+
+
+def test_whitened_factors_minimise_the_whitened_loss(ops):
+    """Theorem 2: the whitened truncation minimises ||Z (dW - L1 L2)||_F over
+    rank-r factors, so it is never worse there than the plain truncation."""
+    from paper_2603_04800_amd import calibrate
+    rng = np.random.default_rng(22)
+    z = rng.standard_normal((200, 96)) * rng.uniform(0.05, 40.0, 96)[None, :]
+    dw = rng.standard_normal((96, 80))
+    dev = torch.device("cuda:0")
+    zt, dwt = torch.from_numpy(z).to(dev), torch.from_numpy(dw).to(dev)
+    for r in (4, 16, 32):
+        a1, a2 = calibrate.cmc_factors_gpu(zt, dwt, r)
+        b1, b2 = calibrate.cmc_factors_gpu(zt, dwt, r, whiten=False)
+        la = np.linalg.norm(z @ (dw - a1 @ a2))
+        lb = np.linalg.norm(z @ (dw - b1 @ b2))
+        assert la <= lb * (1 + 1e-9), (r, la, lb)
+
+
+def test_cmc_study_small_workload(ops):
+    """The study's rows on the 512-wide layer: effective ranks of dW, SQNR
+    for every rank (whitened and not) and the SmoothQuant comparator."""
+    from paper_2603_04800_amd import study
+    rows = study.cmc_study(0, ranks=[0, 16, 64], weight_bits=4)
+    er = [r for r in rows if r["kind"] == "effective_rank"]
+    assert len(er) == 1 and 1.0 <= er[0]["whitened"] and 1.0 <= er[0]["plain"]
+    sq = [r for r in rows if r["kind"] == "sqnr"]
+    assert len(sq) == 1 + 2 + 2 + 1
+    for r in sq:
+        assert all(np.isfinite(v) for v in r["sqnr_db"].values()), r
