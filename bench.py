@@ -69,6 +69,10 @@ def parse():
                          "effective rank of dW before and after whitening, and SQNR against "
                          "the rank ratio, whitened and not, beside the comparators "
                          "(weights at --weight-bits)")
+    ap.add_argument("--mas-opt", action="store_true",
+                    help="only run the MAS factor optimisation (2 epochs, batches of 256 rows) on "
+                         "the workload's first projection: the objective of each modality "
+                         "before and after, and the time per step")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (5 times): the "
                          "reference for scaling HBM traffic counters")
@@ -177,6 +181,54 @@ def calibration_timing(workload: int, reps: int = 20):
                       "gram_frac_fp64_peak": round(gram_flops / gram_ms / 1e9 / 78.6, 4),
                       "gpu_s": round(gpu_cmc_s, 2), "host_s": round(host_cmc_s, 2),
                       "l1l2_relative_difference": rel}), flush=True)
+
+
+def mas_opt_timing(workload: int, bits: int):
+    """The MAS factor optimisation (Sec. 4.2) from the MAS initial factors:
+    each modality's objective over all its rows before and after two epochs,
+    and the wall time of the optimisation (every step's products, quantizers
+    and reductions on the GPU; Adam on the host)."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2603_04800_amd import calibrate, mas_opt
+    cfg = synth.CONFIGS[workload]
+    p = cfg.projections[0]
+    li = synth.make_layer_inputs(cfg, 0, projections=[p.name])
+    x = np.asarray(li.x[p.input_key], np.float32)
+    mod = np.asarray(li.modality, np.int32)
+    w = np.asarray(li.w[p.name], np.float32)
+    s0, _ = calibrate.smoothing_factors(x, mod, w, cfg.n_mod)
+    dev = torch.device("cuda:0")
+    wt = torch.from_numpy(np.ascontiguousarray(w)).to(dev)
+
+    def objective(s):
+        out = {}
+        for m in range(cfg.n_mod):
+            rows = x[mod == m]
+            if rows.shape[0]:
+                st = mas_opt._Step(torch.from_numpy(np.ascontiguousarray(rows)).to(dev),
+                                   wt.double(), wt, bits)
+                out[str(m)] = st(s[m])[0]
+                del st
+        return out
+
+    before = objective(s0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    s1, hist = mas_opt.optimise(x, mod, w, s0, epochs=2, batch=256, bits=bits)
+    torch.cuda.synchronize()
+    secs = time.perf_counter() - t0
+    after = objective(s1)
+    steps = sum(len(h) for h in hist)
+    print(json.dumps({"metric": "MAS factor optimisation (2 epochs, batches of 256 rows)",
+                      "workload": cfg.name, "weight_bits": bits, "c_in": int(w.shape[0]),
+                      "c_out": int(w.shape[1]), "steps": steps, "seconds": round(secs, 2),
+                      "ms_per_step": round(secs * 1e3 / max(steps, 1), 2),
+                      "mae_before": before, "mae_after": after,
+                      "factor_change_max_ratio": float(np.max(np.maximum(s1 / s0, s0 / s1)))}),
+          flush=True)
 
 
 def kernel_source_hash() -> str:
@@ -466,6 +518,9 @@ def main():
         return
     if args.calibrate:
         calibration_timing(args.workload)
+        return
+    if args.mas_opt:
+        mas_opt_timing(args.workload, args.weight_bits)
         return
     if args.cmc_study:
         from paper_2603_04800_amd import study

@@ -267,6 +267,44 @@ masq_status masq_dgemm(int64_t m, int64_t n, int64_t k, const double* a, int64_t
                        int64_t a_col_stride, const double* b, int64_t b_row_stride,
                        int64_t b_col_stride, double beta, double* c, int64_t ldc, void* stream);
 
+/* The MAS factor optimisation (Sec. 4.2, eq. mas_quant): per modality m,
+ * minimise L(S_m) = mean |Q(X_m S_m^-1) Q(S_m W) - X_m W| over the
+ * smoothing factors, with the inference quantizers (masq_smooth_quant,
+ * masq_quantize_weight) in the forward pass and the straight-through
+ * estimator in the backward pass:
+ *   dL/ds_i = -(1 / s_i^2) sum_t x_ti A_ti + sum_o w_io B_io,
+ *   G = sign(Xq Wq - X W) / (T N), A = G Wq^T, B = Xq^T G
+ * (Xq, Wq the dequantized operands; A and B formed with masq_dgemm).
+ *
+ * masq_dequantize_rows: out[r][c] = codes[r][c] * scale[r] in fp64 (exact)
+ * for codes [rows][cols] int8 and scale [rows] f32: Xq from the per-token
+ * codes and steps, or Wq^T [c_out][c_in] from the shared-weight codes.
+ *
+ * masq_mae_sign: g[e] = sign(y[e] - ref[e]) / count (0 on ties) for the
+ * count elements of y and ref (fp64); partial[b] = the sum of |y - ref|
+ * over elements [4096 b, 4096 b + 4096), in a fixed order, for the
+ * masq_mae_partials(count) blocks: the loss is their sum / count.
+ * g must not overlap y or ref.
+ *
+ * masq_mas_gradient: grad[i] = -colpart[i] / s_i^2 + sum_o w[i][o] b[i][o]
+ * with colpart[i] = sum_t x[t][i] a[t][i] (written to colpart, [c_in] f64
+ * caller scratch): x, a [T][c_in] f64 (the batch's raw rows and A), w, b
+ * [c_in][c_out] f64 (W and B), smooth [c_in] f32 (the factors used in the
+ * forward pass), grad [c_in] f64.  Sums run in increasing t and in a fixed
+ * lane order over o.
+ *
+ * Pointers 16-byte (dequantize) or 8-byte (the others) aligned; violations
+ * return an error before anything is enqueued.
+ */
+masq_status masq_dequantize_rows(const int8_t* codes, const float* scale, int64_t rows,
+                                 int64_t cols, double* out, void* stream);
+int64_t masq_mae_partials(int64_t count);
+masq_status masq_mae_sign(const double* y, const double* ref, int64_t count, double* g,
+                          double* partial, void* stream);
+masq_status masq_mas_gradient(const double* x, const double* a, const double* w, const double* b,
+                              const float* smooth, int64_t T, int64_t c_in, int64_t c_out,
+                              double* colpart, double* grad, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -298,6 +298,78 @@ __global__ __launch_bounds__(256) void k_dgemm(int64_t M, int64_t N, int64_t K,
     }
 }
 
+// ------------------------------------------------------- MAS optimisation
+// The per-modality objective mean |Q(X S^-1) Q(S W) - X W| (Sec. 4.2, eq.
+// mas_quant) and its straight-through gradient: the quantizers are the
+// inference ones above; these kernels dequantize their codes, take the
+// residual's sign and assemble dL/ds from the two products of the backward
+// pass (formed with k_dgemm).
+
+// out [R][C] fp64 = codes [R][C] * scale[r] (exact: 8 x 24 significant bits).
+__global__ __launch_bounds__(256) void k_dequantize_rows(const int8_t* __restrict__ codes,
+                                                         const float* __restrict__ scale,
+                                                         int64_t R, int64_t C,
+                                                         double* __restrict__ out) {
+    const int64_t n = R * C;
+    for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < n; e += gridDim.x * 256ll)
+        out[e] = static_cast<double>(codes[e]) * static_cast<double>(scale[e / C]);
+}
+
+// g_e = sign(y_e - ref_e) * inv_count; partial[b] = the sum of |y_e - ref_e|
+// over block b's kMaeChunk elements (a fixed tree order, so the loss the
+// caller adds up is reproducible).
+constexpr int kMaeChunk = 4096;
+__global__ __launch_bounds__(256) void k_mae_sign(const double* __restrict__ y,
+                                                  const double* __restrict__ ref, int64_t n,
+                                                  double inv_count, double* __restrict__ g,
+                                                  double* __restrict__ partial) {
+    __shared__ double red[4];
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kMaeChunk;
+    double acc = 0.0;
+    for (int j = threadIdx.x; j < kMaeChunk; j += 256) {
+        const int64_t e = base + j;
+        if (e >= n) break;
+        const double r = y[e] - ref[e];
+        g[e] = r > 0.0 ? inv_count : (r < 0.0 ? -inv_count : 0.0);
+        acc += fabs(r);
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) partial[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// colpart[i] = sum_t x[t][i] a[t][i] (thread per column, t in order).
+__global__ __launch_bounds__(256) void k_column_dot(const double* __restrict__ x,
+                                                    const double* __restrict__ a, int64_t T,
+                                                    int64_t K, double* __restrict__ out) {
+    const int64_t i = blockIdx.x * 256ll + threadIdx.x;
+    if (i >= K) return;
+    double acc = 0.0;
+    for (int64_t t = 0; t < T; ++t) acc = fma(x[t * K + i], a[t * K + i], acc);
+    out[i] = acc;
+}
+
+// grad[i] = -colpart[i] / (s_i s_i) + sum_o w[i][o] b[i][o] (a wave per row i).
+__global__ __launch_bounds__(256) void k_mas_grad(const double* __restrict__ colpart,
+                                                  const double* __restrict__ w,
+                                                  const double* __restrict__ b,
+                                                  const float* __restrict__ s, int64_t K,
+                                                  int64_t N, double* __restrict__ grad) {
+    const int lane = threadIdx.x & 63;
+    const int64_t i = blockIdx.x * 4ll + (threadIdx.x >> 6);
+    if (i >= K) return;
+    double acc = 0.0;
+    for (int64_t o = lane; o < N; o += 64) acc = fma(w[i * N + o], b[i * N + o], acc);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o);
+    if (lane == 0) {
+        const double si = static_cast<double>(s[i]);
+        grad[i] = -colpart[i] / (si * si) + acc;
+    }
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
 
@@ -428,6 +500,55 @@ masq_status masq_dgemm(int64_t m, int64_t n, int64_t k, const double* a, int64_t
                     static_cast<unsigned>((m + kDgTile - 1) / kDgTile));
     hipLaunchKernelGGL(k_dgemm, grid, dim3(256), 0, static_cast<hipStream_t>(stream), m, n, k, a,
                        a_row_stride, a_col_stride, b, b_row_stride, b_col_stride, beta, c, ldc);
+    return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
+}
+
+masq_status masq_dequantize_rows(const int8_t* codes, const float* scale, int64_t rows,
+                                 int64_t cols, double* out, void* stream) {
+    if (rows < 0 || cols < 0 || (cols > 0 && rows > (1LL << 40) / cols)) return MASQ_ERR_SHAPE;
+    if (rows == 0 || cols == 0) return MASQ_OK;
+    if (!codes || !scale || !out) return MASQ_ERR_NULL;
+    if (!aligned16(codes) || !aligned16(scale) || !aligned16(out)) return MASQ_ERR_ALIGN;
+    (void)hipGetLastError();
+    const int64_t n = rows * cols;
+    const int64_t blocks = (n + 255) / 256 < 8192 ? (n + 255) / 256 : 8192;
+    hipLaunchKernelGGL(k_dequantize_rows, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                       static_cast<hipStream_t>(stream), codes, scale, rows, cols, out);
+    return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
+}
+
+int64_t masq_mae_partials(int64_t count) {
+    return count <= 0 ? 0 : (count + kMaeChunk - 1) / kMaeChunk;
+}
+
+masq_status masq_mae_sign(const double* y, const double* ref, int64_t count, double* g,
+                          double* partial, void* stream) {
+    if (count < 0 || masq_mae_partials(count) > 0x7fffffffLL) return MASQ_ERR_SHAPE;
+    if (count == 0) return MASQ_OK;
+    if (!y || !ref || !g || !partial) return MASQ_ERR_NULL;
+    if (!aligned8(y) || !aligned8(ref) || !aligned8(g) || !aligned8(partial)) return MASQ_ERR_ALIGN;
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(k_mae_sign, dim3(static_cast<unsigned>(masq_mae_partials(count))), dim3(256),
+                       0, static_cast<hipStream_t>(stream), y, ref, count,
+                       1.0 / static_cast<double>(count), g, partial);
+    return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
+}
+
+masq_status masq_mas_gradient(const double* x, const double* a, const double* w, const double* b,
+                              const float* smooth, int64_t T, int64_t c_in, int64_t c_out,
+                              double* colpart, double* grad, void* stream) {
+    if (T < 0 || c_in <= 0 || c_out <= 0 || c_in > (1LL << 30) || c_out > (1LL << 30))
+        return MASQ_ERR_SHAPE;
+    if (!w || !b || !smooth || !colpart || !grad || (T > 0 && (!x || !a))) return MASQ_ERR_NULL;
+    if (!aligned8(w) || !aligned8(b) || !aligned8(smooth) || !aligned8(colpart) ||
+        !aligned8(grad) || (T > 0 && (!aligned8(x) || !aligned8(a))))
+        return MASQ_ERR_ALIGN;
+    (void)hipGetLastError();
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipLaunchKernelGGL(k_column_dot, dim3(static_cast<unsigned>((c_in + 255) / 256)), dim3(256), 0,
+                       st, x, a, T, c_in, colpart);
+    hipLaunchKernelGGL(k_mas_grad, dim3(static_cast<unsigned>((c_in + 3) / 4)), dim3(256), 0, st,
+                       colpart, w, b, smooth, c_in, c_out, grad);
     return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
 }
 

@@ -1,0 +1,98 @@
+"""MAS factor optimisation on the GPU (Sec. 4.2, eq. mas_quant).
+
+For each modality m, starting from the MAS initial factors, minimise
+
+    L(S_m) = mean | Q(X_m S_m^-1) Q(S_m W) - X_m W |
+
+over the calibration rows of m, with the inference quantizers in the
+forward pass (masq_smooth_quant: per-token int8 of the fp32 smoothed row;
+masq_quantize_weight: per-output-channel b-bit Q(S_m W)) and the
+straight-through estimator in the backward pass.  The factors are optimised
+in log space (s = exp(theta)) with Adam, one step per batch of rows, for
+`epochs` passes (2, as in the paper's ablation), each modality's gradient
+scaled by its loss weight lambda_m (1, as in the paper).  Every product,
+quantizer and reduction of a step runs in the library's kernels; the Adam
+update of the K-vector theta runs on the host.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def _adam(theta, m1, m2, g, step, lr, b1=0.9, b2=0.999, eps=1e-8):
+    m1 = b1 * m1 + (1 - b1) * g
+    m2 = b2 * m2 + (1 - b2) * g * g
+    return theta - lr * (m1 / (1 - b1 ** step)) / (np.sqrt(m2 / (1 - b2 ** step)) + eps), m1, m2
+
+
+class _Step:
+    """One modality's forward and straight-through backward pass on a batch."""
+
+    def __init__(self, xb, w64, wt, bits):
+        import torch
+
+        from . import ops
+        self.ops, self.torch = ops, torch
+        self.xb, self.wt, self.w64, self.bits = xb, wt, w64, bits
+        dev = xb.device
+        ones = torch.ones(xb.shape[1], dtype=torch.float32, device=dev)
+        self.x64 = ops.gather_smoothed(xb, torch.arange(xb.shape[0], dtype=torch.int32,
+                                                        device=dev), ones)
+        self.ref = ops.dgemm(self.x64, w64)                  # X W, fp64
+        self.mod0 = torch.zeros(xb.shape[0], dtype=torch.int32, device=dev)
+
+    def __call__(self, s32: np.ndarray):
+        """(loss, dL/ds) at the factors s32 [K] (float32)."""
+        ops, torch = self.ops, self.torch
+        dev = self.xb.device
+        s_t = torch.from_numpy(np.ascontiguousarray(s32, np.float32)).to(dev)
+        inv = torch.from_numpy((np.float32(1.0) / s32).astype(np.float32)[None, :]).to(dev)
+        q, delta = ops.smooth_quant(self.xb, self.mod0, inv)
+        wq, wd = ops.quantize_weight(self.wt, s_t, bits=self.bits)
+        xq = ops.dequantize_rows(q, delta)                   # [T][K]
+        wq_t = ops.dequantize_rows(wq, wd)                   # Wq^T [N][K]
+        g, loss = ops.mae_sign(ops.dgemm(xq, wq_t.T), self.ref)
+        a = ops.dgemm(g, wq_t)                               # G Wq^T  [T][K]
+        b = ops.dgemm(xq.T, g)                               # Xq^T G  [K][N]
+        grad = ops.mas_gradient(self.x64, a, self.w64, b, s_t)
+        return loss, grad.cpu().numpy()
+
+
+def optimise(x, modality, w, s_init, lam=None, epochs: int = 2, batch: int = 256,
+             lr: float = 1e-2, bits: int = 8, device: str = "cuda:0"):
+    """Optimised factors s32 [M][K] (float32) and each modality's per-step
+    losses.  x [T][K] float32 calibration rows, modality [T] ids, w [K][N]
+    float32 weight (paper layout), s_init [M][K] the MAS initial factors."""
+    import torch
+    x = np.asarray(x, np.float32)
+    modality = np.asarray(modality)
+    s_init = np.asarray(s_init, np.float32)
+    n_mod = s_init.shape[0]
+    lam = np.ones(n_mod) if lam is None else np.asarray(lam, np.float64)
+    dev = torch.device(device)
+    wt = torch.from_numpy(np.ascontiguousarray(w, np.float32)).to(dev)
+    w64 = wt.double()
+    out = s_init.copy()
+    losses = []
+    for m in range(n_mod):
+        rows = x[modality == m]
+        hist = []
+        if rows.shape[0] == 0 or lam[m] == 0:
+            losses.append(hist)
+            continue
+        steps = [_Step(torch.from_numpy(np.ascontiguousarray(rows[b0:b0 + batch])).to(dev),
+                       w64, wt, bits) for b0 in range(0, rows.shape[0], batch)]
+        theta = np.log(s_init[m].astype(np.float64))
+        m1 = np.zeros_like(theta)
+        m2 = np.zeros_like(theta)
+        k = 0
+        for _ in range(epochs):
+            for st in steps:
+                s32 = np.exp(theta).astype(np.float32)
+                loss, g = st(s32)
+                hist.append(loss)
+                k += 1
+                theta, m1, m2 = _adam(theta, m1, m2, lam[m] * s32.astype(np.float64) * g, k, lr)
+        out[m] = np.exp(theta).astype(np.float32)
+        losses.append(hist)
+    return out, losses

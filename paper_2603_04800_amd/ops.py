@@ -52,6 +52,10 @@ _SIGS = {
     "masq_weight_difference": ([_p, _p, _p, _p, _i64, _i64, _p, _p], ctypes.c_int),
     "masq_dgemm": ([_i64, _i64, _i64, _p, _i64, _i64, _p, _i64, _i64, ctypes.c_double, _p, _i64,
                     _p], ctypes.c_int),
+    "masq_dequantize_rows": ([_p, _p, _i64, _i64, _p, _p], ctypes.c_int),
+    "masq_mae_partials": ([_i64], _i64),
+    "masq_mae_sign": ([_p, _p, _i64, _p, _p, _p], ctypes.c_int),
+    "masq_mas_gradient": ([_p, _p, _p, _p, _p, _i64, _i64, _i64, _p, _p, _p], ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -255,6 +259,50 @@ def dgemm(a, b, c=None, beta=0.0, stream=None):
         m, n, k, _view_ptr(a), a.stride(0), a.stride(1), _view_ptr(b), b.stride(0), b.stride(1),
         float(beta), _ptr(c), n, _stream(stream)))
     return c
+
+
+def dequantize_rows(codes, scale, stream=None):
+    """codes [R][C] int8 times scale [R] f32, as fp64 [R][C] (exact)."""
+    _need(codes, torch.int8, "codes")
+    _need(scale, torch.float32, "scale")
+    R, C = codes.shape
+    out = torch.empty((R, C), dtype=torch.float64, device=codes.device)
+    _check("masq_dequantize_rows", _lib.masq_dequantize_rows(
+        _ptr(codes), _ptr(scale), R, C, _ptr(out), _stream(stream)))
+    return out
+
+
+def mae_sign(y, ref, stream=None):
+    """(G = sign(y - ref) / count, mean |y - ref|) for fp64 tensors of one
+    shape; the loss is added on the host from fixed-order block sums."""
+    _need(y, torch.float64, "y")
+    _need(ref, torch.float64, "ref")
+    if y.shape != ref.shape:
+        raise ValueError("y and ref differ in shape")
+    n = y.numel()
+    g = torch.empty_like(y)
+    part = torch.empty((max(int(_lib.masq_mae_partials(n)), 1),), dtype=torch.float64,
+                       device=y.device)
+    _check("masq_mae_sign", _lib.masq_mae_sign(_ptr(y), _ptr(ref), n, _ptr(g), _ptr(part),
+                                               _stream(stream)))
+    loss = float(part[:int(_lib.masq_mae_partials(n))].cpu().numpy().sum()) / n if n else 0.0
+    return g, loss
+
+
+def mas_gradient(x, a, w, b, smooth, stream=None):
+    """dL/ds [K] fp64 of the MAS objective from the batch's rows x [T][K],
+    A [T][K], W [K][N], B [K][N] (fp64) and the factors s [K] f32."""
+    T, K = x.shape
+    N = w.shape[1]
+    for t, name in ((x, "x"), (a, "a"), (w, "w"), (b, "b")):
+        _need(t, torch.float64, name)
+    _need(smooth, torch.float32, "smooth")
+    colpart = torch.empty((K,), dtype=torch.float64, device=w.device)
+    grad = torch.empty((K,), dtype=torch.float64, device=w.device)
+    _check("masq_mas_gradient", _lib.masq_mas_gradient(
+        _ptr(x), _ptr(a), _ptr(w), _ptr(b), _ptr(smooth), T, K, N, _ptr(colpart), _ptr(grad),
+        _stream(stream)))
+    return grad
 
 
 def workspace_bytes(T, K, N, rank, n_mod) -> int:

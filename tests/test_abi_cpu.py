@@ -208,3 +208,26 @@ def test_cmc_calibration_calls_validate(lib):
     assert dg(4, 4, 0, None, 0, 0, None, 0, 0, one, None, 4, None) == 1   # k = 0 still writes c
     assert dg(4, 4, 4, P + 4, 4, 1, P, 4, 1, one, P, 4, None) == 4    # misaligned A
     assert dg(0, 4, 4, None, 4, 1, None, 4, 1, one, None, 4, None) == 0   # empty output
+
+
+def test_mas_optimisation_calls_validate(lib):
+    """masq_dequantize_rows, masq_mae_sign and masq_mas_gradient check their
+    arguments before enqueueing anything; masq_mae_partials is plain host
+    arithmetic."""
+    P = 1 << 20
+    dq, ms, mg = lib.masq_dequantize_rows, lib.masq_mae_sign, lib.masq_mas_gradient
+    assert dq(P, P, -1, 4, P, None) == 2                         # rows < 0
+    assert dq(None, P, 4, 4, P, None) == 1                       # no codes
+    assert dq(P, P, 4, 4, P + 8, None) == 4                      # misaligned output
+    assert dq(None, None, 0, 4, None, None) == 0                 # empty
+    assert lib.masq_mae_partials(0) == 0
+    assert lib.masq_mae_partials(1) == 1
+    assert lib.masq_mae_partials(4096) == 1
+    assert lib.masq_mae_partials(4097) == 2
+    assert ms(P, P, -1, P, P, None) == 2
+    assert ms(P, None, 8, P, P, None) == 1
+    assert ms(P, P, 8, P + 4, P, None) == 4
+    assert ms(None, None, 0, None, None, None) == 0
+    assert mg(P, P, P, P, P, 4, 0, 16, P, P, None) == 2          # c_in = 0
+    assert mg(P, P, P, None, P, 4, 16, 16, P, P, None) == 1      # no B
+    assert mg(P, P, P, P, P, 4, 16, 16, P, P + 4, None) == 4     # misaligned grad
