@@ -255,6 +255,9 @@ def dgemm(a, b, c=None, beta=0.0, stream=None):
     _need(c, torch.float64, "c")
     if tuple(c.shape) != (m, n):
         raise ValueError(f"c must be [{m}][{n}]")
+    if c.numel() and any(t.numel() and t.untyped_storage().data_ptr() ==
+                         c.untyped_storage().data_ptr() for t in (a, b)):
+        raise ValueError("c must not share memory with a or b")
     _check("masq_dgemm", _lib.masq_dgemm(
         m, n, k, _view_ptr(a), a.stride(0), a.stride(1), _view_ptr(b), b.stride(0), b.stride(1),
         float(beta), _ptr(c), n, _stream(stream)))

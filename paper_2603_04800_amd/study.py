@@ -95,7 +95,6 @@ def cmc_study(workload: int, ranks=None, weight_bits: int = 4, device: str = "cu
                          whitened=round(effective_rank(_singular_values_gpu(wh.apply(dw))), 2)))
         del z, dw, wh
     # SQNR against the rank ratio: the factors at the largest rank, truncated
-    lr = torch.bfloat16 if cfg.lr_dtype == "bf16" else torch.float32
     for whiten in (True, False):
         art = calibrate.calibrate_layer_gpu(x, mod, w, cfg.n_mod, top, "f32",
                                             weight_bits=weight_bits, device=device,
@@ -105,10 +104,7 @@ def cmc_study(workload: int, ranks=None, weight_bits: int = 4, device: str = "cu
                 continue
             a = dict(art, l_down=art["l_down"][:, :r], r_up=np.ascontiguousarray(art["r_up"][:, :, :r]),
                      lr_dtype=cfg.lr_dtype)
-            lin = ops.Linear.from_arrays(a, device)
-            if lin.l_down.dtype != lr:
-                raise RuntimeError("factor dtype")
-            y = lin(xt, mt, out_dtype=torch.float32)
+            y = ops.Linear.from_arrays(a, device)(xt, mt, out_dtype=torch.float32)
             sqnr_row(y, method="masquant" if r else "shared weight, rank 0",
                      whitened=whiten if r else None, rank=r,
                      rank_ratio=round(r / min(k, n), 4))

@@ -231,3 +231,14 @@ def test_mas_optimisation_calls_validate(lib):
     assert mg(P, P, P, P, P, 4, 0, 16, P, P, None) == 2          # c_in = 0
     assert mg(P, P, P, None, P, 4, 16, 16, P, P, None) == 1      # no B
     assert mg(P, P, P, P, P, 4, 16, 16, P, P + 4, None) == 4     # misaligned grad
+
+
+def test_dgemm_binding_refuses_an_output_aliasing_an_input():
+    import torch
+    from paper_2603_04800_amd import ops
+    a = torch.zeros((4, 4), dtype=torch.float64)
+    with pytest.raises(ValueError, match="share memory"):
+        ops.dgemm(a, a, c=a)
+    b = torch.zeros((4, 4), dtype=torch.float64)
+    with pytest.raises(ValueError, match="share memory"):
+        ops.dgemm(b.T, a, c=b)
