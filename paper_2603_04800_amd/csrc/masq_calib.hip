@@ -212,57 +212,62 @@ __global__ __launch_bounds__(256) void k_weight_difference(const float* __restri
 
 // C [m][n] (row stride ldc) = A B (+ beta C), fp64, with A (i, k) at
 // a[i * ars + k * acs] and B (k, j) at b[k * brs + j * bcs], so transposed
-// operands are strides, not copies.  128 x 128 tiles, 256 threads of 8 x 8
+// operands are strides, not copies.  TL x TL tiles (128, or 64 when the
+// 128-tiles would not give every CU one), 256 threads of TL/16 x TL/16
 // outputs (rows ty + 16 u, columns tx + 16 v), k in steps of 16 staged
 // through LDS with the next step's loads in flight.  Every element is summed
-// in increasing k by fused multiply-adds; beta C is added after.
+// in increasing k by fused multiply-adds, whatever the tile size; beta C is
+// added after.
 constexpr int kDgTile = 128;
 constexpr int kDgStep = 16;
+template <int TL>
 __global__ __launch_bounds__(256) void k_dgemm(int64_t M, int64_t N, int64_t K,
                                                const double* __restrict__ a, int64_t ars,
                                                int64_t acs, const double* __restrict__ b,
                                                int64_t brs, int64_t bcs, double beta,
                                                double* __restrict__ c, int64_t ldc) {
-    __shared__ double as[kDgStep][kDgTile + 1];
-    __shared__ double bs[kDgStep][kDgTile + 1];
+    constexpr int NU = TL / 16, NQ = TL * kDgStep / 256;     // outputs a row, loads per operand
+    constexpr int LT = TL == 128 ? 7 : 6;                    // log2(TL)
+    __shared__ double as[kDgStep][TL + 1];
+    __shared__ double bs[kDgStep][TL + 1];
     const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
-    const int64_t i0 = static_cast<int64_t>(blockIdx.y) * kDgTile;
-    const int64_t j0 = static_cast<int64_t>(blockIdx.x) * kDgTile;
-    // staging: element e = tid + 256 q of each 128 x 16 operand block; the
+    const int64_t i0 = static_cast<int64_t>(blockIdx.y) * TL;
+    const int64_t j0 = static_cast<int64_t>(blockIdx.x) * TL;
+    // staging: element e = tid + 256 q of each TL x 16 operand block; the
     // fastest-moving index follows the operand's unit-stride direction
     const bool a_k_fast = acs == 1, b_k_fast = bcs != 1;
-    double ra[8], rb[8];
+    double ra[NQ], rb[NQ];
     auto load = [&](int64_t k0) __attribute__((always_inline)) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
+        for (int q = 0; q < NQ; ++q) {
             const int e = tid + 256 * q;
-            const int kk = a_k_fast ? (e & 15) : (e >> 7);
-            const int ii = a_k_fast ? (e >> 4) : (e & 127);
+            const int kk = a_k_fast ? (e & 15) : (e >> LT);
+            const int ii = a_k_fast ? (e >> 4) : (e & (TL - 1));
             const int64_t i = i0 + ii, k = k0 + kk;
             ra[q] = (i < M && k < K) ? a[i * ars + k * acs] : 0.0;
         }
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
+        for (int q = 0; q < NQ; ++q) {
             const int e = tid + 256 * q;
-            const int kk = b_k_fast ? (e & 15) : (e >> 7);
-            const int jj = b_k_fast ? (e >> 4) : (e & 127);
+            const int kk = b_k_fast ? (e & 15) : (e >> LT);
+            const int jj = b_k_fast ? (e >> 4) : (e & (TL - 1));
             const int64_t j = j0 + jj, k = k0 + kk;
             rb[q] = (j < N && k < K) ? b[k * brs + j * bcs] : 0.0;
         }
     };
     auto stash = [&]() __attribute__((always_inline)) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
+        for (int q = 0; q < NQ; ++q) {
             const int e = tid + 256 * q;
-            as[a_k_fast ? (e & 15) : (e >> 7)][a_k_fast ? (e >> 4) : (e & 127)] = ra[q];
-            bs[b_k_fast ? (e & 15) : (e >> 7)][b_k_fast ? (e >> 4) : (e & 127)] = rb[q];
+            as[a_k_fast ? (e & 15) : (e >> LT)][a_k_fast ? (e >> 4) : (e & (TL - 1))] = ra[q];
+            bs[b_k_fast ? (e & 15) : (e >> LT)][b_k_fast ? (e >> 4) : (e & (TL - 1))] = rb[q];
         }
     };
-    double acc[8][8];
+    double acc[NU][NU];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
+    for (int u = 0; u < NU; ++u)
 #pragma unroll
-        for (int v = 0; v < 8; ++v) acc[u][v] = 0.0;
+        for (int v = 0; v < NU; ++v) acc[u][v] = 0.0;
     if (K > 0) load(0);
     for (int64_t k0 = 0; k0 < K; k0 += kDgStep) {
         __syncthreads();
@@ -271,23 +276,23 @@ __global__ __launch_bounds__(256) void k_dgemm(int64_t M, int64_t N, int64_t K,
         if (k0 + kDgStep < K) load(k0 + kDgStep);
 #pragma unroll 4
         for (int kk = 0; kk < kDgStep; ++kk) {
-            double av[8], bv[8];
+            double av[NU], bv[NU];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) av[u] = as[kk][ty + 16 * u];
+            for (int u = 0; u < NU; ++u) av[u] = as[kk][ty + 16 * u];
 #pragma unroll
-            for (int v = 0; v < 8; ++v) bv[v] = bs[kk][tx + 16 * v];
+            for (int v = 0; v < NU; ++v) bv[v] = bs[kk][tx + 16 * v];
 #pragma unroll
-            for (int u = 0; u < 8; ++u)
+            for (int u = 0; u < NU; ++u)
 #pragma unroll
-                for (int v = 0; v < 8; ++v) acc[u][v] = fma(av[u], bv[v], acc[u][v]);
+                for (int v = 0; v < NU; ++v) acc[u][v] = fma(av[u], bv[v], acc[u][v]);
         }
     }
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < NU; ++u) {
         const int64_t i = i0 + ty + 16 * u;
         if (i >= M) break;
 #pragma unroll
-        for (int v = 0; v < 8; ++v) {
+        for (int v = 0; v < NU; ++v) {
             const int64_t j = j0 + tx + 16 * v;
             if (j < N) {
                 double r = acc[u][v];
@@ -496,10 +501,17 @@ masq_status masq_dgemm(int64_t m, int64_t n, int64_t k, const double* a, int64_t
     if (!c || (k > 0 && (!a || !b))) return MASQ_ERR_NULL;
     if (!aligned8(c) || (k > 0 && (!aligned8(a) || !aligned8(b)))) return MASQ_ERR_ALIGN;
     (void)hipGetLastError();
-    const dim3 grid(static_cast<unsigned>((n + kDgTile - 1) / kDgTile),
-                    static_cast<unsigned>((m + kDgTile - 1) / kDgTile));
-    hipLaunchKernelGGL(k_dgemm, grid, dim3(256), 0, static_cast<hipStream_t>(stream), m, n, k, a,
-                       a_row_stride, a_col_stride, b, b_row_stride, b_col_stride, beta, c, ldc);
+    const int64_t tiles = ((n + kDgTile - 1) / kDgTile) * ((m + kDgTile - 1) / kDgTile);
+    const int tl = (tiles < 256 && (m + 63) / 64 <= 65535) ? 64 : kDgTile;
+    const dim3 grid(static_cast<unsigned>((n + tl - 1) / tl), static_cast<unsigned>((m + tl - 1) / tl));
+    if (tl == 64)
+        hipLaunchKernelGGL(k_dgemm<64>, grid, dim3(256), 0, static_cast<hipStream_t>(stream), m, n,
+                           k, a, a_row_stride, a_col_stride, b, b_row_stride, b_col_stride, beta, c,
+                           ldc);
+    else
+        hipLaunchKernelGGL(k_dgemm<kDgTile>, grid, dim3(256), 0, static_cast<hipStream_t>(stream), m,
+                           n, k, a, a_row_stride, a_col_stride, b, b_row_stride, b_col_stride, beta,
+                           c, ldc);
     return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
 }
 

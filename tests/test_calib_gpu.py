@@ -93,6 +93,7 @@ def test_gpu_assisted_layer_calibration_equals_host(ops, cfg_index, bits):
 
 # ------------------------------------------------- compensation-factor inputs
 _U = 2.0 ** -53
+DEV_CALIB = torch.device("cuda:0")
 
 
 def _dgemm_bound(a, b):
@@ -278,3 +279,18 @@ def test_cmc_study_small_workload(ops):
     assert len(sq) == 1 + 2 + 2 + 1
     for r in sq:
         assert all(np.isfinite(v) for v in r["sqnr_db"].values()), r
+
+
+def test_dgemm_result_does_not_depend_on_the_tile_size(ops):
+    """Small grids take 64 x 64 tiles, large ones 128 x 128; each element is
+    the same increasing-k chain of fused multiply-adds either way, so a
+    block of rows computed alone (a small grid) equals the same rows of the
+    whole product (a large grid) bit for bit."""
+    rng = np.random.default_rng(33)
+    a = torch.from_numpy(rng.standard_normal((2048, 96))).to(DEV_CALIB)
+    b = torch.from_numpy(rng.standard_normal((96, 2048))).to(DEV_CALIB)
+    whole = ops.dgemm(a, b)                                  # 256 tiles of 128
+    part = ops.dgemm(a[256:384], b)                          # 16 tiles of 128: 64 x 64
+    assert torch.equal(whole[256:384], part)
+    part_t = ops.dgemm(b.T[:200], a.T)                      # transposed views, small grid
+    assert torch.equal(ops.dgemm(b.T, a.T)[:200], part_t)
