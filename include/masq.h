@@ -34,6 +34,10 @@
  *    enqueued and outputs are untouched): non-null pointers (except where
  *    marked nullable), T >= 0, c_in > 0 and c_in % 16 == 0, c_out > 0 and
  *    c_out % 16 == 0, rank == 0 or rank % 16 == 0 (rank <= 256),
+ *    for every call that accumulates (GEMM and whole layer) c_in small enough
+ *    that int32 accumulation is exact: c_in <= 133136 (= 127 * 127 * c_in
+ *    below 2^31, a multiple of 16) with int8 codes, c_in <= 150976 with the
+ *    packed 4-bit weight (127 * 112 * c_in below 2^31, a multiple of 64),
  *    1 <= n_mod <= 4, 16-byte aligned pointers, a large enough workspace.
  *    T == 0 is a successful no-op once sizes and dtypes are valid (pointers
  *    may then be NULL: nothing is read or written).

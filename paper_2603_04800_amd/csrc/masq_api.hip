@@ -115,6 +115,18 @@ masq_status check_dims(int64_t T, int64_t c_in, int64_t c_out, bool need_out) {
     return MASQ_OK;
 }
 
+// Longest rows whose int32 accumulation stays exact: |acc| <= 127 * 127 * c_in
+// for int8 codes, and 127 * 112 * c_in for the 4-bit weight (its codes enter
+// the MFMA as 16 x code, |16 x code| <= 112, and the sum is shifted back by 4),
+// each below 2^31 and rounded down to the width granularity of its path.
+constexpr int64_t kMaxCinW8 = ((((1LL << 31) - 1) / (127 * 127)) / 16) * 16;   // 133136
+constexpr int64_t kMaxCinW4 = ((((1LL << 31) - 1) / (127 * 112)) / 64) * 64;   // 150976
+static_assert(kMaxCinW8 * 127 * 127 < (1LL << 31) && kMaxCinW4 * 127 * 112 < (1LL << 31), "");
+
+masq_status check_exact_acc(int64_t c_in, bool w4) {
+    return c_in > (w4 ? kMaxCinW4 : kMaxCinW8) ? MASQ_ERR_SHAPE : MASQ_OK;
+}
+
 masq_status check_rank(int32_t rank, int32_t n_mod) {
     if (n_mod < 1 || n_mod > 4) return MASQ_ERR_SHAPE;
     if (rank < 0 || rank > masq::kMaxRank || (rank % 16) != 0) return MASQ_ERR_SHAPE;
@@ -135,6 +147,7 @@ masq_status validate_fused(const Fused& a) {
     masq_status st = check_dims(a.T, a.c_in, a.c_out, true);
     if (st != MASQ_OK) return st;
     if (a.w4 && a.c_in % 64 != 0) return MASQ_ERR_SHAPE;
+    if ((st = check_exact_acc(a.c_in, a.w4)) != MASQ_OK) return st;
     if ((st = check_rank(a.rank, a.n_mod)) != MASQ_OK) return st;
     if (!valid_dt(a.x_dt) || !valid_dt(a.y_dt) || !valid_dt(a.lr_dt)) return MASQ_ERR_DTYPE;
     if (a.T == 0) return MASQ_OK;      // empty batch: nothing is read or written
@@ -253,6 +266,7 @@ static masq_status gemm_call(const int8_t* q, const float* x_scale, const int8_t
     masq_status st = check_dims(T, c_in, c_out, true);
     if (st != MASQ_OK) return st;
     if (w4 && c_in % 64 != 0) return MASQ_ERR_SHAPE;
+    if ((st = check_exact_acc(c_in, w4)) != MASQ_OK) return st;
     if (!valid_dt(y_dt)) return MASQ_ERR_DTYPE;
     if (T == 0) return MASQ_OK;
     if (!q || !x_scale || !wq || !w_scale || (!acc && !y)) return MASQ_ERR_NULL;

@@ -118,6 +118,27 @@ def test_unfused_calls_validate(lib):
     assert lib.masq_lowrank_comp(P, 1, P, P, None, None, 1, 8, 64, 64, 0, 2, P, 1, None) == 0
 
 
+def test_accumulating_calls_refuse_rows_too_long_for_exact_int32(lib):
+    """|acc| <= 127 * 127 * c_in (int8) or 127 * 112 * c_in (4-bit codes taken
+    as 16 x code) must stay below 2^31: the longest accepted rows are 133136
+    and 150976 columns."""
+    w8, w4 = 133136, 150976
+    assert 127 * 127 * w8 < 2 ** 31 <= 127 * 127 * (w8 + 16)
+    assert 127 * 112 * w4 < 2 ** 31 <= 127 * 112 * (w4 + 64)
+    g8, g4 = lib.masq_w8a8_gemm, lib.masq_w4a8_gemm
+    assert g8(P, P, P, P, 0, w8, 64, P, None, 0, None) == 0
+    assert g8(P, P, P, P, 0, w8 + 16, 64, P, None, 0, None) == 2
+    assert g4(P, P, P, P, 0, w4, 64, P, None, 0, None) == 0
+    assert g4(P, P, P, P, 0, w4 + 64, 64, P, None, 0, None) == 2
+    assert _fused(lib, T=0, K=w8, work=None, work_bytes=0) == 0
+    assert _fused(lib, T=0, K=w8 + 16, work=None, work_bytes=0) == 2
+    assert _fused(lib, K=w8 + 16) == 2
+    assert _fused_w4(lib, T=0, K=w4, work=None, work_bytes=0) == 0
+    assert _fused_w4(lib, T=0, K=w4 + 64, work=None, work_bytes=0) == 2
+    # quantisation alone does not accumulate
+    assert lib.masq_smooth_quant(P, 1, P, P, 0, w8 + 16, 2, P, P, None) == 0
+
+
 def test_binding_refuses_host_tensors():
     import torch
     from paper_2603_04800_amd import ops

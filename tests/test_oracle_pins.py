@@ -180,6 +180,54 @@ def test_compensation_brute_force_and_routing():
             assert abs(c[t, o] - s) <= 1e-12 * (1 + abs(s))
 
 
+def _round_f32_once(v):
+    """The binary32 value nearest to the rational v, ties to even: one rounding
+    of the exact value (the nearest double's binary32 neighbours are the only
+    candidates, chosen by exact rational distance)."""
+    from fractions import Fraction
+    f = np.float32(float(v))
+    cands = [f, np.nextafter(f, np.float32(np.inf)), np.nextafter(f, np.float32(-np.inf))]
+    dist = [abs(Fraction(float(c)) - v) for c in cands]
+    best = min(dist)
+    tied = [c for c, d in zip(cands, dist) if d == best]
+    if len(tied) > 1:
+        tied = [c for c in tied if int(c.view(np.uint32)) % 2 == 0]
+    return np.float32(tied[0])
+
+
+def test_lowrank_comp_brute_force_one_rounding():
+    """The reference of the standalone compensation call (Sec. 4.3, final case
+    equation): text rows of y_in come back bit for bit; a row of modality m is
+    y_in + (xs L1^m) L2^m computed exactly in rationals, with xs = fl(x inv_s)
+    in float32 scalars, and rounded once to binary32."""
+    from fractions import Fraction
+    rng = np.random.default_rng(11)
+    T, K, N, r, M = 9, 8, 6, 2, 3
+    x = (rng.standard_normal((T, K)) * 3).astype(np.float32)
+    mod = np.array([0, 1, 2, 0, 2, 1, 1, 0, 2], np.int32)
+    inv = rng.uniform(0.2, 3, (M, K)).astype(np.float32)
+    ld = rng.standard_normal((M - 1, r, K)).astype(np.float32)
+    ru = rng.standard_normal((M - 1, N, r)).astype(np.float32)
+    y_in = rng.standard_normal((T, N)).astype(np.float32)
+    out = inf.lowrank_comp(x, mod, inv, ld, ru, y_in)
+    assert out.dtype == np.float32 and out.shape == (T, N)
+    twice = 0                         # elements where rounding the term first would differ
+    for t in range(T):
+        m = int(mod[t])
+        if m == 0:
+            assert np.array_equal(out[t].view(np.uint32), y_in[t].view(np.uint32))
+            continue
+        xs = [Fraction(float(np.float32(x[t, i]) * np.float32(inv[m, i]))) for i in range(K)]
+        u = [sum(xs[i] * Fraction(float(ld[m - 1, k, i])) for i in range(K)) for k in range(r)]
+        for o in range(N):
+            c = sum(u[k] * Fraction(float(ru[m - 1, o, k])) for k in range(r))
+            ref = _round_f32_once(Fraction(float(y_in[t, o])) + c)
+            assert out[t, o].view(np.uint32) == ref.view(np.uint32), (t, o)
+            alt = _round_f32_once(Fraction(float(y_in[t, o])) + Fraction(float(np.float32(float(c)))))
+            twice += int(alt.view(np.uint32) != ref.view(np.uint32))
+    assert twice > 0, "the case does not tell one rounding from two"
+
+
 def test_text_rows_equal_the_plain_w8a8_product():
     rng = np.random.default_rng(10)
     T, K, N = 12, 64, 40
