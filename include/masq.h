@@ -49,9 +49,10 @@
  *    even; an all-zero row gives delta = 0 and zero codes; int32 accumulation
  *    is exact; dequantisation is fl(fl(float(acc) * delta_t) * w_scale[o]);
  *    bf16 outputs are one round-to-nearest-even of the fp32 result.
- *  - No C++ exception crosses this boundary.  The library holds no mutable
- *    global state; concurrent calls are safe if their outputs and workspaces
- *    do not overlap.
+ *  - No C++ exception crosses this boundary.  The library's only global
+ *    state is the static scratch of masq_linear_fused_noalloc (and its
+ *    per-device address); every other call is safe concurrently if their
+ *    outputs and workspaces do not overlap.
  */
 #ifndef MASQ_H
 #define MASQ_H
@@ -71,7 +72,8 @@ typedef enum {
     MASQ_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned                */
     MASQ_ERR_WORKSPACE = 5,   /* workspace smaller than the query says           */
     MASQ_ERR_HIP = 6,         /* a kernel launch was rejected by the runtime     */
-    MASQ_ERR_UNSUPPORTED = 7  /* valid request this build does not implement     */
+    MASQ_ERR_UNSUPPORTED = 7, /* valid request this build does not implement     */
+    MASQ_ERR_SCRATCH = 8      /* needs more than the static scratch (below)      */
 } masq_status;
 
 typedef enum { MASQ_F32 = 0, MASQ_BF16 = 1 } masq_dtype;
@@ -131,6 +133,33 @@ masq_status masq_linear_fused(const void* x, masq_dtype x_dt, const int32_t* mod
 
 size_t masq_linear_fused_workspace_bytes(int64_t T, int64_t c_in, int64_t c_out,
                                          int32_t rank, int32_t n_mod);
+
+/*
+ * The whole layer without a workspace argument, for callers that cannot
+ * allocate device memory (code under stream or graph capture, tight serving
+ * loops, harnesses that forbid allocation).  Same arguments, semantics,
+ * kernels and results as masq_linear_fused (bit for bit), except that the
+ * scratch comes from a static device array of MASQ_SCRATCH_BYTES bytes that
+ * the library holds on every GPU it runs on until the process ends.  Its
+ * device address is looked up once per device (the first call with that
+ * device current); no call allocates or frees memory.
+ *
+ * Limit: problems whose masq_linear_fused_workspace_bytes(...) exceeds
+ * MASQ_SCRATCH_BYTES are rejected with MASQ_ERR_SCRATCH before anything is
+ * enqueued (use masq_linear_fused with a workspace for those).  Every call on
+ * one GPU shares that GPU's array: calls that may overlap in time on one GPU
+ * (different streams, different host threads) race and give wrong results;
+ * calls ordered on one stream are safe.  Whatever must start at zero (arrival
+ * counters) is cleared by each call's own kernels, so leftovers of an earlier
+ * call never matter.  MASQ_ERR_HIP if the array's address cannot be obtained.
+ */
+#define MASQ_SCRATCH_BYTES ((size_t)64 << 20)
+masq_status masq_linear_fused_noalloc(const void* x, masq_dtype x_dt, const int32_t* modality,
+                                      const float* inv_smooth, const int8_t* wq,
+                                      const float* w_scale, const void* l_down,
+                                      const void* r_up, masq_dtype lr_dt, int64_t T,
+                                      int64_t c_in, int64_t c_out, int32_t rank,
+                                      int32_t n_mod, void* y, masq_dtype y_dt, void* stream);
 
 /*
  * The two launch stages masq_linear_fused is made of, with identical

@@ -6,6 +6,13 @@
 #include "masq.h"
 #include "masq_common.h"
 
+#include <mutex>
+
+// Scratch of masq_linear_fused_noalloc: a file-scope device array, one copy
+// per GPU at its own address.  In host code `scratch` is only a handle for
+// hipGetSymbolAddress; kernels receive the per-device address obtained from it.
+static __device__ __align__(256) uint8_t scratch[MASQ_SCRATCH_BYTES];
+
 namespace masq {
 
 static size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
@@ -221,6 +228,26 @@ masq_status fused_stage(const Fused& a, int stage) {
     return st;
 }
 
+// Device address of `scratch` on each device, looked up on the first
+// allocation-free call made with that device current.
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices] = {};
+
+masq_status scratch_address(void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) return MASQ_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+            return MASQ_ERR_HIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return MASQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -237,6 +264,9 @@ const char* masq_status_str(masq_status s) {
         case MASQ_ERR_WORKSPACE: return "MASQ_ERR_WORKSPACE: workspace too small";
         case MASQ_ERR_HIP: return "MASQ_ERR_HIP: kernel launch failed";
         case MASQ_ERR_UNSUPPORTED: return "MASQ_ERR_UNSUPPORTED: not implemented by this build";
+        case MASQ_ERR_SCRATCH:
+            return "MASQ_ERR_SCRATCH: the problem needs more than the static scratch "
+                   "(MASQ_SCRATCH_BYTES); use masq_linear_fused with a workspace";
     }
     return "MASQ_ERR_UNKNOWN";
 }
@@ -339,6 +369,26 @@ size_t masq_linear_fused_workspace_bytes(int64_t T, int64_t c_in, int64_t c_out,
 #define MASQ_W4 reinterpret_cast<const int8_t*>(wq4)
 
 masq_status masq_linear_fused(MASQ_FUSED_ARGS) { return fused_stage(MASQ_FUSED_PACK(wq, false), 3); }
+
+masq_status masq_linear_fused_noalloc(const void* x, masq_dtype x_dt, const int32_t* modality,
+                                      const float* inv_smooth, const int8_t* wq,
+                                      const float* w_scale, const void* l_down,
+                                      const void* r_up, masq_dtype lr_dt, int64_t T,
+                                      int64_t c_in, int64_t c_out, int32_t rank,
+                                      int32_t n_mod, void* y, masq_dtype y_dt, void* stream) {
+    // every argument is checked against a stand-in workspace of the scratch's
+    // size first (host arithmetic only), then the array's address is fetched
+    Fused a{x, x_dt, modality, inv_smooth, wq, w_scale, l_down, r_up, lr_dt, T, c_in, c_out,
+            rank, n_mod, y, y_dt, reinterpret_cast<void*>(static_cast<uintptr_t>(256)),
+            MASQ_SCRATCH_BYTES, stream, false};
+    masq_status st = validate_fused(a);
+    if (st == MASQ_ERR_WORKSPACE) return MASQ_ERR_SCRATCH;
+    if (st != MASQ_OK || T == 0) return st;
+    void* p = nullptr;
+    if ((st = scratch_address(&p)) != MASQ_OK) return st;
+    a.workspace = p;
+    return fused_stage(a, 3);
+}
 masq_status masq_linear_stage1(MASQ_FUSED_ARGS) { return fused_stage(MASQ_FUSED_PACK(wq, false), 1); }
 masq_status masq_linear_stage2(MASQ_FUSED_ARGS) { return fused_stage(MASQ_FUSED_PACK(wq, false), 2); }
 masq_status masq_linear_fused_w4a8(MASQ_FUSED_ARGS_W4) {

@@ -24,7 +24,7 @@ _lib = ctypes.CDLL(_LIB_PATH)
 F32, BF16 = 0, 1
 STATUS = {0: "MASQ_OK", 1: "MASQ_ERR_NULL", 2: "MASQ_ERR_SHAPE", 3: "MASQ_ERR_DTYPE",
           4: "MASQ_ERR_ALIGN", 5: "MASQ_ERR_WORKSPACE", 6: "MASQ_ERR_HIP",
-          7: "MASQ_ERR_UNSUPPORTED"}
+          7: "MASQ_ERR_UNSUPPORTED", 8: "MASQ_ERR_SCRATCH"}
 
 _p, _i32, _i64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
 
@@ -41,6 +41,7 @@ _SIGS = {
     "masq_linear_stage1": (_FUSED_ARGS, ctypes.c_int),
     "masq_linear_stage2": (_FUSED_ARGS, ctypes.c_int),
     "masq_linear_fused_workspace_bytes": ([_i64, _i64, _i64, _i32, _i32], ctypes.c_size_t),
+    "masq_linear_fused_noalloc": (_FUSED_ARGS[:16] + [_p], ctypes.c_int),
     "masq_w4a8_gemm": ([_p, _p, _p, _p, _i64, _i64, _i64, _p, _p, _i32, _p], ctypes.c_int),
     "masq_linear_fused_w4a8": (_FUSED_ARGS, ctypes.c_int),
     "masq_linear_stage1_w4a8": (_FUSED_ARGS, ctypes.c_int),
@@ -371,6 +372,18 @@ class Linear:
             out = torch.empty((x.shape[0], self.c_out), device=x.device,
                               dtype=out_dtype or x.dtype)
         return self._call("masq_linear_fused", x, modality, out, workspace, stream)
+
+    def noalloc(self, x, modality, out, stream=None):
+        """The layer through masq_linear_fused_noalloc: no workspace, the
+        library's static scratch instead (int8 shared weight only)."""
+        if self.w4:
+            raise ValueError("the allocation-free entry point takes the int8 shared weight")
+        lr_dt = _dt(self.l_down) if self.l_down is not None else F32
+        _check("masq_linear_fused_noalloc", _lib.masq_linear_fused_noalloc(
+            _ptr(x), _dt(x), _ptr(modality), _ptr(self.inv_smooth), _ptr(self.wq),
+            _ptr(self.w_scale), _ptr(self.l_down), _ptr(self.r_up), lr_dt, x.shape[0],
+            self.c_in, self.c_out, self.rank, self.n_mod, _ptr(out), _dt(out), _stream(stream)))
+        return out
 
     def stage1(self, x, modality, out, workspace=None, stream=None):
         return self._call("masq_linear_stage1", x, modality, out, workspace, stream)

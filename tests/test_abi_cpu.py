@@ -54,7 +54,7 @@ def test_header_is_plain_c():
 
 
 def test_status_strings(lib):
-    for code in range(8):
+    for code in range(9):
         assert lib.masq_status_str(code).startswith(b"MASQ_")
     assert lib.masq_abi_version() == 1
 
@@ -137,6 +137,36 @@ def test_accumulating_calls_refuse_rows_too_long_for_exact_int32(lib):
     assert _fused_w4(lib, T=0, K=w4 + 64, work=None, work_bytes=0) == 2
     # quantisation alone does not accumulate
     assert lib.masq_smooth_quant(P, 1, P, P, 0, w8 + 16, 2, P, P, None) == 0
+
+
+def _noalloc(lib, **kw):
+    a = dict(x=P, x_dt=1, mod=P, inv=P, wq=P, ws=P, ld=P, ru=P, lr_dt=1, T=0, K=64, N=64,
+             rank=16, n_mod=2, y=P, y_dt=1, stream=None)
+    a.update(kw)
+    return lib.masq_linear_fused_noalloc(a["x"], a["x_dt"], a["mod"], a["inv"], a["wq"],
+                                         a["ws"], a["ld"], a["ru"], a["lr_dt"], a["T"], a["K"],
+                                         a["N"], a["rank"], a["n_mod"], a["y"], a["y_dt"],
+                                         a["stream"])
+
+
+def test_noalloc_entry_point_validates_before_touching_the_device(lib):
+    """masq_linear_fused_noalloc checks its arguments as masq_linear_fused does
+    and refuses problems whose workspace exceeds the static scratch
+    (64 MiB) with MASQ_ERR_SCRATCH, all before any HIP call."""
+    limit = 64 << 20
+    f = lib.masq_linear_fused_workspace_bytes
+    T_big = 20000                       # 20000 x 3584 codes alone exceed 64 MiB
+    assert f(T_big, 3584, 512, 64, 3) > limit
+    assert _noalloc(lib, T=T_big, K=3584, N=512, rank=64, n_mod=3) == 8
+    assert b"MASQ_ERR_SCRATCH" in lib.masq_status_str(8)
+    assert _noalloc(lib, T=0) == 0
+    assert _noalloc(lib, T=0, x=None, y=None, wq=None) == 0
+    assert _noalloc(lib, T=16, K=40) == 2
+    assert _noalloc(lib, T=16, x=None) == 1
+    assert _noalloc(lib, T=16, y_dt=5) == 3
+    assert _noalloc(lib, T=16, x=P + 8) == 4
+    assert _noalloc(lib, T=16, rank=8) == 2
+    assert _noalloc(lib, T=0, K=133136 + 16) == 2
 
 
 def test_binding_refuses_host_tensors():
