@@ -21,6 +21,9 @@ INCLUDE = os.path.join(ROOT, "include")
 LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "libmasq.so")
 SOURCES = ("masq_kernels.hip", "masq_api.hip", "masq_calib.hip")
+# the benchmark's peak probes, a library of their own (not part of the layer)
+PROBE_SOURCES = ("masq_probe.hip",)
+PROBE_LIB = os.path.join(LIBDIR, "libmasq_probe.so")
 
 
 def hipcc() -> str:
@@ -43,9 +46,15 @@ def compile_flags(remarks: bool = False):
 
 
 def build(remarks: bool = False, verbose: bool = True) -> str:
+    _build_lib(SOURCES, LIB, remarks, verbose)
+    _build_lib(PROBE_SOURCES, PROBE_LIB, remarks, verbose)
+    return LIB
+
+
+def _build_lib(sources, lib, remarks: bool, verbose: bool) -> str:
     os.makedirs(LIBDIR, exist_ok=True)
     objs = []
-    for src in SOURCES:
+    for src in sources:
         obj = os.path.join(LIBDIR, src.replace(".hip", ".o"))
         cmd = [hipcc(), *compile_flags(remarks), "-c", os.path.join(CSRC, src), "-o", obj]
         res = subprocess.run(cmd, capture_output=True, text=True)
@@ -56,15 +65,15 @@ def build(remarks: bool = False, verbose: bool = True) -> str:
         if res.returncode != 0:
             raise RuntimeError(f"hipcc failed for {src}:\n{out}")
         objs.append(obj)
-    tmp = LIB + ".tmp"
+    tmp = lib + ".tmp"
     cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{res.stdout}{res.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
     for o in objs:
         os.remove(o)
-    return LIB
+    return lib
 
 
 if __name__ == "__main__":

@@ -186,6 +186,13 @@ masq_status fused_stage(const Fused& a, int stage) {
                                                 a.n_mod, cmc, w, s));
         if (st != MASQ_OK) return st;
     } else if ((stage & 1) && cmc && masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt)) &&
+               masq::stage1_fr_ok(to_dt(a.x_dt), a.c_in, a.n_mod)) {
+        // rows held in registers: one kernel, each row read once
+        st = from_hip(masq::launch_stage1_fused(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
+                                                a.l_down, a.T, a.c_in, a.rank, a.n_mod, w.q,
+                                                w.x_scale, w.u, w.u_hl, w.zero_base, w.n_zero, s));
+        if (st != MASQ_OK) return st;
+    } else if ((stage & 1) && cmc && masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt)) &&
                w.dw_part != nullptr) {
         // large batch: wide down-projection, then quantisation adding its partials
         st = from_hip(masq::launch_down_wide(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth, a.l_down,

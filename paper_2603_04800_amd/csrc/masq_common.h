@@ -155,6 +155,19 @@ hipError_t launch_lowrank_down(const void* x, DT x_dt, const int32_t* mod, const
 inline bool fused_stage1_ok(int64_t T, int64_t K, int rank, DT lr_dt) {
     return !small_path(T, K) && lr_dt == DT::BF16 && rank > 0 && rank <= 64;
 }
+// The register-resident form of stage 1 (smoothing, quantisation and, for
+// bf16 factors of rank <= 64, the down-projection): bf16 activations, 16 rows
+// per workgroup of kFrWaves waves, rows of a multiple of 64 columns up to
+// kFrWaves x kFrMaxPairs x 64 (each wave holds at most kFrMaxPairs 64-column
+// pairs of its 16 rows in registers), and the smoothing factors of every
+// modality within kFrInvFloats floats of LDS.
+constexpr int kFrWaves = 8;
+constexpr int kFrMaxPairs = 8;
+constexpr int kFrInvFloats = 12288;
+inline bool stage1_fr_ok(DT x_dt, int64_t K, int n_mod) {
+    return x_dt == DT::BF16 && K % 64 == 0 && K <= int64_t{kFrWaves} * kFrMaxPairs * 64 &&
+           ((static_cast<int64_t>(n_mod) * K * 4 + 1023) / 1024) * 1024 <= kFrInvFloats * 4;
+}
 hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
                                int8_t* q, float* x_scale, float* u, uint8_t* u_hl,

@@ -1090,6 +1090,313 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
     }
 }
 
+// ---------------------------------------------------------------- fused stage 1, rows in registers
+// Stage 1 for bf16 activations (stage1_fr_ok shapes): a workgroup of
+// kFrWaves waves owns 16 RG rows, each wave a slice of the row in 64-column
+// pairs.  Every lane issues all of its slice's loads at once (one instruction
+// reads 16 rows x 64 bytes) and keeps the raw bf16 values in registers, so
+// each row comes from HBM once and the second pass (the codes) reads nothing.
+// Lane l covers row l % 16 of each row group and, in pair p, the columns
+// 64 p + 16 (l / 16) .. + 15 as two 8-column halves, each one k group of
+// v_mfma_f32_16x16x32_bf16; the L1 fragments are read in the same column
+// order, so the MFMA's k order is a permutation of the row's (which changes
+// only the fp32 rounding order of u).  The fragments come from L2 and are
+// shared by the RG row groups; their L2 traffic (|L1^m| per 16 RG rows) is
+// what bounds the down-projection.  The waves' u partials are added in LDS in
+// a fixed order.
+constexpr int kFrLook = 2;          // k steps of L1 fragments in flight ahead of their MFMAs
+
+template <int P, int RG>
+__global__ __launch_bounds__(64 * kFrWaves) void k_stage1_fr(
+    const bf16_t* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
+    const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod,
+    int8_t* __restrict__ q, float* __restrict__ x_scale, float* __restrict__ u,
+    uint8_t* __restrict__ u_hl, int* __restrict__ zero_ints, int n_zero) {
+    constexpr int kRows = 16 * RG;
+    if (blockIdx.x == 0)                           // arrival counters of stage 2
+        for (int i = threadIdx.x; i < n_zero; i += blockDim.x) zero_ints[i] = 0;
+    __shared__ __attribute__((aligned(16))) float s_inv[kFrInvFloats];
+    __shared__ __attribute__((aligned(16))) float red[kFrWaves / 2][kRows][64];
+    __shared__ int smod[kRows];
+    __shared__ float samax[kFrWaves][kRows];
+    __shared__ float srq[kRows];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kRows;
+    const int ar = lane & 15, kg = lane >> 4;
+    const int npairs = K >> 6;
+    const int pb = wave * P;                       // this wave's first pair
+
+    // the smoothing factors of every modality into LDS (1 KB DMA blocks; the
+    // last block's pieces past the end repeat the last piece, the host checks
+    // the fit), then this lane's share of its rows, every load in flight
+    {
+        const int pieces = n_mod * K / 4;
+        const uint32_t b0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(s_inv));
+        for (int i = wave; i * 64 < pieces; i += kFrWaves)
+            lds_dma16(inv_s + 4 * min(i * 64 + lane, pieces - 1), b0 + i * 1024);
+    }
+    int mymod = 0;
+    if (tid < kRows) {
+        const int64_t t = row0 + tid;
+        mymod = t < T ? sane_mod(mod[t], n_mod) : 0;
+    }
+    bool valid[RG];
+    const bf16_t* xr[RG];
+#pragma unroll
+    for (int g = 0; g < RG; ++g) {
+        const int64_t t = row0 + 16 * g + ar;
+        valid[g] = t < T;
+        xr[g] = x + (valid[g] ? t : row0) * static_cast<int64_t>(K) + 16 * kg;
+    }
+    v4i xa[RG][P], xb[RG][P];
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+        const int gp = min(pb + p, npairs - 1);
+#pragma unroll
+        for (int g = 0; g < RG; ++g) {
+            xa[g][p] = *reinterpret_cast<const v4i*>(xr[g] + 64 * gp);
+            xb[g][p] = *reinterpret_cast<const v4i*>(xr[g] + 64 * gp + 8);
+        }
+    }
+    asm volatile("" ::: "memory");
+    if (tid < kRows) smod[tid] = mymod;
+    // the DMA and the id loads are older than this lane's 2 P RG row loads
+    MASQ_WAIT_VMCNT_LGKM0(2 * P * RG);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+
+    unsigned pres = 0;
+#pragma unroll
+    for (int i = 0; i < kRows; ++i)
+        if (smod[i] > 0) pres |= 1u << smod[i];
+    const unsigned present = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(pres)));
+    int mods[3] = {0, 0, 0};
+    int np = 0;
+    if (r > 0)                                     // rank 0: quantisation only
+        for (int m = 1; m < n_mod; ++m)
+            if (present & (1u << m)) mods[np++] = m;
+    const int ncb = r >> 4;                        // 16-column MFMA blocks (<= 4)
+    int mrow[RG];
+    const float* srow[RG];
+#pragma unroll
+    for (int g = 0; g < RG; ++g) {
+        mrow[g] = smod[16 * g + ar];
+        srow[g] = s_inv + mrow[g] * K + 16 * kg;
+    }
+
+    // xs of half h of pair p of row group g (8 values) from the registers
+    // and the factors
+    auto smoothed = [&](int g, int p, int h, float (&xs)[8]) __attribute__((always_inline)) {
+        const int gp = min(pb + p, npairs - 1);
+        const v4i raw = h ? xb[g][p] : xa[g][p];
+        const float* sp = srow[g] + 64 * gp + 8 * h;
+        const v4f s0 = *reinterpret_cast<const v4f*>(sp);
+        const v4f s1 = *reinterpret_cast<const v4f*>(sp + 4);
+        const float sv[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            xs[2 * j] = __uint_as_float(static_cast<uint32_t>(raw[j]) << 16) * sv[2 * j];
+            xs[2 * j + 1] = __uint_as_float(static_cast<uint32_t>(raw[j]) & 0xFFFF0000u) * sv[2 * j + 1];
+        }
+    };
+
+    // pass 1: the rows' absmax and, for non-text rows, u = xs L1^m
+    float amax[RG];
+    v4f acc[RG][4];
+#pragma unroll
+    for (int g = 0; g < RG; ++g) {
+        amax[g] = 0.f;
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb) acc[g][jb] = v4f{0.f, 0.f, 0.f, 0.f};
+    }
+    const v4i zero = {0, 0, 0, 0};
+    if (np == 0) {
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+#pragma unroll
+            for (int g = 0; g < RG; ++g)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    float xs[8];
+                    smoothed(g, p, h, xs);
+                    if (valid[g] && pb + p < npairs)
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) amax[g] = fmaxf(amax[g], fabsf(xs[e]));
+                }
+    } else {
+        // L1 fragments of k step s2 = 2 p + h: rows 16 jb + (l % 16) of
+        // (L1^m)^T for the four N blocks jb (blocks past r repeat the last
+        // one; their sums are never stored), the step's columns of this
+        // lane's group
+        const int64_t rowK = static_cast<int64_t>(K);
+        auto step_off = [&](int s2) __attribute__((always_inline)) {
+            return 64 * min(pb + (s2 >> 1), npairs - 1) + 8 * (s2 & 1);
+        };
+        // one modality's MFMAs over the wave's k steps, its fragments kFrLook
+        // steps ahead; rows of other modalities enter as zeros
+        auto project = [&](int m, bool first) __attribute__((always_inline)) {
+            const bf16_t* fp[4];
+#pragma unroll
+            for (int jb = 0; jb < 4; ++jb)
+                fp[jb] = l_down + (static_cast<int64_t>(m - 1) * r + 16 * min(jb, ncb - 1) + ar) * rowK +
+                         16 * kg;
+            v4i fb[2 * P][4];
+#pragma unroll
+            for (int s2 = 0; s2 < kFrLook && s2 < 2 * P; ++s2)
+#pragma unroll
+                for (int jb = 0; jb < 4; ++jb)
+                    fb[s2][jb] = *reinterpret_cast<const v4i*>(fp[jb] + step_off(s2));
+#pragma unroll
+            for (int s2 = 0; s2 < 2 * P; ++s2) {
+                if (s2 + kFrLook < 2 * P) {
+#pragma unroll
+                    for (int jb = 0; jb < 4; ++jb)
+                        fb[s2 + kFrLook][jb] =
+                            *reinterpret_cast<const v4i*>(fp[jb] + step_off(s2 + kFrLook));
+                }
+                const int p = s2 >> 1, h = s2 & 1;
+#pragma unroll
+                for (int g = 0; g < RG; ++g) {
+                    const bool ok = valid[g] && pb + p < npairs;
+                    float xs[8];
+                    smoothed(g, p, h, xs);
+                    if (first && ok)
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) amax[g] = fmaxf(amax[g], fabsf(xs[e]));
+                    v4i hi, lo;
+                    split_bf16x8(xs, hi, lo);
+                    const bool use = ok && mrow[g] == m;
+                    const v4i hh = use ? hi : zero, ll = use ? lo : zero;
+#pragma unroll
+                    for (int jb = 0; jb < 4; ++jb)
+                        acc[g][jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            __builtin_bit_cast(v8bf, hh), __builtin_bit_cast(v8bf, fb[s2][jb]),
+                            acc[g][jb], 0, 0, 0);
+#pragma unroll
+                    for (int jb = 0; jb < 4; ++jb)
+                        acc[g][jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            __builtin_bit_cast(v8bf, ll), __builtin_bit_cast(v8bf, fb[s2][jb]),
+                            acc[g][jb], 0, 0, 0);
+                }
+            }
+        };
+        project(mods[0], true);
+        // tiles that hold a second or third non-text modality (run borders)
+        for (int mi = 1; mi < np; ++mi) project(mods[mi], false);
+    }
+    // the four lanes of a row (lane % 16) hold its four column groups
+#pragma unroll
+    for (int g = 0; g < RG; ++g) {
+        float a = amax[g];
+        a = fmaxf(a, __shfl_xor(a, 16));
+        a = fmaxf(a, __shfl_xor(a, 32));
+        if (lane < 16) samax[wave][16 * g + lane] = a;
+    }
+    // u partials: waves kFrWaves / 2 .. hand theirs to the first half,
+    // which add them
+    constexpr int half = kFrWaves / 2;
+    if (np > 0 && wave >= half) {
+#pragma unroll
+        for (int g = 0; g < RG; ++g)
+#pragma unroll
+            for (int jb = 0; jb < 4; ++jb) {
+                if (jb >= ncb) break;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    red[wave - half][16 * g + 4 * kg + i][16 * jb + ar] = acc[g][jb][i];
+            }
+    }
+    __syncthreads();
+    if (tid < kRows) {
+        float a = samax[0][tid];
+#pragma unroll
+        for (int w = 1; w < kFrWaves; ++w) a = fmaxf(a, samax[w][tid]);
+        const bool nz = a > 0.f;
+        srq[tid] = nz ? 127.0f / a : 0.f;                     // correctly rounded
+        if (row0 + tid < T) x_scale[row0 + tid] = nz ? a / 127.0f : 0.f;
+    }
+    if (np > 0 && wave < half) {
+#pragma unroll
+        for (int g = 0; g < RG; ++g)
+#pragma unroll
+            for (int jb = 0; jb < 4; ++jb) {
+                if (jb >= ncb) break;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    float& slot = red[wave][16 * g + 4 * kg + i][16 * jb + ar];
+                    slot = acc[g][jb][i] + slot;
+                }
+            }
+    }
+    __syncthreads();
+    // u (fp32, written when the tile has non-text rows) and its bf16 hi/lo
+    // rows [hi 64 | lo 64] for the GEMM epilogue (text rows and columns past
+    // r zero there): thread (row, c) adds columns 8 c .. 8 c + 7 of the
+    // partials in a fixed order
+    static_assert(kRows * 8 <= 64 * kFrWaves, "one thread per (row, 8 columns)");
+    if (tid < kRows * 8 && (np > 0 || u_hl != nullptr)) {
+        const int row = tid >> 3, c = tid & 7;
+        const int64_t t = row0 + row;
+        if (t < T) {
+            float v[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = 0.f;
+            if (np > 0 && 8 * c < r) {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    v4f a = *reinterpret_cast<const v4f*>(&red[0][row][8 * c + 4 * h]);
+#pragma unroll
+                    for (int w = 1; w < half; ++w)
+                        a += *reinterpret_cast<const v4f*>(&red[w][row][8 * c + 4 * h]);
+                    v[4 * h] = a.x; v[4 * h + 1] = a.y; v[4 * h + 2] = a.z; v[4 * h + 3] = a.w;
+                    *reinterpret_cast<v4f*>(u + t * r + 8 * c + 4 * h) = a;
+                }
+            }
+            if (u_hl != nullptr) {
+                v4i hi, lo;
+                split_bf16x8(v, hi, lo);
+                const bool live = smod[row] > 0;
+                *reinterpret_cast<v4i*>(u_hl + t * 256 + 16 * c) = live ? hi : zero;
+                *reinterpret_cast<v4i*>(u_hl + t * 256 + 128 + 16 * c) = live ? lo : zero;
+            }
+        }
+    }
+
+    // pass 2: the codes of this lane's 16 columns of each pair, one 16-byte
+    // store each, from the registers
+#pragma unroll
+    for (int g = 0; g < RG; ++g) {
+        const float rq = srq[16 * g + ar];
+        int8_t* qr = q + (valid[g] ? row0 + 16 * g + ar : row0) * static_cast<int64_t>(K) + 16 * kg;
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+            uint32_t w[4];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                float xs[8];
+                smoothed(g, p, h, xs);
+                uint32_t w0 = 0u, w1 = 0u;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    float c = rintf(xs[e] * rq);
+                    c = fminf(fmaxf(c, -127.0f), 127.0f);
+                    const uint32_t b = (static_cast<uint32_t>(static_cast<int32_t>(c)) & 0xFFu)
+                                       << (8 * (e & 3));
+                    if (e < 4) w0 |= b; else w1 |= b;
+                }
+                w[2 * h] = w0;
+                w[2 * h + 1] = w1;
+            }
+            if (valid[g] && pb + p < npairs)
+                *reinterpret_cast<v4i*>(qr + 64 * (pb + p)) =
+                    v4i{static_cast<int32_t>(w[0]), static_cast<int32_t>(w[1]),
+                        static_cast<int32_t>(w[2]), static_cast<int32_t>(w[3])};
+        }
+    }
+}
+
 // ================================================================ standalone CMC
 template <typename XT, typename LT, typename YT>
 __global__ __launch_bounds__(256) void k_lowrank_comp(const XT* __restrict__ x,
@@ -2635,9 +2942,34 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
 // 128 x 128; 4: eight waves of 128 x 64, two per SIMD).
 constexpr int kGemmWavesN = 4;
 
+// The register-resident stage 1 (stage1_fr_ok shapes): rank 0 (or no
+// factors) quantises only.
+static hipError_t launch_stage1_fr(const void* x, const int32_t* mod, const float* inv_s,
+                                   const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
+                                   int8_t* q, float* x_scale, float* u, uint8_t* u_hl,
+                                   int* zero_ints, int n_zero, hipStream_t s) {
+    const int P = static_cast<int>(((K / 64) + kFrWaves - 1) / kFrWaves);
+    // one row group: two (sharing each L1 fragment) need more than a lane's
+    // 256 registers from 4 pairs a wave on
+    const dim3 grid(static_cast<unsigned>((T + 15) / 16)), block(64 * kFrWaves);
+#define MASQ_FR(PP) case PP: hipLaunchKernelGGL((k_stage1_fr<PP, 1>), grid, block, 0, s, \
+        static_cast<const bf16_t*>(x), mod, inv_s, static_cast<const bf16_t*>(l_down), T, \
+        static_cast<int>(K), rank, n_mod, q, x_scale, u, u_hl, zero_ints, n_zero); break;
+    switch (P) {
+        MASQ_FR(1) MASQ_FR(2) MASQ_FR(3) MASQ_FR(4) MASQ_FR(5) MASQ_FR(6) MASQ_FR(7) MASQ_FR(8)
+        default: return hipErrorInvalidValue;
+    }
+#undef MASQ_FR
+    static_assert(kFrMaxPairs == 8, "one case per pair count");
+    return hipGetLastError();
+}
+
 hipError_t launch_smooth_quant(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                int64_t T, int64_t K, int n_mod, int8_t* q, float* x_scale,
                                int* zero_ints, int n_zero, hipStream_t s, const UFinish* fin_in) {
+    if (fin_in == nullptr && T > kSmallMaxT && stage1_fr_ok(x_dt, K, n_mod))
+        return launch_stage1_fr(x, mod, inv_s, nullptr, T, K, 0, n_mod, q, x_scale, nullptr,
+                                nullptr, zero_ints, n_zero, s);
     const UFinish fin = fin_in ? *fin_in : UFinish{nullptr, 0, 0, nullptr, nullptr};
     // a wave per row for large batches whose rows fit its register cache
     if (T >= kRowsPerWaveMinT && K <= 64 * 8 * 8) {
@@ -2708,6 +3040,9 @@ hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const
                                const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
                                int8_t* q, float* x_scale, float* u, uint8_t* u_hl,
                                int* zero_ints, int n_zero, hipStream_t s) {
+    if (stage1_fr_ok(x_dt, K, n_mod))
+        return launch_stage1_fr(x, mod, inv_s, l_down, T, K, rank, n_mod, q, x_scale, u, u_hl,
+                                zero_ints, n_zero, s);
     // 32 rows per workgroup halve the L1 re-reads once the batch fills the
     // chip at that size; smaller batches keep 16 rows for more workgroups
     const bool wide = T >= kFuseWideMinT;
