@@ -58,7 +58,7 @@ def parse():
     ap.add_argument("--method", default="masquant", choices=("masquant", "smoothquant", "mas"),
                     help="comparators on the same kernels: smoothquant (one unified smoothing "
                          "factor, no compensation) or mas (MAS-only: a weight per modality, no "
-                         "compensation; layouts whose runs start at multiples of 4 tokens)")
+                         "compensation)")
     ap.add_argument("--copies", type=int, default=2,
                     help="rotating input/output sets so no step reuses the last one's cache")
     ap.add_argument("--no-cpu", action="store_true")
@@ -703,7 +703,8 @@ def measure_workload(cfg_index, method, bits, steps, warmup, copies_min, dev, pc
            "bytes": sum(algorithmic_bytes(L) for L in layers),
            "gemm_bytes": sum(gemm_bytes(L) for L in layers),
            "kernel": (gemm_kernel_label(layers) if method != "mas" else
-                      "masq_w8a8_gemm per run of one modality (stage 2: int8 GEMM + dequant)")}
+                      "masq_mas_only_linear (rows grouped by modality on the device, "
+                      "quantisation, grouped int8 GEMM with a weight per modality)")}
     del sets
     torch.cuda.synchronize()
     torch.cuda.empty_cache()

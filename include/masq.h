@@ -162,6 +162,33 @@ masq_status masq_linear_fused_noalloc(const void* x, masq_dtype x_dt, const int3
                                       int32_t n_mod, void* y, masq_dtype y_dt, void* stream);
 
 /*
+ * The MAS-only comparator (Sec. 4.2, the inference with per-modality
+ * smoothing factors and per-modality weights before the shared weight of
+ * Sec. 4.3): for a token row x_t of modality m,
+ *     y_t = (float(Q(x_t S_m^-1) . wq[m]^T) * delta_t) * w_scale[m]
+ * with the same smoothing, per-token quantisation, exact int32 accumulation,
+ * dequantisation order and output rounding as masq_linear_fused, and no
+ * compensation.  The rows are grouped by modality on the device (a stable
+ * counting sort of the ids) and each 256-row tile of one modality's rows is
+ * multiplied by that modality's weight; the host never reads the ids, and
+ * any layout of modalities works.
+ *   wq       [n_mod][c_out][c_in] int8, Q(S_m W) transposed, per modality
+ *   w_scale  [n_mod][c_out] f32
+ *   inv_smooth, x, modality, y as for masq_linear_fused (ids outside
+ *   [0, n_mod) are treated as text).
+ * workspace: at least masq_mas_only_workspace_bytes(...) bytes, 256-byte
+ * aligned, contents need not be initialised; not shared by concurrent calls.
+ * c_in must be a multiple of 64 (else MASQ_ERR_UNSUPPORTED); the other
+ * preconditions and errors are masq_linear_fused's (rank does not apply).
+ */
+masq_status masq_mas_only_linear(const void* x, masq_dtype x_dt, const int32_t* modality,
+                                 const float* inv_smooth, const int8_t* wq, const float* w_scale,
+                                 int64_t T, int64_t c_in, int64_t c_out, int32_t n_mod, void* y,
+                                 masq_dtype y_dt, void* workspace, size_t workspace_bytes,
+                                 void* stream);
+size_t masq_mas_only_workspace_bytes(int64_t T, int64_t c_in, int64_t c_out, int32_t n_mod);
+
+/*
  * The two launch stages masq_linear_fused is made of, with identical
  * arguments, exposed so that a caller can place events or other stream work
  * between them.  stage1: smoothing, quantisation and the rank-r

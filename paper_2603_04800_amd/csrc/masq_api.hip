@@ -102,6 +102,48 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
     return w;
 }
 
+// Workspace of the MAS-only comparator: codes, scales, the rows grouped by
+// modality, the tile table and its length, and (K split over few tiles)
+// arrival counters and slice accumulators.
+struct MasOnlyWs {
+    int8_t* q;
+    float* x_scale;
+    int32_t* rows;
+    int32_t* tab;
+    int* tab_n;
+    int* tickets;
+    int n_tickets;
+    int32_t* part;
+    int S;
+    size_t bytes;
+};
+
+MasOnlyWs plan_mas_only(void* base, int64_t T, int64_t K, int64_t N, int n_mod) {
+    MasOnlyWs w{};
+    size_t off = 0;
+    uint8_t* b = static_cast<uint8_t*>(base);
+    auto carve = [&](size_t bytes) {
+        uint8_t* p = b ? b + off : nullptr;
+        off += align256(bytes);
+        return p;
+    };
+    const int tab_max = grouped_tab_max(T, n_mod);
+    const int64_t tiles = static_cast<int64_t>(tab_max) * ((N + kTileN - 1) / kTileN);
+    w.q = reinterpret_cast<int8_t*>(carve(static_cast<size_t>(T) * static_cast<size_t>(K)));
+    w.x_scale = reinterpret_cast<float*>(carve(static_cast<size_t>(T) * sizeof(float)));
+    w.rows = reinterpret_cast<int32_t*>(carve(static_cast<size_t>(T) * sizeof(int32_t)));
+    w.tab = reinterpret_cast<int32_t*>(carve(static_cast<size_t>(tab_max) * 4 * sizeof(int32_t)));
+    w.tab_n = reinterpret_cast<int*>(carve(sizeof(int)));
+    w.S = plan_gemm_splits(static_cast<int64_t>(tab_max) * kTileM, K, N);
+    w.n_tickets = w.S > 1 ? static_cast<int>(tiles) : 0;
+    w.tickets = w.S > 1 ? reinterpret_cast<int*>(carve(static_cast<size_t>(tiles) * sizeof(int))) : nullptr;
+    w.part = w.S > 1 ? reinterpret_cast<int32_t*>(carve(static_cast<size_t>(tiles) * w.S * kTileM *
+                                                        kTileN * sizeof(int32_t)))
+                     : nullptr;
+    w.bytes = off;
+    return w;
+}
+
 }  // namespace masq
 
 using masq::DT;
@@ -352,6 +394,43 @@ masq_status masq_lowrank_comp(const void* x, masq_dtype x_dt, const int32_t* mod
     return from_hip(masq::launch_lowrank_comp(x, to_dt(x_dt), modality, inv_smooth, l_down, r_up,
                                               to_dt(lr_dt), T, c_in, c_out, rank, n_mod, y,
                                               to_dt(y_dt), static_cast<hipStream_t>(stream)));
+}
+
+size_t masq_mas_only_workspace_bytes(int64_t T, int64_t c_in, int64_t c_out, int32_t n_mod) {
+    if (T < 0 || c_in <= 0 || c_out <= 0 || n_mod < 1 || n_mod > 4) return 0;
+    return masq::plan_mas_only(nullptr, T, c_in, c_out, n_mod).bytes;
+}
+
+masq_status masq_mas_only_linear(const void* x, masq_dtype x_dt, const int32_t* modality,
+                                 const float* inv_smooth, const int8_t* wq, const float* w_scale,
+                                 int64_t T, int64_t c_in, int64_t c_out, int32_t n_mod, void* y,
+                                 masq_dtype y_dt, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+    masq_status st = check_dims(T, c_in, c_out, true);
+    if (st != MASQ_OK) return st;
+    if ((st = check_exact_acc(c_in, false)) != MASQ_OK) return st;
+    if (n_mod < 1 || n_mod > 4) return MASQ_ERR_SHAPE;
+    if (!valid_dt(x_dt) || !valid_dt(y_dt)) return MASQ_ERR_DTYPE;
+    if (c_in % 64 != 0) return MASQ_ERR_UNSUPPORTED;
+    if (T == 0) return MASQ_OK;
+    if (!x || !modality || !inv_smooth || !wq || !w_scale || !y || !workspace) return MASQ_ERR_NULL;
+    if (!aligned16(x) || !aligned16(modality) || !aligned16(inv_smooth) || !aligned16(wq) ||
+        !aligned16(w_scale) || !aligned16(y))
+        return MASQ_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return MASQ_ERR_ALIGN;
+    const masq::MasOnlyWs w = masq::plan_mas_only(workspace, T, c_in, c_out, n_mod);
+    if (workspace_bytes < w.bytes) return MASQ_ERR_WORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    st = from_hip(masq::launch_group_rows(modality, T, n_mod, w.rows, w.tab, w.tab_n, w.tickets,
+                                          w.n_tickets, s));
+    if (st != MASQ_OK) return st;
+    st = from_hip(masq::launch_smooth_quant(x, to_dt(x_dt), modality, inv_smooth, T, c_in, n_mod,
+                                            w.q, w.x_scale, nullptr, 0, s));
+    if (st != MASQ_OK) return st;
+    return from_hip(masq::launch_gemm_grouped(w.q, w.x_scale, wq, w_scale, T, c_in, c_out, n_mod,
+                                              w.rows, w.tab, w.tab_n, y, to_dt(y_dt), w.S, w.part,
+                                              w.tickets, s));
 }
 
 size_t masq_linear_fused_workspace_bytes(int64_t T, int64_t c_in, int64_t c_out, int32_t rank,

@@ -193,6 +193,20 @@ hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        int rank, int n_mod, const void* r_up, DT lr_dt, bool cmc, int32_t* acc,
                        void* y, DT y_dt, hipStream_t s, bool w4 = false);
 
+// MAS-only comparator (a weight per modality, no compensation): rows grouped
+// by modality on the device, then the direct-to-LDS GEMM over tiles of one
+// modality each (K % 64 == 0).  The tile table holds at most
+// grouped_tab_max entries {first row, rows, modality, 0}.
+inline int grouped_tab_max(int64_t T, int n_mod) {
+    return static_cast<int>((T + kTileM - 1) / kTileM) + n_mod - 1;
+}
+hipError_t launch_group_rows(const int32_t* mod, int64_t T, int n_mod, int32_t* rows,
+                             int32_t* tab, int* tab_n, int* zero_ints, int n_zero, hipStream_t s);
+hipError_t launch_gemm_grouped(const int8_t* q, const float* x_scale, const int8_t* wq,
+                               const float* w_scale, int64_t T, int64_t K, int64_t N, int n_mod,
+                               const int32_t* rows, const int32_t* tab, const int* tab_n, void* y,
+                               DT y_dt, int S, int32_t* part, int* tickets, hipStream_t s);
+
 hipError_t launch_lowrank_comp(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, const void* r_up, DT lr_dt, int64_t T,
                                int64_t K, int64_t N, int rank, int n_mod, void* y, DT y_dt,

@@ -1727,13 +1727,15 @@ struct EpiDma {
     unsigned present;
     bool pre;
     int off_uh, off_ul, off_r[2];
+    int grp_rows;      // grouped tile (GRP): its valid rows; sm.rawmod holds their token indices
 };
 
 // NWN waves along the channels (2: four waves of 128 x 128, 4: eight waves of
 // 128 x 64); NJ = 8 / NWN channel blocks of 32 per wave.  DMA: called from
 // the DMA kernel (state in ed; pf unused), else the per-thread operands pf
 // are written to LDS here.
-template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2, bool DMA = false>
+template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2, bool DMA = false,
+          bool GRP = false>
 __device__ __forceinline__ void gemm_epilogue(
     v16i (&acc)[4][8 / NWN], GemmSmem& sm, const EpiPrefetch& pf, int64_t T, int N, int64_t row0,
     int col0, const float* __restrict__ u, int r, int n_mod, const LT* __restrict__ r_up,
@@ -1810,7 +1812,16 @@ __device__ __forceinline__ void gemm_epilogue(
     // wm*128 + 32 i + (lane % 32) and channel wn*kWaveCols + 32 j + 8 (e / 4) +
     // 4 (lane / 32) + e % 4.  Loops over blocks are fully unrolled: the
     // accumulators are registers and must be indexed by constants.
-    const bool interior = (row0 + kTileM <= T) && (col0 + kTileN <= N);
+    static_assert(!GRP || (DMA && !CMC && !ACC), "grouped tiles: plain product, DMA kernel");
+    // GRP: local row l of the tile is token sm.rawmod[l], valid for l < ed.grp_rows
+    const bool interior = GRP ? (ed.grp_rows == kTileM && col0 + kTileN <= N)
+                              : (row0 + kTileM <= T) && (col0 + kTileN <= N);
+    auto row_ok = [&](int local) __attribute__((always_inline)) {
+        return GRP ? local < ed.grp_rows : row0 + local < T;
+    };
+    auto out_row = [&](int local) __attribute__((always_inline)) -> int64_t {
+        return GRP ? static_cast<int64_t>(sm.rawmod[local]) : row0 + local;
+    };
     auto tok_of = [&](int i) { return wm * 128 + i * 32 + (lane & 31); };
     auto ch_of = [&](int j, int g) { return wn * kWaveCols + j * 32 + 8 * g + 4 * (lane >> 5); };
 
@@ -1866,7 +1877,7 @@ __device__ __forceinline__ void gemm_epilogue(
     // instruction); LDS operations of one wave execute in order, so the
     // buffer needs no further synchronisation.
     auto store_rowblock = [&](const int i, const v16f (&ybs)[NJ]) __attribute__((always_inline)) {
-        const int64_t tok0 = row0 + wm * 128 + i * 32;
+        const int loc0 = wm * 128 + i * 32;
         if constexpr (sizeof(YT) == 2) {
             uint8_t* scr = sm.tr + wave * 32 * kPitch;
             const int rw = lane & 31, h = lane >> 5;
@@ -1890,19 +1901,20 @@ __device__ __forceinline__ void gemm_epilogue(
                 for (int k = 0; k < 32 / kRowsPerRead; ++k) {
                     const int rr = k * kRowsPerRead + lane / kLanesPerRow;
                     const v4i d = *reinterpret_cast<const v4i*>(scr + rr * kPitch + (lane % kLanesPerRow) * 16);
-                    const int64_t tok = tok0 + rr;
-                    if (interior || (tok < T && ch < N))
-                        *reinterpret_cast<v4i*>(y + tok * N + ch) = d;
+                    if (interior || (row_ok(loc0 + rr) && ch < N))
+                        *reinterpret_cast<v4i*>(y + out_row(loc0 + rr) * N + ch) = d;
                 }
             }
         } else {
-            const int64_t tok = tok0 + (lane & 31);
+            const int loc = loc0 + (lane & 31);
+            const bool ok = row_ok(loc);
+            const int64_t tok = out_row(loc);
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
                     const int ch = col0 + ch_of(j, g);
-                    if (interior || (tok < T && ch < N)) {
+                    if (interior || (ok && ch < N)) {
                         const v4f w = {ybs[j][4 * g], ybs[j][4 * g + 1], ybs[j][4 * g + 2], ybs[j][4 * g + 3]};
                         *reinterpret_cast<v4f*>(y + tok * N + ch) = w;
                     }
@@ -2187,14 +2199,24 @@ __device__ __forceinline__ int swz4(int row) { return (row >> 2) & 3; }
 // spread over the banks); lane group h of a wave takes the codes of half h
 // (k chunks 2h and 2h + 1 of the stage, one per k step), and the q
 // fragments follow the same k order.
+//
+// GRP (the MAS-only comparator, a weight per modality): tile row tm is entry
+// tm of a table built on the device, {first, count, modality}: its rows are
+// tokens grows[first .. first + count) (one modality, in token order), its
+// weight and channel scales those of that modality (B + modality b_stride,
+// w_scale + modality N).  A rows and their scales are gathered by the DMA,
+// outputs are written to the tokens' own rows; table entries past *gtab_n
+// (the grid is sized for the largest possible table) exit at once.
 template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2, bool SPLIT = false,
-          bool W4 = false>
+          bool W4 = false, bool GRP = false>
 __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
     const float* __restrict__ w_scale, int64_t T, int K, int N, int tiles_m, int tiles_n,
     const int32_t* __restrict__ mod, const float* __restrict__ u, const uint8_t* __restrict__ u_hl,
     int r, int n_mod, const LT* __restrict__ r_up, int32_t* __restrict__ acc_out,
-    YT* __restrict__ y, int S, int32_t* __restrict__ part, int* __restrict__ tickets) {
+    YT* __restrict__ y, int S, int32_t* __restrict__ part, int* __restrict__ tickets,
+    const int32_t* __restrict__ grows, const v4i* __restrict__ gtab,
+    const int* __restrict__ gtab_n, int64_t b_stride) {
     __shared__ __attribute__((aligned(16))) GemmSmem sm;
     static_assert(kDmaStages * kDmaStageBytes <= static_cast<int>(sizeof(GemmSmem::buf)), "LDS");
     static_assert(kDmaStageBytes == kTileM * 128, "an epilogue operand fills one K stage buffer");
@@ -2210,8 +2232,25 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     const int nk_all = K / kDmaStageK;
     const int nk_slice = SPLIT ? (nk_all + S - 1) / S : nk_all;
     const int kst0 = sl * nk_slice;
-    const int64_t row0 = static_cast<int64_t>(tm) * kTileM;
+    const int64_t row0 = GRP ? 0 : static_cast<int64_t>(tm) * kTileM;
     const int col0 = tn * kTileN;
+    // GRP: the tile's rows grows[gfirst .. gfirst + grows_n), modality gmod
+    int gfirst = 0, grows_n = kTileM, gmod = 0;
+    if constexpr (GRP) {
+        if (tm >= *gtab_n) return;                      // wave-uniform
+        const v4i e = gtab[tm];
+        gfirst = e.x;
+        grows_n = e.y;
+        gmod = e.z;
+        B += gmod * b_stride;
+        w_scale += static_cast<int64_t>(gmod) * N;
+    }
+    // token of the tile's local row l (rows past the tile's end repeat its
+    // last row; their results are discarded)
+    auto a_row = [&](int l) __attribute__((always_inline)) -> int64_t {
+        if constexpr (GRP) return grows[gfirst + min(l, grows_n - 1)];
+        else return min(row0 + l, T - 1);
+    };
     constexpr int NJ = 8 / NWN, NW = 2 * NWN;
     constexpr int kRowsPerWave = kTileM / NW;           // DMA rows of A and of B per wave
     constexpr int kStepB = W4 ? kDmaStageK / 2 : kDmaStageK;   // B bytes per row and stage
@@ -2235,19 +2274,21 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     // scales, channel scales, modality ids; 4 each) issued by wave c % NW;
     // indices past T or N are clamped (their results are discarded)
     {
-        constexpr int kPieces = CMC ? 12 : 8;
+        // (GRP: the third group is the tiles' token indices, the output rows)
+        constexpr int kPieces = (CMC || GRP) ? 12 : 8;
         for (int c = wave; c < kPieces; c += NW) {
             const int part = c & 3, e = 64 * part + lane;
             const void* src;
             uint32_t dst;
             if (c < 4) {
-                src = x_scale + min(row0 + e, T - 1);
+                src = x_scale + a_row(e);
                 dst = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&sm.dx[64 * part]));
             } else if (c < 8) {
                 src = w_scale + min(col0 + e, N - 1);
                 dst = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&sm.ws[64 * part]));
             } else {
-                src = mod + min(row0 + e, T - 1);
+                src = GRP ? static_cast<const void*>(grows + gfirst + min(e, grows_n - 1))
+                          : static_cast<const void*>(mod + min(row0 + e, T - 1));
                 dst = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&sm.rawmod[64 * part]));
             }
             lds_dma4(src, static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(dst))));
@@ -2266,7 +2307,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     for (int j = 0; j < kDmaA; ++j) {
         const int row = wave * kRowsPerWave + 16 * j + (lane >> 2);
         const int chunk = (lane & 3) ^ swz4(row);
-        src[j] = A + min(row0 + row, T - 1) * K + kst0 * kDmaStageK + 16 * chunk;
+        src[j] = A + a_row(row) * K + kst0 * kDmaStageK + 16 * chunk;
         dst_off[j] = static_cast<uint32_t>(
             __builtin_amdgcn_readfirstlane((wave * kRowsPerWave + 16 * j) * kDmaStageK));
     }
@@ -2477,6 +2518,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     EpiDma ed{};
     ed.present = present;
     ed.pre = pre;
+    ed.grp_rows = grows_n;
     if constexpr (CMC) {
         if (pre) {
             // the K buffers are free once every wave is past its last reads
@@ -2492,7 +2534,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
         }
     }
     MASQ_WAIT_VMCNT_LGKM0(0);
-    gemm_epilogue<YT, LT, CMC, ACC, NWN, true>(acc, sm, EpiPrefetch{}, T, N, row0, col0, u, r, n_mod,
+    gemm_epilogue<YT, LT, CMC, ACC, NWN, true, GRP>(acc, sm, EpiPrefetch{}, T, N, row0, col0, u, r, n_mod,
                                                r_up, acc_out, y, ed);
 }
 
@@ -2935,6 +2977,67 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
     }
 }
 
+// ================================================================ MAS-only routing
+// Rows grouped by modality (the MAS-only comparator, whose tiles each take
+// one modality's weight): a stable counting sort of the token ids (ids
+// outside [0, n_mod) read as text) by one workgroup.  rows[T]: token
+// indices, modality 0's first, each modality's in token order.  tab: one
+// entry {first, count, modality, 0} per 256-row tile of a modality's rows
+// (count <= 256), modality by modality; *tab_n: the number of entries.
+// Also clears n_zero ints at zero_ints (the grouped GEMM's arrival counters).
+constexpr int kGrpThreads = 1024;
+
+__global__ __launch_bounds__(kGrpThreads) void k_group_rows(
+    const int32_t* __restrict__ mod, int64_t T, int n_mod, int32_t* __restrict__ rows,
+    v4i* __restrict__ tab, int* __restrict__ tab_n, int* __restrict__ zero_ints, int n_zero) {
+    __shared__ v4i scan[2][kGrpThreads];
+    __shared__ int base[4];
+    const int tid = threadIdx.x;
+    for (int i = tid; i < n_zero; i += kGrpThreads) zero_ints[i] = 0;
+    const int64_t per = (T + kGrpThreads - 1) / kGrpThreads;
+    const int64_t t0 = min(T, tid * per), t1 = min(T, t0 + per);
+    v4i c = {0, 0, 0, 0};
+    for (int64_t t = t0; t < t1; ++t) {
+        const int m = sane_mod(mod[t], n_mod);
+        c[0] += m == 0; c[1] += m == 1; c[2] += m == 2; c[3] += m == 3;
+    }
+    // inclusive scan over the threads (Hillis-Steele, double-buffered)
+    int cur = 0;
+    scan[0][tid] = c;
+    __syncthreads();
+    for (int off = 1; off < kGrpThreads; off <<= 1) {
+        v4i v = scan[cur][tid];
+        if (tid >= off) v += scan[cur][tid - off];
+        scan[cur ^ 1][tid] = v;
+        cur ^= 1;
+        __syncthreads();
+    }
+    const v4i incl = scan[cur][tid];
+    const v4i total = scan[cur][kGrpThreads - 1];
+    if (tid == 0) {
+        base[0] = 0;
+        base[1] = total[0];
+        base[2] = total[0] + total[1];
+        base[3] = total[0] + total[1] + total[2];
+    }
+    __syncthreads();
+    int pos[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m) pos[m] = base[m] + incl[m] - c[m];
+    for (int64_t t = t0; t < t1; ++t) {
+        const int m = sane_mod(mod[t], n_mod);
+        const int at = m == 0 ? pos[0]++ : m == 1 ? pos[1]++ : m == 2 ? pos[2]++ : pos[3]++;
+        rows[at] = static_cast<int32_t>(t);
+    }
+    if (tid == 0) {
+        int k = 0;
+        for (int m = 0; m < n_mod; ++m)
+            for (int off = 0; off < total[m]; off += kTileM)
+                tab[k++] = v4i{base[m] + off, min(kTileM, total[m] - off), m, 0};
+        *tab_n = k;
+    }
+}
+
 }  // namespace
 
 // ================================================================ launchers
@@ -3136,17 +3239,63 @@ static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* w
                                dim3(128 * kGemmWavesN), 0, s, q, wq, x_scale, w_scale, T,
                                static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
                                u_hl, rank, n_mod, static_cast<const LT*>(r_up), acc,
-                               static_cast<YT*>(y), S, part, tickets);
+                               static_cast<YT*>(y), S, part, tickets, nullptr, nullptr, nullptr, 0);
         else
             hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN, false, W4>), gridk,
                                dim3(128 * kGemmWavesN), 0, s, q, wq, x_scale, w_scale, T,
                                static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
                                u_hl, rank, n_mod, static_cast<const LT*>(r_up), acc,
-                               static_cast<YT*>(y), 1, nullptr, nullptr);
+                               static_cast<YT*>(y), 1, nullptr, nullptr, nullptr, nullptr, nullptr, 0);
     } else if constexpr (!W4)
         hipLaunchKernelGGL((k_gemm<YT, LT, CMC, ACC>), grid, block, 0, s, q, wq, x_scale, w_scale, T,
                            static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
                            rank, n_mod, static_cast<const LT*>(r_up), acc, static_cast<YT*>(y));
+}
+
+hipError_t launch_group_rows(const int32_t* mod, int64_t T, int n_mod, int32_t* rows,
+                             int32_t* tab, int* tab_n, int* zero_ints, int n_zero, hipStream_t s) {
+    hipLaunchKernelGGL(k_group_rows, dim3(1), dim3(kGrpThreads), 0, s, mod, T, n_mod, rows,
+                       reinterpret_cast<v4i*>(tab), tab_n, zero_ints, n_zero);
+    return hipGetLastError();
+}
+
+template <typename YT>
+static void launch_gemm_grouped_t(const int8_t* q, const float* x_scale, const int8_t* wq,
+                                  const float* w_scale, int64_t T, int64_t K, int64_t N,
+                                  int n_mod, const int32_t* rows, const int32_t* tab,
+                                  const int* tab_n, void* y, int S, int32_t* part, int* tickets,
+                                  hipStream_t s) {
+    const int tiles_m = grouped_tab_max(T, n_mod);
+    const int tiles_n = static_cast<int>((N + kTileN - 1) / kTileN);
+    const dim3 grid(8 * ((tiles_m * tiles_n * S + 7) / 8)), block(128 * kGemmWavesN);
+    const v4i* tb = reinterpret_cast<const v4i*>(tab);
+    if (S > 1)
+        hipLaunchKernelGGL((k_gemm_dma<YT, bf16_t, false, false, kGemmWavesN, true, false, true>), grid,
+                           block, 0, s, q, wq, x_scale, w_scale, T, static_cast<int>(K),
+                           static_cast<int>(N), tiles_m, tiles_n, nullptr, nullptr, nullptr, 0, n_mod,
+                           nullptr, nullptr, static_cast<YT*>(y), S, part, tickets, rows, tb, tab_n,
+                           N * K);
+    else
+        hipLaunchKernelGGL((k_gemm_dma<YT, bf16_t, false, false, kGemmWavesN, false, false, true>), grid,
+                           block, 0, s, q, wq, x_scale, w_scale, T, static_cast<int>(K),
+                           static_cast<int>(N), tiles_m, tiles_n, nullptr, nullptr, nullptr, 0, n_mod,
+                           nullptr, nullptr, static_cast<YT*>(y), 1, nullptr, nullptr, rows, tb,
+                           tab_n, N * K);
+}
+
+hipError_t launch_gemm_grouped(const int8_t* q, const float* x_scale, const int8_t* wq,
+                               const float* w_scale, int64_t T, int64_t K, int64_t N, int n_mod,
+                               const int32_t* rows, const int32_t* tab, const int* tab_n, void* y,
+                               DT y_dt, int S, int32_t* part, int* tickets, hipStream_t s) {
+    if (K % kDmaStageK != 0) return hipErrorInvalidValue;
+    if (part == nullptr || tickets == nullptr) S = 1;
+    if (y_dt == DT::BF16)
+        launch_gemm_grouped_t<bf16_t>(q, x_scale, wq, w_scale, T, K, N, n_mod, rows, tab, tab_n, y,
+                                      S, part, tickets, s);
+    else
+        launch_gemm_grouped_t<float>(q, x_scale, wq, w_scale, T, K, N, n_mod, rows, tab, tab_n, y,
+                                     S, part, tickets, s);
+    return hipGetLastError();
 }
 
 hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,

@@ -42,6 +42,9 @@ _SIGS = {
     "masq_linear_stage2": (_FUSED_ARGS, ctypes.c_int),
     "masq_linear_fused_workspace_bytes": ([_i64, _i64, _i64, _i32, _i32], ctypes.c_size_t),
     "masq_linear_fused_noalloc": (_FUSED_ARGS[:16] + [_p], ctypes.c_int),
+    "masq_mas_only_linear": ([_p, _i32, _p, _p, _p, _p, _i64, _i64, _i64, _i32, _p, _i32, _p, _sz,
+                              _p], ctypes.c_int),
+    "masq_mas_only_workspace_bytes": ([_i64, _i64, _i64, _i32], ctypes.c_size_t),
     "masq_w4a8_gemm": ([_p, _p, _p, _p, _i64, _i64, _i64, _p, _p, _i32, _p], ctypes.c_int),
     "masq_linear_fused_w4a8": (_FUSED_ARGS, ctypes.c_int),
     "masq_linear_stage1_w4a8": (_FUSED_ARGS, ctypes.c_int),
@@ -434,27 +437,11 @@ class BoundLinear:
             raise MasqError(self._names[2], code)
 
 
-def modality_runs(modality) -> list:
-    """Maximal runs (start, length, modality id) of equal ids, from a host copy
-    of the per-token ids (a layout plan, made once per batch layout)."""
-    import numpy as np
-    m = np.asarray(modality.cpu() if hasattr(modality, "cpu") else modality)
-    if m.size == 0:
-        return []
-    cut = np.flatnonzero(np.diff(m)) + 1
-    starts = np.concatenate([[0], cut])
-    ends = np.concatenate([cut, [m.size]])
-    return [(int(a), int(b - a), int(m[a])) for a, b in zip(starts, ends)]
-
-
 class MasOnlyLinear:
     """The MAS-only comparator (Sec. 4.2 without the shared weight): every
-    modality has its own int8 weight Q(S_m W), no compensation.  It runs on
-    the library's own entry points: masq_smooth_quant over all rows (each
-    with its modality's factors), then masq_w8a8_gemm on each run of equal
-    modality ids with that modality's weight, reading and writing the run's
-    rows in place.  Runs must start at multiples of 4 tokens (16-byte
-    alignment of the per-token scales), as in contiguous layouts.
+    modality has its own int8 weight Q(S_m W), no compensation, through
+    masq_mas_only_linear (rows grouped by modality on the device; any
+    layout of modalities).
 
     Holds inv_smooth [M][K] f32, wq [M][N][K] int8, w_scale [M][N] f32."""
 
@@ -464,6 +451,8 @@ class MasOnlyLinear:
         self.inv_smooth, self.wq, self.w_scale = inv_smooth, wq, w_scale
         self.n_mod, self.c_out, self.c_in = wq.shape
         self.rank = 0
+        self.w4 = False
+        self._ws = None
 
     @classmethod
     def from_arrays(cls, art: dict, device="cuda"):
@@ -473,62 +462,46 @@ class MasOnlyLinear:
                    dev(art["w_scale"], torch.float32))
 
     def workspace(self, T, device):
-        """Codes [T][K] int8 then scales [T] f32 (256-byte aligned)."""
-        q_bytes = (T * self.c_in + 255) // 256 * 256
-        return torch.empty(max(q_bytes + 4 * T, 256), dtype=torch.uint8, device=device)
+        need = int(_lib.masq_mas_only_workspace_bytes(T, self.c_in, self.c_out, self.n_mod))
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=device)
+        return self._ws
 
     def bind(self, x, modality, out, workspace=None, stream=None):
         return BoundMasOnly(self, x, modality, out, workspace, stream)
 
-    def __call__(self, x, modality, out=None, out_dtype=None, stream=None):
+    def __call__(self, x, modality, out=None, out_dtype=None, workspace=None, stream=None):
         if out is None:
             out = torch.empty((x.shape[0], self.c_out), device=x.device,
                               dtype=out_dtype or x.dtype)
-        if x.shape[0]:
-            self.bind(x, modality, out, stream=stream)()
+        self.bind(x, modality, out, workspace, stream)()
         return out
 
 
 class BoundMasOnly:
-    """Pre-marshalled calls of :class:`MasOnlyLinear` on fixed buffers:
-    stage1() quantises every row, stage2() runs the per-run GEMMs."""
+    """A pre-marshalled masq_mas_only_linear call on fixed buffers; stage1()
+    is a no-op and stage2() the whole call, so that it times like a layer."""
 
     def __init__(self, lin, x, modality, out, workspace=None, stream=None):
-        T, K = x.shape
-        N = lin.c_out
+        T = x.shape[0]
         ws = workspace if workspace is not None else lin.workspace(T, x.device)
-        q_bytes = (T * K + 255) // 256 * 256
-        if ws.numel() < q_bytes + 4 * T:
+        need = int(_lib.masq_mas_only_workspace_bytes(T, lin.c_in, lin.c_out, lin.n_mod))
+        if ws.numel() < need:
             raise ValueError("workspace too small")
-        q = ws[: T * K].view(torch.int8).view(T, K)
-        dx = ws[q_bytes: q_bytes + 4 * T].view(torch.float32)
-        runs = modality_runs(modality)
-        if any(a % 4 for a, _, _ in runs):
-            raise ValueError("the MAS-only comparator needs runs starting at multiples of 4 tokens")
-        st = _stream(stream)
-        self._sq = (_ptr(x), _dt(x), _ptr(modality), _ptr(lin.inv_smooth), T, K, lin.n_mod,
-                    _ptr(q), _ptr(dx), st)
-        ydt, esz = _dt(out), out.element_size()
-        self._gemms = []
-        for a, n, m in runs:
-            mm = m if 0 <= m < lin.n_mod else 0          # out-of-range ids read as text
-            self._gemms.append((ctypes.c_void_p(q.data_ptr() + a * K),
-                                ctypes.c_void_p(dx.data_ptr() + 4 * a),
-                                ctypes.c_void_p(lin.wq[mm].data_ptr()),
-                                ctypes.c_void_p(lin.w_scale[mm].data_ptr()), n, K, N, None,
-                                ctypes.c_void_p(out.data_ptr() + a * N * esz), ydt, st))
+        _need(modality, torch.int32, "modality")
+        self._args = (_ptr(x), _dt(x), _ptr(modality), _ptr(lin.inv_smooth), _ptr(lin.wq),
+                      _ptr(lin.w_scale), T, lin.c_in, lin.c_out, lin.n_mod, _ptr(out), _dt(out),
+                      _ptr(ws), ws.numel(), _stream(stream))
         self._keep = (lin, x, modality, out, ws)
 
+    def __call__(self):
+        _check("masq_mas_only_linear", _lib.masq_mas_only_linear(*self._args))
+
     def stage1(self):
-        _check("masq_smooth_quant", _lib.masq_smooth_quant(*self._sq))
+        pass
 
     def stage2(self):
-        for g in self._gemms:
-            _check("masq_w8a8_gemm", _lib.masq_w8a8_gemm(*g))
-
-    def __call__(self):
-        self.stage1()
-        self.stage2()
+        self()
 
 
 def linear_fused(x, modality, inv_smooth, wq, w_scale, l_down=None, r_up=None,

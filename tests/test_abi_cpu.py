@@ -169,6 +169,33 @@ def test_noalloc_entry_point_validates_before_touching_the_device(lib):
     assert _noalloc(lib, T=0, K=133136 + 16) == 2
 
 
+def test_mas_only_entry_point_validates(lib):
+    """masq_mas_only_linear checks sizes, dtypes, pointers, alignment and the
+    workspace before enqueueing anything; c_in must be a multiple of 64."""
+    f, wsb = lib.masq_mas_only_linear, lib.masq_mas_only_workspace_bytes
+    big = 1 << 30
+
+    def call(**kw):
+        a = dict(x=P, x_dt=1, mod=P, inv=P, wq=P, ws=P, T=16, K=128, N=64, M=3, y=P, y_dt=1,
+                 work=P, wb=big)
+        a.update(kw)
+        return f(a["x"], a["x_dt"], a["mod"], a["inv"], a["wq"], a["ws"], a["T"], a["K"], a["N"],
+                 a["M"], a["y"], a["y_dt"], a["work"], a["wb"], None)
+    assert call(K=96) == 7                       # c_in % 64 != 0: not supported
+    assert call(K=40) == 2
+    assert call(N=24) == 2
+    assert call(M=0) == 2 and call(M=5) == 2
+    assert call(x_dt=4) == 3
+    assert call(wq=None) == 1 and call(work=None) == 1
+    assert call(ws=P + 4) == 4 and call(work=P + 128) == 4
+    assert call(wb=16) == 5
+    assert call(T=0, x=None, y=None, work=None, wb=0) == 0
+    assert call(T=0, K=133136 + 64) == 2          # exact int32 accumulation bound
+    assert wsb(16, 128, 64, 3) >= 16 * 128 + 16 * 4 * 2
+    assert wsb(4096, 128, 64, 3) > wsb(16, 128, 64, 3)
+    assert wsb(-1, 128, 64, 3) == 0 and wsb(16, 128, 64, 5) == 0
+
+
 def test_binding_refuses_host_tensors():
     import torch
     from paper_2603_04800_amd import ops

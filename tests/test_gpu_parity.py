@@ -206,28 +206,92 @@ def test_smoothquant_comparator_parity(ops, cfg_index):
     _check_layer(ops, L, name=f"smoothquant/cfg{cfg_index}")
 
 
-@pytest.mark.parametrize("cfg_index", [0, 1, 2])
-def test_mas_only_comparator_parity(ops, cfg_index):
-    """The MAS-only comparator (a weight per modality, no compensation;
-    Sec. 4.2) through masq_smooth_quant and per-run masq_w8a8_gemm calls:
-    outputs bit-exact against the oracle's layer, modality by modality
-    (every row)."""
+def _check_mas_only(L, mod_gpu=None, name=""):
+    """MAS-only layer through masq_mas_only_linear against the oracle's
+    layer run with each modality's own artifacts, every row bit for bit."""
     from paper_2603_04800_amd import workload
-    L = workload.layer(cfg_index, method="mas")
     x, mod, lin = workload.to_device(L)
+    if mod_gpu is not None:
+        mod = torch.from_numpy(mod_gpu).to(x.device)
     act = L["act_dtype"]
+    print(f"[mas-only] {name} T={x.shape[0]} K={lin.c_in} N={lin.c_out} M={lin.n_mod}", flush=True)
     y = lin(x, mod, out_dtype=torch.bfloat16 if act == "bf16" else torch.float32)
+    y2 = lin(x, mod, out_dtype=torch.bfloat16 if act == "bf16" else torch.float32)
     torch.cuda.synchronize()
+    assert torch.equal(y, y2), "reruns differ"
     mod_np = L["modality"]
-    rows = np.arange(mod_np.shape[0])
     y_np = _np(y)
     for m in range(L["n_mod"]):
-        rm = rows[mod_np[rows] == m]
+        rm = np.flatnonzero(mod_np == m)
         if rm.size == 0:
             continue
         ref = oinf.linear(L["x"][rm], np.zeros(rm.size, np.int32), L["inv_smooth"][m][None],
                           L["wq"][m], L["w_scale"][m])
-        assert np.array_equal(y_np[rm], oinf.to_output(ref, act)), f"modality {m} differs"
+        ref = oinf.to_output(ref, act)
+        bad = np.flatnonzero(np.any(y_np[rm] != ref, axis=1))
+        assert bad.size == 0, f"modality {m}: {bad.size} rows differ (first token {rm[bad[:4]]})"
+
+
+_MAS = [(c.index, p.name) for c in synth.CONFIGS for p in c.projections]
+
+
+@pytest.mark.parametrize("cfg_index,proj", _MAS, ids=[f"cfg{c}-{p}" for c, p in _MAS])
+def test_mas_only_comparator_parity(ops, cfg_index, proj):
+    """The MAS-only comparator (a weight per modality, no compensation;
+    Sec. 4.2) through masq_mas_only_linear: rows grouped by modality on the
+    device, every row bit-exact against the oracle's layer, on every
+    workload (interleaved runs included)."""
+    from paper_2603_04800_amd import workload
+    L = workload.layer(cfg_index, proj, method="mas")
+    _check_mas_only(L, name=f"cfg{cfg_index}/{proj}")
+
+
+def _random_mas_layer(T, K, N, M, act, layout="alternating", seed=0, counts=None):
+    rng = np.random.default_rng(seed)
+    if counts is None:
+        counts = [T // M + (1 if m < T % M else 0) for m in range(M)]
+    mod = synth.make_modality_layout(counts, layout, 0, seed)
+    x = rng.standard_normal((T, K)).astype(np.float32)
+    for m, sc in enumerate([1.0, 30.0, 2.0, 5.0][:M]):
+        x[mod == m] *= np.float32(sc)
+    from oracle.bf16 import bf16_round
+    if act == "bf16":
+        x = bf16_round(x)
+    return dict(x=x, modality=mod, inv_smooth=rng.uniform(0.05, 3.0, (M, K)).astype(np.float32),
+                wq=rng.integers(-127, 128, (M, N, K)).astype(np.int8),
+                w_scale=rng.uniform(1e-4, 1e-2, (M, N)).astype(np.float32),
+                l_down=np.zeros((max(M - 1, 0), 0, K), np.float32),
+                r_up=np.zeros((max(M - 1, 0), N, 0), np.float32), n_mod=M, rank=0,
+                act_dtype=act, lr_dtype="bf16", weight_bits=8, method="mas")
+
+
+_MAS_EDGE = {
+    "T1": dict(T=1, K=64, N=32, M=2, act="bf16"),
+    "alternating_3mod_ragged": dict(T=517, K=192, N=272, M=3, act="bf16"),
+    "runs_4mod_fp32": dict(T=1300, K=256, N=96, M=4, act="f32", layout="runs"),
+    "empty_modality": dict(T=300, K=128, N=64, M=3, act="bf16", counts=[150, 0, 150]),
+    "single_modality": dict(T=257, K=64, N=48, M=1, act="bf16"),
+    "all_vision": dict(T=600, K=128, N=80, M=2, act="bf16", counts=[0, 600]),
+    "decode_t16_split_k": dict(T=16, K=4096, N=512, M=2, act="bf16"),
+    "few_tiles_split_k": dict(T=700, K=2048, N=528, M=3, act="bf16", layout="runs"),
+}
+
+
+@pytest.mark.parametrize("name", list(_MAS_EDGE))
+def test_mas_only_edge_cases(ops, name):
+    kw = dict(_MAS_EDGE[name])
+    L = _random_mas_layer(kw.pop("T"), kw.pop("K"), kw.pop("N"), kw.pop("M"), kw.pop("act"),
+                          seed=11, **kw)
+    _check_mas_only(L, name=name)
+
+
+def test_mas_only_invalid_ids_read_as_text(ops):
+    L = _random_mas_layer(300, 128, 64, 3, "bf16", seed=5)
+    bad = np.array([0, 7, 150, 299])
+    mod_gpu = L["modality"].copy()
+    mod_gpu[bad] = np.array([3, -1, 1 << 20, 9], np.int32)
+    L["modality"][bad] = 0
+    _check_mas_only(L, mod_gpu=mod_gpu, name="invalid ids")
 
 
 # ------------------------------------------------------------------ edge cases
