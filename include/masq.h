@@ -73,10 +73,21 @@ typedef enum {
     MASQ_ERR_WORKSPACE = 5,   /* workspace smaller than the query says           */
     MASQ_ERR_HIP = 6,         /* a kernel launch was rejected by the runtime     */
     MASQ_ERR_UNSUPPORTED = 7, /* valid request this build does not implement     */
-    MASQ_ERR_SCRATCH = 8      /* needs more than the static scratch (below)      */
+    MASQ_ERR_SCRATCH = 8,     /* needs more than the static scratch (below)      */
+    /* not statuses: they make every int32 a value of the type, so that any
+     * integer a caller passes to masq_status_str is well defined */
+    MASQ_STATUS_RANGE_LO_ = -2147483647 - 1,
+    MASQ_STATUS_RANGE_HI_ = 2147483647
 } masq_status;
 
-typedef enum { MASQ_F32 = 0, MASQ_BF16 = 1 } masq_dtype;
+typedef enum {
+    MASQ_F32 = 0,
+    MASQ_BF16 = 1,
+    /* not dtypes: every int32 is a value of the type, so an unknown value
+     * reaches the library's check and gives MASQ_ERR_DTYPE */
+    MASQ_DTYPE_RANGE_LO_ = -2147483647 - 1,
+    MASQ_DTYPE_RANGE_HI_ = 2147483647
+} masq_dtype;
 
 /* Version of this interface (bumped on any signature or semantics change). */
 int masq_abi_version(void);

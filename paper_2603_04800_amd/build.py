@@ -71,9 +71,42 @@ def _build_lib(sources, lib, remarks: bool, verbose: bool) -> str:
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{res.stdout}{res.stderr}")
     os.replace(tmp, lib)
-    for o in objs:
-        os.remove(o)
     return lib
+
+
+SANITIZED_LIB = os.path.join(LIBDIR, "libmasq_sanitized.so")
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    """libmasq_sanitized.so: the library with the host code of its entry
+    points (argument validation, workspace planning, dispatch: masq_api.hip,
+    masq_calib.hip) built with AddressSanitizer and UndefinedBehaviorSanitizer;
+    device code is not instrumented.  Reuses the kernel object of build()
+    when it is present."""
+    os.makedirs(LIBDIR, exist_ok=True)
+    san = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+           "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-fno-sanitize-recover=all"]
+    objs = []
+    for src in SOURCES:
+        obj = os.path.join(LIBDIR, src.replace(".hip", ".o"))
+        if src in ("masq_api.hip", "masq_calib.hip"):
+            obj = os.path.join(LIBDIR, src.replace(".hip", "_sanitized.o"))
+            flags = [*compile_flags(), *san]
+        elif os.path.exists(obj):
+            objs.append(obj)
+            continue
+        else:
+            flags = compile_flags()
+        res = subprocess.run([hipcc(), *flags, "-c", os.path.join(CSRC, src), "-o", obj],
+                             capture_output=True, text=True)
+        if res.returncode != 0:
+            raise RuntimeError(f"hipcc failed for {src}:\n{res.stdout}{res.stderr}")
+        objs.append(obj)
+    res = subprocess.run([hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *san, *objs, "-o",
+                          SANITIZED_LIB], capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"link failed:\n{res.stdout}{res.stderr}")
+    return SANITIZED_LIB
 
 
 if __name__ == "__main__":

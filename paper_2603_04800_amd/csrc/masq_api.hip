@@ -316,6 +316,7 @@ const char* masq_status_str(masq_status s) {
         case MASQ_ERR_SCRATCH:
             return "MASQ_ERR_SCRATCH: the problem needs more than the static scratch "
                    "(MASQ_SCRATCH_BYTES); use masq_linear_fused with a workspace";
+        default: break;
     }
     return "MASQ_ERR_UNKNOWN";
 }

@@ -196,6 +196,33 @@ def test_mas_only_entry_point_validates(lib):
     assert wsb(-1, 128, 64, 3) == 0 and wsb(16, 128, 64, 5) == 0
 
 
+def test_validation_under_address_and_undefined_behaviour_sanitizers(tmp_path):
+    """tests/sanitized_validation.c, linked against the library whose
+    entry-point host code is built with ASan and UBSan, calls every entry
+    point with invalid arguments (and empty batches) and checks the status
+    codes; any sanitizer report fails the run."""
+    import shutil
+    import subprocess
+    clang = "/opt/rocm/llvm/bin/clang"
+    if not os.path.exists(clang) or shutil.which("hipcc") is None and not os.path.exists(
+            "/opt/rocm/bin/hipcc"):
+        pytest.skip("ROCm clang/hipcc not available")
+    from paper_2603_04800_amd import build
+    lib = build.build_sanitized()
+    exe = str(tmp_path / "sanitized_validation")
+    r = subprocess.run([clang, "-fsanitize=address,undefined", "-fno-omit-frame-pointer",
+                        "-fno-sanitize-recover=all", "-I", os.path.join(ROOT, "include"),
+                        os.path.join(ROOT, "tests", "sanitized_validation.c"),
+                        "-L", os.path.dirname(lib), "-lmasq_sanitized",
+                        "-Wl,-rpath," + os.path.dirname(lib), "-o", exe],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:halt_on_error=1",
+               UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
+    r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=120)
+    assert r.returncode == 0 and r.stdout.strip().endswith("ok"), r.stdout + r.stderr
+
+
 def test_binding_refuses_host_tensors():
     import torch
     from paper_2603_04800_amd import ops
