@@ -6,6 +6,7 @@
 #include "masq.h"
 #include "masq_common.h"
 
+#include <algorithm>
 #include <mutex>
 
 // Scratch of masq_linear_fused_noalloc: a file-scope device array, one copy
@@ -87,12 +88,23 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
         if (n_down_tickets > 0) w.tickets = w.zero_base;
         if (n_gk_tickets > 0) w.gk_tickets = w.zero_base ? w.zero_base + n_down_tickets : nullptr;
     }
+    // the slice partials of the wide down-projection (any activation dtype)
+    // and of k_down_lds (bf16 activations) are never needed by one call:
+    // they share one region, as large as the larger of the two
     w.dw_slices = w.dw_kslice = 0;
     w.dw_part = nullptr;
-    if (rank > 0 && rank <= 64 && n_mod > 1 && !small_path(T, K) && down_wide(T, K)) {
-        plan_down_wide(T, K, w.dw_slices, w.dw_kslice);
-        w.dw_part = reinterpret_cast<float*>(carve(static_cast<size_t>(w.dw_slices) * T *
-                                                   static_cast<size_t>(rank) * sizeof(float)));
+    w.dl_part = nullptr;
+    const bool cmc64 = rank > 0 && rank <= 64 && n_mod > 1 && !small_path(T, K);
+    const bool dw = cmc64 && down_wide(T, K);
+    const bool dl = kStage1SplitDown && cmc64 && K % 64 == 0;
+    if (dw) plan_down_wide(T, K, w.dw_slices, w.dw_kslice);
+    const size_t row_bytes = static_cast<size_t>(T) * static_cast<size_t>(rank) * sizeof(float);
+    const size_t part_bytes = std::max(dw ? w.dw_slices * row_bytes : 0,
+                                       dl ? down_lds_slices(K) * row_bytes : 0);
+    if (part_bytes > 0) {
+        float* p = reinterpret_cast<float*>(carve(part_bytes));
+        if (dw) w.dw_part = p;
+        if (dl) w.dl_part = p;
     }
     w.gk_part = nullptr;
     if (n_gk_tickets > 0)
@@ -233,6 +245,19 @@ masq_status fused_stage(const Fused& a, int stage) {
         st = from_hip(masq::launch_stage1_fused(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                 a.l_down, a.T, a.c_in, a.rank, a.n_mod, w.q,
                                                 w.x_scale, w.u, w.u_hl, w.zero_base, w.n_zero, s));
+        if (st != MASQ_OK) return st;
+    } else if ((stage & 1) && cmc && masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt)) &&
+               masq::down_lds_ok(to_dt(a.x_dt), a.c_in) && w.dl_part != nullptr) {
+        // rows too long for the registers: down-projection over 128-row
+        // tiles, then the quantisation adding its slice partials into u (and
+        // its bf16 hi/lo rows)
+        st = from_hip(masq::launch_down_lds(a.x, a.modality, a.inv_smooth, a.l_down, a.T, a.c_in,
+                                            a.rank, a.n_mod, w.dl_part, s));
+        if (st != MASQ_OK) return st;
+        const masq::UFinish fin{w.dl_part, masq::down_lds_slices(a.c_in), a.rank, w.u, w.u_hl};
+        st = from_hip(masq::launch_smooth_quant(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
+                                                a.T, a.c_in, a.n_mod, w.q, w.x_scale,
+                                                w.zero_base, w.n_zero, s, &fin));
         if (st != MASQ_OK) return st;
     } else if ((stage & 1) && cmc && masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt)) &&
                w.dw_part != nullptr) {

@@ -120,6 +120,7 @@ struct Workspace {
     int* zero_base;
     int dw_slices, dw_kslice;   // plan_down_wide (dw_part != nullptr)
     float* dw_part;    // [dw_slices][T][rank] fp32 partials of the wide down-projection
+    float* dl_part;    // [down_lds_slices(K)][T][rank] fp32 partials of k_down_lds
     int n_kslices;
     int kslice;
     size_t bytes;
@@ -168,6 +169,20 @@ inline bool stage1_fr_ok(DT x_dt, int64_t K, int n_mod) {
     return x_dt == DT::BF16 && K % 64 == 0 && K <= int64_t{kFrWaves} * kFrMaxPairs * 64 &&
            ((static_cast<int64_t>(n_mod) * K * 4 + 1023) / 1024) * 1024 <= kFrInvFloats * 4;
 }
+// Down-projection with the L1 fragments staged in LDS (k_down_lds): bf16
+// activations and factors, rank <= 64, K % 64 == 0; slice partials
+// [down_lds_slices(K)][T][rank] for the quantisation kernel to add.
+constexpr int64_t kDownLdsCols = 256;
+inline int down_lds_slices(int64_t K) { return static_cast<int>((K + kDownLdsCols - 1) / kDownLdsCols); }
+inline bool down_lds_ok(DT x_dt, int64_t K) { return x_dt == DT::BF16 && K % 64 == 0; }
+// Stage 1 of the fused layer for rows that k_stage1_fr cannot hold: k_down_lds,
+// then the quantisation adding its partials.  (For rows that it can hold,
+// k_stage1_fr doing both per 16 rows measured faster.)
+constexpr bool kStage1SplitDown = true;
+hipError_t launch_down_lds(const void* x, const int32_t* mod, const float* inv_s,
+                           const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
+                           float* part, hipStream_t s);
+
 hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
                                int8_t* q, float* x_scale, float* u, uint8_t* u_hl,

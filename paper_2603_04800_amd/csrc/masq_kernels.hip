@@ -1090,6 +1090,164 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
     }
 }
 
+// ---------------------------------------------------------------- down-projection, fragments in LDS
+// u = xs L1^m for bf16 activations and factors (rank <= 64), as slice
+// partials part[s][t][0 .. r) over k slices of kDlCols columns; grid
+// (ceil(T / 128), S).  A workgroup of 8 waves owns 128 rows and one slice:
+// the L1^m fragments of the slice (every k step and N block of up to two
+// non-text modalities present in the rows) are copied once into LDS by DMA,
+// in the MFMA operand order (one 1 KB block per fragment, lane l's 16 bytes
+// at 16 l), and shared by the 8 waves, each of which holds its 16 rows of the
+// slice in registers (the row layout of k_stage1_fr: lane l, row l % 16,
+// columns 64 p + 16 (l / 16) .. + 15 of pair p as two k steps).  So L1^m is
+// read from L2 once per 128 rows, not once per 16.  Rows of a third non-text
+// modality in the same 128 rows read their fragments from global memory.
+// Tiles without non-text rows return at once: text rows' partials are never
+// read (finish_u_row).
+constexpr int kDlPairs = 4;                         // 64-column pairs per slice
+constexpr int kDlCols = 64 * kDlPairs;
+static_assert(kDlCols == kDownLdsCols, "slice width of the workspace plan");
+constexpr int kDlRows = 128;
+constexpr int kDlWaves = kDlRows / 16;
+
+__global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
+    const bf16_t* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
+    const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod,
+    float* __restrict__ part) {
+    constexpr int kSteps = 2 * kDlPairs;
+    __shared__ __attribute__((aligned(16))) v4i sfrag[2][kSteps][4][64];    // 64 KB
+    __shared__ __attribute__((aligned(16))) float s_inv[4][kDlCols];
+    __shared__ int smod[kDlRows];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int ar = lane & 15, kg = lane >> 4;
+    const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kDlRows;
+    const int s = blockIdx.y;
+    const int npairs = K >> 6;
+    const int pb = s * kDlPairs;                    // first pair of the slice
+
+    if (tid < kDlRows) {
+        const int64_t t = row0 + tid;
+        smod[tid] = t < T ? sane_mod(mod[t], n_mod) : 0;
+    }
+    __syncthreads();
+    unsigned pres = 0;
+    {
+        const int m2 = smod[2 * lane], m3 = smod[2 * lane + 1];
+        for (int m = 1; m < n_mod; ++m)
+            if (__ballot(m2 == m || m3 == m) != 0ull) pres |= 1u << m;
+    }
+    const unsigned present = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(pres)));
+    if (present == 0) return;                      // uniform over the workgroup
+    int mods[3] = {0, 0, 0};
+    int np = 0;
+    for (int m = 1; m < n_mod; ++m)
+        if (present & (1u << m)) mods[np++] = m;
+    const int ncb = r >> 4;
+    const int nsl = min(np, 2);                     // modalities staged in LDS
+
+    // slice's factors of every modality (16-byte pieces, columns past K
+    // repeat the last piece), then the staged fragments: block b = (slot,
+    // step, N block), lane l's piece from row 16 nb + l % 16 of (L1^m)^T
+    {
+        const uint32_t si0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(s_inv));
+        const int pieces = n_mod * (kDlCols / 4);              // <= 256
+        for (int i = wave; i * 64 < pieces; i += kDlWaves) {
+            const int pc = min(i * 64 + lane, pieces - 1);
+            const int m = pc / (kDlCols / 4), c = 4 * (pc % (kDlCols / 4));
+            const int col = min(pb * 64 + c, K - 4);
+            lds_dma16(inv_s + static_cast<int64_t>(m) * K + col, si0 + i * 1024);
+        }
+        const uint32_t sf0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sfrag));
+        const int blocks = nsl * kSteps * 4;
+        for (int b = wave; b < blocks; b += kDlWaves) {
+            const int slot = b / (kSteps * 4), st = (b / 4) % kSteps, nb = b % 4;
+            const int gp = min(pb + (st >> 1), npairs - 1);
+            const bf16_t* src = l_down +
+                (static_cast<int64_t>(mods[slot] - 1) * r + 16 * min(nb, ncb - 1) + ar) * K +
+                64 * gp + 16 * kg + 8 * (st & 1);
+            lds_dma16(src, sf0 + b * 1024);
+        }
+    }
+    // this wave's 16 rows of the slice, every load in flight
+    const int64_t trow = row0 + 16 * wave + ar;
+    const bool valid = trow < T;
+    const bf16_t* xr = x + (valid ? trow : row0) * static_cast<int64_t>(K) + 16 * kg;
+    v4i xa[kDlPairs], xb[kDlPairs];
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int p = 0; p < kDlPairs; ++p) {
+        const int gp = min(pb + p, npairs - 1);
+        xa[p] = *reinterpret_cast<const v4i*>(xr + 64 * gp);
+        xb[p] = *reinterpret_cast<const v4i*>(xr + 64 * gp + 8);
+    }
+    asm volatile("" ::: "memory");
+    MASQ_WAIT_VMCNT_LGKM0(0);
+    __syncthreads();
+
+    const int mrow = smod[16 * wave + ar];
+    const v4i zero = {0, 0, 0, 0};
+    v4f acc[4];
+#pragma unroll
+    for (int jb = 0; jb < 4; ++jb) acc[jb] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int mi = 0; mi < np; ++mi) {
+        const int m = mods[mi];
+        const bool mine = valid && mrow == m;
+        if (__ballot(mine) == 0ull) continue;      // uniform over the wave
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st) {
+            const int p = st >> 1, h = st & 1;
+            const bool ok = mine && pb + p < npairs;
+            const int gp = min(pb + p, npairs - 1);
+            const v4i raw = h ? xb[p] : xa[p];
+            const float* sp = &s_inv[mrow][64 * p + 16 * kg + 8 * h];
+            const v4f s0 = *reinterpret_cast<const v4f*>(sp);
+            const v4f s1 = *reinterpret_cast<const v4f*>(sp + 4);
+            const float sv[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+            float xs[8];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                xs[2 * j] = __uint_as_float(static_cast<uint32_t>(raw[j]) << 16) * sv[2 * j];
+                xs[2 * j + 1] = __uint_as_float(static_cast<uint32_t>(raw[j]) & 0xFFFF0000u) * sv[2 * j + 1];
+            }
+            v4i hi, lo;
+            split_bf16x8(xs, hi, lo);
+            const v4i hh = ok ? hi : zero, ll = ok ? lo : zero;
+            v4i fb[4];
+            if (mi < 2) {
+#pragma unroll
+                for (int jb = 0; jb < 4; ++jb) fb[jb] = sfrag[mi][st][jb][lane];
+            } else {
+#pragma unroll
+                for (int jb = 0; jb < 4; ++jb)
+                    fb[jb] = *reinterpret_cast<const v4i*>(
+                        l_down + (static_cast<int64_t>(m - 1) * r + 16 * min(jb, ncb - 1) + ar) * K +
+                        64 * gp + 16 * kg + 8 * h);
+            }
+#pragma unroll
+            for (int jb = 0; jb < 4; ++jb)
+                acc[jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    __builtin_bit_cast(v8bf, hh), __builtin_bit_cast(v8bf, fb[jb]), acc[jb], 0, 0, 0);
+#pragma unroll
+            for (int jb = 0; jb < 4; ++jb)
+                acc[jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    __builtin_bit_cast(v8bf, ll), __builtin_bit_cast(v8bf, fb[jb]), acc[jb], 0, 0, 0);
+        }
+    }
+    // partials of the wave's rows: lane holds rows 4 (l / 16) + i, column
+    // 16 jb + l % 16
+    float* pp = part + static_cast<int64_t>(s) * T * r;
+#pragma unroll
+    for (int jb = 0; jb < 4; ++jb) {
+        if (jb >= ncb) break;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t t = row0 + 16 * wave + 4 * kg + i;
+            if (t < T) pp[t * r + 16 * jb + ar] = acc[jb][i];
+        }
+    }
+}
+
 // ---------------------------------------------------------------- fused stage 1, rows in registers
 // Stage 1 for bf16 activations (stage1_fr_ok shapes): a workgroup of
 // kFrWaves waves owns 16 RG rows, each wave a slice of the row in 64-column
@@ -1111,10 +1269,11 @@ __global__ __launch_bounds__(64 * kFrWaves) void k_stage1_fr(
     const bf16_t* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
     const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod,
     int8_t* __restrict__ q, float* __restrict__ x_scale, float* __restrict__ u,
-    uint8_t* __restrict__ u_hl, int* __restrict__ zero_ints, int n_zero) {
+    uint8_t* __restrict__ u_hl, int* __restrict__ zero_ints, int n_zero, UFinish fin) {
     constexpr int kRows = 16 * RG;
     if (blockIdx.x == 0)                           // arrival counters of stage 2
         for (int i = threadIdx.x; i < n_zero; i += blockDim.x) zero_ints[i] = 0;
+
     __shared__ __attribute__((aligned(16))) float s_inv[kFrInvFloats];
     __shared__ __attribute__((aligned(16))) float red[kFrWaves / 2][kRows][64];
     __shared__ int smod[kRows];
@@ -1166,6 +1325,15 @@ __global__ __launch_bounds__(64 * kFrWaves) void k_stage1_fr(
     MASQ_WAIT_VMCNT_LGKM0(2 * P * RG);
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
+    if (fin.part != nullptr) {
+        // u of the tile's rows from the down-projection's slice partials, while
+        // the rows are still arriving (wave w finishes rows w, w + kFrWaves, ..)
+        for (int i = wave; i < kRows; i += kFrWaves) {
+            const int64_t t = row0 + i;
+            if (t < T)
+                finish_u_row(t, T, smod[i] == 0, fin.part, fin.slices, fin.r, fin.u, fin.u_hl, lane);
+        }
+    }
 
     unsigned pres = 0;
 #pragma unroll
@@ -3050,14 +3218,15 @@ constexpr int kGemmWavesN = 4;
 static hipError_t launch_stage1_fr(const void* x, const int32_t* mod, const float* inv_s,
                                    const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
                                    int8_t* q, float* x_scale, float* u, uint8_t* u_hl,
-                                   int* zero_ints, int n_zero, hipStream_t s) {
+                                   int* zero_ints, int n_zero, hipStream_t s,
+                                   const UFinish& fin = UFinish{nullptr, 0, 0, nullptr, nullptr}) {
     const int P = static_cast<int>(((K / 64) + kFrWaves - 1) / kFrWaves);
     // one row group: two (sharing each L1 fragment) need more than a lane's
     // 256 registers from 4 pairs a wave on
     const dim3 grid(static_cast<unsigned>((T + 15) / 16)), block(64 * kFrWaves);
 #define MASQ_FR(PP) case PP: hipLaunchKernelGGL((k_stage1_fr<PP, 1>), grid, block, 0, s, \
         static_cast<const bf16_t*>(x), mod, inv_s, static_cast<const bf16_t*>(l_down), T, \
-        static_cast<int>(K), rank, n_mod, q, x_scale, u, u_hl, zero_ints, n_zero); break;
+        static_cast<int>(K), rank, n_mod, q, x_scale, u, u_hl, zero_ints, n_zero, fin); break;
     switch (P) {
         MASQ_FR(1) MASQ_FR(2) MASQ_FR(3) MASQ_FR(4) MASQ_FR(5) MASQ_FR(6) MASQ_FR(7) MASQ_FR(8)
         default: return hipErrorInvalidValue;
@@ -3070,10 +3239,10 @@ static hipError_t launch_stage1_fr(const void* x, const int32_t* mod, const floa
 hipError_t launch_smooth_quant(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                int64_t T, int64_t K, int n_mod, int8_t* q, float* x_scale,
                                int* zero_ints, int n_zero, hipStream_t s, const UFinish* fin_in) {
-    if (fin_in == nullptr && T > kSmallMaxT && stage1_fr_ok(x_dt, K, n_mod))
-        return launch_stage1_fr(x, mod, inv_s, nullptr, T, K, 0, n_mod, q, x_scale, nullptr,
-                                nullptr, zero_ints, n_zero, s);
     const UFinish fin = fin_in ? *fin_in : UFinish{nullptr, 0, 0, nullptr, nullptr};
+    if (T > kSmallMaxT && stage1_fr_ok(x_dt, K, n_mod))
+        return launch_stage1_fr(x, mod, inv_s, nullptr, T, K, 0, n_mod, q, x_scale, nullptr,
+                                nullptr, zero_ints, n_zero, s, fin);
     // a wave per row for large batches whose rows fit its register cache
     if (T >= kRowsPerWaveMinT && K <= 64 * 8 * 8) {
         const dim3 grid(static_cast<unsigned>((T + 3) / 4)), block(256);
@@ -3167,6 +3336,18 @@ hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const
         if (wide) MASQ_F1(float, 2, false); else MASQ_F1(float, 1, false);
     }
 #undef MASQ_F1
+    return hipGetLastError();
+}
+
+hipError_t launch_down_lds(const void* x, const int32_t* mod, const float* inv_s,
+                           const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
+                           float* part, hipStream_t s) {
+    const dim3 grid(static_cast<unsigned>((T + kDlRows - 1) / kDlRows),
+                    static_cast<unsigned>(down_lds_slices(K))),
+        block(64 * kDlWaves);
+    hipLaunchKernelGGL(k_down_lds, grid, block, 0, s, static_cast<const bf16_t*>(x), mod, inv_s,
+                       static_cast<const bf16_t*>(l_down), T, static_cast<int>(K), rank, n_mod,
+                       part);
     return hipGetLastError();
 }
 

@@ -371,6 +371,16 @@ _EDGE = {
                                       layout="runs"),
     "down_wide_f32_t1030_k8192_r48": dict(T=1030, K=8192, N=16, r=48, M=2, act="f32",
                                           lr="bf16"),
+    # down-projection with the L1 fragments in LDS (rows too long for the
+    # register-resident stage 1, or four modalities' factors too large for
+    # its LDS), then the quantisation adding the slice partials: ragged
+    # batch, rank 48, and a third non-text modality in one 128-row tile
+    # (its fragments read from global memory)
+    "down_lds_t600_k5120_r48": dict(T=600, K=5120, N=48, r=48, M=3, act="bf16", lr="bf16",
+                                    layout="runs"),
+    "down_lds_four_mod_alternating_k3584": dict(T=300, K=3584, N=32, r=64, M=4, act="bf16",
+                                                lr="bf16"),
+    "down_lds_t40_k4160_r16": dict(T=40, K=4160, N=64, r=16, M=2, act="bf16", lr="bf16"),
     # 32-row stage-1 workgroups (batches of 8192 tokens and more), ragged tail
     "stage1_wide_ragged_t8200": dict(T=8200, K=128, N=32, r=64, M=3, act="bf16", lr="bf16",
                                      layout="runs"),
