@@ -538,6 +538,10 @@ def _probe_lib():
     lib.masq_probe_mfma_i8_ops.restype = i64
     lib.masq_probe_read.argtypes = [p, i64, i32, p, p]
     lib.masq_probe_read.restype = ctypes.c_int
+    lib.masq_probe_lds_dma.argtypes = [p, i64, i32, i32, p, p]
+    lib.masq_probe_lds_dma.restype = ctypes.c_int
+    lib.masq_probe_lds_dma_bytes.argtypes = [i32, i32]
+    lib.masq_probe_lds_dma_bytes.restype = i64
     return lib
 
 
@@ -587,14 +591,26 @@ def measured_peaks(dev, reps: int = 7):
     half = nbytes // 2
     src, dst = buf[:half], buf[half:]
     t_copy = timed(lambda: dst.copy_(src))
-    del buf, out, rout
+    # L2 -> LDS by LDS DMA, rows spread over 3 MB (L2-resident on every XCD)
+    dblocks, diters = 256, 4000
+    dout = torch.empty(dblocks, dtype=torch.int32, device=dev)
+
+    def dma():
+        if lib.masq_probe_lds_dma(ctypes.c_void_p(buf.data_ptr()), 3 << 20, dblocks, diters,
+                                  ctypes.c_void_p(dout.data_ptr()), st) != 0:
+            raise RuntimeError("masq_probe_lds_dma failed")
+    t_dma = timed(dma)
+    dma_bytes = lib.masq_probe_lds_dma_bytes(dblocks, diters)
+    del buf, out, rout, dout
     torch.cuda.empty_cache()
     return {"int8_mfma_tops": round(ops / t_mfma / 1e12, 1),
             "hbm_read_gbps": round(nbytes / t_read / 1e9, 1),
             "hbm_copy_gbps": round(2 * half / t_copy / 1e9, 1),
+            "l2_to_lds_dma_gbps": round(dma_bytes / t_dma / 1e9, 1),
             "method": "median of 7 launches: v_mfma_i32_32x32x32_i8 issue loop (8 chains a "
                       "wave, 2048 x 4 waves, no memory traffic); linear 16-byte read of 4 GiB; "
-                      "2 GiB device copy"}
+                      "2 GiB device copy; LDS DMA of 16-row x 64-byte pieces from an "
+                      "L2-resident 3 MB region (256 x 8 waves)"}
 
 
 def _pct(vals, q):

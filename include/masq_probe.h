@@ -30,6 +30,17 @@ int64_t masq_probe_mfma_i8_ops(int32_t blocks, int32_t iters);
  * [blocks * 256], an xor of what each thread read. */
 int masq_probe_read(const void* buf, int64_t bytes, int32_t blocks, int32_t* out, void* stream);
 
+/* L2 -> LDS transfer through LDS DMA (global_load_lds_dwordx4), the path
+ * that feeds the GEMM's K stages: `blocks` workgroups of 8 waves, each wave
+ * moving `iters` rounds of four 1 KB instructions (16 rows x 64 bytes, the
+ * GEMM's stage-row pattern) into LDS, from rows spread over the first
+ * `region` bytes of buf (4 KB pitch; region >= 256 KB, buf 16-byte
+ * aligned).  Bytes moved: masq_probe_lds_dma_bytes(blocks, iters).  out:
+ * int32 [blocks]. */
+int masq_probe_lds_dma(const void* buf, int64_t region, int32_t blocks, int32_t iters,
+                       int32_t* out, void* stream);
+int64_t masq_probe_lds_dma_bytes(int32_t blocks, int32_t iters);
+
 #ifdef __cplusplus
 }
 #endif
