@@ -303,7 +303,8 @@ masq_status masq_quantize_weight(const float* w, const float* smooth_text, int64
  * smoothed calibration rows Z_m = X_m S_m^-1 of modality m, with the weight
  * difference dW_m = S_m W - Q(S_t W).  The whitening of Z_m (from its Gram
  * matrix) and the truncated SVD are built from these calls; their small
- * eigen-, QR and SVD decompositions stay with the caller.
+ * decompositions are the calls below (masq_cholesky, masq_trsm_right,
+ * masq_jacobi_svd).
  *
  * masq_gather_smoothed: z[i][c] = x[rows[i]][c] / smooth[c] in fp64 (the
  * operands are exact, the division correctly rounded), for i < n_rows; a
@@ -337,6 +338,58 @@ masq_status masq_weight_difference(const float* w, const float* smooth, const in
 masq_status masq_dgemm(int64_t m, int64_t n, int64_t k, const double* a, int64_t a_row_stride,
                        int64_t a_col_stride, const double* b, int64_t b_row_stride,
                        int64_t b_col_stride, double beta, double* c, int64_t ldc, void* stream);
+
+/* Factorisations of the compensation factors' calibration (Sec. 3.2 and
+ * 4.3; eq. l1l2), in fp64 on the GPU.  The whitening T of Z_m only has to
+ * satisfy T^T T = C with C = Z_m^T Z_m + eps I: the Cholesky factor T = L^T
+ * (C = L L^T) serves as well as the symmetric root, since T' = Q T with Q
+ * orthogonal leaves L1 = T^-1 U_r and L2 = Sigma_r V_r^T of the truncated
+ * SVD of T dW unchanged.  The randomized range finder's orthogonalisations
+ * are CholeskyQR (Gram matrix, its Cholesky factor, a triangular solve), and
+ * the SVD of the small projected matrix is a one-sided Jacobi SVD.
+ *
+ * masq_cholesky: a [n][n] (row stride lda >= n), symmetric, overwritten by
+ * L, lower triangular with L L^T = a + (ridge * tr(a) / n) I (only the lower
+ * triangle of a is read; the strict upper triangle of the result is zero).
+ * Blocked right-looking factorisation with 64 x 64 diagonal blocks.  info
+ * (device int32, 4-byte aligned) := 0, or k + 1 for the first pivot k that
+ * is not positive (which is then taken as 1 so that the call runs to its
+ * end; L is then meaningless); trace (device fp64, optional) := tr(a) before
+ * the shift.  0 <= n <= 65535 (n = 0 enqueues nothing and writes neither
+ * info nor trace); ridge >= 0 and finite.
+ *
+ * masq_trsm_right: y [m][n] (row stride ldy >= n) overwritten by the X with
+ * X L^T = Y (trans = 1) or X L = Y (trans = 0), for l [n][n] (row stride ldl
+ * >= n) lower triangular with a nonzero diagonal, as masq_cholesky leaves it
+ * (entries above the diagonal are not read).  Blocked by 64 columns: each
+ * diagonal block's solves row by row, the rest on the fp64 GEMM.  l and y
+ * must not overlap.
+ *
+ * masq_jacobi_svd: the SVD of the m x n matrix A whose column j is a[j * m ..
+ * j * m + m) (a is overwritten), 1 <= n <= 1024, by one-sided Jacobi
+ * rotations (round-robin pairs, a pair left alone when |a_p . a_q| <= 1e-15
+ * |a_p| |a_q| or when a column's squared norm is at most 1e-28 |A|_F^2, a
+ * numerically zero column) until a sweep rotates nothing or max_sweeps
+ * (1..1000) sweeps have run; the count goes to *sweeps (device int32,
+ * 4-byte aligned, required).  Each round of disjoint pairs is one launch (a
+ * workgroup a pair); unlike the other calls this one waits for the stream
+ * once per sweep, to read whether the sweep rotated anything.  Outputs, in
+ * decreasing singular value (ties in column order): sigma [n]; u [n][m], row
+ * j the left singular vector u_j (0 when sigma_j = 0), or sigma_j u_j with
+ * flags bit 0; v [n][n], row j the right singular vector v_j, or sigma_j v_j
+ * with flags bit 1; A = sum_j sigma_j u_j v_j^T.  v_work [n][n] is scratch.
+ * No output may overlap another or a.
+ *
+ * Pointers 8-byte aligned unless stated; violations return an error before
+ * anything is enqueued.
+ */
+masq_status masq_cholesky(int64_t n, double* a, int64_t lda, double ridge, int32_t* info,
+                          double* trace, void* stream);
+masq_status masq_trsm_right(int64_t m, int64_t n, const double* l, int64_t ldl, int32_t trans,
+                            double* y, int64_t ldy, void* stream);
+masq_status masq_jacobi_svd(int64_t m, int64_t n, double* a, double* v_work, double* sigma,
+                            double* u, double* v, int32_t flags, int32_t max_sweeps,
+                            int32_t* sweeps, void* stream);
 
 /* The MAS factor optimisation (Sec. 4.2, eq. mas_quant): per modality m,
  * minimise L(S_m) = mean |Q(X_m S_m^-1) Q(S_m W) - X_m W| over the

@@ -20,7 +20,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "libmasq.so")
-SOURCES = ("masq_kernels.hip", "masq_api.hip", "masq_calib.hip")
+SOURCES = ("masq_kernels.hip", "masq_api.hip", "masq_calib.hip", "masq_linalg.hip")
 # the benchmark's peak probes, a library of their own (not part of the layer)
 PROBE_SOURCES = ("masq_probe.hip",)
 PROBE_LIB = os.path.join(LIBDIR, "libmasq_probe.so")
@@ -80,7 +80,7 @@ SANITIZED_LIB = os.path.join(LIBDIR, "libmasq_sanitized.so")
 def build_sanitized(verbose: bool = False) -> str:
     """libmasq_sanitized.so: the library with the host code of its entry
     points (argument validation, workspace planning, dispatch: masq_api.hip,
-    masq_calib.hip) built with AddressSanitizer and UndefinedBehaviorSanitizer;
+    masq_calib.hip, masq_linalg.hip) built with AddressSanitizer and UndefinedBehaviorSanitizer;
     device code is not instrumented.  Reuses the kernel object of build()
     when it is present."""
     os.makedirs(LIBDIR, exist_ok=True)
@@ -89,7 +89,7 @@ def build_sanitized(verbose: bool = False) -> str:
     objs = []
     for src in SOURCES:
         obj = os.path.join(LIBDIR, src.replace(".hip", ".o"))
-        if src in ("masq_api.hip", "masq_calib.hip"):
+        if src in ("masq_api.hip", "masq_calib.hip", "masq_linalg.hip"):
             obj = os.path.join(LIBDIR, src.replace(".hip", "_sanitized.o"))
             flags = [*compile_flags(), *san]
         elif os.path.exists(obj):

@@ -155,120 +155,148 @@ def cmc_factors(z: np.ndarray, dw: np.ndarray, rank: int, ridge: float = 1e-6, s
     return l1, l2
 
 
-class _WhiteningGPU:
-    """_Whitening with its large products on the GPU (masq_dgemm): the Gram
-    matrix of Z (Z^T Z, or Z Z^T when Z has fewer rows than columns), the
-    thin basis P = Z^T U_z Sigma^-1, and every application of T or T^-1.
-    The eigen-decomposition of the Gram matrix and the diagonal scaling of
-    the small intermediate P^T A stay on the host, in the same order of
-    operations as _Whitening."""
+class _CholeskyWhitening:
+    """The whitening on the GPU: C = Z^T Z (masq_dgemm) + eps I with eps =
+    ridge * tr(Z^T Z) / K, factored C = L L^T (masq_cholesky), T = L^T.  T is
+    not the symmetric root that _Whitening applies, but T^T T = C is all the
+    factors depend on: with T' = Q T (Q orthogonal) the SVD of T' dW has left
+    vectors Q U and the same Sigma, V, so T'^-1 (Q U_r) = T^-1 U_r and L2 are
+    unchanged (and the seeded range finder's subspaces rotate by Q alike)."""
 
-    def __init__(self, z, ridge: float):
-        import torch
-
+    def __init__(self, z, ridge: float, info):
         from . import ops
-        self.ops, self.torch, self.dev = ops, torch, z.device
-        n, k = z.shape
-        if n >= k:
-            c = ops.dgemm(z.T, z).cpu().numpy()
-            eps = ridge * np.trace(c) / k
-            lam, p = np.linalg.eigh(c + eps * np.eye(k))
-            lam = np.maximum(lam, 0.0)
-            self.p = torch.from_numpy(np.ascontiguousarray(p)).to(self.dev)
-            self.sq = np.sqrt(lam)
-            self.isq = np.where(lam > 0, 1.0 / np.sqrt(np.where(lam > 0, lam, 1.0)), 0.0)
-            self.add = self.add_inv = 0.0
-        else:
-            mu, uz = np.linalg.eigh(ops.dgemm(z, z.T).cpu().numpy())
-            keep = mu > mu.max() * 1e-13 if mu.size and mu.max() > 0 else np.zeros(mu.shape, bool)
-            mu, uz = mu[keep], uz[:, keep]
-            sig = np.sqrt(mu)
-            eps = ridge * np.sum(mu) / k
-            self.p = ops.dgemm(z.T, torch.from_numpy(np.ascontiguousarray(uz / sig[None, :]))
-                               .to(self.dev))                 # [K][n] orthonormal columns
-            self.add = np.sqrt(eps)
-            self.sq = np.sqrt(sig ** 2 + eps) - self.add
-            with np.errstate(divide="ignore"):
-                base = 1.0 / self.add if eps > 0 else 0.0
-                self.isq = np.where(sig ** 2 + eps > 0, 1.0 / np.sqrt(sig ** 2 + eps), 0.0) - base
-            self.add_inv = base
+        self.ops = ops
+        self.l = ops.dgemm(z.T, z)                            # [K][K], then L in place
+        _, self.trace = ops.cholesky(self.l, ridge, info=info)
 
-    def _apply(self, a, d: np.ndarray, add: float):
-        t = self.ops.dgemm(self.p.T, a).cpu().numpy()
-        t = self.torch.from_numpy(np.ascontiguousarray(d[:, None] * t)).to(self.dev)
-        if add == 0.0:
-            return self.ops.dgemm(self.p, t)
-        return self.ops.dgemm(self.p, t, c=a.contiguous().clone(), beta=add)
+    def apply(self, a):                                    # T a = L^T a
+        return self.ops.dgemm(self.l.T, a)
 
-    def apply(self, a):                                    # T @ a, a [K][c] on the device
-        return self._apply(a, self.sq, self.add)
+    def apply_t(self, a):                                  # T^T a = L a
+        return self.ops.dgemm(self.l, a)
 
-    def apply_inv(self, a):                                # T^-1 @ a
-        return self._apply(a, self.isq, self.add_inv)
+    def solve_rows(self, ut):                              # rows of (T^-1 U)^T = U^T L^-1
+        return self.ops.trsm_right(self.l, ut, trans=False)
 
 
 class _NoWhitening:
     """T = I: the plain truncated SVD of dW, the non-whitened baseline that
     the paper's SQNR-against-rank comparison sets beside CMC (Sec. 5)."""
 
-    sq = np.ones(1)
+    l = None
 
     def apply(self, a):
         return a
 
-    def apply_inv(self, a):
+    def apply_t(self, a):
         return a
 
-
-def _qr_q(a):
-    """Q of the reduced QR factorisation of a device matrix (on the host)."""
-    import torch
-    q, _ = np.linalg.qr(a.cpu().numpy())
-    return torch.from_numpy(np.ascontiguousarray(q)).to(a.device)
+    def solve_rows(self, ut):
+        return ut
 
 
-def _truncated_svd_gpu(wh: _WhiteningGPU, dw, r: int, seed: int):
-    """_truncated_svd with the products on the GPU: the same seeded range
-    finder and power iterations; the QR factorisations of the K x ell and
-    N x ell blocks and the final SVDs on the host.  Returns host arrays."""
+class _InfoSlots:
+    """Device int32 slots for the info words of every Cholesky factorisation
+    of one calibration, checked once at the end (no synchronisation
+    between the steps)."""
+
+    def __init__(self, device, n: int = 64):
+        import torch
+        self.buf = torch.zeros((n,), dtype=torch.int32, device=device)
+        self.used = 0
+
+    def next(self):
+        if self.used == self.buf.shape[0]:
+            raise RuntimeError("too many factorisations for the info slots")
+        self.used += 1
+        return self.buf[self.used - 1:self.used]
+
+    def failed(self) -> bool:
+        return bool(self.buf[:self.used].any().item())
+
+
+def _cholqr(y, infos: _InfoSlots):
+    """Q of Y [m][n] (m >= n) = Q R, in place of Y, by shifted CholeskyQR3
+    (Fukaya, Kannan, Nakatsukasa, Yamamoto and Yanagisawa 2020): a first pass
+    with G + s I, s = 11 (m n + n (n + 1)) u tr(G) (robust for condition
+    numbers up to about 1/u), then two plain passes (CholeskyQR2); each pass
+    is G = Y^T Y (masq_dgemm), G + s I = L L^T (masq_cholesky) and Y := Y
+    L^-T (masq_trsm_right)."""
+    from . import ops
+    m, n = y.shape
+    shift_ridge = 11.0 * (m * n + n * (n + 1)) * 2.0 ** -53 * n   # s = ridge * tr(G) / n
+    for p in range(3):
+        g = ops.dgemm(y.T, y)
+        ops.cholesky(g, shift_ridge if p == 0 else 0.0, info=infos.next())
+        ops.trsm_right(g, y, trans=True)
+    return y
+
+
+def _cmc_factors_device(wh, dw, r: int, seed: int, infos: _InfoSlots):
+    """L1^T [r][K] and L2^T [N][r] on the GPU from the whitening wh and dW
+    [K][N], as _truncated_svd and cmc_factors define them: the exact SVD of
+    T dW for small layers, else the seeded randomized range finder (the same
+    Gaussian test matrix as the host's, drawn by NumPy from the seed, with
+    CholeskyQR orthogonalisations) and the SVD of q^T T dW.  Each SVD is the
+    one-sided Jacobi SVD (masq_jacobi_svd) of the matrix whose columns are
+    the rows of the factored matrix M: M^T = U S V^T, so M = V S U^T."""
     import torch
 
     from . import ops
     k, n = dw.shape
+    dev = dw.device
     if min(k, n) <= EXACT_SVD_MAX or r >= min(k, n) // 2:
-        u, s, vt = np.linalg.svd(wh.apply(dw).cpu().numpy(), full_matrices=False)
-        return u[:, :r], s[:r], vt[:r]
+        if k <= n:
+            # M = T dW [K][N]: left vectors V, L2^T = (U S)_r
+            a = wh.apply(dw) if wh.l is not None else dw.clone()
+            _, us_rows, v_rows, _ = ops.jacobi_svd(a, flags=1)
+            return wh.solve_rows(v_rows[:r].contiguous()), us_rows[:r].T
+        # M = (T dW)^T = dW^T L [N][K]: T dW = U S V^T with U, V the Jacobi
+        # SVD's of the columns of T dW (the rows of M); L2 = S V^T
+        at = ops.dgemm(dw.T, wh.l) if wh.l is not None else dw.T.contiguous()
+        _, u_rows, vs_rows, _ = ops.jacobi_svd(at, flags=2)
+        return wh.solve_rows(u_rows[:r].contiguous()), vs_rows[:r].T
     rng = np.random.default_rng(seed)
     ell = min(r + 10, k, n)
-    omega = torch.from_numpy(rng.standard_normal((n, ell))).to(dw.device)
-    q = _qr_q(wh.apply(ops.dgemm(dw, omega)))
+    omega = torch.from_numpy(rng.standard_normal((n, ell))).to(dev)
+    q = _cholqr(wh.apply(ops.dgemm(dw, omega)), infos)                # [K][ell]
     for _ in range(2):
-        q = _qr_q(ops.dgemm(dw.T, wh.apply(q)))
-        q = _qr_q(wh.apply(ops.dgemm(dw, q)))
-    b = ops.dgemm(dw.T, wh.apply(q)).cpu().numpy().T     # q^T T dW, ell x n
-    ub, s, vt = np.linalg.svd(b, full_matrices=False)
-    return (q.cpu().numpy() @ ub)[:, :r], s[:r], vt[:r]
+        q = _cholqr(ops.dgemm(dw.T, wh.apply_t(q)), infos)            # [N][ell]
+        q = _cholqr(wh.apply(ops.dgemm(dw, q)), infos)                # [K][ell]
+    # B = q^T T dW = (L q)^T dW [ell][N], its rows the columns of B^T = U S
+    # V^T: B = V S U^T, the left vectors of T dW are q V, L2^T = (U S)_r
+    b = ops.dgemm(wh.apply_t(q).T, dw)
+    _, us_rows, v_rows, _ = ops.jacobi_svd(b, flags=1)
+    return wh.solve_rows(ops.dgemm(v_rows[:r], q.T)), us_rows[:r].T
 
 
 def cmc_factors_gpu(z, dw, rank: int, ridge: float = 1e-6, seed: int = 0,
                     whiten: bool = True):
     """cmc_factors from device inputs: z [n][K] and dw [K][N] fp64 tensors
-    (masq_gather_smoothed, masq_weight_difference).  Returns host L1 [K][r],
-    L2 [r][N].  whiten=False drops the whitening (T = I): the best rank-r
-    approximation of dW itself."""
-    import torch
+    (masq_gather_smoothed, masq_weight_difference), every step on the GPU:
+    the Gram matrix and its Cholesky factor (the whitening), the exact or
+    seeded randomized truncated SVD (CholeskyQR orthogonalisations, Jacobi
+    SVD of the small factor) and T^-1 U_r by triangular solves.  Returns host
+    L1 [K][r], L2 [r][N] (copied back once, with the check of every
+    factorisation's info word).  whiten=False drops the whitening (T = I):
+    the best rank-r approximation of dW itself."""
     k, n = dw.shape
     l1 = np.zeros((k, rank))
     l2 = np.zeros((rank, n))
     if rank == 0 or z.shape[0] == 0:
         return l1, l2
-    wh = _WhiteningGPU(z, ridge) if whiten else _NoWhitening()
-    if not np.any(wh.sq):                 # Z = 0: no whitening, no compensation
+    infos = _InfoSlots(dw.device)
+    wh = _CholeskyWhitening(z, ridge, infos.next()) if whiten else _NoWhitening()
+    rr = min(rank, k, n)
+    l1t, l2t = _cmc_factors_device(wh, dw, rr, seed, infos)
+    l1t_h, l2t_h = l1t.cpu().numpy(), l2t.cpu().numpy()
+    if whiten and float(wh.trace.item()) == 0.0:          # Z = 0: no whitening, no compensation
         return l1, l2
-    u, s, vt = _truncated_svd_gpu(wh, dw, min(rank, k, n), seed)
-    rr = s.shape[0]
-    l1[:, :rr] = wh.apply_inv(torch.from_numpy(np.ascontiguousarray(u)).to(dw.device)).cpu().numpy()
-    l2[:rr] = s[:, None] * vt
+    if infos.failed():
+        raise RuntimeError("a Cholesky factorisation of the calibration failed "
+                           "(matrix not positive definite)")
+    l1[:, :rr] = l1t_h.T
+    l2[:rr] = l2t_h.T
     return l1, l2
 
 

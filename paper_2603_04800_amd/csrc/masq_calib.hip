@@ -210,22 +210,24 @@ __global__ __launch_bounds__(256) void k_weight_difference(const float* __restri
     }
 }
 
-// C [m][n] (row stride ldc) = A B (+ beta C), fp64, with A (i, k) at
-// a[i * ars + k * acs] and B (k, j) at b[k * brs + j * bcs], so transposed
-// operands are strides, not copies.  TL x TL tiles (128, or 64 when the
-// 128-tiles would not give every CU one), 256 threads of TL/16 x TL/16
-// outputs (rows ty + 16 u, columns tx + 16 v), k in steps of 16 staged
+// C (i, j) at c[i * crs + j * ccs] = alpha A B (+ beta C), fp64, with A (i,
+// k) at a[i * ars + k * acs] and B (k, j) at b[k * brs + j * bcs], so
+// transposed operands are strides, not copies.  TL x TL tiles (128, or 64
+// when the 128-tiles would not give every CU one), 256 threads of TL/16 x
+// TL/16 outputs (rows ty + 16 u, columns tx + 16 v), k in steps of 16 staged
 // through LDS with the next step's loads in flight.  Every element is summed
-// in increasing k by fused multiply-adds, whatever the tile size; beta C is
-// added after.
+// in increasing k by fused multiply-adds, whatever the tile size; the sum is
+// then multiplied by alpha (exact for alpha = +-1) and beta C added.  With
+// lower, tiles wholly above the diagonal (every j > i) are skipped.
 constexpr int kDgTile = 128;
 constexpr int kDgStep = 16;
 template <int TL>
 __global__ __launch_bounds__(256) void k_dgemm(int64_t M, int64_t N, int64_t K,
                                                const double* __restrict__ a, int64_t ars,
                                                int64_t acs, const double* __restrict__ b,
-                                               int64_t brs, int64_t bcs, double beta,
-                                               double* __restrict__ c, int64_t ldc) {
+                                               int64_t brs, int64_t bcs, double alpha, double beta,
+                                               double* __restrict__ c, int64_t crs, int64_t ccs,
+                                               int lower) {
     constexpr int NU = TL / 16, NQ = TL * kDgStep / 256;     // outputs a row, loads per operand
     constexpr int LT = TL == 128 ? 7 : 6;                    // log2(TL)
     __shared__ double as[kDgStep][TL + 1];
@@ -233,6 +235,7 @@ __global__ __launch_bounds__(256) void k_dgemm(int64_t M, int64_t N, int64_t K,
     const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
     const int64_t i0 = static_cast<int64_t>(blockIdx.y) * TL;
     const int64_t j0 = static_cast<int64_t>(blockIdx.x) * TL;
+    if (lower && j0 > i0 + TL - 1) return;                   // block-uniform
     // staging: element e = tid + 256 q of each TL x 16 operand block; the
     // fastest-moving index follows the operand's unit-stride direction
     const bool a_k_fast = acs == 1, b_k_fast = bcs != 1;
@@ -295,9 +298,9 @@ __global__ __launch_bounds__(256) void k_dgemm(int64_t M, int64_t N, int64_t K,
         for (int v = 0; v < NU; ++v) {
             const int64_t j = j0 + tx + 16 * v;
             if (j < N) {
-                double r = acc[u][v];
-                if (beta != 0.0) r = r + beta * c[i * ldc + j];
-                c[i * ldc + j] = r;
+                double r = alpha * acc[u][v];
+                if (beta != 0.0) r = r + beta * c[i * crs + j * ccs];
+                c[i * crs + j * ccs] = r;
             }
         }
     }
@@ -379,6 +382,27 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 bool aligned8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
 
 }  // namespace
+
+namespace masq {
+
+hipError_t launch_dgemm(int64_t m, int64_t n, int64_t k, const double* a, int64_t ars,
+                        int64_t acs, const double* b, int64_t brs, int64_t bcs, double alpha,
+                        double beta, double* c, int64_t crs, int64_t ccs, bool lower,
+                        hipStream_t s) {
+    if (m <= 0 || n <= 0) return hipSuccess;
+    const int64_t tiles = ((n + kDgTile - 1) / kDgTile) * ((m + kDgTile - 1) / kDgTile);
+    const int tl = (tiles < 256 && (m + 63) / 64 <= 65535) ? 64 : kDgTile;
+    const dim3 grid(static_cast<unsigned>((n + tl - 1) / tl), static_cast<unsigned>((m + tl - 1) / tl));
+    if (tl == 64)
+        hipLaunchKernelGGL(k_dgemm<64>, grid, dim3(256), 0, s, m, n, k, a, ars, acs, b, brs, bcs,
+                           alpha, beta, c, crs, ccs, lower ? 1 : 0);
+    else
+        hipLaunchKernelGGL(k_dgemm<kDgTile>, grid, dim3(256), 0, s, m, n, k, a, ars, acs, b, brs,
+                           bcs, alpha, beta, c, crs, ccs, lower ? 1 : 0);
+    return hipGetLastError();
+}
+
+}  // namespace masq
 
 extern "C" {
 
@@ -501,18 +525,11 @@ masq_status masq_dgemm(int64_t m, int64_t n, int64_t k, const double* a, int64_t
     if (!c || (k > 0 && (!a || !b))) return MASQ_ERR_NULL;
     if (!aligned8(c) || (k > 0 && (!aligned8(a) || !aligned8(b)))) return MASQ_ERR_ALIGN;
     (void)hipGetLastError();
-    const int64_t tiles = ((n + kDgTile - 1) / kDgTile) * ((m + kDgTile - 1) / kDgTile);
-    const int tl = (tiles < 256 && (m + 63) / 64 <= 65535) ? 64 : kDgTile;
-    const dim3 grid(static_cast<unsigned>((n + tl - 1) / tl), static_cast<unsigned>((m + tl - 1) / tl));
-    if (tl == 64)
-        hipLaunchKernelGGL(k_dgemm<64>, grid, dim3(256), 0, static_cast<hipStream_t>(stream), m, n,
-                           k, a, a_row_stride, a_col_stride, b, b_row_stride, b_col_stride, beta, c,
-                           ldc);
-    else
-        hipLaunchKernelGGL(k_dgemm<kDgTile>, grid, dim3(256), 0, static_cast<hipStream_t>(stream), m,
-                           n, k, a, a_row_stride, a_col_stride, b, b_row_stride, b_col_stride, beta,
-                           c, ldc);
-    return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
+    return masq::launch_dgemm(m, n, k, a, a_row_stride, a_col_stride, b, b_row_stride,
+                              b_col_stride, 1.0, beta, c, ldc, 1, false,
+                              static_cast<hipStream_t>(stream)) == hipSuccess
+               ? MASQ_OK
+               : MASQ_ERR_HIP;
 }
 
 masq_status masq_dequantize_rows(const int8_t* codes, const float* scale, int64_t rows,

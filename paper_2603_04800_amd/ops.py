@@ -56,6 +56,9 @@ _SIGS = {
     "masq_weight_difference": ([_p, _p, _p, _p, _i64, _i64, _p, _p], ctypes.c_int),
     "masq_dgemm": ([_i64, _i64, _i64, _p, _i64, _i64, _p, _i64, _i64, ctypes.c_double, _p, _i64,
                     _p], ctypes.c_int),
+    "masq_cholesky": ([_i64, _p, _i64, ctypes.c_double, _p, _p, _p], ctypes.c_int),
+    "masq_trsm_right": ([_i64, _i64, _p, _i64, _i32, _p, _i64, _p], ctypes.c_int),
+    "masq_jacobi_svd": ([_i64, _i64, _p, _p, _p, _p, _p, _i32, _i32, _p, _p], ctypes.c_int),
     "masq_dequantize_rows": ([_p, _p, _i64, _i64, _p, _p], ctypes.c_int),
     "masq_mae_partials": ([_i64], _i64),
     "masq_mae_sign": ([_p, _p, _i64, _p, _p, _p], ctypes.c_int),
@@ -266,6 +269,60 @@ def dgemm(a, b, c=None, beta=0.0, stream=None):
         m, n, k, _view_ptr(a), a.stride(0), a.stride(1), _view_ptr(b), b.stride(0), b.stride(1),
         float(beta), _ptr(c), n, _stream(stream)))
     return c
+
+
+def _square_f64(a, name):
+    _need(a, torch.float64, name)
+    if a.dim() != 2 or a.shape[0] != a.shape[1]:
+        raise ValueError(f"{name} must be a square matrix")
+
+
+def cholesky(a, ridge=0.0, info=None, trace=None, stream=None):
+    """In place: a := L with L L^T = a + (ridge tr(a) / n) I, L lower (the
+    upper triangle zeroed).  Returns (info, trace): device int32 [1] (0, or
+    k + 1 when the leading minor of order k + 1 is not positive) and fp64 [1]
+    (tr(a) before the shift); pass views to have them written elsewhere."""
+    _square_f64(a, "a")
+    n = a.shape[0]
+    if info is None:
+        info = torch.zeros((1,), dtype=torch.int32, device=a.device)
+    if trace is None:
+        trace = torch.zeros((1,), dtype=torch.float64, device=a.device)
+    _check("masq_cholesky", _lib.masq_cholesky(n, _ptr(a), n, float(ridge), _view_ptr(info),
+                                               _view_ptr(trace), _stream(stream)))
+    return info, trace
+
+
+def trsm_right(l, y, trans, stream=None):
+    """In place on y [m][n]: X with X L^T = Y (trans) or X L = Y, for the
+    lower-triangular L [n][n] of cholesky()."""
+    _square_f64(l, "l")
+    _need(y, torch.float64, "y")
+    m, n = y.shape
+    if l.shape[0] != n:
+        raise ValueError(f"l must be [{n}][{n}]")
+    _check("masq_trsm_right", _lib.masq_trsm_right(m, n, _ptr(l), n, 1 if trans else 0, _ptr(y), n,
+                                                   _stream(stream)))
+    return y
+
+
+def jacobi_svd(cols, flags=0, max_sweeps=60, stream=None):
+    """SVD of the m x n matrix whose columns are the rows of cols [n][m]
+    (overwritten): (sigma [n] decreasing, u [n][m], v [n][n], sweeps) with
+    the matrix = sum_j sigma_j u_j v_j^T; u_j is scaled by sigma_j with flag
+    bit 0, v_j with bit 1."""
+    _need(cols, torch.float64, "cols")
+    n, m = cols.shape
+    dev = cols.device
+    vw = torch.empty((n, n), dtype=torch.float64, device=dev)
+    sigma = torch.empty((n,), dtype=torch.float64, device=dev)
+    u = torch.empty((n, m), dtype=torch.float64, device=dev)
+    v = torch.empty((n, n), dtype=torch.float64, device=dev)
+    sweeps = torch.empty((1,), dtype=torch.int32, device=dev)
+    _check("masq_jacobi_svd", _lib.masq_jacobi_svd(m, n, _ptr(cols), _ptr(vw), _ptr(sigma),
+                                                   _ptr(u), _ptr(v), flags, max_sweeps,
+                                                   _ptr(sweeps), _stream(stream)))
+    return sigma, u, v, sweeps
 
 
 def dequantize_rows(codes, scale, stream=None):

@@ -36,12 +36,13 @@ def sqnr_db(y_ref: np.ndarray, y: np.ndarray) -> np.ndarray:
 
 
 def _singular_values_gpu(a):
-    """Singular values of a device fp64 matrix from the eigenvalues of its
-    smaller Gram matrix (masq_dgemm, then the host's symmetric eigensolver)."""
+    """Singular values (decreasing) of a device fp64 matrix whose smaller
+    dimension is at most 1024: the one-sided Jacobi SVD (masq_jacobi_svd) of
+    the matrix whose columns are the rows (or the columns) of a."""
     from . import ops
-    g = ops.dgemm(a.T, a) if a.shape[0] >= a.shape[1] else ops.dgemm(a, a.T)
-    lam = np.linalg.eigvalsh(g.cpu().numpy())
-    return np.sqrt(np.maximum(lam, 0.0))[::-1]
+    cols = a.clone() if a.shape[0] <= a.shape[1] else a.T.contiguous()
+    sigma, _, _, _ = ops.jacobi_svd(cols)
+    return sigma.cpu().numpy()
 
 
 def cmc_study(workload: int, ranks=None, weight_bits: int = 4, device: str = "cuda:0"):
@@ -88,7 +89,8 @@ def cmc_study(workload: int, ranks=None, weight_bits: int = 4, device: str = "cu
         sm = s_t[m].contiguous()
         z = ops.gather_smoothed(xt, sel, sm)
         dw = ops.weight_difference(wt, sm, wq_t, ws_t)
-        wh = calibrate._WhiteningGPU(z, 1e-6)
+        wh = calibrate._CholeskyWhitening(z, 1e-6, torch.zeros((1,), dtype=torch.int32,
+                                                                device=dev))
         rows.append(dict(kind="effective_rank", workload=cfg.name, modality=m,
                          weight_bits=weight_bits, c_in=k, c_out=n,
                          plain=round(effective_rank(_singular_values_gpu(dw)), 2),

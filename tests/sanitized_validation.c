@@ -65,6 +65,14 @@ int main(void) {
                                 NULL), MASQ_ERR_WORKSPACE);
     expect("dgemm negative m",
            masq_dgemm(-1, 4, 4, P, 4, 1, P, 4, 1, 0.0, P, 4, NULL), MASQ_ERR_SHAPE);
+    expect("cholesky lda < n", masq_cholesky(8, (double*)P, 4, 0.0, (int32_t*)P, NULL, NULL),
+           MASQ_ERR_SHAPE);
+    expect("cholesky empty", masq_cholesky(0, NULL, 0, 0.0, (int32_t*)P, NULL, NULL), MASQ_OK);
+    expect("trsm bad trans",
+           masq_trsm_right(4, 8, (const double*)P, 8, 2, (double*)P, 8, NULL), MASQ_ERR_SHAPE);
+    expect("jacobi too wide",
+           masq_jacobi_svd(4, 1025, (double*)P, (double*)P, (double*)P, (double*)P, (double*)P, 0,
+                           10, NULL, NULL), MASQ_ERR_SHAPE);
     expect("channel range bad dtype",
            masq_channel_range(P, (masq_dtype)7, P, 8, 64, 2, P, NULL), MASQ_ERR_DTYPE);
     if (masq_linear_fused_workspace_bytes(-1, 64, 64, 16, 2) != 0) {

@@ -315,6 +315,44 @@ def test_cmc_calibration_calls_validate(lib):
     assert dg(0, 4, 4, None, 4, 1, None, 4, 1, one, None, 4, None) == 0   # empty output
 
 
+def test_factorisation_calls_validate(lib):
+    """masq_cholesky, masq_trsm_right and masq_jacobi_svd check sizes,
+    pointers and alignment before enqueueing anything; empty problems
+    enqueue nothing."""
+    import ctypes
+    P = 1 << 20
+    ch, tr, jb = lib.masq_cholesky, lib.masq_trsm_right, lib.masq_jacobi_svd
+    z = ctypes.c_double(0.0)
+    assert ch(-1, P, 4, z, P, None, None) == 2                   # n < 0
+    assert ch(8, P, 4, z, P, None, None) == 2                    # lda < n
+    assert ch(65536, P, 65536, z, P, None, None) == 2            # n too large
+    assert ch(8, P, 8, ctypes.c_double(-1.0), P, None, None) == 2    # negative ridge
+    assert ch(8, P, 8, ctypes.c_double(float("nan")), P, None, None) == 2
+    assert ch(8, P, 8, ctypes.c_double(float("inf")), P, None, None) == 2
+    assert ch(8, P, 8, z, None, None, None) == 1                 # no info word
+    assert ch(8, None, 8, z, P, None, None) == 1                 # no matrix
+    assert ch(8, P + 4, 8, z, P, None, None) == 4                # misaligned matrix
+    assert ch(8, P, 8, z, P + 2, None, None) == 4                # misaligned info
+    assert ch(8, P, 8, z, P, P + 4, None) == 4                   # misaligned trace
+    assert ch(0, None, 0, z, P, None, None) == 0                 # empty
+    assert tr(-1, 4, P, 4, 1, P, 4, None) == 2                   # m < 0
+    assert tr(4, 8, P, 4, 1, P, 8, None) == 2                    # ldl < n
+    assert tr(4, 8, P, 8, 1, P, 4, None) == 2                    # ldy < n
+    assert tr(4, 8, P, 8, 2, P, 8, None) == 2                    # trans not 0 or 1
+    assert tr(4, 8, None, 8, 1, P, 8, None) == 1                 # no factor
+    assert tr(4, 8, P, 8, 0, P + 4, 8, None) == 4                # misaligned Y
+    assert tr(0, 8, None, 8, 1, None, 8, None) == 0              # no rows
+    assert jb(4, 0, P, P, P, P, P, 0, 10, None, None) == 2       # n < 1
+    assert jb(4, 1025, P, P, P, P, P, 0, 10, None, None) == 2    # n > 1024
+    assert jb(0, 4, P, P, P, P, P, 0, 10, None, None) == 2       # m < 1
+    assert jb(4, 4, P, P, P, P, P, 4, 10, None, None) == 2       # unknown flag
+    assert jb(4, 4, P, P, P, P, P, 0, 0, None, None) == 2        # no sweeps allowed
+    assert jb(4, 4, P, P, None, P, P, 0, 10, P, None) == 1       # no sigma
+    assert jb(4, 4, P, P, P, P, P, 0, 10, None, None) == 1       # no sweep counter
+    assert jb(4, 4, P, P, P, P + 4, P, 0, 10, P, None) == 4      # misaligned u
+    assert jb(4, 4, P, P, P, P, P, 0, 10, P + 2, None) == 4      # misaligned sweeps
+
+
 def test_mas_optimisation_calls_validate(lib):
     """masq_dequantize_rows, masq_mae_sign and masq_mas_gradient check their
     arguments before enqueueing anything; masq_mae_partials is plain host

@@ -294,3 +294,125 @@ def test_dgemm_result_does_not_depend_on_the_tile_size(ops):
     assert torch.equal(whole[256:384], part)
     part_t = ops.dgemm(b.T[:200], a.T)                      # transposed views, small grid
     assert torch.equal(ops.dgemm(b.T, a.T)[:200], part_t)
+
+
+# ------------------------------------------------ factorisations (Sec. 3.2, 4.3)
+
+def _spd(rng, n, cond=1e3):
+    q, _ = np.linalg.qr(rng.standard_normal((n, n)))
+    lam = np.geomspace(1.0, 1.0 / cond, n)
+    return (q * lam[None, :]) @ q.T
+
+
+@pytest.mark.parametrize("n", [1, 5, 63, 64, 65, 200, 700])
+def test_cholesky_matches_lapack(ops, n):
+    """masq_cholesky: lower L with L L^T = C + (ridge tr(C) / n) I, the upper
+    triangle zero, the trace reported, against LAPACK's factor of the same
+    shifted matrix (unique for an SPD matrix) within its perturbation bound."""
+    rng = np.random.default_rng(n)
+    c = _spd(rng, n)
+    c = (c + c.T) / 2
+    ridge = 1e-3
+    a = torch.from_numpy(c.copy()).to("cuda:0")
+    info, trace = ops.cholesky(a, ridge)
+    l = a.cpu().numpy()
+    assert int(info.item()) == 0
+    assert abs(float(trace.item()) - np.trace(c)) <= 1e-13 * abs(np.trace(c))
+    cs = c + ridge * np.trace(c) / n * np.eye(n)
+    ref = np.linalg.cholesky(cs)
+    assert np.all(np.triu(l, 1) == 0.0)
+    assert np.abs(l - ref).max() <= 1e-12 * np.abs(ref).max() * max(n, 1)
+    assert np.abs(l @ l.T - cs).max() <= 1e-14 * n * np.abs(cs).max()
+
+
+def test_cholesky_reports_the_first_bad_pivot(ops):
+    """A matrix whose third leading minor is not positive: info = 3 (across a
+    block boundary too: the pivot of row 70 gives 71)."""
+    for bad in (2, 70):
+        c = np.eye(100)
+        c[bad, bad] = -1.0
+        a = torch.from_numpy(c).to("cuda:0")
+        info, _ = ops.cholesky(a)
+        assert int(info.item()) == bad + 1
+
+
+@pytest.mark.parametrize("m,n", [(1, 1), (300, 130), (37, 64), (1000, 74), (5, 200)])
+@pytest.mark.parametrize("trans", [True, False])
+def test_trsm_right_solves(ops, m, n, trans):
+    """masq_trsm_right: X L^T = Y or X L = Y for a Cholesky factor L, against
+    the host solve, within the conditioning bound."""
+    rng = np.random.default_rng(m * 7 + n + trans)
+    l = np.linalg.cholesky(_spd(rng, n, cond=1e2))
+    y = rng.standard_normal((m, n))
+    ref = np.linalg.solve(l, y.T).T if trans else np.linalg.solve(l.T, y.T).T
+    lt = torch.from_numpy(l).to("cuda:0")
+    yt = torch.from_numpy(y.copy()).to("cuda:0")
+    ops.trsm_right(lt, yt, trans)
+    x = yt.cpu().numpy()
+    assert np.abs(x - ref).max() <= 1e-11 * np.abs(ref).max()
+
+
+@pytest.mark.parametrize("m,n", [(1, 1), (3, 2), (74, 74), (500, 74), (40, 90), (512, 256)])
+@pytest.mark.parametrize("flags", [0, 1, 2])
+def test_jacobi_svd_matches_lapack(ops, m, n, flags):
+    """masq_jacobi_svd of the m x n matrix given by columns: singular values
+    (decreasing) equal LAPACK's to fp64 rounding, the factors reconstruct
+    the matrix and are orthonormal (u_j and v_j scaled by sigma_j as the
+    flags ask)."""
+    rng = np.random.default_rng(m + 3 * n + flags)
+    a = rng.standard_normal((m, n)) * np.geomspace(1.0, 1e-3, n)[None, :]
+    cols = torch.from_numpy(np.ascontiguousarray(a.T)).to("cuda:0")
+    sigma, u, v, sweeps = ops.jacobi_svd(cols, flags=flags)
+    s = sigma.cpu().numpy()
+    ref = np.linalg.svd(a, compute_uv=False)
+    k = min(m, n)
+    assert 1 <= int(sweeps.item()) < 60
+    assert np.all(np.diff(s) <= 0)
+    assert np.abs(s[:k] - ref).max() <= 1e-13 * ref[0] * max(m, n)
+    assert np.all(s[k:] <= 1e-13 * ref[0] * max(m, n))
+    uu, vv = u.cpu().numpy(), v.cpu().numpy()
+    su = uu if flags & 1 else uu * s[:, None]                   # rows sigma_j u_j
+    vn = vv / np.where(s > 0, s, 1.0)[:, None] if flags & 2 else vv   # rows v_j
+    assert np.abs(su.T @ vn - a).max() <= 1e-12 * ref[0] * max(m, n)
+    un = su[:k] / s[:k, None]
+    assert np.abs(un @ un.T - np.eye(k)).max() <= 1e-11 * max(m, n)
+    assert np.abs(vn[:k] @ vn[:k].T - np.eye(k)).max() <= 1e-11 * max(m, n)
+
+
+def test_jacobi_svd_of_a_rank_deficient_matrix(ops):
+    """Rank 20 in 100 x 50 (and a zero column): the sweeps converge, 20
+    singular values match LAPACK's, the rest are numerically zero."""
+    rng = np.random.default_rng(12)
+    a = rng.standard_normal((100, 20)) @ rng.standard_normal((20, 50))
+    a[:, 7] = 0.0
+    sigma, u, v, sweeps = ops.jacobi_svd(torch.from_numpy(np.ascontiguousarray(a.T)).to("cuda:0"))
+    s = sigma.cpu().numpy()
+    ref = np.linalg.svd(a, compute_uv=False)
+    assert int(sweeps.item()) < 60
+    assert np.abs(s[:20] - ref[:20]).max() <= 1e-12 * ref[0]
+    assert np.all(s[20:] <= 1e-12 * ref[0])
+    rec = (u.cpu().numpy() * s[:, None]).T @ v.cpu().numpy()
+    assert np.abs(rec - a).max() <= 1e-11 * ref[0]
+
+
+def test_prefill_compensation_factors_on_the_gpu_match_the_host(ops):
+    """The compensation factors of the 4096-token, 3584 -> 18944 prefill
+    layer (3072 vision rows: fewer rows than channels, the randomized
+    truncated SVD), every step on the GPU, against the host calibration
+    (symmetric whitening root, Householder QR, LAPACK SVD) from the same
+    seed: L1 L2 within 1e-8 relative."""
+    from paper_2603_04800_amd import calibrate
+    cfg = synth.CONFIGS[1]
+    p = cfg.projections[0]
+    li = synth.make_layer_inputs(cfg, 0, projections=[p.name])
+    x, w = np.asarray(li.x[p.input_key], np.float32), np.asarray(li.w[p.name], np.float32)
+    s32, _ = calibrate.smoothing_factors(x, li.modality, w, cfg.n_mod)
+    wq, ws = calibrate.quantize_shared_weight(w, s32[0])
+    m = 1
+    zh = x[li.modality == m].astype(np.float64) / s32[m].astype(np.float64)[None, :]
+    dwh = calibrate._weight_difference(w, s32[m], wq, ws)
+    dev = torch.device("cuda:0")
+    l1, l2 = calibrate.cmc_factors_gpu(torch.from_numpy(zh).to(dev), torch.from_numpy(dwh).to(dev),
+                                       cfg.rank, seed=m)
+    h1, h2 = calibrate.cmc_factors(zh, dwh, cfg.rank, seed=m)
+    assert _product_relerr(l1, l2, h1, h2) < 1e-8

@@ -117,11 +117,10 @@ def test_synth_bf16_inputs_are_representable():
     assert not np.any(bits & 0xFFFF)
 
 
-def test_gpu_cmc_driver_logic_with_host_products(monkeypatch):
-    """The GPU compensation-factor driver (cmc_factors_gpu) with masq_dgemm
-    replaced by a CPU product: the same L1 L2 as the host calibration, for
-    the dense and thin whitening and the randomized truncation.  This checks
-    the driver's host logic; the kernels themselves are GPU tests."""
+def _host_factorisation_calls(monkeypatch):
+    """ops.dgemm, cholesky, trsm_right and jacobi_svd replaced by CPU
+    computations that follow the C ABI's contracts (masq.h), so that the
+    GPU calibration driver's host logic runs here."""
     import torch
 
     from paper_2603_04800_amd import ops
@@ -133,16 +132,72 @@ def test_gpu_cmc_driver_logic_with_host_products(monkeypatch):
             return c
         return out.contiguous()
 
-    monkeypatch.setattr(ops, "dgemm", dgemm)
+    def cholesky(a, ridge=0.0, info=None, trace=None, stream=None):
+        n = a.shape[0]
+        info = torch.zeros((1,), dtype=torch.int32) if info is None else info
+        trace = torch.zeros((1,), dtype=torch.float64) if trace is None else trace
+        tr = torch.trace(a)
+        trace.fill_(tr)
+        a += ridge * tr / n * torch.eye(n, dtype=a.dtype)
+        low, bad = torch.linalg.cholesky_ex(torch.tril(a) + torch.tril(a, -1).T)
+        info.fill_(int(bad))
+        a.copy_(low if int(bad) == 0 else torch.eye(n, dtype=a.dtype))
+        return info, trace
+
+    def trsm_right(l, y, trans, stream=None):
+        # X L^T = Y  <=>  L X^T = Y^T;  X L = Y  <=>  L^T X^T = Y^T
+        x = torch.linalg.solve_triangular(l if trans else l.T, y.T, upper=not trans).T
+        y.copy_(x)
+        return y
+
+    def jacobi_svd(cols, flags=0, max_sweeps=60, stream=None):
+        n, m = cols.shape
+        u, s, vh = torch.linalg.svd(cols.T, full_matrices=True)     # [m][m], [k], [n][n]
+        k = s.shape[0]
+        sigma = torch.zeros(n, dtype=torch.float64)
+        sigma[:k] = s
+        ur = torch.zeros((n, m), dtype=torch.float64)
+        ur[:k] = u[:, :k].T
+        if flags & 1:
+            ur *= sigma[:, None]
+        vr = vh.clone()
+        if flags & 2:
+            vr *= sigma[:, None]
+        return sigma, ur, vr, torch.ones(1, dtype=torch.int32)
+
+    for name, fn in (("dgemm", dgemm), ("cholesky", cholesky), ("trsm_right", trsm_right),
+                     ("jacobi_svd", jacobi_svd)):
+        monkeypatch.setattr(ops, name, fn)
+
+
+def test_gpu_cmc_driver_logic_with_host_products(monkeypatch):
+    """The GPU compensation-factor driver (cmc_factors_gpu) with the GEMM and
+    the factorisation calls replaced by CPU computations of their contracts:
+    the same L1 L2 as the host calibration for more and fewer rows than
+    channels, the exact SVD in both orientations (K <= N, K > N), the
+    randomized truncation, and without whitening.  This checks the driver's
+    host logic (which factor multiplies which, transposes, orientations);
+    the kernels themselves are GPU tests."""
+    import torch
+
+    _host_factorisation_calls(monkeypatch)
     monkeypatch.setattr(pcal, "EXACT_SVD_MAX", 16)
     rng = np.random.default_rng(8)
-    for n_rows, K, N, r in ((120, 64, 48, 8), (30, 64, 48, 8), (120, 40, 24, 20)):
+    for n_rows, K, N, r in ((120, 64, 48, 8), (30, 64, 48, 8), (120, 40, 24, 20),
+                            (120, 14, 40, 6), (90, 40, 12, 6)):
         z = rng.standard_normal((n_rows, K)) * rng.uniform(0.2, 4, K)[None, :]
         dw = rng.standard_normal((K, N))
         l1, l2 = pcal.cmc_factors_gpu(torch.from_numpy(z), torch.from_numpy(dw), r, seed=3)
         h1, h2 = pcal.cmc_factors(z, dw, r, seed=3)
         lp, lo = l1 @ l2, h1 @ h2
         assert np.abs(lp - lo).max() <= 1e-9 * np.abs(lo).max(), (n_rows, K, N, r)
+    for K, N, r in ((14, 12, 4), (12, 14, 5)):                  # exact SVD, both orientations
+        z = rng.standard_normal((50, K))
+        dw = rng.standard_normal((K, N))
+        l1, l2 = pcal.cmc_factors_gpu(torch.from_numpy(z), torch.from_numpy(dw), r, whiten=False)
+        u, s, vt = np.linalg.svd(dw, full_matrices=False)
+        best = (u[:, :r] * s[:r]) @ vt[:r]
+        assert np.abs(l1 @ l2 - best).max() <= 1e-10 * np.abs(best).max()
     l1, l2 = pcal.cmc_factors_gpu(torch.zeros((0, 64), dtype=torch.float64),
                                   torch.from_numpy(rng.standard_normal((64, 48))), 8)
     assert not np.any(l1) and not np.any(l2)
