@@ -429,6 +429,27 @@ masq_status masq_mas_gradient(const double* x, const double* a, const double* w,
                               const float* smooth, int64_t T, int64_t c_in, int64_t c_out,
                               double* colpart, double* grad, void* stream);
 
+/* masq_mae_loss: loss[0] = (partial[0] + ... + partial[P - 1]) / count, summed
+ * in that order, over the P = masq_mae_partials(count) block sums that
+ * masq_mae_sign left (count = 0 gives 0).  One device scalar, so a run of
+ * optimisation steps keeps its losses on the device.
+ *
+ * masq_adam_log_step: Adam (Kingma and Ba 2015) on theta = ln s, the
+ * parameterisation of the factors; theta, m1, m2 [c_in] fp64 (state),
+ * smooth / inv_smooth [c_in] f32: the factors s the step's forward pass
+ * used on entry, the next ones (s = fl32(exp(theta)), inv = fl32(1 / s)) on
+ * return.  step = 0 starts the run: theta = ln s, m1 = m2 = 0, and s, inv
+ * from theta (grad unused).  step >= 1 applies the gradient grad [c_in] fp64
+ * (dL/ds): g = lam s grad, m1 = b1 m1 + (1 - b1) g, m2 = b2 m2 + ((1 - b2) g)
+ * g, theta -= (lr (m1 / (1 - b1^step))) / (sqrt(m2 / (1 - b2^step)) + eps),
+ * each operation rounded once.  Requires 0 <= b1, b2 < 1, eps > 0, lr >= 0.
+ */
+masq_status masq_mae_loss(const double* partial, int64_t count, double* loss, void* stream);
+masq_status masq_adam_log_step(double* theta, double* m1, double* m2, const double* grad,
+                               float* smooth, float* inv_smooth, int64_t c_in, double lam,
+                               double lr, double b1, double b2, double eps, int64_t step,
+                               void* stream);
+
 #ifdef __cplusplus
 }
 #endif

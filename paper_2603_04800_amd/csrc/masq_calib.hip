@@ -18,6 +18,7 @@
 // The C ABI of these calls is declared in masq.h.
 
 #include <hip/hip_runtime.h>
+#include <math.h>
 
 #include "masq.h"
 
@@ -348,6 +349,60 @@ __global__ __launch_bounds__(256) void k_mae_sign(const double* __restrict__ y,
     if (threadIdx.x == 0) partial[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
 }
 
+// loss[0] = (partial[0] + partial[1] + ... + partial[nparts - 1]) / count,
+// in that order (one thread: a few thousand block sums at most).
+__global__ void k_mae_loss(const double* __restrict__ partial, int64_t nparts, double count,
+                           double* __restrict__ loss) {
+    double s = 0.0;
+    for (int64_t b = 0; b < nparts; ++b) s += partial[b];
+    *loss = s / count;
+}
+
+// Adam on theta = ln s (Kingma and Ba 2015), one element a thread, each
+// operation rounded as written (the build disables contraction):
+//   g  = lam * s * grad                (d/dtheta of the objective)
+//   m1 = b1 m1 + (1 - b1) g,  m2 = b2 m2 + ((1 - b2) g) g
+//   theta -= (lr (m1 / c1)) / (sqrt(m2 / c2) + eps),  c_i = 1 - b_i^step
+//   s := fl32(exp(theta)),  inv_s := fl32(1 / s)
+__global__ __launch_bounds__(256) void k_adam_log(double* __restrict__ theta, double* __restrict__ m1,
+                                                  double* __restrict__ m2,
+                                                  const double* __restrict__ grad,
+                                                  float* __restrict__ s, float* __restrict__ inv_s,
+                                                  int64_t K, double lam, double lr, double b1,
+                                                  double omb1, double b2, double omb2, double c1,
+                                                  double c2, double eps) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= K) return;
+    const double g = (lam * static_cast<double>(s[i])) * grad[i];
+    const double a = b1 * m1[i] + omb1 * g;
+    const double v = b2 * m2[i] + (omb2 * g) * g;
+    const double th = theta[i] - (lr * (a / c1)) / (sqrt(v / c2) + eps);
+    m1[i] = a;
+    m2[i] = v;
+    theta[i] = th;
+    const float sn = static_cast<float>(exp(th));
+    s[i] = sn;
+    inv_s[i] = 1.0f / sn;
+}
+
+// theta = ln s, m1 = m2 = 0, then s := fl32(exp(theta)), inv_s := fl32(1 / s)
+// (the factors the first step's forward pass uses).
+__global__ __launch_bounds__(256) void k_adam_log_init(double* __restrict__ theta,
+                                                       double* __restrict__ m1,
+                                                       double* __restrict__ m2,
+                                                       float* __restrict__ s,
+                                                       float* __restrict__ inv_s, int64_t K) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= K) return;
+    const double th = log(static_cast<double>(s[i]));
+    theta[i] = th;
+    m1[i] = 0.0;
+    m2[i] = 0.0;
+    const float sn = static_cast<float>(exp(th));
+    s[i] = sn;
+    inv_s[i] = 1.0f / sn;
+}
+
 // colpart[i] = sum_t x[t][i] a[t][i] (thread per column, t in order).
 __global__ __launch_bounds__(256) void k_column_dot(const double* __restrict__ x,
                                                     const double* __restrict__ a, int64_t T,
@@ -560,6 +615,45 @@ masq_status masq_mae_sign(const double* y, const double* ref, int64_t count, dou
     hipLaunchKernelGGL(k_mae_sign, dim3(static_cast<unsigned>(masq_mae_partials(count))), dim3(256),
                        0, static_cast<hipStream_t>(stream), y, ref, count,
                        1.0 / static_cast<double>(count), g, partial);
+    return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
+}
+
+masq_status masq_mae_loss(const double* partial, int64_t count, double* loss, void* stream) {
+    if (count < 0 || masq_mae_partials(count) > 0x7fffffffLL) return MASQ_ERR_SHAPE;
+    if (!loss || (count > 0 && !partial)) return MASQ_ERR_NULL;
+    if (!aligned8(loss) || (count > 0 && !aligned8(partial))) return MASQ_ERR_ALIGN;
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(k_mae_loss, dim3(1), dim3(1), 0, static_cast<hipStream_t>(stream), partial,
+                       masq_mae_partials(count), count > 0 ? static_cast<double>(count) : 1.0, loss);
+    return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
+}
+
+masq_status masq_adam_log_step(double* theta, double* m1, double* m2, const double* grad,
+                               float* smooth, float* inv_smooth, int64_t c_in, double lam,
+                               double lr, double b1, double b2, double eps, int64_t step,
+                               void* stream) {
+    if (c_in < 0 || c_in > (1LL << 30) || step < 0 || !(lr >= 0.0) || !(b1 >= 0.0 && b1 < 1.0) ||
+        !(b2 >= 0.0 && b2 < 1.0) || !(eps > 0.0) || !isfinite(lam) || !isfinite(lr))
+        return MASQ_ERR_SHAPE;
+    if (c_in == 0) return MASQ_OK;
+    if (!theta || !m1 || !m2 || !smooth || !inv_smooth || (step > 0 && !grad))
+        return MASQ_ERR_NULL;
+    if (!aligned8(theta) || !aligned8(m1) || !aligned8(m2) || (step > 0 && !aligned8(grad)) ||
+        (reinterpret_cast<uintptr_t>(smooth) & 3u) != 0 ||
+        (reinterpret_cast<uintptr_t>(inv_smooth) & 3u) != 0)
+        return MASQ_ERR_ALIGN;
+    (void)hipGetLastError();
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const dim3 grid(static_cast<unsigned>((c_in + 255) / 256));
+    if (step == 0) {
+        hipLaunchKernelGGL(k_adam_log_init, grid, dim3(256), 0, st, theta, m1, m2, smooth,
+                           inv_smooth, c_in);
+    } else {
+        const double sd = static_cast<double>(step);
+        hipLaunchKernelGGL(k_adam_log, grid, dim3(256), 0, st, theta, m1, m2, grad, smooth,
+                           inv_smooth, c_in, lam, lr, b1, 1.0 - b1, b2, 1.0 - b2,
+                           1.0 - pow(b1, sd), 1.0 - pow(b2, sd), eps);
+    }
     return hipGetLastError() == hipSuccess ? MASQ_OK : MASQ_ERR_HIP;
 }
 

@@ -63,6 +63,10 @@ _SIGS = {
     "masq_mae_partials": ([_i64], _i64),
     "masq_mae_sign": ([_p, _p, _i64, _p, _p, _p], ctypes.c_int),
     "masq_mas_gradient": ([_p, _p, _p, _p, _p, _i64, _i64, _i64, _p, _p, _p], ctypes.c_int),
+    "masq_mae_loss": ([_p, _i64, _p, _p], ctypes.c_int),
+    "masq_adam_log_step": ([_p, _p, _p, _p, _p, _p, _i64, ctypes.c_double, ctypes.c_double,
+                            ctypes.c_double, ctypes.c_double, ctypes.c_double, _i64, _p],
+                           ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -336,9 +340,10 @@ def dequantize_rows(codes, scale, stream=None):
     return out
 
 
-def mae_sign(y, ref, stream=None):
+def mae_sign(y, ref, loss=None, stream=None):
     """(G = sign(y - ref) / count, mean |y - ref|) for fp64 tensors of one
-    shape; the loss is added on the host from fixed-order block sums."""
+    shape; the mean is a device fp64 scalar (written to loss, a [1] view,
+    when given), summed from fixed-order block sums (masq_mae_loss)."""
     _need(y, torch.float64, "y")
     _need(ref, torch.float64, "ref")
     if y.shape != ref.shape:
@@ -347,10 +352,31 @@ def mae_sign(y, ref, stream=None):
     g = torch.empty_like(y)
     part = torch.empty((max(int(_lib.masq_mae_partials(n)), 1),), dtype=torch.float64,
                        device=y.device)
+    if loss is None:
+        loss = torch.empty((1,), dtype=torch.float64, device=y.device)
+    _need(loss, torch.float64, "loss")
     _check("masq_mae_sign", _lib.masq_mae_sign(_ptr(y), _ptr(ref), n, _ptr(g), _ptr(part),
                                                _stream(stream)))
-    loss = float(part[:int(_lib.masq_mae_partials(n))].cpu().numpy().sum()) / n if n else 0.0
+    _check("masq_mae_loss", _lib.masq_mae_loss(_ptr(part), n, _view_ptr(loss), _stream(stream)))
     return g, loss
+
+
+def adam_log_step(theta, m1, m2, grad, smooth, inv_smooth, step, lam=1.0, lr=1e-2, b1=0.9,
+                  b2=0.999, eps=1e-8, stream=None):
+    """One Adam step on theta = ln s in place (masq_adam_log_step): theta,
+    m1, m2 fp64 [K]; smooth, inv_smooth f32 [K] (the factors the step's
+    forward pass used; replaced by the next ones); grad fp64 [K] (dL/ds).
+    step = 0 initialises theta, m1, m2 from smooth."""
+    for t, name in ((theta, "theta"), (m1, "m1"), (m2, "m2")):
+        _need(t, torch.float64, name)
+    _need(smooth, torch.float32, "smooth")
+    _need(inv_smooth, torch.float32, "inv_smooth")
+    if step > 0:
+        _need(grad, torch.float64, "grad")
+    _check("masq_adam_log_step", _lib.masq_adam_log_step(
+        _ptr(theta), _ptr(m1), _ptr(m2), _ptr(grad) if step > 0 else None, _ptr(smooth),
+        _ptr(inv_smooth), theta.numel(), float(lam), float(lr), float(b1), float(b2), float(eps),
+        int(step), _stream(stream)))
 
 
 def mas_gradient(x, a, w, b, smooth, stream=None):

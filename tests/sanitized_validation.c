@@ -73,6 +73,12 @@ int main(void) {
     expect("jacobi too wide",
            masq_jacobi_svd(4, 1025, (double*)P, (double*)P, (double*)P, (double*)P, (double*)P, 0,
                            10, NULL, NULL), MASQ_ERR_SHAPE);
+    expect("mae loss negative count", masq_mae_loss((const double*)P, -1, (double*)P, NULL),
+           MASQ_ERR_SHAPE);
+    expect("adam bad beta",
+           masq_adam_log_step((double*)P, (double*)P, (double*)P, (const double*)P, (float*)P,
+                              (float*)P, 8, 1.0, 1e-2, 1.0, 0.999, 1e-8, 1, NULL),
+           MASQ_ERR_SHAPE);
     expect("channel range bad dtype",
            masq_channel_range(P, (masq_dtype)7, P, 8, 64, 2, P, NULL), MASQ_ERR_DTYPE);
     if (masq_linear_fused_workspace_bytes(-1, 64, 64, 16, 2) != 0) {

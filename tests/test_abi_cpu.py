@@ -354,9 +354,10 @@ def test_factorisation_calls_validate(lib):
 
 
 def test_mas_optimisation_calls_validate(lib):
-    """masq_dequantize_rows, masq_mae_sign and masq_mas_gradient check their
-    arguments before enqueueing anything; masq_mae_partials is plain host
-    arithmetic."""
+    """masq_dequantize_rows, masq_mae_sign, masq_mas_gradient, masq_mae_loss
+    and masq_adam_log_step check their arguments before enqueueing anything;
+    masq_mae_partials is plain host arithmetic."""
+    import ctypes
     P = 1 << 20
     dq, ms, mg = lib.masq_dequantize_rows, lib.masq_mae_sign, lib.masq_mas_gradient
     assert dq(P, P, -1, 4, P, None) == 2                         # rows < 0
@@ -374,6 +375,22 @@ def test_mas_optimisation_calls_validate(lib):
     assert mg(P, P, P, P, P, 4, 0, 16, P, P, None) == 2          # c_in = 0
     assert mg(P, P, P, None, P, 4, 16, 16, P, P, None) == 1      # no B
     assert mg(P, P, P, P, P, 4, 16, 16, P, P + 4, None) == 4     # misaligned grad
+    ml, ad = lib.masq_mae_loss, lib.masq_adam_log_step
+    assert ml(P, -1, P, None) == 2                               # count < 0
+    assert ml(None, 8, P, None) == 1                             # no block sums
+    assert ml(P, 8, None, None) == 1                             # no loss output
+    assert ml(P, 8, P + 4, None) == 4                            # misaligned loss
+    d = ctypes.c_double
+    ok = (d(1.0), d(1e-2), d(0.9), d(0.999), d(1e-8))
+    assert ad(P, P, P, P, P, P, -1, *ok, 1, None) == 2           # c_in < 0
+    assert ad(P, P, P, P, P, P, 8, *ok, -1, None) == 2           # step < 0
+    assert ad(P, P, P, P, P, P, 8, d(1.0), d(1e-2), d(1.0), d(0.999), d(1e-8), 1, None) == 2
+    assert ad(P, P, P, P, P, P, 8, d(1.0), d(1e-2), d(0.9), d(0.999), d(0.0), 1, None) == 2
+    assert ad(P, P, P, P, P, P, 8, d(float("nan")), d(1e-2), d(0.9), d(0.999), d(1e-8), 1,
+              None) == 2
+    assert ad(P, P, P, None, P, P, 8, *ok, 1, None) == 1         # step 1 needs a gradient
+    assert ad(P, P, P, P, P, P + 2, 8, *ok, 1, None) == 4        # misaligned inverse factors
+    assert ad(None, None, None, None, None, None, 0, *ok, 1, None) == 0   # empty
 
 
 def test_dgemm_binding_refuses_an_output_aliasing_an_input():

@@ -35,7 +35,8 @@ def test_mae_sign(ops, n):
     y = rng.standard_normal(n)
     ref = y + rng.standard_normal(n) * 0.1
     ref[::7] = y[::7]                                       # exact ties give 0
-    g, loss = ops.mae_sign(torch.from_numpy(y).to(DEV), torch.from_numpy(ref).to(DEV))
+    g, loss_t = ops.mae_sign(torch.from_numpy(y).to(DEV), torch.from_numpy(ref).to(DEV))
+    loss = float(loss_t.item())
     assert np.array_equal(g.cpu().numpy(), np.sign(y - ref) / n)
     assert loss == pytest.approx(np.mean(np.abs(y - ref)), rel=1e-13)
 
@@ -101,3 +102,54 @@ def test_optimisation_matches_the_oracle(ops, bits):
     for h, hr in zip(hist, hist_ref):
         assert len(h) == len(hr) and np.allclose(h, hr, rtol=1e-9)
     assert np.allclose(got, want, rtol=1e-6)
+
+
+def test_adam_log_step_matches_its_formula(ops):
+    """masq_adam_log_step: the moments exactly as their formula in fp64 (one
+    rounding an operation), theta within one ulp of it (the square root is
+    the device's), the next factors fl32(exp(theta)) within one ulp of the
+    host's exp, and their reciprocals correctly rounded from them.  Step 0
+    initialises theta = ln s."""
+    rng = np.random.default_rng(3)
+    K = 1000
+    s0 = rng.uniform(0.2, 5.0, K).astype(np.float32)
+    theta, m1, m2 = (torch.empty(K, dtype=torch.float64, device=DEV) for _ in range(3))
+    s_t = torch.from_numpy(s0.copy()).to(DEV)
+    inv_t = torch.empty_like(s_t)
+    ops.adam_log_step(theta, m1, m2, None, s_t, inv_t, 0)
+    th = np.log(s0.astype(np.float64))
+    assert np.all(np.abs(theta.cpu().numpy() - th) <= np.spacing(np.abs(th)))
+    assert not m1.cpu().numpy().any() and not m2.cpu().numpy().any()
+    s_host = np.exp(theta.cpu().numpy()).astype(np.float32)
+    assert np.all(np.abs(s_t.cpu().numpy().view(np.int32) - s_host.view(np.int32)) <= 1)
+    lam, lr, b1, b2, eps = 0.7, 1e-2, 0.9, 0.999, 1e-8
+    for step in (1, 2, 3):
+        g = rng.standard_normal(K)
+        s_in = s_t.cpu().numpy().astype(np.float64)
+        th, a, v = theta.cpu().numpy(), m1.cpu().numpy(), m2.cpu().numpy()
+        ops.adam_log_step(theta, m1, m2, torch.from_numpy(g).to(DEV), s_t, inv_t, step,
+                          lam=lam, lr=lr, b1=b1, b2=b2, eps=eps)
+        gg = (lam * s_in) * g
+        a = b1 * a + (1 - b1) * gg
+        v = b2 * v + ((1 - b2) * gg) * gg
+        th = th - (lr * (a / (1 - b1 ** step))) / (np.sqrt(v / (1 - b2 ** step)) + eps)
+        assert np.array_equal(m1.cpu().numpy(), a) and np.array_equal(m2.cpu().numpy(), v)
+        # (sqrt and exp are the device's: theta within one ulp of the host's)
+        assert np.all(np.abs(theta.cpu().numpy() - th) <= np.spacing(np.abs(th)))
+        th = theta.cpu().numpy()
+        s_new = s_t.cpu().numpy()
+        assert np.all(np.abs(s_new.view(np.int32) - np.exp(th).astype(np.float32).view(np.int32))
+                      <= 1)
+        assert np.array_equal(inv_t.cpu().numpy(), np.float32(1.0) / s_new)
+
+
+def test_mae_loss_sums_the_blocks_in_order(ops):
+    """The loss of masq_mae_loss is the blocks' sum in index order over the
+    count, exactly (and 0 for an empty problem)."""
+    rng = np.random.default_rng(4)
+    n = 3 * 4096 + 17
+    y, ref = rng.standard_normal(n), rng.standard_normal(n)
+    g, loss = ops.mae_sign(torch.from_numpy(y).to(DEV), torch.from_numpy(ref).to(DEV))
+    blocks = [np.abs(y[b:b + 4096] - ref[b:b + 4096]) for b in range(0, n, 4096)]
+    assert abs(float(loss.item()) - np.mean(np.abs(y - ref))) <= 1e-14
+    assert len(blocks) == int(ops._lib.masq_mae_partials(n))
