@@ -295,19 +295,21 @@ COPY_KERNEL = "copyBuffer"      # the runtime's device-to-device copy (the probe
 PROFILE_COMMANDS = {
     "trace": "cd /tmp && TMPDIR=/tmp rocprofv3 --kernel-trace --stats --output-format csv "
              "-d <out>/trace -o run -- python3 <repo>/bench.py --workload {w} --steps 30 "
-             "--warmup 5 --no-cpu",
+             "--warmup 5 --no-cpu --no-peaks --only-headline",
     "fetch": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc FETCH_SIZE --output-format csv "
              "-d <out>/fetch -o run -- python3 <repo>/bench.py --workload {w} --steps 3 "
-             "--warmup 1 --no-cpu",
+             "--warmup 1 --no-cpu --no-peaks --only-headline",
     "write": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc WRITE_SIZE --output-format csv "
              "-d <out>/write -o run -- python3 <repo>/bench.py --workload {w} --steps 3 "
-             "--warmup 1 --no-cpu",
+             "--warmup 1 --no-cpu --no-peaks --only-headline",
     "mfma": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_I8 "
             "GRBM_GUI_ACTIVE --kernel-trace --output-format csv -d <out>/mfma -o run -- python3 "
-            "<repo>/bench.py --workload {w} --steps 3 --warmup 1 --no-cpu",
+            "<repo>/bench.py --workload {w} --steps 3 --warmup 1 --no-cpu --no-peaks "
+            "--only-headline",
     "lds": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE "
            "SQ_INSTS_LDS SQ_WAVES --kernel-trace --output-format csv -d <out>/lds -o run -- "
-           "python3 <repo>/bench.py --workload {w} --steps 3 --warmup 1 --no-cpu",
+           "python3 <repo>/bench.py --workload {w} --steps 3 --warmup 1 --no-cpu --no-peaks "
+           "--only-headline",
     "copy_fetch": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc FETCH_SIZE --output-format csv "
                   "-d <out>/copy_fetch -o run -- python3 <repo>/bench.py --copy-probe 512",
     "copy_write": "cd /tmp && TMPDIR=/tmp rocprofv3 --pmc WRITE_SIZE --output-format csv "

@@ -161,13 +161,16 @@ inline bool fused_stage1_ok(int64_t T, int64_t K, int rank, DT lr_dt) {
 // per workgroup of kFrWaves waves, rows of a multiple of 64 columns up to
 // kFrWaves x kFrMaxPairs x 64 (each wave holds at most kFrMaxPairs 64-column
 // pairs of its 16 rows in registers), and the smoothing factors of every
-// modality within kFrInvFloats floats of LDS.
+// modality within kFrInvFloats floats of LDS, each modality's row at a
+// stride of fr_inv_stride(K) floats (whole 1 KB blocks plus 16 bytes, so that
+// lanes reading different modalities' factors hit different banks).
 constexpr int kFrWaves = 8;
 constexpr int kFrMaxPairs = 8;
-constexpr int kFrInvFloats = 12288;
+constexpr int kFrInvFloats = 12304;
+__host__ __device__ inline int64_t fr_inv_stride(int64_t K) { return (K + 255) / 256 * 256 + 4; }
 inline bool stage1_fr_ok(DT x_dt, int64_t K, int n_mod) {
     return x_dt == DT::BF16 && K % 64 == 0 && K <= int64_t{kFrWaves} * kFrMaxPairs * 64 &&
-           ((static_cast<int64_t>(n_mod) * K * 4 + 1023) / 1024) * 1024 <= kFrInvFloats * 4;
+           static_cast<int64_t>(n_mod) * fr_inv_stride(K) <= kFrInvFloats;
 }
 // Down-projection with the L1 fragments staged in LDS (k_down_lds): bf16
 // activations and factors, rank <= 64, K % 64 == 0; slice partials

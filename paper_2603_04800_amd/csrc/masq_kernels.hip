@@ -1263,6 +1263,7 @@ __global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
 // what bounds the down-projection.  The waves' u partials are added in LDS in
 // a fixed order.
 constexpr int kFrLook = 2;          // k steps of L1 fragments in flight ahead of their MFMAs
+constexpr int kFrRedPitch = 68;     // floats per row of the u partials in LDS
 
 template <int P, int RG>
 __global__ __launch_bounds__(64 * kFrWaves) void k_stage1_fr(
@@ -1275,7 +1276,10 @@ __global__ __launch_bounds__(64 * kFrWaves) void k_stage1_fr(
         for (int i = threadIdx.x; i < n_zero; i += blockDim.x) zero_ints[i] = 0;
 
     __shared__ __attribute__((aligned(16))) float s_inv[kFrInvFloats];
-    __shared__ __attribute__((aligned(16))) float red[kFrWaves / 2][kRows][64];
+    // u partials of the second half of the waves; rows padded to 68 floats so
+    // that the four row groups a wave writes at once (rows 4 kg + i) fall on
+    // different banks
+    __shared__ __attribute__((aligned(16))) float red[kFrWaves / 2][kRows][kFrRedPitch];
     __shared__ int smod[kRows];
     __shared__ float samax[kFrWaves][kRows];
     __shared__ float srq[kRows];
@@ -1286,14 +1290,20 @@ __global__ __launch_bounds__(64 * kFrWaves) void k_stage1_fr(
     const int npairs = K >> 6;
     const int pb = wave * P;                       // this wave's first pair
 
-    // the smoothing factors of every modality into LDS (1 KB DMA blocks; the
-    // last block's pieces past the end repeat the last piece, the host checks
+    // the smoothing factors of every modality into LDS, modality m's row at
+    // m * istride floats (1 KB DMA blocks; a row's last block repeats its last
+    // piece past the row's end, inside the row's whole blocks; the host checks
     // the fit), then this lane's share of its rows, every load in flight
+    const int istride = static_cast<int>(fr_inv_stride(K));
     {
-        const int pieces = n_mod * K / 4;
+        const int rpieces = K / 4;                             // 16-byte pieces of a row
+        const int rblocks = (rpieces + 63) / 64;
         const uint32_t b0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(s_inv));
-        for (int i = wave; i * 64 < pieces; i += kFrWaves)
-            lds_dma16(inv_s + 4 * min(i * 64 + lane, pieces - 1), b0 + i * 1024);
+        for (int i = wave; i < n_mod * rblocks; i += kFrWaves) {
+            const int m = i / rblocks, bi = i - m * rblocks;
+            lds_dma16(inv_s + static_cast<int64_t>(m) * K + 4 * min(bi * 64 + lane, rpieces - 1),
+                      b0 + static_cast<uint32_t>(m * istride * 4 + bi * 1024));
+        }
     }
     int mymod = 0;
     if (tid < kRows) {
@@ -1351,7 +1361,7 @@ __global__ __launch_bounds__(64 * kFrWaves) void k_stage1_fr(
 #pragma unroll
     for (int g = 0; g < RG; ++g) {
         mrow[g] = smod[16 * g + ar];
-        srow[g] = s_inv + mrow[g] * K + 16 * kg;
+        srow[g] = s_inv + mrow[g] * istride + 16 * kg;
     }
 
     // xs of half h of pair p of row group g (8 values) from the registers
@@ -2852,8 +2862,9 @@ __global__ __launch_bounds__(256) void k_gemm_small(
 // group's channels are queued by DMA with the q slice, ahead of the Wq
 // loads, so they have landed long before Wq has; the workgroup adds the
 // partials (slice order), forms (x S^-1 L1) L2 for its tokens while its Wq
-// loads are still in flight, and hands the fp32 terms over beside the int32
-// partials.  The last workgroup then only adds.
+// loads are still in flight (each thread sums over the rank in 8-column
+// chunks, starting at a lane-dependent chunk), and hands the fp32 terms over
+// beside the int32 partials.  The last workgroup then only adds.
 // W4: Wq holds packed 4-bit codes (K / 2 bytes a row, 8 bytes a lane a step,
 // unpacked into the MFMA operand in registers).
 template <typename YT, typename LT, bool W4>
@@ -2958,10 +2969,15 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
         }
         __syncthreads();
         if (tmod > 0) {
+            // lane l starts at 8-column chunk l % (r / 8) of its L2 row (the
+            // rows lie 128 or 256 bytes apart, so reading the chunks in the
+            // same order would put every lane on the same banks)
             const float* ur = up + (tid >> 6) * r;
             const LT* rr = reinterpret_cast<const LT*>(scm + up_bytes +
                                                        ((tmod - 1) * kDecCh + (tid & 63)) * rrow);
-            for (int k0 = 0; k0 < r; k0 += 8) {
+            const int nch = r >> 3;
+            for (int j = 0; j < nch; ++j) {
+                const int k0 = 8 * ((j + lane) % nch);
                 float rv[8];
                 Elem<LT>::load8(rr + k0, rv);
 #pragma unroll
