@@ -45,7 +45,9 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
         off += align256(bytes);
         return p;
     };
-    w.q = reinterpret_cast<int8_t*>(carve(static_cast<size_t>(T) * static_cast<size_t>(K)));
+    w.pair = paired_codes(T, K);
+    const int64_t q_rows = w.pair ? (T + 1) / 2 * 2 : T;    // whole row pairs
+    w.q = reinterpret_cast<int8_t*>(carve(static_cast<size_t>(q_rows) * static_cast<size_t>(K)));
     w.x_scale = reinterpret_cast<float*>(carve(static_cast<size_t>(T) * sizeof(float)));
     w.u = nullptr;
     w.u_hl = nullptr;
@@ -244,7 +246,8 @@ masq_status fused_stage(const Fused& a, int stage) {
         // rows held in registers: one kernel, each row read once
         st = from_hip(masq::launch_stage1_fused(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                 a.l_down, a.T, a.c_in, a.rank, a.n_mod, w.q,
-                                                w.x_scale, w.u, w.u_hl, w.zero_base, w.n_zero, s));
+                                                w.x_scale, w.u, w.u_hl, w.zero_base, w.n_zero, s,
+                                                w.pair));
         if (st != MASQ_OK) return st;
     } else if ((stage & 1) && cmc && masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt)) &&
                masq::down_lds_ok(to_dt(a.x_dt), a.c_in) && w.dl_part != nullptr) {
@@ -257,7 +260,7 @@ masq_status fused_stage(const Fused& a, int stage) {
         const masq::UFinish fin{w.dl_part, masq::down_lds_slices(a.c_in), a.rank, w.u, w.u_hl};
         st = from_hip(masq::launch_smooth_quant(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                 a.T, a.c_in, a.n_mod, w.q, w.x_scale,
-                                                w.zero_base, w.n_zero, s, &fin));
+                                                w.zero_base, w.n_zero, s, &fin, w.pair));
         if (st != MASQ_OK) return st;
     } else if ((stage & 1) && cmc && masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt)) &&
                w.dw_part != nullptr) {
@@ -268,17 +271,18 @@ masq_status fused_stage(const Fused& a, int stage) {
         const masq::UFinish fin{w.dw_part, w.dw_slices, a.rank, w.u, w.u_hl};
         st = from_hip(masq::launch_smooth_quant(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                 a.T, a.c_in, a.n_mod, w.q, w.x_scale,
-                                                w.zero_base, w.n_zero, s, &fin));
+                                                w.zero_base, w.n_zero, s, &fin, w.pair));
         if (st != MASQ_OK) return st;
     } else if ((stage & 1) && cmc && masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt))) {
         st = from_hip(masq::launch_stage1_fused(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                 a.l_down, a.T, a.c_in, a.rank, a.n_mod, w.q,
-                                                w.x_scale, w.u, w.u_hl, w.zero_base, w.n_zero, s));
+                                                w.x_scale, w.u, w.u_hl, w.zero_base, w.n_zero, s,
+                                                w.pair));
         if (st != MASQ_OK) return st;
     } else if (stage & 1) {
         st = from_hip(masq::launch_smooth_quant(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                 a.T, a.c_in, a.n_mod, w.q, w.x_scale,
-                                                w.zero_base, w.n_zero, s));
+                                                w.zero_base, w.n_zero, s, nullptr, w.pair));
         if (st != MASQ_OK) return st;
         if (cmc) {
             st = from_hip(masq::launch_lowrank_down(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
@@ -297,7 +301,7 @@ masq_status fused_stage(const Fused& a, int stage) {
                                         w.u_part,
                                         w.n_kslices, a.rank, a.n_mod,
                                         a.r_up, to_dt(a.lr_dt), cmc, nullptr, a.y, to_dt(a.y_dt),
-                                        s, a.w4));
+                                        s, a.w4, w.pair));
     }
     return st;
 }

@@ -24,6 +24,20 @@ constexpr int kUBatch = 16;        // slice partials of u a thread keeps in flig
 // down-projection's k-slice partials itself.
 inline bool small_path(int64_t T, int64_t K) { return T <= kSmallMaxT && K % 64 == 0; }
 
+// Layout of the fused layer's int8 activation codes in its workspace.  Plain:
+// code (t, k) at byte t K + k.  Row-paired (paired_codes: K % 64 == 0 and a
+// batch past the small path, whose GEMM takes its A operand by LDS DMA): rows
+// 2i and 2i + 1 interleave in 64-byte pieces, code (t, k) at byte
+// (t / 2) 2K + (k / 64) 128 + (t % 2) 64 + k % 64, so that the two rows'
+// 64-column pieces of one K stage are a single 128-byte line (one L2 request
+// where the plain rows take two 64-byte ones).  An odd batch's last pair has
+// an unused second row (the workspace holds T rounded up to even rows).
+inline bool paired_codes(int64_t T, int64_t K) { return !small_path(T, K) && K % 64 == 0; }
+__host__ __device__ inline int64_t code_row(int64_t t, int64_t K, bool pair) {
+    return pair ? (t >> 1) * 2 * K + (t & 1) * 64 : t * K;
+}
+__host__ __device__ inline int code_col(int k, bool pair) { return pair ? k + (k & ~63) : k; }
+
 // Stage 1 of large batches with bf16 factors, rank <= 64 (fused_stage1_ok),
 // in its wide form: the down-projection runs over 128-row tiles and S k
 // slices of kslice columns (about 512 workgroups, slices of at least 256
@@ -103,7 +117,8 @@ struct LinearArgs {
 
 // Workspace carve-up of the fused layer.
 struct Workspace {
-    int8_t* q;
+    int8_t* q;         // codes, row-paired when `pair` (code_row / code_col)
+    bool pair;         // paired_codes(T, K)
     float* x_scale;
     float* u;          // [T][rank] fp32 down-projection u = (x S^-1) L1
     uint8_t* u_hl;     // [T][256 B] u as bf16 hi | lo rows (rank <= 64, large batches)
@@ -131,7 +146,8 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
 // zero_ints / n_zero: optional array the kernel clears on the way (the
 // down-projection's tickets, which must start at zero).
 // fin (optional): add the wide down-projection's slice partials into u (and
-// its bf16 hi/lo rows) while quantising.
+// its bf16 hi/lo rows) while quantising.  pair: write the codes row-paired
+// (code_row / code_col; K % 64 == 0).
 struct UFinish {
     const float* part;   // [slices][T][r]
     int slices, r;
@@ -141,7 +157,7 @@ struct UFinish {
 hipError_t launch_smooth_quant(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                int64_t T, int64_t K, int n_mod, int8_t* q, float* x_scale,
                                int* zero_ints, int n_zero, hipStream_t s,
-                               const UFinish* fin = nullptr);
+                               const UFinish* fin = nullptr, bool pair = false);
 
 hipError_t launch_down_wide(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                             const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
@@ -189,7 +205,7 @@ hipError_t launch_down_lds(const void* x, const int32_t* mod, const float* inv_s
 hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
                                int8_t* q, float* x_scale, float* u, uint8_t* u_hl,
-                               int* zero_ints, int n_zero, hipStream_t s);
+                               int* zero_ints, int n_zero, hipStream_t s, bool pair = false);
 
 // Stage 1 of the small-batch path (small_path): quantisation of every row
 // and the k-sliced down-projection (partials) in one launch.
@@ -202,14 +218,17 @@ hipError_t launch_stage1_small(const void* x, DT x_dt, const int32_t* mod, const
 // (optional): u as bf16 hi/lo rows, written by the fused stage 1.  dec_part /
 // dec_tickets (optional, small-batch path): workspace of the k-sliced decode
 // GEMM; without them the single-pass small-batch GEMM runs.  w4: wq holds
-// packed 4-bit codes ([N][K / 2] bytes, K % 64 == 0).
+// packed 4-bit codes ([N][K / 2] bytes, K % 64 == 0).  a_pair: q is
+// row-paired (code_row / code_col), which only the LDS-DMA GEMM reads
+// (K % 64 == 0, batches past the small path).
 hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        const float* w_scale, int64_t T, int64_t K, int64_t N,
                        const int32_t* mod, const float* u, const uint8_t* u_hl,
                        int32_t* dec_part, int* dec_tickets, int gk_splits, int32_t* gk_part,
                        int* gk_tickets, const float* u_part, int n_kslices,
                        int rank, int n_mod, const void* r_up, DT lr_dt, bool cmc, int32_t* acc,
-                       void* y, DT y_dt, hipStream_t s, bool w4 = false);
+                       void* y, DT y_dt, hipStream_t s, bool w4 = false,
+                       bool a_pair = false);
 
 // MAS-only comparator (a weight per modality, no compensation): rows grouped
 // by modality on the device, then the direct-to-LDS GEMM over tiles of one

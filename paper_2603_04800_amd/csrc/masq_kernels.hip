@@ -172,12 +172,12 @@ template <typename XT, int NT, int NCH>
 __device__ __forceinline__ void sq_row(const XT* __restrict__ x, const int32_t* __restrict__ mod,
                                        const float* __restrict__ inv_s, int K, int n_mod,
                                        int8_t* __restrict__ q, float* __restrict__ x_scale,
-                                       int64_t t) {
+                                       int64_t t, bool pair) {
     __shared__ float red[NT / 64];
     const int m = sane_mod(mod[t], n_mod);
     const XT* xr = x + t * static_cast<int64_t>(K);
     const float* sr = inv_s + static_cast<int64_t>(m) * K;
-    int8_t* qr = q + t * static_cast<int64_t>(K);
+    int8_t* qr = q + code_row(t, K, pair);
     const int nv = K >> 3;
 
     float xs[NCH][8];
@@ -230,7 +230,7 @@ __device__ __forceinline__ void sq_row(const XT* __restrict__ x, const int32_t* 
         v2i out;
         out.x = static_cast<int32_t>(w[0]);
         out.y = static_cast<int32_t>(w[1]);
-        *reinterpret_cast<v2i*>(qr + 8 * v) = out;
+        *reinterpret_cast<v2i*>(qr + code_col(8 * v, pair)) = out;
     };
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
@@ -285,13 +285,13 @@ __global__ __launch_bounds__(256) void k_smooth_quant(const XT* __restrict__ x,
                                                       int n_mod, int8_t* __restrict__ q,
                                                       float* __restrict__ x_scale,
                                                       int* __restrict__ zero_ints, int n_zero,
-                                                      int64_t T, UFinish fin) {
+                                                      int64_t T, UFinish fin, bool pair) {
     if (blockIdx.x == 0)
         for (int i = threadIdx.x; i < n_zero; i += 256) zero_ints[i] = 0;
     if (fin.part != nullptr && threadIdx.x < 64)
         finish_u_row(blockIdx.x, T, sane_mod(mod[blockIdx.x], n_mod) == 0, fin.part, fin.slices,
                      fin.r, fin.u, fin.u_hl, threadIdx.x);
-    sq_row<XT, 256, kSqChunks>(x, mod, inv_s, K, n_mod, q, x_scale, blockIdx.x);
+    sq_row<XT, 256, kSqChunks>(x, mod, inv_s, K, n_mod, q, x_scale, blockIdx.x, pair);
 }
 
 __device__ __forceinline__ void split_bf16x8(const float (&v)[8], v4i& hi, v4i& lo) {
@@ -318,7 +318,7 @@ __global__ __launch_bounds__(256) void k_smooth_quant_rows(const XT* __restrict_
                                                            int8_t* __restrict__ q,
                                                            float* __restrict__ x_scale,
                                                            int* __restrict__ zero_ints,
-                                                           int n_zero, UFinish fin) {
+                                                           int n_zero, UFinish fin, bool pair) {
     if (blockIdx.x == 0)
         for (int i = threadIdx.x; i < n_zero; i += 256) zero_ints[i] = 0;
     const int lane = threadIdx.x & 63;
@@ -328,7 +328,7 @@ __global__ __launch_bounds__(256) void k_smooth_quant_rows(const XT* __restrict_
     if (fin.part != nullptr) finish_u_row(t, T, m == 0, fin.part, fin.slices, fin.r, fin.u, fin.u_hl, lane);
     const XT* xr = x + t * static_cast<int64_t>(K);
     const float* sr = inv_s + static_cast<int64_t>(m) * K;
-    int8_t* qr = q + t * static_cast<int64_t>(K);
+    int8_t* qr = q + code_row(t, K, pair);
     const int nv = K >> 3;
 
     float xs[NC][8];
@@ -371,7 +371,7 @@ __global__ __launch_bounds__(256) void k_smooth_quant_rows(const XT* __restrict_
         v2i out;
         out.x = static_cast<int32_t>(w[0]);
         out.y = static_cast<int32_t>(w[1]);
-        *reinterpret_cast<v2i*>(qr + 8 * v) = out;
+        *reinterpret_cast<v2i*>(qr + code_col(8 * v, pair)) = out;
     };
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
@@ -783,7 +783,7 @@ __global__ __launch_bounds__(256) void k_stage1_small(
     if (blockIdx.x == 0)
         for (int i = threadIdx.x; i < n_zero; i += blockDim.x) zero_ints[i] = 0;
     if (static_cast<int>(blockIdx.x) < T) {
-        sq_row<XT, 256, kSqChunks>(x, mod, inv_s, K, n_mod, q, x_scale, blockIdx.x);
+        sq_row<XT, 256, kSqChunks>(x, mod, inv_s, K, n_mod, q, x_scale, blockIdx.x, false);
     } else if (l_down != nullptr) {
         down_tile_in<4, XT, LT>(x, mod, inv_s, l_down, T, K, r, n_mod, kslice, n_kslices, u,
                                 u_part, nullptr, 0, blockIdx.x - T, smod, red, &last);
@@ -811,7 +811,7 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
     const XT* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
     const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod,
     int8_t* __restrict__ q, float* __restrict__ x_scale, float* __restrict__ u,
-    uint8_t* __restrict__ u_hl, int* __restrict__ zero_ints, int n_zero) {
+    uint8_t* __restrict__ u_hl, int* __restrict__ zero_ints, int n_zero, bool pair) {
     constexpr int kRows = 16 * RG;                 // RG groups of 16 rows share each L1 fragment
     if (blockIdx.x == 0)                           // arrival counters of stage 2
         for (int i = threadIdx.x; i < n_zero; i += blockDim.x) zero_ints[i] = 0;
@@ -1083,7 +1083,7 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
                 c = fminf(fmaxf(c, -127.0f), 127.0f);
                 w[e >> 2] |= (static_cast<uint32_t>(static_cast<int32_t>(c)) & 0xFFu) << (8 * (e & 3));
             }
-            *reinterpret_cast<v4i*>(q + (row0 + qr) * static_cast<int64_t>(K) + k) =
+            *reinterpret_cast<v4i*>(q + code_row(row0 + qr, K, pair) + code_col(k, pair)) =
                 v4i{static_cast<int32_t>(w[0]), static_cast<int32_t>(w[1]), static_cast<int32_t>(w[2]),
                     static_cast<int32_t>(w[3])};
         }
@@ -1270,7 +1270,8 @@ __global__ __launch_bounds__(64 * kFrWaves) void k_stage1_fr(
     const bf16_t* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
     const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod,
     int8_t* __restrict__ q, float* __restrict__ x_scale, float* __restrict__ u,
-    uint8_t* __restrict__ u_hl, int* __restrict__ zero_ints, int n_zero, UFinish fin) {
+    uint8_t* __restrict__ u_hl, int* __restrict__ zero_ints, int n_zero, UFinish fin,
+    bool pair) {
     constexpr int kRows = 16 * RG;
     if (blockIdx.x == 0)                           // arrival counters of stage 2
         for (int i = threadIdx.x; i < n_zero; i += blockDim.x) zero_ints[i] = 0;
@@ -1547,7 +1548,7 @@ __global__ __launch_bounds__(64 * kFrWaves) void k_stage1_fr(
 #pragma unroll
     for (int g = 0; g < RG; ++g) {
         const float rq = srq[16 * g + ar];
-        int8_t* qr = q + (valid[g] ? row0 + 16 * g + ar : row0) * static_cast<int64_t>(K) + 16 * kg;
+        int8_t* qr = q + code_row(valid[g] ? row0 + 16 * g + ar : row0, K, pair) + 16 * kg;
 #pragma unroll
         for (int p = 0; p < P; ++p) {
             uint32_t w[4];
@@ -1568,7 +1569,7 @@ __global__ __launch_bounds__(64 * kFrWaves) void k_stage1_fr(
                 w[2 * h + 1] = w1;
             }
             if (valid[g] && pb + p < npairs)
-                *reinterpret_cast<v4i*>(qr + 64 * (pb + p)) =
+                *reinterpret_cast<v4i*>(qr + code_col(64 * (pb + p), pair)) =
                     v4i{static_cast<int32_t>(w[0]), static_cast<int32_t>(w[1]),
                         static_cast<int32_t>(w[2]), static_cast<int32_t>(w[3])};
         }
@@ -2394,7 +2395,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     int r, int n_mod, const LT* __restrict__ r_up, int32_t* __restrict__ acc_out,
     YT* __restrict__ y, int S, int32_t* __restrict__ part, int* __restrict__ tickets,
     const int32_t* __restrict__ grows, const v4i* __restrict__ gtab,
-    const int* __restrict__ gtab_n, int64_t b_stride) {
+    const int* __restrict__ gtab_n, int64_t b_stride, bool a_pair) {
     __shared__ __attribute__((aligned(16))) GemmSmem sm;
     static_assert(kDmaStages * kDmaStageBytes <= static_cast<int>(sizeof(GemmSmem::buf)), "LDS");
     static_assert(kDmaStageBytes == kTileM * 128, "an epilogue operand fills one K stage buffer");
@@ -2479,13 +2480,16 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     // (W4 B rows: 32 rows per instruction, lane i covers row 32 j + i / 2 at
     // half i % 2.)  Rows past T or N are clamped into the matrix; their
     // results are discarded.
+    // (Row-paired A, code_row / code_col: a stage of a row pair is one
+    // 128-byte line, the next stage 128 bytes on.)
     const int8_t* src[kDmaPerStage];      // [0, kDmaA): A rows, then B rows
     uint32_t dst_off[kDmaPerStage];
+    const int a_step = a_pair ? 2 * kDmaStageK : kDmaStageK;   // A bytes between stages
 #pragma unroll
     for (int j = 0; j < kDmaA; ++j) {
         const int row = wave * kRowsPerWave + 16 * j + (lane >> 2);
         const int chunk = (lane & 3) ^ swz4(row);
-        src[j] = A + a_row(row) * K + kst0 * kDmaStageK + 16 * chunk;
+        src[j] = A + code_row(a_row(row), K, a_pair) + kst0 * a_step + 16 * chunk;
         dst_off[j] = static_cast<uint32_t>(
             __builtin_amdgcn_readfirstlane((wave * kRowsPerWave + 16 * j) * kDmaStageK));
     }
@@ -2502,7 +2506,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     }
     auto issue_one = [&](int st, int q) __attribute__((always_inline)) {
         const uint32_t sbase = lds0 + (st % kDmaStages) * kDmaStageBytes;
-        lds_dma16(src[q] + st * (q < kDmaA ? kDmaStageK : kStepB), sbase + dst_off[q]);
+        lds_dma16(src[q] + st * (q < kDmaA ? a_step : kStepB), sbase + dst_off[q]);
     };
     auto issue = [&](int st) __attribute__((always_inline)) {
 #pragma unroll
@@ -3234,7 +3238,7 @@ constexpr int kGemmWavesN = 4;
 static hipError_t launch_stage1_fr(const void* x, const int32_t* mod, const float* inv_s,
                                    const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
                                    int8_t* q, float* x_scale, float* u, uint8_t* u_hl,
-                                   int* zero_ints, int n_zero, hipStream_t s,
+                                   int* zero_ints, int n_zero, hipStream_t s, bool pair,
                                    const UFinish& fin = UFinish{nullptr, 0, 0, nullptr, nullptr}) {
     const int P = static_cast<int>(((K / 64) + kFrWaves - 1) / kFrWaves);
     // one row group: two (sharing each L1 fragment) need more than a lane's
@@ -3242,7 +3246,7 @@ static hipError_t launch_stage1_fr(const void* x, const int32_t* mod, const floa
     const dim3 grid(static_cast<unsigned>((T + 15) / 16)), block(64 * kFrWaves);
 #define MASQ_FR(PP) case PP: hipLaunchKernelGGL((k_stage1_fr<PP, 1>), grid, block, 0, s, \
         static_cast<const bf16_t*>(x), mod, inv_s, static_cast<const bf16_t*>(l_down), T, \
-        static_cast<int>(K), rank, n_mod, q, x_scale, u, u_hl, zero_ints, n_zero, fin); break;
+        static_cast<int>(K), rank, n_mod, q, x_scale, u, u_hl, zero_ints, n_zero, fin, pair); break;
     switch (P) {
         MASQ_FR(1) MASQ_FR(2) MASQ_FR(3) MASQ_FR(4) MASQ_FR(5) MASQ_FR(6) MASQ_FR(7) MASQ_FR(8)
         default: return hipErrorInvalidValue;
@@ -3254,33 +3258,35 @@ static hipError_t launch_stage1_fr(const void* x, const int32_t* mod, const floa
 
 hipError_t launch_smooth_quant(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                int64_t T, int64_t K, int n_mod, int8_t* q, float* x_scale,
-                               int* zero_ints, int n_zero, hipStream_t s, const UFinish* fin_in) {
+                               int* zero_ints, int n_zero, hipStream_t s, const UFinish* fin_in,
+                               bool pair) {
     const UFinish fin = fin_in ? *fin_in : UFinish{nullptr, 0, 0, nullptr, nullptr};
+    if (pair && K % 64 != 0) return hipErrorInvalidValue;
     if (T > kSmallMaxT && stage1_fr_ok(x_dt, K, n_mod))
         return launch_stage1_fr(x, mod, inv_s, nullptr, T, K, 0, n_mod, q, x_scale, nullptr,
-                                nullptr, zero_ints, n_zero, s, fin);
+                                nullptr, zero_ints, n_zero, s, pair, fin);
     // a wave per row for large batches whose rows fit its register cache
     if (T >= kRowsPerWaveMinT && K <= 64 * 8 * 8) {
         const dim3 grid(static_cast<unsigned>((T + 3) / 4)), block(256);
         if (x_dt == DT::BF16)
             hipLaunchKernelGGL((k_smooth_quant_rows<bf16_t, 8>), grid, block, 0, s,
                                static_cast<const bf16_t*>(x), mod, inv_s, T, static_cast<int>(K),
-                               n_mod, q, x_scale, zero_ints, n_zero, fin);
+                               n_mod, q, x_scale, zero_ints, n_zero, fin, pair);
         else
             hipLaunchKernelGGL((k_smooth_quant_rows<float, 8>), grid, block, 0, s,
                                static_cast<const float*>(x), mod, inv_s, T, static_cast<int>(K),
-                               n_mod, q, x_scale, zero_ints, n_zero, fin);
+                               n_mod, q, x_scale, zero_ints, n_zero, fin, pair);
         return hipGetLastError();
     }
     const dim3 grid(static_cast<unsigned>(T)), block(256);
     if (x_dt == DT::BF16)
         hipLaunchKernelGGL(k_smooth_quant<bf16_t>, grid, block, 0, s,
                            static_cast<const bf16_t*>(x), mod, inv_s, static_cast<int>(K), n_mod,
-                           q, x_scale, zero_ints, n_zero, T, fin);
+                           q, x_scale, zero_ints, n_zero, T, fin, pair);
     else
         hipLaunchKernelGGL(k_smooth_quant<float>, grid, block, 0, s,
                            static_cast<const float*>(x), mod, inv_s, static_cast<int>(K), n_mod,
-                           q, x_scale, zero_ints, n_zero, T, fin);
+                           q, x_scale, zero_ints, n_zero, T, fin, pair);
     return hipGetLastError();
 }
 
@@ -3327,10 +3333,11 @@ hipError_t launch_down_wide(const void* x, DT x_dt, const int32_t* mod, const fl
 hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const float* inv_s,
                                const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
                                int8_t* q, float* x_scale, float* u, uint8_t* u_hl,
-                               int* zero_ints, int n_zero, hipStream_t s) {
+                               int* zero_ints, int n_zero, hipStream_t s, bool pair) {
+    if (pair && K % 64 != 0) return hipErrorInvalidValue;
     if (stage1_fr_ok(x_dt, K, n_mod))
         return launch_stage1_fr(x, mod, inv_s, l_down, T, K, rank, n_mod, q, x_scale, u, u_hl,
-                                zero_ints, n_zero, s);
+                                zero_ints, n_zero, s, pair);
     // 32 rows per workgroup halve the L1 re-reads once the batch fills the
     // chip at that size; smaller batches keep 16 rows for more workgroups
     const bool wide = T >= kFuseWideMinT;
@@ -3338,7 +3345,7 @@ hipError_t launch_stage1_fused(const void* x, DT x_dt, const int32_t* mod, const
     const dim3 grid(static_cast<unsigned>((T + rows - 1) / rows)), block(64 * kFuseWaves);
 #define MASQ_F1(XT, RG, SL) hipLaunchKernelGGL((k_stage1_fused<XT, RG, SL>), grid, block, 0, s, \
         static_cast<const XT*>(x), mod, inv_s, static_cast<const bf16_t*>(l_down), T, \
-        static_cast<int>(K), rank, n_mod, q, x_scale, u, u_hl, zero_ints, n_zero)
+        static_cast<int>(K), rank, n_mod, q, x_scale, u, u_hl, zero_ints, n_zero, pair)
     // 32 rows: smoothing factors from LDS when all modalities' fit (bf16
     // activations); 16 rows keep them in registers (their pass 1 was no
     // faster with them in LDS and a deeper load pipeline)
@@ -3423,7 +3430,7 @@ static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* w
                           const float* w_scale, int64_t T, int64_t K, int64_t N,
                           const int32_t* mod, const float* u, const uint8_t* u_hl, int rank,
                           int n_mod, const void* r_up, int32_t* acc, void* y, int S,
-                          int32_t* part, int* tickets, hipStream_t s) {
+                          int32_t* part, int* tickets, hipStream_t s, bool a_pair) {
     const int tiles_m = static_cast<int>((T + kTileM - 1) / kTileM);
     const int tiles_n = static_cast<int>((N + kTileN - 1) / kTileN);
     const int nt = tiles_m * tiles_n;
@@ -3436,13 +3443,15 @@ static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* w
                                dim3(128 * kGemmWavesN), 0, s, q, wq, x_scale, w_scale, T,
                                static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
                                u_hl, rank, n_mod, static_cast<const LT*>(r_up), acc,
-                               static_cast<YT*>(y), S, part, tickets, nullptr, nullptr, nullptr, 0);
+                               static_cast<YT*>(y), S, part, tickets, nullptr, nullptr, nullptr, 0,
+                               a_pair);
         else
             hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN, false, W4>), gridk,
                                dim3(128 * kGemmWavesN), 0, s, q, wq, x_scale, w_scale, T,
                                static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
                                u_hl, rank, n_mod, static_cast<const LT*>(r_up), acc,
-                               static_cast<YT*>(y), 1, nullptr, nullptr, nullptr, nullptr, nullptr, 0);
+                               static_cast<YT*>(y), 1, nullptr, nullptr, nullptr, nullptr, nullptr, 0,
+                               a_pair);
     } else if constexpr (!W4)
         hipLaunchKernelGGL((k_gemm<YT, LT, CMC, ACC>), grid, block, 0, s, q, wq, x_scale, w_scale, T,
                            static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
@@ -3471,13 +3480,13 @@ static void launch_gemm_grouped_t(const int8_t* q, const float* x_scale, const i
                            block, 0, s, q, wq, x_scale, w_scale, T, static_cast<int>(K),
                            static_cast<int>(N), tiles_m, tiles_n, nullptr, nullptr, nullptr, 0, n_mod,
                            nullptr, nullptr, static_cast<YT*>(y), S, part, tickets, rows, tb, tab_n,
-                           N * K);
+                           N * K, false);
     else
         hipLaunchKernelGGL((k_gemm_dma<YT, bf16_t, false, false, kGemmWavesN, false, false, true>), grid,
                            block, 0, s, q, wq, x_scale, w_scale, T, static_cast<int>(K),
                            static_cast<int>(N), tiles_m, tiles_n, nullptr, nullptr, nullptr, 0, n_mod,
                            nullptr, nullptr, static_cast<YT*>(y), 1, nullptr, nullptr, rows, tb,
-                           tab_n, N * K);
+                           tab_n, N * K, false);
 }
 
 hipError_t launch_gemm_grouped(const int8_t* q, const float* x_scale, const int8_t* wq,
@@ -3501,10 +3510,12 @@ hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
                        int32_t* dec_part, int* dec_tickets, int gk_splits, int32_t* gk_part,
                        int* gk_tickets, const float* u_part, int n_kslices,
                        int rank, int n_mod, const void* r_up, DT lr_dt, bool cmc, int32_t* acc,
-                       void* y, DT y_dt, hipStream_t s, bool w4) {
+                       void* y, DT y_dt, hipStream_t s, bool w4, bool a_pair) {
     // packed 4-bit Wq: K % 64 == 0 (checked by the caller), so every batch
     // takes the decode, small-batch or direct-to-LDS kernel
     if (w4 && K % 64 != 0) return hipErrorInvalidValue;
+    // row-paired codes are read by the direct-to-LDS GEMM only
+    if (a_pair && !paired_codes(T, K)) return hipErrorInvalidValue;
     int dns = 0, dsp = 0, dng = 0;
     if (small_path(T, K)) plan_decode(K, N, dns, dsp, dng);
     if (small_path(T, K) && dec_part != nullptr && dec_tickets != nullptr && acc == nullptr &&
@@ -3534,7 +3545,7 @@ hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
 #undef MASQ_SMALL
         return hipGetLastError();
     }
-#define MASQ_GEMM(YT, LT, C, A) (w4 ? launch_gemm_t<YT, LT, C, A, true> : launch_gemm_t<YT, LT, C, A, false>)(q, x_scale, wq, w_scale, T, K, N, mod, u, u_hl, rank, n_mod, r_up, acc, y, gk_splits, gk_part, gk_tickets, s)
+#define MASQ_GEMM(YT, LT, C, A) (w4 ? launch_gemm_t<YT, LT, C, A, true> : launch_gemm_t<YT, LT, C, A, false>)(q, x_scale, wq, w_scale, T, K, N, mod, u, u_hl, rank, n_mod, r_up, acc, y, gk_splits, gk_part, gk_tickets, s, a_pair)
     // the int32 accumulator output exists only for the plain product (no
     // compensation); it is a separate instantiation because storing the
     // accumulators as well raises the epilogue's register pressure

@@ -45,9 +45,18 @@ def _tol(act_dtype, lr_dtype="f32"):
 
 def _ws_codes(ws, T, K):
     """The codes q [T][K] and scales [T] stage 1 leaves in the fused layer's
-    workspace: q at offset 0, the scales at the next 256-byte boundary."""
-    off = (T * K + 255) // 256 * 256
-    q = ws[: T * K].view(torch.int8).view(T, K)
+    workspace: q at offset 0, the scales at the next 256-byte boundary.  Past
+    the small-batch path (T > 16) with K % 64 == 0 the codes are row-paired:
+    rows 2i and 2i + 1 alternate in 64-byte pieces ([T/2][K/64][2][64]), the
+    batch rounded up to whole pairs."""
+    paired = T > 16 and K % 64 == 0
+    rows = (T + 1) // 2 * 2 if paired else T
+    off = (rows * K + 255) // 256 * 256
+    q = ws[: rows * K].view(torch.int8)
+    if paired:
+        q = q.view(rows // 2, K // 64, 2, 64).permute(0, 2, 1, 3).reshape(rows, K)[:T]
+    else:
+        q = q.view(T, K)
     dx = ws[off: off + 4 * T].view(torch.float32)
     return q, dx
 
