@@ -182,7 +182,9 @@ masq_status masq_linear_fused_noalloc(const void* x, masq_dtype x_dt, const int3
  * compensation.  The rows are grouped by modality on the device (a stable
  * counting sort of the ids) and each 256-row tile of one modality's rows is
  * multiplied by that modality's weight; the host never reads the ids, and
- * any layout of modalities works.
+ * any layout of modalities works.  Batches of at most 16 tokens (with
+ * c_in <= 20480) instead stream each modality's weight once through the
+ * small-batch GEMM, which stores only the rows of that modality's tokens.
  *   wq       [n_mod][c_out][c_in] int8, Q(S_m W) transposed, per modality
  *   w_scale  [n_mod][c_out] f32
  *   inv_smooth, x, modality, y as for masq_linear_fused (ids outside

@@ -118,9 +118,15 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
 
 // Workspace of the MAS-only comparator: codes, scales, the rows grouped by
 // modality, the tile table and its length, and (K split over few tiles)
-// arrival counters and slice accumulators.
+// arrival counters and slice accumulators; for small batches (the decode
+// GEMM per modality) codes, scales and the decode GEMM's partials and
+// counters.
 struct MasOnlyWs {
-    int8_t* q;
+    bool decode;       // small batch: the decode GEMM once per modality, plain codes
+    int32_t* dec_part; // its partial sums [ns + 1][kSmallMaxT][N]
+    int* dec_tickets;  // and arrival counters [groups]
+    int dec_groups;
+    int8_t* q;         // codes: plain when `decode`, else row-paired (code_row / code_col)
     float* x_scale;
     int32_t* rows;
     int32_t* tab;
@@ -141,9 +147,25 @@ MasOnlyWs plan_mas_only(void* base, int64_t T, int64_t K, int64_t N, int n_mod) 
         off += align256(bytes);
         return p;
     };
+    int ns = 0, sp = 0;
+    w.decode = T > 0 && N > 0 && small_path(T, K);
+    if (w.decode) {
+        plan_decode(K, N, ns, sp, w.dec_groups);
+        w.decode = ns <= kDecMaxSlices;
+    }
+    if (w.decode) {
+        w.q = reinterpret_cast<int8_t*>(carve(static_cast<size_t>(T) * static_cast<size_t>(K)));
+        w.x_scale = reinterpret_cast<float*>(carve(static_cast<size_t>(T) * sizeof(float)));
+        w.dec_part = reinterpret_cast<int32_t*>(carve(static_cast<size_t>(ns + 1) * kSmallMaxT *
+                                                      static_cast<size_t>(N) * sizeof(int32_t)));
+        w.dec_tickets = reinterpret_cast<int*>(carve(static_cast<size_t>(w.dec_groups) * sizeof(int)));
+        w.bytes = off;
+        return w;
+    }
     const int tab_max = grouped_tab_max(T, n_mod);
     const int64_t tiles = static_cast<int64_t>(tab_max) * ((N + kTileN - 1) / kTileN);
-    w.q = reinterpret_cast<int8_t*>(carve(static_cast<size_t>(T) * static_cast<size_t>(K)));
+    // codes row-paired (code_row / code_col; K % 64 == 0), whole row pairs
+    w.q = reinterpret_cast<int8_t*>(carve(static_cast<size_t>((T + 1) / 2 * 2) * static_cast<size_t>(K)));
     w.x_scale = reinterpret_cast<float*>(carve(static_cast<size_t>(T) * sizeof(float)));
     w.rows = reinterpret_cast<int32_t*>(carve(static_cast<size_t>(T) * sizeof(int32_t)));
     w.tab = reinterpret_cast<int32_t*>(carve(static_cast<size_t>(tab_max) * 4 * sizeof(int32_t)));
@@ -452,11 +474,23 @@ masq_status masq_mas_only_linear(const void* x, masq_dtype x_dt, const int32_t* 
     if (workspace_bytes < w.bytes) return MASQ_ERR_WORKSPACE;
     hipStream_t s = static_cast<hipStream_t>(stream);
     (void)hipGetLastError();
+    if (w.decode) {
+        // a small batch streams each modality's weight once: the decode GEMM
+        // per weight, storing its own tokens' rows (the quantiser clears the
+        // arrival counters)
+        st = from_hip(masq::launch_smooth_quant(x, to_dt(x_dt), modality, inv_smooth, T, c_in,
+                                                n_mod, w.q, w.x_scale, w.dec_tickets,
+                                                w.dec_groups, s));
+        if (st != MASQ_OK) return st;
+        return from_hip(masq::launch_gemm_decode_mas(w.q, w.x_scale, wq, w_scale, T, c_in, c_out,
+                                                     modality, n_mod, w.dec_part, w.dec_tickets,
+                                                     y, to_dt(y_dt), s));
+    }
     st = from_hip(masq::launch_group_rows(modality, T, n_mod, w.rows, w.tab, w.tab_n, w.tickets,
                                           w.n_tickets, s));
     if (st != MASQ_OK) return st;
     st = from_hip(masq::launch_smooth_quant(x, to_dt(x_dt), modality, inv_smooth, T, c_in, n_mod,
-                                            w.q, w.x_scale, nullptr, 0, s));
+                                            w.q, w.x_scale, nullptr, 0, s, nullptr, true));
     if (st != MASQ_OK) return st;
     return from_hip(masq::launch_gemm_grouped(w.q, w.x_scale, wq, w_scale, T, c_in, c_out, n_mod,
                                               w.rows, w.tab, w.tab_n, y, to_dt(y_dt), w.S, w.part,

@@ -233,12 +233,23 @@ hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
 // MAS-only comparator (a weight per modality, no compensation): rows grouped
 // by modality on the device, then the direct-to-LDS GEMM over tiles of one
 // modality each (K % 64 == 0).  The tile table holds at most
-// grouped_tab_max entries {first row, rows, modality, 0}.
+// grouped_tab_max entries {first row, rows, modality, 0}.  The codes q are
+// row-paired (code_row / code_col), the quantiser's pair layout.
 inline int grouped_tab_max(int64_t T, int n_mod) {
     return static_cast<int>((T + kTileM - 1) / kTileM) + n_mod - 1;
 }
 hipError_t launch_group_rows(const int32_t* mod, int64_t T, int n_mod, int32_t* rows,
                              int32_t* tab, int* tab_n, int* zero_ints, int n_zero, hipStream_t s);
+// MAS-only at small batches (small_path, plan_decode's slices within
+// kDecMaxSlices): the decode GEMM once per modality's weight (wq
+// [n_mod][N][K], w_scale [n_mod][N]), each launch storing the outputs of its
+// modality's tokens only; plain codes.  part / tickets: the decode GEMM's
+// workspace (tickets zero before the first launch; each launch leaves them
+// zero).
+hipError_t launch_gemm_decode_mas(const int8_t* q, const float* x_scale, const int8_t* wq,
+                                  const float* w_scale, int64_t T, int64_t K, int64_t N,
+                                  const int32_t* mod, int n_mod, int32_t* part, int* tickets,
+                                  void* y, DT y_dt, hipStream_t s);
 hipError_t launch_gemm_grouped(const int8_t* q, const float* x_scale, const int8_t* wq,
                                const float* w_scale, int64_t T, int64_t K, int64_t N, int n_mod,
                                const int32_t* rows, const int32_t* tab, const int* tab_n, void* y,

@@ -2871,6 +2871,8 @@ __global__ __launch_bounds__(256) void k_gemm_small(
 // beside the int32 partials.  The last workgroup then only adds.
 // W4: Wq holds packed 4-bit codes (K / 2 bytes a row, 8 bytes a lane a step,
 // unpacked into the MFMA operand in registers).
+// only_mod >= 0 (the MAS-only comparator, one launch per modality's weight):
+// only the outputs of tokens of that modality are stored.
 template <typename YT, typename LT, bool W4>
 __global__ __launch_bounds__(256, 2) void k_gemm_decode(
     const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
@@ -2878,7 +2880,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
     const int32_t* __restrict__ mod, const float* __restrict__ u,
     const float* __restrict__ u_part, int n_kslices, int r, int n_mod,
     const LT* __restrict__ r_up, int32_t* __restrict__ part, int* __restrict__ tickets,
-    YT* __restrict__ y) {
+    YT* __restrict__ y, int only_mod) {
     __shared__ __attribute__((aligned(16))) uint8_t sq[kDecSteps * 1024];
     // compensation operands (u partials of the token share, then L2 rows of
     // the group's channels) or, when they do not fit, the u rows of the batch
@@ -3051,7 +3053,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
     constexpr int kOut = kSmallMaxT * kDecCh / 256;
     constexpr int kRStage = 16384;
     constexpr int kRPieces = kRStage / 16 / 256;                       // per thread
-    int pv[kOut][kDecMaxSlices], mv[kOut];
+    int pv[kOut][kDecMaxSlices], mv[kOut], om[kOut];
     float dxv[kOut], dwv[kOut], cv[kOut];
 #pragma unroll
     for (int i = 0; i < kOut; ++i) {
@@ -3068,6 +3070,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
         dxv[i] = x_scale[t];
         dwv[i] = w_scale[ch];
         mv[i] = cmc ? sane_mod(mod[t], n_mod) : 0;
+        om[i] = only_mod >= 0 ? sane_mod(mod[t], n_mod) : -1;
     }
     const int row_bytes = r * static_cast<int>(sizeof(LT));
     const bool staged = cmc && !early && (n_mod - 1) * kDecCh * row_bytes <= kRStage;
@@ -3132,7 +3135,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_decode(
     for (int i = 0; i < kOut; ++i) {
         const int idx = tid + 256 * i;
         const int t = idx / kDecCh, o = idx % kDecCh, ch = g * kDecCh + o;
-        if (t >= T || ch >= N) continue;
+        if (t >= T || ch >= N || om[i] != only_mod) continue;
         int a = pv[i][0];
 #pragma unroll
         for (int q = 1; q < kDecMaxSlices; ++q) a += q < ns ? pv[i][q] : 0;
@@ -3404,13 +3407,39 @@ static void launch_gemm_decode_t(const int8_t* q, const float* x_scale, const in
                                  const float* w_scale, int64_t T, int64_t K, int64_t N,
                                  const int32_t* mod, const float* u, const float* u_part,
                                  int n_kslices, int rank, int n_mod, const void* r_up,
-                                 int32_t* part, int* tickets, void* y, hipStream_t s) {
+                                 int32_t* part, int* tickets, void* y, hipStream_t s,
+                                 int only_mod = -1) {
     int ns, sp, ngroups;
     plan_decode(K, N, ns, sp, ngroups);
     hipLaunchKernelGGL((k_gemm_decode<YT, LT, W4>), dim3(static_cast<unsigned>(ngroups * ns)), dim3(256),
                        0, s, q, wq, x_scale, w_scale, static_cast<int>(T), static_cast<int>(K),
                        static_cast<int>(N), ns, sp, mod, u, u_part, n_kslices, rank, n_mod,
-                       static_cast<const LT*>(r_up), part, tickets, static_cast<YT*>(y));
+                       static_cast<const LT*>(r_up), part, tickets, static_cast<YT*>(y), only_mod);
+}
+
+hipError_t launch_gemm_decode_mas(const int8_t* q, const float* x_scale, const int8_t* wq,
+                                  const float* w_scale, int64_t T, int64_t K, int64_t N,
+                                  const int32_t* mod, int n_mod, int32_t* part, int* tickets,
+                                  void* y, DT y_dt, hipStream_t s) {
+    int ns = 0, sp = 0, ng = 0;
+    if (!small_path(T, K)) return hipErrorInvalidValue;
+    plan_decode(K, N, ns, sp, ng);
+    if (ns > kDecMaxSlices) return hipErrorInvalidValue;
+    for (int m = 0; m < n_mod; ++m) {
+        const int8_t* wm = wq + static_cast<int64_t>(m) * N * K;
+        const float* sm = w_scale + static_cast<int64_t>(m) * N;
+        if (y_dt == DT::BF16)
+            launch_gemm_decode_t<bf16_t, bf16_t, false>(q, x_scale, wm, sm, T, K, N, mod, nullptr,
+                                                         nullptr, 1, 0, n_mod, nullptr, part,
+                                                         tickets, y, s, m);
+        else
+            launch_gemm_decode_t<float, bf16_t, false>(q, x_scale, wm, sm, T, K, N, mod, nullptr,
+                                                        nullptr, 1, 0, n_mod, nullptr, part,
+                                                        tickets, y, s, m);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 template <typename YT, typename LT, bool W4>
@@ -3480,13 +3509,13 @@ static void launch_gemm_grouped_t(const int8_t* q, const float* x_scale, const i
                            block, 0, s, q, wq, x_scale, w_scale, T, static_cast<int>(K),
                            static_cast<int>(N), tiles_m, tiles_n, nullptr, nullptr, nullptr, 0, n_mod,
                            nullptr, nullptr, static_cast<YT*>(y), S, part, tickets, rows, tb, tab_n,
-                           N * K, false);
+                           N * K, true);
     else
         hipLaunchKernelGGL((k_gemm_dma<YT, bf16_t, false, false, kGemmWavesN, false, false, true>), grid,
                            block, 0, s, q, wq, x_scale, w_scale, T, static_cast<int>(K),
                            static_cast<int>(N), tiles_m, tiles_n, nullptr, nullptr, nullptr, 0, n_mod,
                            nullptr, nullptr, static_cast<YT*>(y), 1, nullptr, nullptr, rows, tb,
-                           tab_n, N * K, false);
+                           tab_n, N * K, true);
 }
 
 hipError_t launch_gemm_grouped(const int8_t* q, const float* x_scale, const int8_t* wq,
@@ -3521,7 +3550,7 @@ hipError_t launch_gemm(const int8_t* q, const float* x_scale, const int8_t* wq,
     if (small_path(T, K) && dec_part != nullptr && dec_tickets != nullptr && acc == nullptr &&
         dns <= kDecMaxSlices) {
         const float* uu = cmc ? u : nullptr;
-#define MASQ_DEC(YT, LT) (w4 ? launch_gemm_decode_t<YT, LT, true> : launch_gemm_decode_t<YT, LT, false>)(q, x_scale, wq, w_scale, T, K, N, mod, uu, u_part, n_kslices, rank, n_mod, r_up, dec_part, dec_tickets, y, s)
+#define MASQ_DEC(YT, LT) (w4 ? launch_gemm_decode_t<YT, LT, true> : launch_gemm_decode_t<YT, LT, false>)(q, x_scale, wq, w_scale, T, K, N, mod, uu, u_part, n_kslices, rank, n_mod, r_up, dec_part, dec_tickets, y, s, -1)
         if (y_dt == DT::BF16) {
             if (lr_dt == DT::BF16) MASQ_DEC(bf16_t, bf16_t);
             else MASQ_DEC(bf16_t, float);
