@@ -1837,10 +1837,11 @@ template <> struct Cmc<float> {           // fp32 operands, v_mfma_f32_32x32x2f3
 // range of tiles, ordered in groups of 8 tile-rows, so that tiles running
 // together on one XCD share A and B stages in its L2.  Returns false for the
 // padding workgroups of the last XCD range.
-__device__ __forceinline__ bool tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+__device__ __forceinline__ bool tile_coords_at(int b, int tiles_m, int tiles_n, int& tm, int& tn) {
     const int nt = tiles_m * tiles_n;
     const int per_xcd = (nt + 7) >> 3;
-    const int L = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if ((b >> 3) >= per_xcd) return false;
+    const int L = (b & 7) * per_xcd + (b >> 3);
     if (L >= nt) return false;
     constexpr int GM = 8;
     const int gsize = GM * tiles_n;
@@ -1852,6 +1853,9 @@ __device__ __forceinline__ bool tile_coords(int tiles_m, int tiles_n, int& tm, i
     tn = li / gm;
     return true;
 }
+__device__ __forceinline__ bool tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+    return tile_coords_at(static_cast<int>(blockIdx.x), tiles_m, tiles_n, tm, tn);
+}
 
 // Shared LDS of both GEMM kernels: the K stages during the main loop, then
 // the compensation pieces in the epilogue.
@@ -1861,12 +1865,16 @@ __device__ __forceinline__ bool tile_coords(int tiles_m, int tiles_n, int& tm, i
 constexpr int tr_pitch(int tw) { return 2 * tw + 16; }
 constexpr int kTrBytes = 20480;       // max(4 x 32 x pitch(64), 8 x 32 x pitch(32))
 
-struct GemmSmem {
-    uint8_t buf[2 * 65536];
+// Per-row and per-channel epilogue operands of a tile.
+struct RowOps {
     float dx[kTileM];
     float ws[kTileN];
     int mod[kTileM];          // modality of each row (invalid ids read as text)
     int rawmod[kTileM];       // modality ids as given (LDS-DMA target)
+};
+struct GemmSmem {
+    uint8_t buf[2 * 65536];
+    RowOps ro[2];             // the tile's set and (persistent grid) the next tile's
     unsigned wpresent[8];     // per wave: bit m set if a row of modality m is in its rows
     uint8_t tr[kTrBytes];     // 16-byte aligned (the transposes use 16-byte LDS accesses)
     int last;                 // split K: this workgroup is the last slice of its tile to arrive
@@ -1906,7 +1914,7 @@ struct EpiDma {
     unsigned present;
     bool pre;
     int off_uh, off_ul, off_r[2];
-    int grp_rows;      // grouped tile (GRP): its valid rows; sm.rawmod holds their token indices
+    int grp_rows;      // grouped tile (GRP): its valid rows; the rawmod operands hold their token indices
 };
 
 // NWN waves along the channels (2: four waves of 128 x 128, 4: eight waves of
@@ -1918,23 +1926,26 @@ template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2, bool DMA = 
 __device__ __forceinline__ void gemm_epilogue(
     v16i (&acc)[4][8 / NWN], GemmSmem& sm, const EpiPrefetch& pf, int64_t T, int N, int64_t row0,
     int col0, const float* __restrict__ u, int r, int n_mod, const LT* __restrict__ r_up,
-    int32_t* __restrict__ acc_out, YT* __restrict__ y, const EpiDma& ed = EpiDma{}) {
+    int32_t* __restrict__ acc_out, YT* __restrict__ y, const EpiDma& ed = EpiDma{}, int rb = 0,
+    int tid_in = -1) {
     constexpr int NJ = 8 / NWN, NW = 2 * NWN, NT = 64 * NW;
     constexpr int kWaveCols = 32 * NJ;                 // channels per wave
     constexpr int TW = NJ == 4 ? 64 : 32;              // transpose unit width (channels)
     constexpr int kPitch = tr_pitch(TW);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = tid_in >= 0 ? tid_in : static_cast<int>(threadIdx.x);
+    const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave / NWN, wn = wave % NWN;
+    RowOps& ro = sm.ro[rb];
     // dx, ws, mod and wpresent lie outside the K-stage buffers, so they can be
     // written before the barrier; after it every wave is also done with the
     // K stages
     if constexpr (!DMA) {
         if (tid < kTileM) {                    // threads past 256 carry no prefetch
-            sm.dx[tid] = pf.dx;
-            sm.ws[tid] = pf.ws;
+            ro.dx[tid] = pf.dx;
+            ro.ws[tid] = pf.ws;
         }
         if constexpr (CMC) {
-            if (tid < kTileM) sm.mod[tid] = pf.mod;
+            if (tid < kTileM) ro.mod[tid] = pf.mod;
             unsigned wp = 0;
             for (int m = 1; m < n_mod; ++m)
                 if (__ballot(tid < kTileM && pf.mod == m) != 0ull) wp |= 1u << m;
@@ -1973,7 +1984,7 @@ __device__ __forceinline__ void gemm_epilogue(
         } else if (n_present > 0 && staged && y != nullptr) {
             for (int c = 0; c < n_chunks; ++c) {
                 uint8_t* base = sm.buf + c * chunk_bytes;
-                Cmc<LT>::template stage_u<NT>(base, sm.mod, u, row0, T, r, 64 * c, tid);
+                Cmc<LT>::template stage_u<NT>(base, ro.mod, u, row0, T, r, 64 * c, tid);
                 int p = 0;
                 for (int m = 1; m < n_mod; ++m) {
                     if (!(present & (1u << m))) continue;
@@ -1992,14 +2003,14 @@ __device__ __forceinline__ void gemm_epilogue(
     // 4 (lane / 32) + e % 4.  Loops over blocks are fully unrolled: the
     // accumulators are registers and must be indexed by constants.
     static_assert(!GRP || (DMA && !CMC && !ACC), "grouped tiles: plain product, DMA kernel");
-    // GRP: local row l of the tile is token sm.rawmod[l], valid for l < ed.grp_rows
+    // GRP: local row l of the tile is token ro.rawmod[l], valid for l < ed.grp_rows
     const bool interior = GRP ? (ed.grp_rows == kTileM && col0 + kTileN <= N)
                               : (row0 + kTileM <= T) && (col0 + kTileN <= N);
     auto row_ok = [&](int local) __attribute__((always_inline)) {
         return GRP ? local < ed.grp_rows : row0 + local < T;
     };
     auto out_row = [&](int local) __attribute__((always_inline)) -> int64_t {
-        return GRP ? static_cast<int64_t>(sm.rawmod[local]) : row0 + local;
+        return GRP ? static_cast<int64_t>(ro.rawmod[local]) : row0 + local;
     };
     auto tok_of = [&](int i) { return wm * 128 + i * 32 + (lane & 31); };
     auto ch_of = [&](int j, int g) { return wn * kWaveCols + j * 32 + 8 * g + 4 * (lane >> 5); };
@@ -2030,7 +2041,7 @@ __device__ __forceinline__ void gemm_epilogue(
     // dequantisation of block (i, j) with the channel scales ws[g] of its
     // four 4-channel groups
     auto dequant_with = [&](const int i, const int j, const v4f (&ws)[4]) __attribute__((always_inline)) {
-        const float dx = sm.dx[tok_of(i)];
+        const float dx = ro.dx[tok_of(i)];
         const v16i a = acc[i][j];
         v16f yb;
 #pragma unroll
@@ -2042,7 +2053,7 @@ __device__ __forceinline__ void gemm_epilogue(
     };
     auto load_ws = [&](const int j, v4f (&ws)[4]) __attribute__((always_inline)) {
 #pragma unroll
-        for (int g = 0; g < 4; ++g) ws[g] = *reinterpret_cast<const v4f*>(&sm.ws[ch_of(j, g)]);
+        for (int g = 0; g < 4; ++g) ws[g] = *reinterpret_cast<const v4f*>(&ro.ws[ch_of(j, g)]);
     };
     auto dequant = [&](const int i, const int j) __attribute__((always_inline)) {
         v4f ws[4];
@@ -2133,7 +2144,7 @@ __device__ __forceinline__ void gemm_epilogue(
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int trow = tok_of(i);
-                const int tm_ = sm.mod[trow];
+                const int tm_ = ro.mod[trow];
                 v16f ybs[NJ];
 #pragma unroll
                 for (int j = 0; j < NJ; ++j) ybs[j] = dequant(i, j);
@@ -2179,7 +2190,7 @@ __device__ __forceinline__ void gemm_epilogue(
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int trow = tok_of(i);
-                const int tm_ = sm.mod[trow];
+                const int tm_ = ro.mod[trow];
                 v16f ybs[NJ];
 #pragma unroll
                 for (int j = 0; j < NJ; ++j) ybs[j] = dequant(i, j);
@@ -2206,7 +2217,7 @@ __device__ __forceinline__ void gemm_epilogue(
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int trow = tok_of(i);
-            const int tm_ = sm.mod[trow];
+            const int tm_ = ro.mod[trow];
             v16f ybs[NJ];
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
@@ -2386,8 +2397,16 @@ __device__ __forceinline__ int swz4(int row) { return (row >> 2) & 3; }
 // w_scale + modality N).  A rows and their scales are gathered by the DMA,
 // outputs are written to the tokens' own rows; table entries past *gtab_n
 // (the grid is sized for the largest possible table) exit at once.
+//
+// PERSIST (whole tiles of one weight, no split): a grid of at most one
+// workgroup per compute unit walks the tiles blockIdx.x, + gridDim.x, ...
+// (gridDim.x a multiple of 8, so every tile keeps its XCD).  While a tile's
+// epilogue runs, the next tile's per-row operands go to the other of two
+// LDS sets and its first stages into the K buffers the epilogue leaves free
+// (all three with no compensation operands staged, one with a single
+// non-text modality's), the ring of K buffers then starting at that buffer.
 template <typename YT, typename LT, bool CMC, bool ACC, int NWN = 2, bool SPLIT = false,
-          bool W4 = false, bool GRP = false>
+          bool W4 = false, bool GRP = false, bool PERSIST = false>
 __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     const int8_t* __restrict__ A, const int8_t* __restrict__ B, const float* __restrict__ x_scale,
     const float* __restrict__ w_scale, int64_t T, int K, int N, int tiles_m, int tiles_n,
@@ -2399,16 +2418,44 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     __shared__ __attribute__((aligned(16))) GemmSmem sm;
     static_assert(kDmaStages * kDmaStageBytes <= static_cast<int>(sizeof(GemmSmem::buf)), "LDS");
     static_assert(kDmaStageBytes == kTileM * 128, "an epilogue operand fills one K stage buffer");
+    static_assert(!PERSIST || (!SPLIT && !GRP), "persistent grid: whole tiles, one weight");
     if constexpr (!SPLIT) S = 1;
+    constexpr int NJ = 8 / NWN, NW = 2 * NWN;
+    constexpr int kRowsPerWave = kTileM / NW;           // DMA rows of A and of B per wave
+    constexpr int kStepB = W4 ? kDmaStageK / 2 : kDmaStageK;   // B bytes per row and stage
+    constexpr int kDmaA = kRowsPerWave / 16;            // DMA instructions per thread per stage:
+    constexpr int kDmaB = kRowsPerWave * kStepB / 1024; //   A rows, B rows
+    constexpr int kDmaPerStage = kDmaA + kDmaB;
+    constexpr int kDmaExtra = kRowsPerWave / 8;         // per epilogue operand (128-byte rows)
+    static_assert(kDmaB >= 1 && kRowsPerWave * kStepB % 1024 == 0, "B rows per DMA");
+    using BRaw = std::conditional_t<W4, v2i, v4i>;      // a lane's B bytes of one k step
+    const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sm.buf));
+    // per-row operand pieces: 64 entries per instruction, piece c (x scales,
+    // channel scales, modality ids; 4 each) issued by wave c % NW
+    constexpr int kPieces = (CMC || GRP) ? 12 : 8;
+    constexpr int kPiecesMin = kPieces / NW;            // the fewest a wave issues
+    const int nk_all = K / kDmaStageK;
+    const int a_step = a_pair ? 2 * kDmaStageK : kDmaStageK;   // A bytes between stages
+    // carried from one tile to the next (PERSIST)
+    int ring = 0;        // K buffer of the tile's stage 0
+    int rb = 0;          // LDS set of the tile's per-row operands
+    int pf = 0;          // the tile's stages already queued
+    for (int vb = static_cast<int>(blockIdx.x);; vb += static_cast<int>(gridDim.x)) {
+    // the thread index through an opaque copy, so that no per-lane address of
+    // a tile's loop or epilogue is hoisted out of the tile loop (where it would
+    // stay live across the main loop)
+    int tid = static_cast<int>(threadIdx.x);
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / NWN, wn = wave % NWN;
     int tm, tn;
-    if (!tile_coords(tiles_m, tiles_n * S, tm, tn)) return;
+    if (!tile_coords_at(vb, tiles_m, tiles_n * S, tm, tn)) break;
     // split K: slice sl of S covers stages [kst0, kst0 + nk) of the tile
     int sl = 0;
     if constexpr (SPLIT) {
         sl = tn % S;
         tn /= S;
     }
-    const int nk_all = K / kDmaStageK;
     const int nk_slice = SPLIT ? (nk_all + S - 1) / S : nk_all;
     const int kst0 = sl * nk_slice;
     const int64_t row0 = GRP ? 0 : static_cast<int64_t>(tm) * kTileM;
@@ -2416,7 +2463,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     // GRP: the tile's rows grows[gfirst .. gfirst + grows_n), modality gmod
     int gfirst = 0, grows_n = kTileM, gmod = 0;
     if constexpr (GRP) {
-        if (tm >= *gtab_n) return;                      // wave-uniform
+        if (tm >= *gtab_n) break;                       // wave-uniform (one tile per workgroup)
         const v4i e = gtab[tm];
         gfirst = e.x;
         grows_n = e.y;
@@ -2430,18 +2477,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
         if constexpr (GRP) return grows[gfirst + min(l, grows_n - 1)];
         else return min(row0 + l, T - 1);
     };
-    constexpr int NJ = 8 / NWN, NW = 2 * NWN;
-    constexpr int kRowsPerWave = kTileM / NW;           // DMA rows of A and of B per wave
-    constexpr int kStepB = W4 ? kDmaStageK / 2 : kDmaStageK;   // B bytes per row and stage
-    constexpr int kDmaA = kRowsPerWave / 16;            // DMA instructions per thread per stage:
-    constexpr int kDmaB = kRowsPerWave * kStepB / 1024; //   A rows, B rows
-    constexpr int kDmaPerStage = kDmaA + kDmaB;
-    constexpr int kDmaExtra = kRowsPerWave / 8;         // per epilogue operand (128-byte rows)
-    static_assert(kDmaB >= 1 && kRowsPerWave * kStepB % 1024 == 0, "B rows per DMA");
-    using BRaw = std::conditional_t<W4, v2i, v4i>;      // a lane's B bytes of one k step
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave / NWN, wn = wave % NWN;
-    const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sm.buf));
+    RowOps& ro = sm.ro[rb];
 
     v16i acc[4][NJ];
 #pragma unroll
@@ -2449,30 +2485,29 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
 #pragma unroll
         for (int j = 0; j < NJ; ++j) acc[i][j] = v16i{0};
 
-    // per-row operands: 64 entries per instruction, piece c of the 12 (x
-    // scales, channel scales, modality ids; 4 each) issued by wave c % NW;
+    // per-row operands of the tile at rows r0.., channels c0.. into set `o`:
     // indices past T or N are clamped (their results are discarded)
-    {
+    auto issue_rowops = [&](RowOps& o, int64_t r0, int c0) __attribute__((always_inline)) {
         // (GRP: the third group is the tiles' token indices, the output rows)
-        constexpr int kPieces = (CMC || GRP) ? 12 : 8;
         for (int c = wave; c < kPieces; c += NW) {
             const int part = c & 3, e = 64 * part + lane;
             const void* src;
             uint32_t dst;
             if (c < 4) {
-                src = x_scale + a_row(e);
-                dst = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&sm.dx[64 * part]));
+                src = x_scale + (GRP ? a_row(e) : min(r0 + e, T - 1));
+                dst = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&o.dx[64 * part]));
             } else if (c < 8) {
-                src = w_scale + min(col0 + e, N - 1);
-                dst = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&sm.ws[64 * part]));
+                src = w_scale + min(c0 + e, N - 1);
+                dst = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&o.ws[64 * part]));
             } else {
                 src = GRP ? static_cast<const void*>(grows + gfirst + min(e, grows_n - 1))
-                          : static_cast<const void*>(mod + min(row0 + e, T - 1));
-                dst = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&sm.rawmod[64 * part]));
+                          : static_cast<const void*>(mod + min(r0 + e, T - 1));
+                dst = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&o.rawmod[64 * part]));
             }
             lds_dma4(src, static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(dst))));
         }
-    }
+    };
+    if (vb == static_cast<int>(blockIdx.x)) issue_rowops(ro, row0, col0);   // later tiles: queued ahead
 
     // Wave w loads rows [w R, w R + R) of the A and of the B tile (R =
     // kRowsPerWave), 16 rows per instruction; lane i covers row 16 j + i / 4
@@ -2482,32 +2517,45 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     // results are discarded.
     // (Row-paired A, code_row / code_col: a stage of a row pair is one
     // 128-byte line, the next stage 128 bytes on.)
+    // (The stage st of a tile goes to K buffer (ring + st) % kDmaStages.)
     const int8_t* src[kDmaPerStage];      // [0, kDmaA): A rows, then B rows
     uint32_t dst_off[kDmaPerStage];
-    const int a_step = a_pair ? 2 * kDmaStageK : kDmaStageK;   // A bytes between stages
+    // sources of the tile at rows r0.., channels c0.. (PERSIST: also the next tile's)
+    auto set_src = [&](const int8_t* (&sp)[kDmaPerStage], int64_t r0, int c0) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < kDmaA; ++j) {
-        const int row = wave * kRowsPerWave + 16 * j + (lane >> 2);
-        const int chunk = (lane & 3) ^ swz4(row);
-        src[j] = A + code_row(a_row(row), K, a_pair) + kst0 * a_step + 16 * chunk;
+        for (int j = 0; j < kDmaA; ++j) {
+            const int row = wave * kRowsPerWave + 16 * j + (lane >> 2);
+            const int chunk = (lane & 3) ^ swz4(row);
+            const int64_t tok = GRP ? a_row(row) : min(r0 + row, T - 1);
+            sp[j] = A + code_row(tok, K, a_pair) + kst0 * a_step + 16 * chunk;
+        }
+#pragma unroll
+        for (int j = 0; j < kDmaB; ++j) {
+            constexpr int kRowsPerDma = 1024 / kStepB;
+            const int lanes_per_row = kStepB / 16;
+            const int row = wave * kRowsPerWave + kRowsPerDma * j + lane / lanes_per_row;
+            const int piece = W4 ? ((lane & 1) ^ ((row >> 3) & 1)) : ((lane & 3) ^ swz4(row));
+            sp[kDmaA + j] = B + static_cast<int64_t>(min(c0 + row, N - 1)) * (W4 ? K / 2 : K) +
+                            kst0 * kStepB + 16 * piece;
+        }
+    };
+    set_src(src, row0, col0);
+#pragma unroll
+    for (int j = 0; j < kDmaA; ++j)
         dst_off[j] = static_cast<uint32_t>(
             __builtin_amdgcn_readfirstlane((wave * kRowsPerWave + 16 * j) * kDmaStageK));
-    }
 #pragma unroll
     for (int j = 0; j < kDmaB; ++j) {
         constexpr int kRowsPerDma = 1024 / kStepB;
-        const int lanes_per_row = kStepB / 16;
-        const int row = wave * kRowsPerWave + kRowsPerDma * j + lane / lanes_per_row;
-        const int piece = W4 ? ((lane & 1) ^ ((row >> 3) & 1)) : ((lane & 3) ^ swz4(row));
-        src[kDmaA + j] = B + static_cast<int64_t>(min(col0 + row, N - 1)) * (W4 ? K / 2 : K) +
-                         kst0 * kStepB + 16 * piece;
         dst_off[kDmaA + j] = kTileM * kDmaStageK + static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(
                                  (wave * kRowsPerWave + kRowsPerDma * j) * kStepB));
     }
-    auto issue_one = [&](int st, int q) __attribute__((always_inline)) {
-        const uint32_t sbase = lds0 + (st % kDmaStages) * kDmaStageBytes;
-        lds_dma16(src[q] + st * (q < kDmaA ? a_step : kStepB), sbase + dst_off[q]);
+    auto issue_from = [&](const int8_t* const (&sp)[kDmaPerStage], int st, int q, int rg)
+                          __attribute__((always_inline)) {
+        const uint32_t sbase = lds0 + ((rg + st) % kDmaStages) * kDmaStageBytes;
+        lds_dma16(sp[q] + st * (q < kDmaA ? a_step : kStepB), sbase + dst_off[q]);
     };
+    auto issue_one = [&](int st, int q) __attribute__((always_inline)) { issue_from(src, st, q, ring); };
     auto issue = [&](int st) __attribute__((always_inline)) {
 #pragma unroll
         for (int q = 0; q < kDmaPerStage; ++q) issue_one(st, q);
@@ -2515,7 +2563,7 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     // fragment f of one 32-byte k step (f < 4: token block f of the q rows,
     // f >= 4: channel block f - 4 of the Wq rows)
     auto read_frag = [&](int st, int ks, int f, v4i (&fa)[4], BRaw (&fb)[NJ]) __attribute__((always_inline)) {
-        const uint8_t* sa = sm.buf + (st % kDmaStages) * kDmaStageBytes;
+        const uint8_t* sa = sm.buf + ((ring + st) % kDmaStages) * kDmaStageBytes;
         const int c = W4 ? 2 * (lane >> 5) + ks : 2 * ks + (lane >> 5);
         if (f < 4) {
             const int row = wm * 128 + f * 32 + (lane & 31);
@@ -2581,7 +2629,9 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     using yes = std::true_type;
     using no = std::false_type;
     const int nk = min(nk_slice, nk_all - kst0);             // >= 1 (plan_gemm_splits)
-    for (int st = 0; st < kDmaStages - 1 && st < nk; ++st) issue(st);
+    // (PERSIST) the previous tile's epilogue is done with the K buffers
+    if (PERSIST && vb != static_cast<int>(blockIdx.x)) __syncthreads();
+    for (int st = pf; st < kDmaStages - 1 && st < nk; ++st) issue(st);
     v4i fa0[4], fa1[4];
     BRaw fb0[NJ], fb1[NJ];
     publish(min(nk - 1, 2));
@@ -2589,29 +2639,29 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     // The per-row operands have landed (they precede stage 0 in every wave's
     // queue).  Modalities present in the tile, as scalars.
     unsigned present = 0;
-    int mods[2] = {0, 0};
+    int mod0 = 0, mod1 = 0;                 // the first two non-text modalities present
     bool pre = false;
     if constexpr (CMC) {
-        if (tid < kTileM) sm.mod[tid] = sane_mod(sm.rawmod[tid], n_mod);   // read after a barrier
-        const v4i m4 = *reinterpret_cast<const v4i*>(&sm.rawmod[4 * lane]);
+        if (tid < kTileM) ro.mod[tid] = sane_mod(ro.rawmod[tid], n_mod);   // read after a barrier
+        const v4i m4 = *reinterpret_cast<const v4i*>(&ro.rawmod[4 * lane]);
         const int s0 = sane_mod(m4.x, n_mod), s1 = sane_mod(m4.y, n_mod);
         const int s2 = sane_mod(m4.z, n_mod), s3 = sane_mod(m4.w, n_mod);
         for (int m = 1; m < n_mod; ++m)
             if (__ballot(s0 == m || s1 == m || s2 == m || s3 == m) != 0ull) present |= 1u << m;
         present = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(present)));
-        int p = 0;
-        for (int m = 1; m < n_mod && p < 2; ++m)
-            if (present & (1u << m)) mods[p++] = m;
+        const unsigned rest = present & (present - 1u);       // bit 0 (text) is never set
+        mod0 = present ? __builtin_ctz(present) : 0;
+        mod1 = rest ? __builtin_ctz(rest) : 0;
         const int np = __builtin_popcount(present);
         pre = sizeof(LT) == 2 && u_hl != nullptr && r <= 64 && np >= 1 && np <= 2 && y != nullptr;
     }
-    // compensation operand v (0: u hi, 1: u lo, 2 + p: L2 rows of mods[p])
+    // compensation operand v (0: u hi, 1: u lo, 2: L2 rows of mod0, 3: of mod1)
     // into K buffer v, 128-byte rows: lane i covers row 8 q + i / 8 of this
     // wave's share at LDS chunk i % 8, which holds logical chunk
     // (i % 8) ^ swz(row)
     auto issue_extra = [&](int v) __attribute__((always_inline)) {
         const uint32_t sbase = lds0 + v * kDmaStageBytes;
-        const LT* rm = r_up + static_cast<int64_t>(max((v == 2 ? mods[0] : mods[1]) - 1, 0)) * N * r;
+        const LT* rm = r_up + static_cast<int64_t>(max((v == 2 ? mod0 : mod1) - 1, 0)) * N * r;
 #pragma unroll
         for (int q = 0; q < kDmaExtra; ++q) {
             const int rw = wave * kRowsPerWave + 8 * q;
@@ -2701,23 +2751,64 @@ __global__ __launch_bounds__(128 * NWN, 1) void k_gemm_dma(
     ed.present = present;
     ed.pre = pre;
     ed.grp_rows = grows_n;
+    bool synced = false;
     if constexpr (CMC) {
         if (pre) {
             // the K buffers are free once every wave is past its last reads
             __syncthreads();
+            synced = true;
             issue_extra(0);
             issue_extra(1);
             issue_extra(2);
-            if (mods[1] != 0) issue_extra(3);
+            if (mod1 != 0) issue_extra(3);
             ed.off_uh = 0;
             ed.off_ul = kDmaStageBytes;
             ed.off_r[0] = 2 * kDmaStageBytes;
             ed.off_r[1] = 3 * kDmaStageBytes;
         }
     }
-    MASQ_WAIT_VMCNT_LGKM0(0);
+    // PERSIST: the next tile's per-row operands (the other LDS set) and its
+    // first stages, into the K buffers this epilogue leaves free: stages 0-2
+    // into buffers 0-2 when it stages no compensation operands, stage 0 into
+    // buffer 3 when they are one modality's (buffers 0-2), none with two
+    int npf = -1, nring = 0;                 // npf < 0: no next tile
+    if constexpr (PERSIST) {
+        int tmn, tnn;
+        if (tile_coords_at(vb + static_cast<int>(gridDim.x), tiles_m, tiles_n, tmn, tnn)) {
+            const int64_t r0n = static_cast<int64_t>(tmn) * kTileM;
+            const int c0n = tnn * kTileN;
+            issue_rowops(sm.ro[rb ^ 1], r0n, c0n);
+            npf = 0;
+            if (!CMC || present == 0) {
+                npf = min(kDmaStages - 1, nk_all);
+            } else if (pre && mod1 == 0) {
+                npf = 1;
+                nring = 3;
+            }
+            if (npf > 0) {
+                if (!synced) __syncthreads();    // every wave is past its reads of the last stages
+                const int8_t* srcn[kDmaPerStage];
+                set_src(srcn, r0n, c0n);
+                for (int st = 0; st < npf; ++st)
+#pragma unroll
+                    for (int q = 0; q < kDmaPerStage; ++q) issue_from(srcn, st, q, nring);
+            }
+        }
+    }
+    // this tile's operands have landed once at most the next tile's (younger)
+    // loads are in flight; a wave queued kPiecesMin or kPiecesMin + 1 pieces
+    if (npf < 0) MASQ_WAIT_VMCNT_LGKM0(0);
+    else if (npf == 0) MASQ_WAIT_VMCNT_LGKM0(kPiecesMin);
+    else if (npf == 1) MASQ_WAIT_VMCNT_LGKM0(kPiecesMin + kDmaPerStage);
+    else if (npf == 2) MASQ_WAIT_VMCNT_LGKM0(kPiecesMin + 2 * kDmaPerStage);
+    else MASQ_WAIT_VMCNT_LGKM0(kPiecesMin + 3 * kDmaPerStage);
     gemm_epilogue<YT, LT, CMC, ACC, NWN, true, GRP>(acc, sm, EpiPrefetch{}, T, N, row0, col0, u, r, n_mod,
-                                               r_up, acc_out, y, ed);
+                                               r_up, acc_out, y, ed, rb, tid);
+    if constexpr (!PERSIST) break;
+    ring = nring;
+    pf = max(npf, 0);
+    rb ^= 1;
+    }
 }
 
 // ================================================================ small-batch GEMM
@@ -3232,6 +3323,23 @@ __global__ __launch_bounds__(kGrpThreads) void k_group_rows(
 }  // namespace
 
 // ================================================================ launchers
+// Workgroups of the persistent GEMM grid: the current device's compute units
+// (one 256 x 256 tile's workgroup fills a unit's LDS), a multiple of 8 so
+// that every tile keeps its XCD.  Looked up once per device.
+static int persistent_blocks() {
+    static int cached[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+    if (cached[dev] == 0) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus < 8)
+            cus = 8;
+        cached[dev] = cus / 8 * 8;
+    }
+    return cached[dev];
+}
+
 // Waves along the channels of the 256 x 256 GEMM workgroup (2: four waves of
 // 128 x 128; 4: eight waves of 128 x 64, two per SIMD).
 constexpr int kGemmWavesN = 4;
@@ -3467,6 +3575,8 @@ static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* w
     if (K % kDmaStageK == 0) {
         if (part == nullptr || tickets == nullptr) S = 1;
         const dim3 gridk(8 * ((nt * S + 7) / 8));
+        // whole tiles: a persistent grid of at most one workgroup per compute unit
+        const dim3 gridp(static_cast<unsigned>(min(8 * ((nt + 7) / 8), persistent_blocks())));
         if (S > 1)
             hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN, true, W4>), gridk,
                                dim3(128 * kGemmWavesN), 0, s, q, wq, x_scale, w_scale, T,
@@ -3475,7 +3585,7 @@ static void launch_gemm_t(const int8_t* q, const float* x_scale, const int8_t* w
                                static_cast<YT*>(y), S, part, tickets, nullptr, nullptr, nullptr, 0,
                                a_pair);
         else
-            hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN, false, W4>), gridk,
+            hipLaunchKernelGGL((k_gemm_dma<YT, LT, CMC, ACC, kGemmWavesN, false, W4, false, true>), gridp,
                                dim3(128 * kGemmWavesN), 0, s, q, wq, x_scale, w_scale, T,
                                static_cast<int>(K), static_cast<int>(N), tiles_m, tiles_n, mod, u,
                                u_hl, rank, n_mod, static_cast<const LT*>(r_up), acc,
