@@ -264,7 +264,8 @@ masq_status fused_stage(const Fused& a, int stage) {
                                                 a.n_mod, cmc, w, s));
         if (st != MASQ_OK) return st;
     } else if ((stage & 1) && cmc && masq::fused_stage1_ok(a.T, a.c_in, a.rank, to_dt(a.lr_dt)) &&
-               masq::stage1_fr_ok(to_dt(a.x_dt), a.c_in, a.n_mod)) {
+               masq::stage1_fr_ok(to_dt(a.x_dt), a.c_in, a.n_mod) &&
+               (masq::stage1_fr_first(a.T, a.n_mod) || w.dl_part == nullptr)) {
         // rows held in registers: one kernel, each row read once
         st = from_hip(masq::launch_stage1_fused(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                 a.l_down, a.T, a.c_in, a.rank, a.n_mod, w.q,

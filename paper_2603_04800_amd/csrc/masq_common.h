@@ -195,9 +195,19 @@ constexpr int64_t kDownLdsCols = 256;
 inline int down_lds_slices(int64_t K) { return static_cast<int>((K + kDownLdsCols - 1) / kDownLdsCols); }
 inline bool down_lds_ok(DT x_dt, int64_t K) { return x_dt == DT::BF16 && K % 64 == 0; }
 // Stage 1 of the fused layer for rows that k_stage1_fr cannot hold: k_down_lds,
-// then the quantisation adding its partials.  (For rows that it can hold,
-// k_stage1_fr doing both per 16 rows measured faster.)
+// then the quantisation adding its partials.
 constexpr bool kStage1SplitDown = true;
+// Rows that k_stage1_fr can hold take it only for batches of kFusedFullT
+// tokens and more with at most one non-text modality; other batches take
+// the split form as well.  k_stage1_fr reads the whole of L1 for every
+// non-text modality present in each 16-row group, k_down_lds once per
+// 128-row tile and k slice; below kFusedFullT tokens k_stage1_fr's T / 16
+// workgroups leave compute units idle, and with two non-text modalities
+// more of its groups read two L1s.  (Measured, rank 64, 3584 columns:
+// 2048 tokens 22.2 -> 17.7 us with one non-text modality, 33.3 -> 19.4 us
+// with two; 4096 tokens 24.1 -> 25.9 us with one, 35.4 -> 31.2 us with two;
+// 8192 tokens 47.7 -> 51.9 us with one, 60.1 -> 57.9 us with two.)
+inline bool stage1_fr_first(int64_t T, int n_mod) { return T >= kFusedFullT && n_mod <= 2; }
 hipError_t launch_down_lds(const void* x, const int32_t* mod, const float* inv_s,
                            const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
                            float* part, hipStream_t s);

@@ -3373,7 +3373,9 @@ hipError_t launch_smooth_quant(const void* x, DT x_dt, const int32_t* mod, const
                                bool pair) {
     const UFinish fin = fin_in ? *fin_in : UFinish{nullptr, 0, 0, nullptr, nullptr};
     if (pair && K % 64 != 0) return hipErrorInvalidValue;
-    if (T > kSmallMaxT && stage1_fr_ok(x_dt, K, n_mod))
+    // (after a split down-projection, fin: the row kernels, whose more
+    // numerous workgroups add the slice partials faster)
+    if (T > kSmallMaxT && stage1_fr_ok(x_dt, K, n_mod) && fin.part == nullptr)
         return launch_stage1_fr(x, mod, inv_s, nullptr, T, K, 0, n_mod, q, x_scale, nullptr,
                                 nullptr, zero_ints, n_zero, s, pair, fin);
     // a wave per row for large batches whose rows fit its register cache
