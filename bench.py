@@ -386,12 +386,15 @@ def summarize_counters(out: str, workload: int, cfg, src_hash: str, cmds: dict):
         h = _bench_hash_in_log(os.path.join(out, f"{kind}.log"))
         if h != src_hash:
             raise SystemExit(f"{kind} run was taken on kernel source {h}, tree is {src_hash}")
-    lines = [f"# rocprofv3 counters of the GEMM (k_gemm*) and stage-1 kernels, workload {cfg.name}",
+    lines = [f"# rocprofv3 counters of the GEMM (k_gemm*) and stage-1 kernels (k_stage1*, or "
+             f"k_down_lds and k_smooth_quant*), workload {cfg.name}",
              f"# command (mfma): {cmds['mfma']}", f"# command (lds): {cmds['lds']}",
              "# per-dispatch means; gemm_clock_ghz = GRBM_GUI_ACTIVE / 8 XCDs / kernel time; "
              "lds_conflict_share = SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE",
              f"kernel_source_sha256_16: {src_hash}"]
-    for label, part in (("gemm", GEMM_KERNEL), ("stage1", "stage1")):
+    # stage 1 is k_stage1_* or, in its split form, k_down_lds then the row quantiser
+    for label, part in (("gemm", GEMM_KERNEL), ("stage1", "stage1"), ("down_lds", "k_down_lds"),
+                        ("quant", "k_smooth_quant")):
         m = list(_per_dispatch_all(os.path.join(out, "mfma"), part).values())
         l = list(_per_dispatch_all(os.path.join(out, "lds"), part).values())
         if not m or not l:
