@@ -398,6 +398,23 @@ _EDGE = {
     "ring_tail_k320_rank32": dict(T=300, K=320, N=256, r=32, M=3, act="bf16", lr="bf16"),
     "ring_tail_k512_rank48_f32_out": dict(T=400, K=512, N=336, r=48, M=3, act="f32", lr="bf16",
                                           layout="runs"),
+    # the stage-1 choice: the register-resident kernel for 4096 tokens and
+    # more with one non-text modality, the split form just below (odd batch:
+    # row-paired codes with an unused last row)
+    "fr_first_t4096_two_mod": dict(T=4096, K=1024, N=32, r=64, M=2, act="bf16", lr="bf16",
+                                   layout="contiguous"),
+    "split_t4095_two_mod": dict(T=4095, K=1024, N=32, r=64, M=2, act="bf16", lr="bf16",
+                                layout="runs"),
+    # more tiles than compute units: persistent GEMM workgroups take a second
+    # tile, with the next tile's first stages queued during the epilogue
+    # (three stages after text-only tiles, one after one-modality tiles,
+    # none after two-modality ones), and rings of 4, 2 and 1 stages
+    "persistent_two_tiles_k256": dict(T=2304, K=256, N=8192, r=64, M=3, act="bf16", lr="bf16",
+                                      layout="runs"),
+    "persistent_two_tiles_k128": dict(T=2304, K=128, N=8192, r=32, M=2, act="bf16", lr="bf16",
+                                      layout="runs"),
+    "persistent_two_tiles_k64_f32_out": dict(T=2304, K=64, N=8192, r=16, M=3, act="f32",
+                                             lr="bf16", layout="runs"),
 }
 
 
