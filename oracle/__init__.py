@@ -31,7 +31,9 @@ Pins (checked by the CPU test suite, not by retyping formulas):
     X_m S_m^-1 dW (Eckart-Young), and no worse than other rank-r choices;
   * Theorem 1 (Sec. 4.2), qualitatively: per-modality factors recover the
     activation SQNR that a unified factor set by another modality loses;
-  * bf16 helpers exhaustively against torch's CPU casts.
-Whole-layer output values beyond these properties are "parity unpinned": the
-paper prints no worked numerical example for the layer.
+  * bf16 helpers exhaustively against torch's CPU casts;
+  * the whole layer element by element against its definition in Python
+    scalars and exact rationals on tiny inputs (brute force).
+The paper prints no worked numerical example for the layer, so no pin uses
+printed values.
 """

@@ -228,6 +228,55 @@ def test_lowrank_comp_brute_force_one_rounding():
     assert twice > 0, "the case does not tell one rounding from two"
 
 
+def test_whole_layer_brute_force():
+    """The whole layer (Sec. 4.3, final case equation; eq. PTQ) element by
+    element in Python scalars and exact rationals, on tiny inputs of three
+    modalities: xs = fl32(x inv_s[m]); Delta = fl32(a / 127) and
+    rq = fl32(127 / a) from the row's absmax a, each one correctly rounded
+    division; codes = clip(rne(fl32(xs rq)), +-127); the integer sum of the
+    code products; y0 = fl32(fl32(acc Delta) w_scale); text rows y0, other
+    rows y0 + (xs L1^m) L2^m taken exactly and rounded once to binary32."""
+    from fractions import Fraction
+    rng = np.random.default_rng(21)
+    T, K, N, r, M = 7, 10, 6, 3, 3
+    x = (rng.standard_normal((T, K)) * 4).astype(np.float32)
+    x[3] = 0                                           # a zero row: zero scale and codes
+    mod = np.array([0, 1, 2, 0, 2, 1, 2], np.int32)
+    inv = rng.uniform(0.2, 3, (M, K)).astype(np.float32)
+    wq = rng.integers(-127, 128, (N, K)).astype(np.int8)
+    ws = rng.uniform(1e-3, 1e-2, N).astype(np.float32)
+    ld = rng.standard_normal((M - 1, r, K)).astype(np.float32)
+    ru = (rng.standard_normal((M - 1, N, r)) * 0.1).astype(np.float32)
+    y = inf.linear(x, mod, inv, wq, ws, ld, ru)
+    assert y.dtype == np.float32 and y.shape == (T, N)
+    for t in range(T):
+        m = int(mod[t])
+        xs = [np.float32(x[t, i]) * np.float32(inv[m, i]) for i in range(K)]
+        a = max(abs(float(v)) for v in xs)
+        if a == 0:
+            delta, rq = np.float32(0), np.float32(0)
+        else:
+            delta = _round_f32_once(Fraction(a) / 127)
+            rq = _round_f32_once(Fraction(127) / Fraction(a))
+        codes = []
+        for v in xs:
+            p = np.float32(v) * rq                     # one binary32 product
+            c = round(Fraction(float(p)))              # Python's round: ties to even
+            codes.append(max(-127, min(127, c)))
+        for o in range(N):
+            acc = sum(codes[i] * int(wq[o, i]) for i in range(K))
+            y0 = np.float32(np.float32(float(acc)) * delta) * np.float32(ws[o])
+            if m == 0:
+                assert y[t, o].view(np.uint32) == np.float32(y0).view(np.uint32), (t, o)
+                continue
+            u = [sum(Fraction(float(xs[i])) * Fraction(float(ld[m - 1, k, i])) for i in range(K))
+                 for k in range(r)]
+            cterm = sum(u[k] * Fraction(float(ru[m - 1, o, k])) for k in range(r))
+            ref = _round_f32_once(Fraction(float(y0)) + cterm)
+            assert y[t, o].view(np.uint32) == ref.view(np.uint32), (t, o)
+    assert np.all(y[3] == 0)
+
+
 def test_text_rows_equal_the_plain_w8a8_product():
     rng = np.random.default_rng(10)
     T, K, N = 12, 64, 40
