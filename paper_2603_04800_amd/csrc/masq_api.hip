@@ -102,7 +102,7 @@ Workspace plan_workspace(void* base, int64_t T, int64_t K, int64_t N, int rank, 
     if (dw) plan_down_wide(T, K, w.dw_slices, w.dw_kslice);
     const size_t row_bytes = static_cast<size_t>(T) * static_cast<size_t>(rank) * sizeof(float);
     const size_t part_bytes = std::max(dw ? w.dw_slices * row_bytes : 0,
-                                       dl ? down_lds_slices(K) * row_bytes : 0);
+                                       dl ? down_lds_slices(T, K) * row_bytes : 0);
     if (part_bytes > 0) {
         float* p = reinterpret_cast<float*>(carve(part_bytes));
         if (dw) w.dw_part = p;
@@ -280,7 +280,7 @@ masq_status fused_stage(const Fused& a, int stage) {
         st = from_hip(masq::launch_down_lds(a.x, a.modality, a.inv_smooth, a.l_down, a.T, a.c_in,
                                             a.rank, a.n_mod, w.dl_part, s));
         if (st != MASQ_OK) return st;
-        const masq::UFinish fin{w.dl_part, masq::down_lds_slices(a.c_in), a.rank, w.u, w.u_hl};
+        const masq::UFinish fin{w.dl_part, masq::down_lds_slices(a.T, a.c_in), a.rank, w.u, w.u_hl};
         st = from_hip(masq::launch_smooth_quant(a.x, to_dt(a.x_dt), a.modality, a.inv_smooth,
                                                 a.T, a.c_in, a.n_mod, w.q, w.x_scale,
                                                 w.zero_base, w.n_zero, s, &fin, w.pair));

@@ -191,8 +191,20 @@ inline bool stage1_fr_ok(DT x_dt, int64_t K, int n_mod) {
 // Down-projection with the L1 fragments staged in LDS (k_down_lds): bf16
 // activations and factors, rank <= 64, K % 64 == 0; slice partials
 // [down_lds_slices(K)][T][rank] for the quantisation kernel to add.
-constexpr int64_t kDownLdsCols = 256;
-inline int down_lds_slices(int64_t K) { return static_cast<int>((K + kDownLdsCols - 1) / kDownLdsCols); }
+constexpr int64_t kDownLdsCols = 256;    // columns staged in LDS at a time (a chunk)
+constexpr int64_t kDownLdsRows = 128;    // rows of a workgroup's tile
+// Chunks per k slice: 2 (4) once the grid of one-chunk slices would keep
+// 2 (4) rounds of 448 workgroups, fewer partials to write and to add then
+// costing less than the fewer, longer workgroups.
+inline int down_lds_chunks(int64_t T, int64_t K) {
+    const int64_t wgs = ((T + kDownLdsRows - 1) / kDownLdsRows) * ((K + kDownLdsCols - 1) / kDownLdsCols);
+    return wgs >= 4 * 448 ? 4 : (wgs >= 2 * 448 ? 2 : 1);
+}
+inline int down_lds_slices(int64_t T, int64_t K) {
+    const int64_t chunks = (K + kDownLdsCols - 1) / kDownLdsCols;
+    const int n = down_lds_chunks(T, K);
+    return static_cast<int>((chunks + n - 1) / n);
+}
 inline bool down_lds_ok(DT x_dt, int64_t K) { return x_dt == DT::BF16 && K % 64 == 0; }
 // Stage 1 of the fused layer for rows that k_stage1_fr cannot hold: k_down_lds,
 // then the quantisation adding its partials.

@@ -1103,16 +1103,19 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
 // read from L2 once per 128 rows, not once per 16.  Rows of a third non-text
 // modality in the same 128 rows read their fragments from global memory.
 // Tiles without non-text rows return at once: text rows' partials are never
-// read (finish_u_row).
-constexpr int kDlPairs = 4;                         // 64-column pairs per slice
+// read (finish_u_row).  A slice may span nchunk chunks of kDlCols columns
+// (down_lds_chunks): the workgroup stages and multiplies them in turn,
+// summing in registers, so that fewer, wider slices write fewer partials.
+constexpr int kDlPairs = 4;                         // 64-column pairs per chunk
 constexpr int kDlCols = 64 * kDlPairs;
-static_assert(kDlCols == kDownLdsCols, "slice width of the workspace plan");
+static_assert(kDlCols == kDownLdsCols, "chunk width of the workspace plan");
 constexpr int kDlRows = 128;
+static_assert(kDlRows == kDownLdsRows, "row tile of the workspace plan");
 constexpr int kDlWaves = kDlRows / 16;
 
 __global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
     const bf16_t* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
-    const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod,
+    const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod, int nchunk,
     float* __restrict__ part) {
     constexpr int kSteps = 2 * kDlPairs;
     __shared__ __attribute__((aligned(16))) v4i sfrag[2][kSteps][4][64];    // 64 KB
@@ -1124,7 +1127,6 @@ __global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
     const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kDlRows;
     const int s = blockIdx.y;
     const int npairs = K >> 6;
-    const int pb = s * kDlPairs;                    // first pair of the slice
 
     if (tid < kDlRows) {
         const int64_t t = row0 + tid;
@@ -1145,8 +1147,20 @@ __global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
         if (present & (1u << m)) mods[np++] = m;
     const int ncb = r >> 4;
     const int nsl = min(np, 2);                     // modalities staged in LDS
+    const int64_t trow = row0 + 16 * wave + ar;
+    const bool valid = trow < T;
+    const bf16_t* xr = x + (valid ? trow : row0) * static_cast<int64_t>(K) + 16 * kg;
+    const int mrow = smod[16 * wave + ar];
+    const v4i zero = {0, 0, 0, 0};
+    v4f acc[4];
+#pragma unroll
+    for (int jb = 0; jb < 4; ++jb) acc[jb] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int ch = 0; ch < nchunk; ++ch) {
+    const int pb = (s * nchunk + ch) * kDlPairs;   // first pair of the chunk
+    if (pb >= npairs) break;                        // uniform: past the row's end
+    if (ch > 0) __syncthreads();                    // every wave is done with the last chunk's LDS
 
-    // slice's factors of every modality (16-byte pieces, columns past K
+    // chunk's factors of every modality (16-byte pieces, columns past K
     // repeat the last piece), then the staged fragments: block b = (slot,
     // step, N block), lane l's piece from row 16 nb + l % 16 of (L1^m)^T
     {
@@ -1169,10 +1183,7 @@ __global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
             lds_dma16(src, sf0 + b * 1024);
         }
     }
-    // this wave's 16 rows of the slice, every load in flight
-    const int64_t trow = row0 + 16 * wave + ar;
-    const bool valid = trow < T;
-    const bf16_t* xr = x + (valid ? trow : row0) * static_cast<int64_t>(K) + 16 * kg;
+    // this wave's 16 rows of the chunk, every load in flight
     v4i xa[kDlPairs], xb[kDlPairs];
     asm volatile("" ::: "memory");
 #pragma unroll
@@ -1185,11 +1196,6 @@ __global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
     MASQ_WAIT_VMCNT_LGKM0(0);
     __syncthreads();
 
-    const int mrow = smod[16 * wave + ar];
-    const v4i zero = {0, 0, 0, 0};
-    v4f acc[4];
-#pragma unroll
-    for (int jb = 0; jb < 4; ++jb) acc[jb] = v4f{0.f, 0.f, 0.f, 0.f};
     for (int mi = 0; mi < np; ++mi) {
         const int m = mods[mi];
         const bool mine = valid && mrow == m;
@@ -1234,6 +1240,7 @@ __global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
                     __builtin_bit_cast(v8bf, ll), __builtin_bit_cast(v8bf, fb[jb]), acc[jb], 0, 0, 0);
         }
     }
+    }   // chunks
     // partials of the wave's rows: lane holds rows 4 (l / 16) + i, column
     // 16 jb + l % 16
     float* pp = part + static_cast<int64_t>(s) * T * r;
@@ -3479,11 +3486,11 @@ hipError_t launch_down_lds(const void* x, const int32_t* mod, const float* inv_s
                            const void* l_down, int64_t T, int64_t K, int rank, int n_mod,
                            float* part, hipStream_t s) {
     const dim3 grid(static_cast<unsigned>((T + kDlRows - 1) / kDlRows),
-                    static_cast<unsigned>(down_lds_slices(K))),
+                    static_cast<unsigned>(down_lds_slices(T, K))),
         block(64 * kDlWaves);
     hipLaunchKernelGGL(k_down_lds, grid, block, 0, s, static_cast<const bf16_t*>(x), mod, inv_s,
                        static_cast<const bf16_t*>(l_down), T, static_cast<int>(K), rank, n_mod,
-                       part);
+                       down_lds_chunks(T, K), part);
     return hipGetLastError();
 }
 
