@@ -390,11 +390,12 @@ _EDGE = {
     "down_lds_four_mod_alternating_k3584": dict(T=300, K=3584, N=32, r=64, M=4, act="bf16",
                                                 lr="bf16"),
     "down_lds_t40_k4160_r16": dict(T=40, K=4160, N=64, r=16, M=2, act="bf16", lr="bf16"),
-    # k slices spanning two and four 256-column chunks (large grids), the
-    # last slice short of chunks and its last chunk short of columns
-    "down_lds_two_chunks_t4096_k7168": dict(T=4096, K=7168, N=32, r=64, M=3, act="bf16",
+    # k slices spanning two and four 256-column chunks (long rows, large
+    # grids), the last slice short of chunks and its last chunk short of
+    # columns
+    "down_lds_two_chunks_t4096_k8192": dict(T=4096, K=8192, N=32, r=64, M=3, act="bf16",
                                             lr="bf16", layout="runs"),
-    "down_lds_four_chunks_ragged_t8192_k7232": dict(T=8192, K=7232, N=16, r=32, M=2,
+    "down_lds_four_chunks_ragged_t8192_k8256": dict(T=8192, K=8256, N=16, r=32, M=2,
                                                     act="bf16", lr="bf16",
                                                     layout="contiguous"),
     # 32-row stage-1 workgroups (batches of 8192 tokens and more), ragged tail
