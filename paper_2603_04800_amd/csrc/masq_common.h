@@ -193,17 +193,16 @@ inline bool stage1_fr_ok(DT x_dt, int64_t K, int n_mod) {
 // [down_lds_slices(K)][T][rank] for the quantisation kernel to add.
 constexpr int64_t kDownLdsCols = 256;    // columns staged in LDS at a time (a chunk)
 constexpr int64_t kDownLdsRows = 128;    // rows of a workgroup's tile
-// Chunks per k slice: for rows of 32 chunks and more (8192+ columns, where
-// the partials are a large part of the traffic), 2 (4) once the grid of
-// one-chunk slices would keep 2 (4) rounds of 448 workgroups: fewer
-// partials to write and to add then cost less than the fewer, longer
-// workgroups.  (Measured: 18944 columns, 2048 tokens 79.9 -> 76.8 us;
-// 3584 columns, 8192 tokens no gain, so shorter rows keep one chunk.)
+// Chunks per k slice: the workgroups (two per CU: 66 KB of LDS each) stream
+// the chunks of their slice through a software pipeline, so the slices are
+// made as long as a grid of about kDownLdsWgs workgroups (one round) allows:
+// fewer partials to write and to add.
+constexpr int64_t kDownLdsWgs = 512;
 inline int down_lds_chunks(int64_t T, int64_t K) {
     const int64_t chunks = (K + kDownLdsCols - 1) / kDownLdsCols;
-    if (chunks < 32) return 1;
-    const int64_t wgs = ((T + kDownLdsRows - 1) / kDownLdsRows) * chunks;
-    return wgs >= 4 * 448 ? 4 : (wgs >= 2 * 448 ? 2 : 1);
+    const int64_t tiles = (T + kDownLdsRows - 1) / kDownLdsRows;
+    const int64_t n = (tiles * chunks + kDownLdsWgs - 1) / kDownLdsWgs;
+    return static_cast<int>(n < 1 ? 1 : (n > chunks ? chunks : n));
 }
 inline int down_lds_slices(int64_t T, int64_t K) {
     const int64_t chunks = (K + kDownLdsCols - 1) / kDownLdsCols;

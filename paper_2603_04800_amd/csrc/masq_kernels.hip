@@ -1090,43 +1090,72 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
     }
 }
 
-// ---------------------------------------------------------------- down-projection, fragments in LDS
+// ---------------------------------------------------------------- down-projection, operands in LDS
 // u = xs L1^m for bf16 activations and factors (rank <= 64), as slice
-// partials part[s][t][0 .. r) over k slices of kDlCols columns; grid
-// (ceil(T / 128), S).  A workgroup of 8 waves owns 128 rows and one slice:
-// the L1^m fragments of the slice (every k step and N block of up to two
-// non-text modalities present in the rows) are copied once into LDS by DMA,
-// in the MFMA operand order (one 1 KB block per fragment, lane l's 16 bytes
-// at 16 l), and shared by the 8 waves, each of which holds its 16 rows of the
-// slice in registers (the row layout of k_stage1_fr: lane l, row l % 16,
-// columns 64 p + 16 (l / 16) .. + 15 of pair p as two k steps).  So L1^m is
-// read from L2 once per 128 rows, not once per 16.  Rows of a third non-text
-// modality in the same 128 rows read their fragments from global memory.
+// partials part[s][t][0 .. r) over k slices of nchunk chunks of kDlCols
+// columns; grid (ceil(T / 128), S).  A workgroup of 8 waves owns 128 rows
+// and one slice, which it streams in 64-column quarters through a ring of
+// kDlBufs LDS buffers filled by DMA, kDlAhead quarters ahead of the one
+// being multiplied (one barrier a quarter).  A quarter's buffer holds the
+// 128 rows of X, the 64 (L1^m)^T rows of up to two non-text modalities
+// present in the rows, and the smoothing factors of every modality.  Each
+// DMA instruction reads whole 128-byte lines (eight lanes a row, 16 bytes
+// each), which the CU's memory pipe serves several times faster than the
+// 16-row MFMA operand pattern; the rows are stored 128 bytes apart with the
+// 16-byte pieces of row i at piece ^ swz(i), so that the operand reads (16
+// consecutive rows, one piece each) fall on distinct banks.  Wave w
+// multiplies its rows 16 w .. + 15 (lane l: row l % 16, columns
+// 32 st + 8 (l / 16) .. + 7 of k step st), each step's smoothed values
+// entering v_mfma_f32_16x16x32_bf16 as bf16 hi + lo.  L1^m is read from L2
+// once per 128 rows, not once per 16.  Rows of a third non-text modality in
+// the same 128 rows read their operands from global memory afterwards.
 // Tiles without non-text rows return at once: text rows' partials are never
-// read (finish_u_row).  A slice may span nchunk chunks of kDlCols columns
-// (down_lds_chunks): the workgroup stages and multiplies them in turn,
-// summing in registers, so that fewer, wider slices write fewer partials.
-constexpr int kDlPairs = 4;                         // 64-column pairs per chunk
-constexpr int kDlCols = 64 * kDlPairs;
+// read (finish_u_row).
+constexpr int kDlCols = 256;                        // chunk width of the slice plan
 static_assert(kDlCols == kDownLdsCols, "chunk width of the workspace plan");
 constexpr int kDlRows = 128;
 static_assert(kDlRows == kDownLdsRows, "row tile of the workspace plan");
 constexpr int kDlWaves = kDlRows / 16;
+constexpr int kDlBufs = 2;                          // LDS ring of 64-column quarters
+constexpr int kDlAhead = kDlBufs - 1;               // quarters in flight ahead
+constexpr int kDlFragOps = 64 / (8 * kDlWaves);    // DMA instructions per wave for 64 rank rows
+static_assert(kDlFragOps * 8 * kDlWaves == 64 && 2 * 8 * kDlWaves == kDlRows,
+              "whole DMA instructions of 8 rows per wave");
+struct DlQuarter {
+    v4i x[kDlRows * 8];                             // the tile's rows x 8 pieces
+    v4i f[2][64 * 8];                               // two modalities x 64 rank rows
+    v4i s[64];                                      // 4 modalities x 64 factors
+};
+__device__ __forceinline__ int dl_swz(int row) { return (row ^ (row >> 3)) & 7; }
+// s_waitcnt vmcnt(n) for the few counts the ring needs (n wave-uniform)
+__device__ __forceinline__ void dl_wait(int n) {
+    switch (n) {
+        case 0: MASQ_WAIT_VMCNT_LGKM0(0); break;
+        case 3: MASQ_WAIT_VMCNT_LGKM0(3); break;
+        case 4: MASQ_WAIT_VMCNT_LGKM0(4); break;
+        case 5: MASQ_WAIT_VMCNT_LGKM0(5); break;
+        case 6: MASQ_WAIT_VMCNT_LGKM0(6); break;
+        case 8: MASQ_WAIT_VMCNT_LGKM0(8); break;
+        case 9: MASQ_WAIT_VMCNT_LGKM0(9); break;
+        case 10: MASQ_WAIT_VMCNT_LGKM0(10); break;
+        case 12: MASQ_WAIT_VMCNT_LGKM0(12); break;
+        case 15: MASQ_WAIT_VMCNT_LGKM0(15); break;
+        default: MASQ_WAIT_VMCNT_LGKM0(0); break;  // (over-waits)
+    }
+}
 
 __global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
     const bf16_t* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
     const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod, int nchunk,
     float* __restrict__ part) {
-    constexpr int kSteps = 2 * kDlPairs;
-    __shared__ __attribute__((aligned(16))) v4i sfrag[2][kSteps][4][64];    // 64 KB
-    __shared__ __attribute__((aligned(16))) float s_inv[4][kDlCols];
+    __shared__ __attribute__((aligned(16))) DlQuarter sb[kDlBufs];          // 132 KB
     __shared__ int smod[kDlRows];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int ar = lane & 15, kg = lane >> 4;
     const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kDlRows;
     const int s = blockIdx.y;
-    const int npairs = K >> 6;
+    const int npairs = K >> 6;                      // 64-column quarters of the row
 
     if (tid < kDlRows) {
         const int64_t t = row0 + tid;
@@ -1134,10 +1163,10 @@ __global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
     }
     __syncthreads();
     unsigned pres = 0;
-    {
-        const int m2 = smod[2 * lane], m3 = smod[2 * lane + 1];
-        for (int m = 1; m < n_mod; ++m)
-            if (__ballot(m2 == m || m3 == m) != 0ull) pres |= 1u << m;
+    for (int m = 1; m < n_mod; ++m) {
+        bool any = false;
+        for (int k = lane; k < kDlRows; k += 64) any = any || smod[k] == m;
+        if (__ballot(any) != 0ull) pres |= 1u << m;
     }
     const unsigned present = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(pres)));
     if (present == 0) return;                      // uniform over the workgroup
@@ -1149,98 +1178,123 @@ __global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
     const int nsl = min(np, 2);                     // modalities staged in LDS
     const int64_t trow = row0 + 16 * wave + ar;
     const bool valid = trow < T;
-    const bf16_t* xr = x + (valid ? trow : row0) * static_cast<int64_t>(K) + 16 * kg;
     const int mrow = smod[16 * wave + ar];
+    const int qb = s * nchunk * (kDlCols / 64);     // first quarter of the slice
+    const int nq = min(nchunk * (kDlCols / 64), npairs - qb);   // its quarters, >= 1
+    const int g = 2 + kDlFragOps * nsl + (wave == 0 ? 1 : 0);   // DMA instructions per quarter, this wave
+
+    // quarter h into buffer h % kDlBufs: (wave 0) the factors, lane i those
+    // of modality i / 16 (the last one past n_mod), columns 4 (i % 16) ..;
+    // rows 8 (2 w + j) .. + 7 of X (rows past T repeat row T - 1, their
+    // results unused); rank rows 8 w .. + 7 of each staged modality (rows
+    // past r repeat row r - 1)
+    auto issue = [&](int h) __attribute__((always_inline)) {
+        const int col = 64 * (qb + h);
+        const uint32_t base = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(
+            static_cast<int>(reinterpret_cast<uintptr_t>(&sb[h % kDlBufs]))));
+        if (wave == 0) {
+            const int m = min(lane >> 4, n_mod - 1);
+            lds_dma16(inv_s + static_cast<int64_t>(m) * K + col + 4 * (lane & 15),
+                      base + static_cast<uint32_t>(offsetof(DlQuarter, s)));
+        }
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int row = 8 * (2 * wave + j) + (lane >> 3);
+            const int64_t t = min(row0 + row, T - 1);
+            lds_dma16(x + t * K + col + 8 * ((lane & 7) ^ dl_swz(row)),
+                      base + static_cast<uint32_t>(offsetof(DlQuarter, x)) + 1024u * (2 * wave + j));
+        }
+        for (int j = 0; j < nsl; ++j)
+#pragma unroll
+            for (int o = 0; o < kDlFragOps; ++o) {
+                const int blk = kDlFragOps * wave + o;             // 8 rank rows a block
+                const int rr = 8 * blk + (lane >> 3);
+                lds_dma16(l_down + (static_cast<int64_t>(mods[j] - 1) * r + min(rr, r - 1)) * K + col +
+                              8 * ((lane & 7) ^ dl_swz(rr)),
+                          base + static_cast<uint32_t>(offsetof(DlQuarter, f)) + 8192u * j + 1024u * blk);
+            }
+    };
+
     const v4i zero = {0, 0, 0, 0};
     v4f acc[4];
 #pragma unroll
     for (int jb = 0; jb < 4; ++jb) acc[jb] = v4f{0.f, 0.f, 0.f, 0.f};
-    for (int ch = 0; ch < nchunk; ++ch) {
-    const int pb = (s * nchunk + ch) * kDlPairs;   // first pair of the chunk
-    if (pb >= npairs) break;                        // uniform: past the row's end
-    if (ch > 0) __syncthreads();                    // every wave is done with the last chunk's LDS
-
-    // chunk's factors of every modality (16-byte pieces, columns past K
-    // repeat the last piece), then the staged fragments: block b = (slot,
-    // step, N block), lane l's piece from row 16 nb + l % 16 of (L1^m)^T
-    {
-        const uint32_t si0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(s_inv));
-        const int pieces = n_mod * (kDlCols / 4);              // <= 256
-        for (int i = wave; i * 64 < pieces; i += kDlWaves) {
-            const int pc = min(i * 64 + lane, pieces - 1);
-            const int m = pc / (kDlCols / 4), c = 4 * (pc % (kDlCols / 4));
-            const int col = min(pb * 64 + c, K - 4);
-            lds_dma16(inv_s + static_cast<int64_t>(m) * K + col, si0 + i * 1024);
-        }
-        const uint32_t sf0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sfrag));
-        const int blocks = nsl * kSteps * 4;
-        for (int b = wave; b < blocks; b += kDlWaves) {
-            const int slot = b / (kSteps * 4), st = (b / 4) % kSteps, nb = b % 4;
-            const int gp = min(pb + (st >> 1), npairs - 1);
-            const bf16_t* src = l_down +
-                (static_cast<int64_t>(mods[slot] - 1) * r + 16 * min(nb, ncb - 1) + ar) * K +
-                64 * gp + 16 * kg + 8 * (st & 1);
-            lds_dma16(src, sf0 + b * 1024);
-        }
-    }
-    // this wave's 16 rows of the chunk, every load in flight
-    v4i xa[kDlPairs], xb[kDlPairs];
-    asm volatile("" ::: "memory");
+    // one k step: the smoothed row piece as bf16 hi + lo against the four
+    // N blocks of fragments
+    auto step = [&](v4i raw, v4f s0, v4f s1, const v4i (&fb)[4], bool ok) __attribute__((always_inline)) {
+        const float sm[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+        float xs[8];
 #pragma unroll
-    for (int p = 0; p < kDlPairs; ++p) {
-        const int gp = min(pb + p, npairs - 1);
-        xa[p] = *reinterpret_cast<const v4i*>(xr + 64 * gp);
-        xb[p] = *reinterpret_cast<const v4i*>(xr + 64 * gp + 8);
-    }
-    asm volatile("" ::: "memory");
-    MASQ_WAIT_VMCNT_LGKM0(0);
-    __syncthreads();
+        for (int j = 0; j < 4; ++j) {
+            xs[2 * j] = __uint_as_float(static_cast<uint32_t>(raw[j]) << 16) * sm[2 * j];
+            xs[2 * j + 1] = __uint_as_float(static_cast<uint32_t>(raw[j]) & 0xFFFF0000u) * sm[2 * j + 1];
+        }
+        v4i hi, lo;
+        split_bf16x8(xs, hi, lo);
+        const v4i hh = ok ? hi : zero, ll = ok ? lo : zero;
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb)
+            acc[jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(v8bf, hh), __builtin_bit_cast(v8bf, fb[jb]), acc[jb], 0, 0, 0);
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb)
+            acc[jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(v8bf, ll), __builtin_bit_cast(v8bf, fb[jb]), acc[jb], 0, 0, 0);
+    };
 
-    for (int mi = 0; mi < np; ++mi) {
-        const int m = mods[mi];
+    for (int h = 0; h < kDlAhead && h < nq; ++h) issue(h);
+    const int xrow = 16 * wave + ar;
+    for (int h = 0; h < nq; ++h) {
+        // quarter h has landed once at most the younger quarters' DMA is in
+        // flight; the barrier also retires every read of the buffer the next
+        // issue refills (quarter h - 1's)
+        dl_wait(min(nq - 1 - h, kDlAhead - 1) * g);
+        __syncthreads();
+        if (h + kDlAhead < nq) issue(h + kDlAhead);
+        const DlQuarter& q = sb[h % kDlBufs];
+        const float* sq = reinterpret_cast<const float*>(q.s);
+        for (int mi = 0; mi < nsl; ++mi) {
+            const bool mine = valid && mrow == mods[mi];
+            if (__ballot(mine) == 0ull) continue;  // uniform over the wave
+#pragma unroll
+            for (int st = 0; st < 2; ++st) {
+                const int pc = 4 * st + kg;
+                const float* sp = sq + mrow * 64 + 8 * pc;
+                v4i fb[4];
+#pragma unroll
+                for (int jb = 0; jb < 4; ++jb) {
+                    const int rr = 16 * min(jb, ncb - 1) + ar;
+                    fb[jb] = q.f[mi][rr * 8 + (pc ^ dl_swz(rr))];
+                }
+                step(q.x[xrow * 8 + (pc ^ dl_swz(xrow))], *reinterpret_cast<const v4f*>(sp),
+                     *reinterpret_cast<const v4f*>(sp + 4), fb, mine);
+            }
+        }
+    }
+    if (np == 3) {
+        // rows of a third non-text modality in the tile: their quarters in
+        // turn, operands straight from global memory
+        const int m = mods[2];
         const bool mine = valid && mrow == m;
-        if (__ballot(mine) == 0ull) continue;      // uniform over the wave
+        if (__ballot(mine) != 0ull) {
+            const bf16_t* xr = x + (valid ? trow : row0) * static_cast<int64_t>(K) + 8 * kg;
+            const float* srow = inv_s + static_cast<int64_t>(m) * K + 8 * kg;
+            for (int h = 0; h < nq; ++h) {
 #pragma unroll
-        for (int st = 0; st < kSteps; ++st) {
-            const int p = st >> 1, h = st & 1;
-            const bool ok = mine && pb + p < npairs;
-            const int gp = min(pb + p, npairs - 1);
-            const v4i raw = h ? xb[p] : xa[p];
-            const float* sp = &s_inv[mrow][64 * p + 16 * kg + 8 * h];
-            const v4f s0 = *reinterpret_cast<const v4f*>(sp);
-            const v4f s1 = *reinterpret_cast<const v4f*>(sp + 4);
-            const float sv[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-            float xs[8];
+                for (int st = 0; st < 2; ++st) {
+                    const int c = 64 * (qb + h) + 32 * st;
+                    v4i fb[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                xs[2 * j] = __uint_as_float(static_cast<uint32_t>(raw[j]) << 16) * sv[2 * j];
-                xs[2 * j + 1] = __uint_as_float(static_cast<uint32_t>(raw[j]) & 0xFFFF0000u) * sv[2 * j + 1];
+                    for (int jb = 0; jb < 4; ++jb)
+                        fb[jb] = *reinterpret_cast<const v4i*>(
+                            l_down + (static_cast<int64_t>(m - 1) * r + 16 * min(jb, ncb - 1) + ar) * K + c +
+                            8 * kg);
+                    step(*reinterpret_cast<const v4i*>(xr + c), *reinterpret_cast<const v4f*>(srow + c),
+                         *reinterpret_cast<const v4f*>(srow + c + 4), fb, mine);
+                }
             }
-            v4i hi, lo;
-            split_bf16x8(xs, hi, lo);
-            const v4i hh = ok ? hi : zero, ll = ok ? lo : zero;
-            v4i fb[4];
-            if (mi < 2) {
-#pragma unroll
-                for (int jb = 0; jb < 4; ++jb) fb[jb] = sfrag[mi][st][jb][lane];
-            } else {
-#pragma unroll
-                for (int jb = 0; jb < 4; ++jb)
-                    fb[jb] = *reinterpret_cast<const v4i*>(
-                        l_down + (static_cast<int64_t>(m - 1) * r + 16 * min(jb, ncb - 1) + ar) * K +
-                        64 * gp + 16 * kg + 8 * h);
-            }
-#pragma unroll
-            for (int jb = 0; jb < 4; ++jb)
-                acc[jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    __builtin_bit_cast(v8bf, hh), __builtin_bit_cast(v8bf, fb[jb]), acc[jb], 0, 0, 0);
-#pragma unroll
-            for (int jb = 0; jb < 4; ++jb)
-                acc[jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    __builtin_bit_cast(v8bf, ll), __builtin_bit_cast(v8bf, fb[jb]), acc[jb], 0, 0, 0);
         }
     }
-    }   // chunks
     // partials of the wave's rows: lane holds rows 4 (l / 16) + i, column
     // 16 jb + l % 16
     float* pp = part + static_cast<int64_t>(s) * T * r;
