@@ -390,14 +390,17 @@ _EDGE = {
     "down_lds_four_mod_alternating_k3584": dict(T=300, K=3584, N=32, r=64, M=4, act="bf16",
                                                 lr="bf16"),
     "down_lds_t40_k4160_r16": dict(T=40, K=4160, N=64, r=16, M=2, act="bf16", lr="bf16"),
-    # k slices spanning two and four 256-column chunks (long rows, large
-    # grids), the last slice short of chunks and its last chunk short of
-    # columns
-    "down_lds_two_chunks_t4096_k8192": dict(T=4096, K=8192, N=32, r=64, M=3, act="bf16",
-                                            lr="bf16", layout="runs"),
-    "down_lds_four_chunks_ragged_t8192_k8256": dict(T=8192, K=8256, N=16, r=32, M=2,
-                                                    act="bf16", lr="bf16",
-                                                    layout="contiguous"),
+    # k slices of two and five 256-column chunks streamed in 64-column
+    # quarters (long rows, large grids), the last slice short of chunks and
+    # its last chunk one quarter long; a ragged last row tile of two rows
+    # whose slice ends in an odd number of quarters
+    "down_lds_two_chunk_slices_t4096_k8192": dict(T=4096, K=8192, N=32, r=64, M=3,
+                                                  act="bf16", lr="bf16", layout="runs"),
+    "down_lds_five_chunk_slices_ragged_t8192_k8256": dict(T=8192, K=8256, N=16, r=32, M=2,
+                                                          act="bf16", lr="bf16",
+                                                          layout="contiguous"),
+    "down_lds_ragged_tile_t130_k1216_r32": dict(T=130, K=1216, N=32, r=32, M=3, act="bf16",
+                                                lr="bf16"),
     # 32-row stage-1 workgroups (batches of 8192 tokens and more), ragged tail
     "stage1_wide_ragged_t8200": dict(T=8200, K=128, N=32, r=64, M=3, act="bf16", lr="bf16",
                                      layout="runs"),
