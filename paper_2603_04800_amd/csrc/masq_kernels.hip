@@ -256,15 +256,17 @@ __device__ __forceinline__ void finish_u_row(int64_t t, int64_t T, bool text, co
     const int k = lane;
     float v = 0.f;                      // text rows: u = 0 (their partials are not written)
     if (k < r && !text) {
+        // the slices' partials in flight together (16 a batch; past the last
+        // slice the last is re-read and not added), added in slice order
         const float* p = part + t * r + k;
         const int64_t step = T * r;
-        v = p[0];
-        for (int s0 = 1; s0 < slices; s0 += 8) {
-            float pv[8];
+        for (int s0 = 0; s0 < slices; s0 += 16) {
+            float pv[16];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) pv[q] = p[min(s0 + q, slices - 1) * step];
+            for (int q = 0; q < 16; ++q) pv[q] = p[min(s0 + q, slices - 1) * step];
+            v = s0 == 0 ? pv[0] : v + pv[0];
 #pragma unroll
-            for (int q = 0; q < 8; ++q)
+            for (int q = 1; q < 16; ++q)
                 if (s0 + q < slices) v += pv[q];
         }
     }
@@ -304,28 +306,15 @@ __device__ __forceinline__ void split_bf16x8(const float (&v)[8], v4i& hi, v4i& 
     }
 }
 
-// One wave per token row (four rows per workgroup), the row's smoothed values
-// kept in registers between the absmax and the quantisation pass for rows up
-// to 64 * 8 * NC elements; longer rows stream their remainder twice.  Used
-// for large batches; k_smooth_quant (a whole workgroup per row) serves small
-// ones, where a row's latency matters more than the number of rows in flight.
-
+// One row t quantised by one wave (lane = this lane), its smoothed values
+// kept in registers between the absmax and the codes for rows of up to
+// 64 * 8 * NC elements; longer rows stream their remainder twice.
 template <typename XT, int NC>
-__global__ __launch_bounds__(256) void k_smooth_quant_rows(const XT* __restrict__ x,
-                                                           const int32_t* __restrict__ mod,
-                                                           const float* __restrict__ inv_s,
-                                                           int64_t T, int K, int n_mod,
-                                                           int8_t* __restrict__ q,
-                                                           float* __restrict__ x_scale,
-                                                           int* __restrict__ zero_ints,
-                                                           int n_zero, UFinish fin, bool pair) {
-    if (blockIdx.x == 0)
-        for (int i = threadIdx.x; i < n_zero; i += 256) zero_ints[i] = 0;
-    const int lane = threadIdx.x & 63;
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
-    if (t >= T) return;
+__device__ __forceinline__ void quant_row_wave(const XT* __restrict__ x, const int32_t* __restrict__ mod,
+                                               const float* __restrict__ inv_s, int K, int n_mod,
+                                               int8_t* __restrict__ q, float* __restrict__ x_scale,
+                                               int64_t t, bool pair, int lane) {
     const int m = sane_mod(mod[t], n_mod);
-    if (fin.part != nullptr) finish_u_row(t, T, m == 0, fin.part, fin.slices, fin.r, fin.u, fin.u_hl, lane);
     const XT* xr = x + t * static_cast<int64_t>(K);
     const float* sr = inv_s + static_cast<int64_t>(m) * K;
     int8_t* qr = q + code_row(t, K, pair);
@@ -386,6 +375,28 @@ __global__ __launch_bounds__(256) void k_smooth_quant_rows(const XT* __restrict_
         for (int j = 0; j < 8; ++j) vals[j] = xv[j] * sv[j];
         store8(v, vals);
     }
+}
+
+// One wave per token row (four rows per workgroup).  Used for large
+// batches; k_smooth_quant (a whole workgroup per row) serves small ones,
+// where a row's latency matters more than the number of rows in flight.
+template <typename XT, int NC>
+__global__ __launch_bounds__(256) void k_smooth_quant_rows(const XT* __restrict__ x,
+                                                           const int32_t* __restrict__ mod,
+                                                           const float* __restrict__ inv_s,
+                                                           int64_t T, int K, int n_mod,
+                                                           int8_t* __restrict__ q,
+                                                           float* __restrict__ x_scale,
+                                                           int* __restrict__ zero_ints,
+                                                           int n_zero, UFinish fin, bool pair) {
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < n_zero; i += 256) zero_ints[i] = 0;
+    const int lane = threadIdx.x & 63;
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    if (t >= T) return;
+    if (fin.part != nullptr)
+        finish_u_row(t, T, sane_mod(mod[t], n_mod) == 0, fin.part, fin.slices, fin.r, fin.u, fin.u_hl, lane);
+    quant_row_wave<XT, NC>(x, mod, inv_s, K, n_mod, q, x_scale, t, pair, lane);
 }
 
 // ================================================================ down-projection
@@ -1144,17 +1155,16 @@ __device__ __forceinline__ void dl_wait(int n) {
     }
 }
 
-__global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
+__device__ __forceinline__ void down_lds_tile(
     const bf16_t* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
     const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod, int nchunk,
-    float* __restrict__ part) {
+    float* __restrict__ part, int tile, int s) {
     __shared__ __attribute__((aligned(16))) DlQuarter sb[kDlBufs];          // 132 KB
     __shared__ int smod[kDlRows];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int ar = lane & 15, kg = lane >> 4;
-    const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kDlRows;
-    const int s = blockIdx.y;
+    const int64_t row0 = static_cast<int64_t>(tile) * kDlRows;
     const int npairs = K >> 6;                      // 64-column quarters of the row
 
     if (tid < kDlRows) {
@@ -1307,6 +1317,13 @@ __global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
             if (t < T) pp[t * r + 16 * jb + ar] = acc[jb][i];
         }
     }
+}
+
+__global__ __launch_bounds__(64 * kDlWaves) void k_down_lds(
+    const bf16_t* __restrict__ x, const int32_t* __restrict__ mod, const float* __restrict__ inv_s,
+    const bf16_t* __restrict__ l_down, int64_t T, int K, int r, int n_mod, int nchunk,
+    float* __restrict__ part) {
+    down_lds_tile(x, mod, inv_s, l_down, T, K, r, n_mod, nchunk, part, blockIdx.x, blockIdx.y);
 }
 
 // ---------------------------------------------------------------- fused stage 1, rows in registers
