@@ -1111,10 +1111,9 @@ __global__ __launch_bounds__(64 * kFuseWaves) void k_stage1_fused(
 // 128 rows of X, the 64 (L1^m)^T rows of up to two non-text modalities
 // present in the rows, and the smoothing factors of every modality.  Each
 // DMA instruction reads whole 128-byte lines (eight lanes a row, 16 bytes
-// each), which the CU's memory pipe serves several times faster than the
-// 16-row MFMA operand pattern; the rows are stored 128 bytes apart with the
-// 16-byte pieces of row i at piece ^ swz(i), so that the operand reads (16
-// consecutive rows, one piece each) fall on distinct banks.  Wave w
+// each); the rows are stored 128 bytes apart with the 16-byte pieces of
+// row i at piece ^ (i % 8), so that the operand reads (8 consecutive rows,
+// one piece each, per 128-byte bank cycle) fall on distinct banks.  Wave w
 // multiplies its rows 16 w .. + 15 (lane l: row l % 16, columns
 // 32 st + 8 (l / 16) .. + 7 of k step st), each step's smoothed values
 // entering v_mfma_f32_16x16x32_bf16 as bf16 hi + lo.  L1^m is read from L2
@@ -1137,7 +1136,7 @@ struct DlQuarter {
     v4i f[2][64 * 8];                               // two modalities x 64 rank rows
     v4i s[64];                                      // 4 modalities x 64 factors
 };
-__device__ __forceinline__ int dl_swz(int row) { return (row ^ (row >> 3)) & 7; }
+__device__ __forceinline__ int dl_swz(int row) { return row & 7; }
 // s_waitcnt vmcnt(n) for the few counts the ring needs (n wave-uniform)
 __device__ __forceinline__ void dl_wait(int n) {
     switch (n) {
