@@ -135,7 +135,7 @@ struct Workspace {
     int* zero_base;
     int dw_slices, dw_kslice;   // plan_down_wide (dw_part != nullptr)
     float* dw_part;    // [dw_slices][T][rank] fp32 partials of the wide down-projection
-    float* dl_part;    // [down_lds_slices(K)][T][rank] fp32 partials of k_down_lds
+    float* dl_part;    // [down_lds_slices(T, K)][T][rank] fp32 partials of k_down_lds
     int n_kslices;
     int kslice;
     size_t bytes;
@@ -190,7 +190,7 @@ inline bool stage1_fr_ok(DT x_dt, int64_t K, int n_mod) {
 }
 // Down-projection with the L1 fragments staged in LDS (k_down_lds): bf16
 // activations and factors, rank <= 64, K % 64 == 0; slice partials
-// [down_lds_slices(K)][T][rank] for the quantisation kernel to add.
+// [down_lds_slices(T, K)][T][rank] for the quantisation kernel to add.
 constexpr int64_t kDownLdsCols = 256;    // columns staged in LDS at a time (a chunk)
 constexpr int64_t kDownLdsRows = 128;    // rows of a workgroup's tile
 // Chunks per k slice: the workgroups (two per CU: 66 KB of LDS each) stream
