@@ -203,6 +203,40 @@ def test_random_shape_parity(ops, case):
     _check_layer(ops, L, name="sweep")
 
 
+def _split_cases(n=16, seed=79):
+    """Seeded random shapes for the split stage 1 (bf16 activations and
+    factors, rank 16-64, two to four modalities, 17-4095 tokens, K a
+    multiple of 64 up to 8960): the quarter-streamed down-projection with
+    slices of one or more chunks, last chunks of one to four quarters,
+    ragged row tiles, tiles holding one, two or three non-text modalities,
+    and both row quantisers (a wave per row up to 4096 columns, a workgroup
+    per row beyond)."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        T = int(rng.integers(17, 4096))
+        K = 64 * int(rng.integers(2, 141))
+        N = 16 * int(rng.integers(1, 7))
+        M = int(rng.integers(2, 5))
+        r = 16 * int(rng.integers(1, 5))
+        layout = str(rng.choice(["contiguous", "alternating", "runs"]))
+        cases.append(dict(T=T, K=K, N=N, r=r, M=M, act="bf16", lr="bf16", layout=layout,
+                          seed=int(seed + i)))
+    return cases
+
+
+_SPLIT = _split_cases()
+
+
+@pytest.mark.parametrize("case", _SPLIT, ids=[
+    f"T{c['T']}_K{c['K']}_N{c['N']}_r{c['r']}_M{c['M']}_{c['layout']}" for c in _SPLIT])
+def test_split_stage1_sweep(ops, case):
+    kw = dict(case)
+    L = _random_layer(kw.pop("T"), kw.pop("K"), kw.pop("N"), kw.pop("r"), kw.pop("M"),
+                      kw.pop("act"), kw.pop("lr"), **kw)
+    _check_layer(ops, L, name="split-sweep")
+
+
 # ------------------------------------------------------------------ comparator
 @pytest.mark.parametrize("cfg_index", [0, 2, 3])
 def test_smoothquant_comparator_parity(ops, cfg_index):
