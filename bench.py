@@ -21,7 +21,9 @@ peak (algorithmic int8 ops) or, below the ridge point (the decode
 workload), against 8 TB/s HBM (algorithmic bytes of the kernel), and
 against the measured peaks (an int8 MFMA issue loop, a linear HBM read).
 step_percentiles_ms: median, p10, p90 over max(K, 100) steps with an event
-between consecutive steps.  configs: the same summary for every workload
+between consecutive steps.  sclk_under_load: the shader clock rocm-smi
+reports while the headline step runs back to back for 1.5 s (after the
+timed regions).  configs: the same summary for every workload
 (at least 100 steps each).  cpu_baseline: the CPU oracle on the headline
 workload.
 """
@@ -66,6 +68,9 @@ def parse():
                     help="skip the measured-peak probes (int8 MFMA loop, HBM read and copy)")
     ap.add_argument("--only-headline", action="store_true",
                     help="time only --workload, not every workload's summary object")
+    ap.add_argument("--no-sclk", action="store_true",
+                    help="skip reading the shader clock (rocm-smi) while the headline "
+                         "workload runs back to back")
     ap.add_argument("--summarize-profiles", metavar="DIR", default=None,
                     help="write the profiles/ summaries of the rocprofv3 runs under DIR "
                          "(trace/, fetch/, write/, copy_fetch/, copy_write/ and their .log; "
@@ -643,8 +648,30 @@ def _pct(vals, q):
     return v[lo] + (v[hi] - v[lo]) * (k - lo)
 
 
+def read_sclk(timeout_s: float = 20.0) -> dict:
+    """The shader clock rocm-smi reports for every card it sees (MHz), run as
+    a child process."""
+    import re
+    import subprocess
+    try:
+        out = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True,
+                             text=True, timeout=timeout_s)
+        data = json.loads(out.stdout)
+    except Exception as e:              # the clock is a report, never the measurement
+        return {"error": repr(e)}
+    cards = {}
+    for card, fields in data.items():
+        if not isinstance(fields, dict):
+            continue
+        for k, v in fields.items():
+            m = re.search(r"(\d+)\s*mhz", str(v), re.I)
+            if "sclk" in k.lower() and "speed" in k.lower() and m:
+                cards[card] = int(m.group(1))
+    return {"sclk_mhz": cards} if cards else {"error": "no sclk field", "raw": out.stdout[:300]}
+
+
 def measure_workload(cfg_index, method, bits, steps, warmup, copies_min, dev, pct_steps=100,
-                     keep_layers=False, min_warm_s=0.1):
+                     keep_layers=False, min_warm_s=0.1, sclk_s=0.0):
     """Time one workload.  Three regions, each bracketed by events on the
     launch stream after a synchronisation, on rotating copies of every
     input, weight, output and workspace:
@@ -730,12 +757,35 @@ def measure_workload(cfg_index, method, bits, steps, warmup, copies_min, dev, pc
         evs[i + 1].record()
     torch.cuda.synchronize()
     per = [evs[i].elapsed_time(evs[i + 1]) for i in range(n_pct)]
+    sclk = None
+    if sclk_s > 0:
+        # the clock under this load: steps back to back for sclk_s seconds
+        # while a thread asks rocm-smi once, half a second in
+        import threading
+        box = {}
+
+        def probe():
+            time.sleep(0.5)
+            box.update(read_sclk())
+
+        th = threading.Thread(target=probe)
+        th.start()
+        t_s, i = time.perf_counter(), 0
+        while th.is_alive() or time.perf_counter() - t_s < sclk_s:
+            for _ in range(8):
+                step(i)
+                i += 1
+            torch.cuda.synchronize()
+        th.join()
+        sclk = dict(box, seconds=round(time.perf_counter() - t_s, 2), steps=i,
+                    source="rocm-smi --showclocks, while the steps ran back to back")
     log(f"[bench] {cfg.name}: {step_ms:.4f} ms/step over {steps} steps, stage 2 "
         f"{gemm_ms:.4f} ms; per-step median {_pct(per, 0.5):.4f} ms over {n_pct}")
     res = {"cfg": cfg, "layers": layers if keep_layers else None, "copies": copies,
            "warmup_steps_run": warmup,
            "step_ms": step_ms, "gemm_ms": gemm_ms, "n_pct": n_pct,
            "median_ms": _pct(per, 0.5), "p10_ms": _pct(per, 0.1), "p90_ms": _pct(per, 0.9),
+           "sclk": sclk,
            "ops": sum(2.0 * T * L["x"].shape[1] * L["wq"].shape[-2] for L in layers),
            "bytes": sum(algorithmic_bytes(L) for L in layers),
            "gemm_bytes": sum(gemm_bytes(L) for L in layers),
@@ -836,7 +886,8 @@ def main():
                                  args.warmup, args.copies, dev)
             per[str(ci)] = config_summary(r, peaks)
     head = measure_workload(args.workload, args.method, args.weight_bits, args.steps,
-                            args.warmup, args.copies, dev, keep_layers=True)
+                            args.warmup, args.copies, dev, keep_layers=True,
+                            sclk_s=0.0 if args.no_sclk else 1.5)
     cfg, layers = head["cfg"], head["layers"]
     log(f"[bench] timed {args.steps} steps: {head['step_ms']:.4f} ms/step, stage 2 "
         f"{head['gemm_ms']:.4f} ms")
@@ -889,6 +940,7 @@ def main():
                                 "steps": head["n_pct"]},
         "roofline": roof,
         "measured_peaks": peaks,
+        "sclk_under_load": head["sclk"],
         "kernel_source_sha256_16": src_hash,
     }
     if not args.no_cpu and args.method == "masquant":
