@@ -89,3 +89,31 @@ def test_graph_replays_equal_eager(name):
 def _need(lin):
     from paper_2603_04800_amd import ops
     return ops.workspace_bytes(300, lin.c_in, lin.c_out, lin.rank, lin.n_mod)
+
+
+def test_concurrent_streams_with_separate_workspaces():
+    """Two layers (tiled and split-K shapes) on two streams at the default
+    priority, each with its own workspace, enqueued interleaved so that their
+    kernels can overlap: the workspace entry point keeps no state outside its
+    workspace, so each result equals its sequential one bit for bit."""
+    assert torch.cuda.is_available()
+    from paper_2603_04800_amd import ops, workload
+    layers = [workload.to_device(_layer(*_SHAPES[n], seed=50 + i))
+              for i, n in enumerate(("persistent_t4096_k3584_n2048", "split_k_t700_k1024_n528"))]
+    refs = [_bits(lin(x, mod, out_dtype=torch.bfloat16)) for x, mod, lin in layers]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs, wss = [], []
+    for x, mod, lin in layers:
+        outs.append(torch.empty((x.shape[0], lin.c_out), dtype=torch.bfloat16, device=x.device))
+        need = ops.workspace_bytes(x.shape[0], lin.c_in, lin.c_out, lin.rank, lin.n_mod)
+        wss.append(torch.empty(max(need, 256), dtype=torch.uint8, device=x.device))
+    for st in streams:
+        st.wait_stream(torch.cuda.current_stream())
+    for rep in range(4):
+        for i, (x, mod, lin) in enumerate(layers):
+            with torch.cuda.stream(streams[i]):
+                lin(x, mod, out=outs[i], workspace=wss[i])
+    torch.cuda.synchronize()
+    for i in range(2):
+        assert torch.equal(_bits(outs[i]), refs[i]), f"layer {i}"
